@@ -1,0 +1,359 @@
+"""NumPy float64 definitions of the role-conditional eviction hot path.
+
+TEST INFRASTRUCTURE ONLY (see the package docstring): never imported by the
+product path.
+
+Notation (paper §2, §4 and Algorithm 1):
+  N   cached tokens, W observation window (last W prefill queries),
+  G   query heads per KV head (grouped-query attention),
+  P   candidate prefix [0, N-W); the window [N-W, N) is always kept,
+  B   budget (fraction of the N tokens that may stay in the cache),
+  R   number of role buckets, alpha[r] the per-bucket weight.
+
+Readings taken where the paper is silent (each one is restated in the function
+that uses it):
+  R1  softmax scale defaults to 1/sqrt(d);
+  R2  query head h reads KV head h // G (contiguous groups) and the mass of the
+      G heads of a group is summed;
+  R3  the window queries sit at positions N-W .. N-1 and are causal inside the
+      window (query at position i sees keys t <= i);
+  R4  the max-pool is stride 1, same length, padded with -inf and runs over the
+      candidate prefix only; window scores are left unpooled;
+  R5  the window is inside the budget: K = min(N, ceil(B*N)), K_p = max(0, K-W);
+  R6  the bucket quotas split K_p (the n_kv of the per-bucket ceiling with the
+      window taken out);
+  R7  every ceiling is taken as ceil(x - 1e-9) so that binary64 products such
+      as 0.07*100 = 7.000000000000001 round to the intended integer;
+  R8  alpha is renormalised over the buckets that take part (alpha > 0 and at
+      least one candidate token);
+  R9  "redistribute unused budget from saturated buckets": a bucket whose
+      ceiling share exceeds its population keeps its whole population and the
+      budget it cannot use is re-split, by the same proportional-ceiling rule,
+      over the buckets still open; repeated until no bucket overflows;
+  R10 budget left once every positive-weight bucket is full stays unspent; a
+      budget B >= 1 is the full-cache baseline and keeps all N tokens;
+  R12 equal scores: the lower token index wins;
+  R13 -0.0 ranks equal to +0.0 and NaN ranks below every number.
+"""
+
+from __future__ import annotations
+
+import math
+
+import numpy as np
+
+__all__ = [
+    "CEIL_GUARD",
+    "ceil_guarded",
+    "causal_logits",
+    "causal_softmax",
+    "snapkv_mass",
+    "h2o_mass",
+    "maxpool_prefix",
+    "snapkv_score",
+    "h2o_score",
+    "role_counts",
+    "role_allocate",
+    "role_allocate_batch",
+    "rank_key",
+    "select_keep",
+    "topk_select",
+    "kv_compact",
+    "per_role_mean_mass",
+    "retention_rate",
+    "retained_snr_db",
+]
+
+CEIL_GUARD = 1e-9
+
+
+def ceil_guarded(x: float) -> int:
+    """Integer ceiling with the binary64 guard of reading R7."""
+    return int(math.ceil(float(x) - CEIL_GUARD))
+
+
+# ---------------------------------------------------------------------------
+# Scores: causal softmax, H2O accumulated mass, SnapKV windowed mass, pool
+# ---------------------------------------------------------------------------
+
+def causal_logits(q_rows: np.ndarray, q_pos: np.ndarray, k: np.ndarray,
+                  scale: float) -> np.ndarray:
+    """Scaled logits x[r, t] = scale * <q_r, k_t> for keys t <= q_pos[r].
+
+    Entries with t > q_pos[r] (future keys) are -inf: the prefill attention the
+    scores are read from is causal (§2, p_t(q) is the attention probability a
+    query q puts on key t).  float64 throughout.
+    """
+    q = np.asarray(q_rows, dtype=np.float64)
+    kk = np.asarray(k, dtype=np.float64)
+    x = scale * (q @ kk.T)
+    t = np.arange(kk.shape[0])
+    x = np.where(t[None, :] <= np.asarray(q_pos)[:, None], x, -np.inf)
+    return x
+
+
+def causal_softmax(x: np.ndarray) -> np.ndarray:
+    """Row softmax of causal logits (masked entries, -inf, get probability 0).
+
+    p[r, t] = exp(x[r, t] - m_r) / sum_u exp(x[r, u] - m_r), m_r = max_u x[r, u],
+    the probability p_t(q) of §2 for query row r.
+    """
+    m = np.max(x, axis=1, keepdims=True)
+    e = np.exp(x - m)
+    return e / np.sum(e, axis=1, keepdims=True)
+
+
+def snapkv_mass(q_win: np.ndarray, k: np.ndarray, scale: float | None = None) -> np.ndarray:
+    """SnapKV windowed mass of one KV head (§2; §4 "SnapKV mechanism";
+    Algorithm 1, windowed-mass step).
+
+    q_win : [G, W, d] the last W prefill queries of the G query heads that
+            share this KV head (readings R2, R3);
+    k     : [N, d] the cached keys.
+    Returns s[N] with s(t) = sum over heads h and window queries i >= t of
+    p_h[i, t].  Summed over the G heads (R2).
+    """
+    q_win = np.asarray(q_win, dtype=np.float64)
+    G, W, d = q_win.shape
+    N = k.shape[0]
+    if scale is None:
+        scale = 1.0 / math.sqrt(d)                       # R1
+    pos = np.arange(N - W, N)                            # R3
+    s = np.zeros(N, dtype=np.float64)
+    for h in range(G):
+        p = causal_softmax(causal_logits(q_win[h], pos, k, scale))
+        s += p.sum(axis=0)
+    return s
+
+
+def h2o_mass(q: np.ndarray, k: np.ndarray, scale: float | None = None,
+             row_block: int = 2048) -> np.ndarray:
+    """H2O heavy-hitter score of one KV head: s(t) = sum_q p_t(q) over every
+    prefill query (§2, H2O family), summed over the G query heads (R2).
+
+    q : [G, N, d] all prefill queries of the group, k : [N, d].
+    Rows are processed in blocks only to bound memory; each row's softmax is
+    the full causal row.
+    """
+    q = np.asarray(q, dtype=np.float64)
+    G, N, d = q.shape
+    if scale is None:
+        scale = 1.0 / math.sqrt(d)
+    s = np.zeros(N, dtype=np.float64)
+    for h in range(G):
+        for r0 in range(0, N, row_block):
+            pos = np.arange(r0, min(N, r0 + row_block))
+            p = causal_softmax(causal_logits(q[h, pos], pos, k, scale))
+            s += p.sum(axis=0)
+    return s
+
+
+def maxpool_prefix(s: np.ndarray, W: int, kernel: int) -> np.ndarray:
+    """1-D max-pool along the KV axis (§4 "SnapKV mechanism", kernel 7;
+    Algorithm 1, pooling step), reading R4.
+
+    For t in the prefix P = [0, N-W): s~(t) = max{ s(u) : u in P, |u-t| <= kernel//2 }.
+    Window positions keep their raw score.
+    """
+    if kernel < 1 or kernel % 2 == 0:
+        raise ValueError("pool kernel must be odd and >= 1")
+    s = np.asarray(s, dtype=np.float64)
+    N = s.shape[0]
+    P = N - W
+    out = s.copy()
+    h = kernel // 2
+    for t in range(P):
+        lo, hi = max(0, t - h), min(P, t + h + 1)
+        out[t] = np.max(s[lo:hi])
+    return out
+
+
+def snapkv_score(q_win: np.ndarray, k: np.ndarray, n_kv_heads: int,
+                 pool_kernel: int, scale: float | None = None) -> np.ndarray:
+    """Pooled SnapKV score for whole tensors.
+
+    q_win [L, B, Hq, W, d], k [L, B, Hkv, N, d] -> score [L, B, Hkv, N]
+    (pooled on the prefix, raw on the window).  Query head h belongs to KV head
+    h // G with G = Hq / Hkv (R2).
+    """
+    L, Bt, Hq, W, d = q_win.shape
+    N = k.shape[3]
+    G = Hq // n_kv_heads
+    out = np.zeros((L, Bt, n_kv_heads, N), dtype=np.float64)
+    for l in range(L):
+        for b in range(Bt):
+            for j in range(n_kv_heads):
+                s = snapkv_mass(q_win[l, b, j * G:(j + 1) * G], k[l, b, j], scale)
+                out[l, b, j] = maxpool_prefix(s, W, pool_kernel)
+    return out
+
+
+def h2o_score(q: np.ndarray, k: np.ndarray, n_kv_heads: int,
+              scale: float | None = None) -> np.ndarray:
+    """H2O score for whole tensors: q [L, B, Hq, N, d], k [L, B, Hkv, N, d]
+    -> [L, B, Hkv, N].  No window and no pool (reading R14: W = 0, kernel 1)."""
+    L, Bt, Hq, N, d = q.shape
+    G = Hq // n_kv_heads
+    out = np.zeros((L, Bt, n_kv_heads, N), dtype=np.float64)
+    for l in range(L):
+        for b in range(Bt):
+            for j in range(n_kv_heads):
+                out[l, b, j] = h2o_mass(q[l, b, j * G:(j + 1) * G], k[l, b, j], scale)
+    return out
+
+
+# ---------------------------------------------------------------------------
+# Role-conditional allocation (§4.1, Algorithm 1 per-bucket top-k and
+# redistribution steps)
+# ---------------------------------------------------------------------------
+
+def role_counts(roles: np.ndarray, R: int, W: int) -> np.ndarray:
+    """n_r: number of candidate-prefix tokens (t < N-W) carrying role r."""
+    roles = np.asarray(roles)
+    N = roles.shape[0]
+    pre = roles[:N - W]
+    return np.array([int(np.sum(pre == r)) for r in range(R)], dtype=np.int64)
+
+
+def role_allocate(roles: np.ndarray, R: int, alpha, budget: float, W: int):
+    """Per-bucket quotas for one sample (§4.1 role policy; Algorithm 1).
+
+    Returns (quota[R], kept) where quota[r] tokens of bucket r are kept from
+    the candidate prefix and kept = W + sum(quota) counts the window too.
+    Readings R5-R10.
+    """
+    roles = np.asarray(roles)
+    N = int(roles.shape[0])
+    alpha = [float(a) for a in alpha]
+    if len(alpha) != R:
+        raise ValueError("alpha must have R entries")
+    if not (0 <= W <= N):
+        raise ValueError("need 0 <= W <= N")
+    if budget <= 0:
+        raise ValueError("budget must be > 0")
+    if np.any(roles < 0) or np.any(roles >= R):
+        raise ValueError("role label outside [0, R)")
+    if any(a < 0 for a in alpha) or sum(alpha) <= 0:
+        raise ValueError("alpha must be >= 0 with a positive sum")
+    n = role_counts(roles, R, W)
+    if budget >= 1.0:                                  # R10: full-cache baseline
+        return n.copy(), N
+    K = min(N, ceil_guarded(budget * N))               # R5
+    rem = max(0, K - W)                                # R5/R6
+    quota = np.zeros(R, dtype=np.int64)
+    open_ = [r for r in range(R) if alpha[r] > 0 and n[r] > 0]   # R8
+    while rem > 0 and open_:
+        total = sum(alpha[r] for r in open_)
+        share = {r: ceil_guarded(alpha[r] / total * rem) for r in open_}
+        full = [r for r in open_ if share[r] > n[r]]   # R9: cannot use its share
+        if not full:
+            for r in open_:
+                quota[r] = share[r]
+            break
+        for r in full:
+            quota[r] = n[r]
+            rem -= int(n[r])
+        open_ = [r for r in open_ if r not in full]
+        rem = max(rem, 0)
+    return quota, int(W + quota.sum())
+
+
+def role_allocate_batch(roles: np.ndarray, R: int, alpha, budget: float, W: int):
+    """role_allocate for every sample of roles [B, N]: (quota[B, R], kept[B], k_cap)."""
+    roles = np.asarray(roles)
+    Bt = roles.shape[0]
+    quota = np.zeros((Bt, R), dtype=np.int64)
+    kept = np.zeros(Bt, dtype=np.int64)
+    for b in range(Bt):
+        quota[b], kept[b] = role_allocate(roles[b], R, alpha, budget, W)
+    return quota, kept, int(kept.max()) if Bt else 0
+
+
+# ---------------------------------------------------------------------------
+# Selection and compaction
+# ---------------------------------------------------------------------------
+
+def rank_key(score: np.ndarray) -> np.ndarray:
+    """Value used for ranking: NaN becomes -inf (R13).  -0.0 already compares
+    equal to +0.0 in IEEE arithmetic, so equal keys fall back to the index."""
+    s = np.asarray(score, dtype=np.float64)
+    return np.where(np.isnan(s), -np.inf, s)
+
+
+def select_keep(score: np.ndarray, roles: np.ndarray, quota, W: int) -> np.ndarray:
+    """Kept token indices of one (layer, batch, KV head), ascending.
+
+    Within bucket r the candidate tokens (t < N-W, role r) are ranked by score
+    descending, then index ascending (R12), and the first quota[r] are kept
+    (Algorithm 1, per-bucket top-k).  The window [N-W, N) is always kept.
+    Labels outside [0, len(quota)) are never kept.
+    """
+    score = np.asarray(score)
+    roles = np.asarray(roles)
+    N = score.shape[0]
+    key = rank_key(score)
+    keep = [np.arange(N - W, N)]
+    t_all = np.arange(N - W)
+    for r, q in enumerate(quota):
+        cand = t_all[roles[:N - W] == r]
+        if q <= 0 or cand.size == 0:
+            continue
+        order = np.lexsort((cand, -key[cand]))      # last key is primary
+        keep.append(cand[order[:int(q)]])
+    return np.sort(np.concatenate(keep)).astype(np.int64)
+
+
+def topk_select(score: np.ndarray, roles: np.ndarray, quota: np.ndarray,
+                W: int) -> list:
+    """select_keep over score [L, B, Hkv, N] with roles [B, N], quota [B, R].
+    Returns a nested list idx[l][b][j] of ascending int64 arrays."""
+    L, Bt, H, N = score.shape
+    return [[[select_keep(score[l, b, j], roles[b], quota[b], W)
+              for j in range(H)] for b in range(Bt)] for l in range(L)]
+
+
+def kv_compact(kv: np.ndarray, idx: np.ndarray) -> np.ndarray:
+    """Compacted rows kv[idx] of one (layer, batch, KV head): a pure copy,
+    the dense cache a compacting implementation keeps (§6, systems cost)."""
+    return np.asarray(kv)[np.asarray(idx)]
+
+
+# ---------------------------------------------------------------------------
+# Diagnostics (§3): per-role mass, retention rate, retained-state SNR
+# ---------------------------------------------------------------------------
+
+def per_role_mean_mass(score: np.ndarray, roles: np.ndarray, R: int,
+                       upto: int | None = None) -> np.ndarray:
+    """Mean per-token mass of each role (§3 "Mass concentration", Fig. 1).
+    Only positions t < upto are counted (default: all).  NaN for empty roles."""
+    s = np.asarray(score, dtype=np.float64)
+    roles = np.asarray(roles)
+    n = s.shape[0] if upto is None else upto
+    out = np.full(R, np.nan)
+    for r in range(R):
+        m = roles[:n] == r
+        if np.any(m):
+            out[r] = float(np.mean(s[:n][m]))
+    return out
+
+
+def retention_rate(idx: np.ndarray, roles: np.ndarray, R: int,
+                   upto: int | None = None) -> np.ndarray:
+    """Fraction of each role's tokens that are kept (§3 "Retention bias",
+    Table 1).  Only positions t < upto are counted (default: all)."""
+    roles = np.asarray(roles)
+    n = roles.shape[0] if upto is None else upto
+    kept = np.zeros(roles.shape[0], dtype=bool)
+    kept[np.asarray(idx)] = True
+    out = np.full(R, np.nan)
+    for r in range(R):
+        m = roles[:n] == r
+        if np.any(m):
+            out[r] = float(np.mean(kept[:n][m]))
+    return out
+
+
+def retained_snr_db(signal_energy: float, noise_energy: float) -> float:
+    """Retained-state SNR of §3: 10 log10 of the per-token energy of the
+    answer-carrying role over that of the structural role."""
+    return 10.0 * math.log10(signal_energy / noise_energy)
