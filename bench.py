@@ -1,0 +1,234 @@
+"""Benchmark of the role-conditional eviction step on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload stack32k] [--budget 0.05]
+
+A step is one pass of the whole hot path over one batch already resident in
+HBM: SnapKV windowed score with GQA sum and max-pool (every layer and KV
+head), role allocation, per-role top-k and K/V compaction.  The default
+workload is the 32-layer Llama-3-8B-shaped stack (32 query / 8 KV heads,
+d=128, N=32768, W=32, pool 7, batch 4, B=0.05) on synthetic inputs.
+
+Prints one JSON line.  ``value`` is prefill tokens scored and compressed per
+second (a token counts once it has passed through all layers and KV heads);
+``roofline`` refers to the SnapKV score call, timed with HIP events on the
+stream it is launched on; ``cpu_baseline`` times the float64 CPU oracle on a
+bounded sample of the same workload.
+"""
+
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "prefill tokens scored+compressed/s per GPU; % HBM peak (SnapKV), % MFMA (H2O)"
+HBM_PEAK_GBS = 8000.0
+BF16_MFMA_PEAK_TFLOPS = 2500.0
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="stack32k")
+    ap.add_argument("--budget", type=float, default=None)
+    ap.add_argument("--alpha-key", type=float, default=0.0)
+    ap.add_argument("--cpu-seconds", type=float, default=12.0,
+                    help="target CPU time of the oracle baseline sample")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-h2o", action="store_true", help="skip the H2O scorer leg")
+    return ap.parse_args()
+
+
+def snapkv_algorithmic_bytes(wl, elem=2):
+    """Bytes the score call must move at least once: K and the window
+    queries read, the float32 score written."""
+    segs = wl.L * wl.B * wl.Hkv
+    return (segs * wl.N * wl.d * elem                     # K
+            + wl.L * wl.B * wl.Hq * wl.W * wl.d * elem    # Q window
+            + segs * wl.N * 4)                            # score
+
+
+def step_algorithmic_bytes(wl, kept, elem=2):
+    """Whole step: score call + score read by the select + role labels + kept
+    indices written + kept K and V rows read and written."""
+    segs_per_b = wl.L * wl.Hkv
+    kept_rows = sum(int(k) for k in kept) * segs_per_b
+    return (snapkv_algorithmic_bytes(wl, elem)
+            + wl.L * wl.B * wl.Hkv * wl.N * 4             # score read
+            + wl.B * wl.N                                 # roles
+            + kept_rows * 4                               # indices
+            + kept_rows * wl.d * elem * 4)                # K,V read + write
+
+
+def cpu_baseline(wl, inp, budget, alpha, target_s):
+    """Time the oracle on whole (layer, sample) units of the workload until about
+    target_s seconds have been spent (at least one unit)."""
+    import numpy as np
+
+    import oracle as O
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+    except Exception:  # pragma: no cover
+        threads = 1
+    quota, kept, _ = O.role_allocate_batch(inp["roles"], 4, alpha, budget, wl.W)
+    units = 0
+    t0 = time.perf_counter()
+    order = [(l, b) for l in range(len(inp["layers"])) for b in range(wl.B)]
+    for (l, b) in order:
+        roles = inp["roles"][b]
+        for j in range(wl.Hkv):
+            q = inp["q"][l, b, j * wl.G:(j + 1) * wl.G].double().cpu().numpy()
+            k = inp["k"][l, b, j].double().cpu().numpy()
+            v = inp["v"][l, b, j].cpu()
+            s = O.maxpool_prefix(O.snapkv_mass(q, k), wl.W, wl.pool_k)
+            idx = O.select_keep(s, roles, quota[b], wl.W)
+            O.kv_compact(k, idx)
+            O.kv_compact(v.float().numpy(), idx)
+        units += 1
+        if time.perf_counter() - t0 >= target_s:
+            break
+    el = time.perf_counter() - t0
+    # one unit is N tokens through one layer of one sample; a prefill token
+    # needs all L layers
+    tokens_per_s = units * wl.N / wl.L / el
+    return {"value": tokens_per_s, "unit": "tokens/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"{units} (layer, sample) units of {wl.name} ({wl.Hkv} KV heads, N={wl.N}) "
+                      f"in {el:.1f} s: float64 score, pool, selection and compaction"}
+
+
+def h2o_leg(K, WL, steps):
+    """H2O scorer on the 16k-token workload: MFMA fraction on the causal flops."""
+    import torch
+    wl = WL.get_workload("h2o16k")
+    inp = WL.make_inputs(wl, device="cuda", with_v=False)
+    score = torch.empty((wl.L, wl.B, wl.Hkv, wl.N), dtype=torch.float32, device="cuda")
+    ws = torch.empty(K.h2o_workspace_size(wl.L, wl.B, wl.Hq, wl.Hkv, wl.N, wl.d),
+                     dtype=torch.uint8, device="cuda")
+    for _ in range(2):
+        K.h2o_score(inp["q"], inp["k"], score=score, workspace=ws)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(steps):
+        K.h2o_score(inp["q"], inp["k"], score=score, workspace=ws)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / steps
+    causal = wl.L * wl.B * wl.Hq * wl.N * (wl.N + 1) / 2 * 2 * wl.d
+    tf2 = 2 * causal / (ms * 1e-3) / 1e12
+    del inp, ws
+    torch.cuda.empty_cache()
+    return {"workload": "h2o16k: 1 layer, 32q/8kv heads, d=128, N=16384, bf16",
+            "ms": round(ms, 4), "tflops_2pass": round(tf2, 1),
+            "mfma_frac_2pass": round(tf2 / BF16_MFMA_PEAK_TFLOPS, 4),
+            "mfma_frac_1pass": round(tf2 / 2 / BF16_MFMA_PEAK_TFLOPS, 4)}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only; --gpus {args.gpus} is not supported "
+              "(the eviction path shards by layer or KV head with no exchange; see DESIGN.md)",
+              file=sys.stderr)
+        sys.exit(2)
+    import torch
+
+    import workload as WL
+    from paper_2607_13205_amd.build import ensure_built
+    ensure_built()
+    import paper_2607_13205_amd as K
+    from paper_2607_13205_amd import pipeline
+
+    wl = WL.get_workload(args.workload)
+    budget = args.budget if args.budget is not None else wl.budgets[0]
+    alpha = WL.default_alpha(args.alpha_key)
+    torch.cuda.set_device(0)
+    print(f"[bench] generating {wl.name} inputs on the GPU", file=sys.stderr, flush=True)
+    inp = WL.make_inputs(wl, device="cuda")
+    torch.cuda.synchronize()
+    scorer = wl.scorer
+    W = 0 if scorer == "h2o" else wl.W
+    pool = 1 if scorer == "h2o" else wl.pool_k
+    _, kept, k_cap = K.role_allocate(inp["roles"], 4, alpha, budget, W)
+    bufs = pipeline.alloc_buffers(inp["k"], wl.Hq, W, 4, k_cap, scorer=scorer)
+
+    def step():
+        pipeline.evict(inp["q"], inp["k"], inp["v"], inp["roles"], inp["roles_t"], alpha, budget,
+                       W, pool, bufs, scorer=scorer)
+
+    print(f"[bench] warmup {args.warmup}", file=sys.stderr, flush=True)
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    # score-call timing (HIP events on the launch stream)
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(args.steps)]
+    t_all0 = torch.cuda.Event(enable_timing=True)
+    t_all1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t_all0.record()
+    for i in range(args.steps):
+        pipeline.evict(inp["q"], inp["k"], inp["v"], inp["roles"], inp["roles_t"], alpha, budget,
+                       W, pool, bufs, scorer=scorer, score_events=ev[i])
+    t_all1.record()
+    torch.cuda.synchronize()
+    ms_step = t_all0.elapsed_time(t_all1) / args.steps
+    ms_score = sum(a.elapsed_time(b) for a, b in ev) / args.steps
+    tokens = wl.B * wl.N
+    value = tokens / (ms_step * 1e-3)
+    score_bytes = snapkv_algorithmic_bytes(wl)
+    achieved = score_bytes / (ms_score * 1e-3) / 1e9
+    step_bytes = step_algorithmic_bytes(wl, kept)
+    out = {
+        "metric": METRIC,
+        "value": round(value, 1),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": wl.dtype,
+        "data": "synthetic",
+        "config": {
+            "workload": f"{wl.name}: {wl.L} layers, batch {wl.B}, {wl.Hq}q/{wl.Hkv}kv heads, "
+                        f"d={wl.d}, N={wl.N}, W={wl.W}, pool {wl.pool_k}, B={budget}, "
+                        f"alpha_KEY={args.alpha_key}, role mix {wl.mix}",
+            "global_batch": wl.B, "seq_len": wl.N, "parallelism": "none (1 GPU)",
+            "layer_tokens_per_s": round(value * wl.L, 1),
+            "k_cap": k_cap,
+            "step_algorithmic_GBs": round(step_bytes / (ms_step * 1e-3) / 1e9, 1),
+            "step_hbm_frac": round(step_bytes / (ms_step * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+        },
+        "roofline": {
+            "kernel": "kve_snapkv_score (score passes + pool)",
+            "bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+            "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+            "ms": round(ms_score, 4), "algorithmic_bytes": score_bytes,
+        },
+    }
+    if not args.no_h2o and wl.name != "h2o16k":
+        del bufs
+        torch.cuda.empty_cache()
+        print("[bench] H2O leg", file=sys.stderr, flush=True)
+        out["h2o"] = h2o_leg(K, WL, max(3, args.steps // 2))
+    if not args.no_cpu_baseline:
+        print("[bench] CPU oracle baseline", file=sys.stderr, flush=True)
+        out["cpu_baseline"] = cpu_baseline(wl, inp, budget, alpha, args.cpu_seconds)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

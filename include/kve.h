@@ -1,0 +1,207 @@
+/*
+ * kve.h -- C ABI of the role-conditional KV-cache eviction library (libkve.so)
+ *
+ * The library computes, on one MI355X (gfx950) GPU, the eviction path of
+ * "Adaptive Filtering of the KV Cache: Diagnosing and Correcting Structural-Role
+ * Bias in LLM Inference": the SnapKV windowed attention score with its 1-D
+ * max-pool, the H2O accumulated score used as the baseline scorer, the
+ * role-conditional budget allocation, the per-role top-k and the compaction of
+ * the kept K/V rows into a dense cache.
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * - Every call returns a kve_status_t.  On any error nothing is launched and no
+ *   output is written; kve_last_error() returns a message for the calling
+ *   thread.  No exception crosses the ABI.
+ * - Arguments are validated before any launch.  Device-side contents (role
+ *   labels, quotas, indices) cannot be validated on the host without a
+ *   synchronisation; the kernels treat out-of-range device values defensively
+ *   (documented per call) and never read or write outside the buffers.
+ * - Device buffers belong to the caller.  The library never frees or retains
+ *   them and performs no device allocation inside these calls: scratch memory
+ *   comes from a caller-provided workspace whose size the matching
+ *   *_workspace_size() call returns (0 is a valid size; pass NULL then).
+ *   Workspaces must be 256-byte aligned (hipMalloc memory is).
+ * - All device work is enqueued on `stream` (a hipStream_t; NULL is the
+ *   default stream) without host synchronisation.  Calls on different streams
+ *   with different workspaces may run concurrently.
+ * - Tensors are dense and row-major in the order of their shape; the last
+ *   dimension (head_dim d) is contiguous.  Element type is selected by
+ *   kve_dtype_t: bfloat16 or float32.  head_dim d must be 64 or 128.
+ * - Shapes use L layers, B batch samples, Hq query heads, Hkv KV heads (Hq a
+ *   multiple of Hkv, G = Hq / Hkv query heads share KV head h / G), N cached
+ *   tokens, W observation-window tokens (the last W positions), R role
+ *   buckets (1..8).
+ */
+#ifndef KVE_H
+#define KVE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define KVE_ABI_VERSION 1
+
+typedef enum kve_status {
+    KVE_OK = 0,
+    KVE_ERR_INVALID_ARG = 1, /* a pointer, size or parameter is invalid        */
+    KVE_ERR_UNSUPPORTED = 2, /* dtype / head_dim / size outside what is built  */
+    KVE_ERR_WORKSPACE = 3,   /* workspace or output capacity too small         */
+    KVE_ERR_HIP = 4          /* the HIP runtime reported an error at launch    */
+} kve_status_t;
+
+typedef enum kve_dtype {
+    KVE_DTYPE_BF16 = 0,
+    KVE_DTYPE_F32 = 1
+} kve_dtype_t;
+
+/* ABI version (KVE_ABI_VERSION of the built library). */
+int kve_version(void);
+
+/* Message describing the last error returned on the calling thread ("" if none).
+ * The pointer stays valid until the next kve_* call on the same thread. */
+const char* kve_last_error(void);
+
+/* ------------------------------------------------------------------------- */
+/* SnapKV windowed score (paper §2 and §4 "SnapKV mechanism"; Algorithm 1,    */
+/* windowed-mass and pooling steps).                                          */
+/* ------------------------------------------------------------------------- */
+
+/* Workspace bytes kve_snapkv_score needs for these shapes. */
+size_t kve_snapkv_workspace_size(int L, int B, int Hq, int Hkv, int N, int W, int d);
+
+/*
+ * For every (layer l, sample b, KV head j) the last W prefill queries of the G
+ * query heads of group j attend causally over all N keys (query at position
+ * N-W+i sees keys t <= N-W+i), softmax-normalised per query row.  The raw score
+ *     s(t) = sum over the G heads and W window queries of p(query -> t)
+ * is max-pooled with an odd kernel `pool_k` (stride 1, same length) over the
+ * candidate prefix [0, N-W) only; window positions keep their raw score.
+ *
+ *   q_win  [L, B, Hq, W, d]  window queries (device, dtype)
+ *   k      [L, B, Hkv, N, d] keys           (device, dtype)
+ *   scale  softmax scale of the logits <q, k>; 0 selects 1/sqrt(d)
+ *   pool_k odd, >= 1 (1 disables pooling)
+ *   score  [L, B, Hkv, N] float32 output (device)
+ *
+ * Requires 1 <= W <= N, G*W <= 256.  Scores are accumulated in float32 from
+ * products of the input type; the two-pass softmax subtracts each row's
+ * maximum before exponentiating.
+ */
+kve_status_t kve_snapkv_score(const void* q_win, const void* k, kve_dtype_t dtype,
+                              int L, int B, int Hq, int Hkv, int N, int W, int d,
+                              float scale, int pool_k, float* score,
+                              void* workspace, size_t workspace_bytes, void* stream);
+
+/* ------------------------------------------------------------------------- */
+/* H2O accumulated score, the baseline scorer (paper §2, H2O family).         */
+/* ------------------------------------------------------------------------- */
+
+/* Workspace bytes kve_h2o_score needs for these shapes. */
+size_t kve_h2o_workspace_size(int L, int B, int Hq, int Hkv, int N, int d);
+
+/*
+ * s(t) = sum over the G query heads of group j and over every prefill query
+ * i >= t of the causal softmax probability p_h(i -> t).  No window, no pool.
+ *
+ *   q      [L, B, Hq, N, d]  all prefill queries (device, dtype)
+ *   k      [L, B, Hkv, N, d] keys (device, dtype)
+ *   scale  0 selects 1/sqrt(d)
+ *   score  [L, B, Hkv, N] float32 output (device)
+ *
+ * Two passes: per-row log-sum-exp over the causal row, then column sums.
+ */
+kve_status_t kve_h2o_score(const void* q, const void* k, kve_dtype_t dtype,
+                           int L, int B, int Hq, int Hkv, int N, int d, float scale,
+                           float* score, void* workspace, size_t workspace_bytes,
+                           void* stream);
+
+/* ------------------------------------------------------------------------- */
+/* Role-conditional allocation (paper §4.1 role policy; Algorithm 1,          */
+/* per-bucket top-k and redistribution steps).  HOST function.                */
+/* ------------------------------------------------------------------------- */
+
+/*
+ * Per-sample bucket quotas.  With K = min(N, ceil(budget*N)) the kept tokens
+ * and K_p = max(0, K - W) the slots left for the candidate prefix [0, N-W),
+ * K_p is split over the buckets with alpha_r > 0 and at least one candidate,
+ * in proportion to alpha renormalised over those buckets, each quota the
+ * ceiling of its share.  A bucket whose share exceeds its candidate
+ * population keeps its whole population and the budget it cannot use is
+ * re-split the same way over the buckets still open, until no bucket
+ * overflows.  Budget left once every positive-weight bucket is full is not
+ * spent.  budget >= 1 is the full-cache baseline: every token is kept.
+ * Ceilings are taken as ceil(x - 1e-9) to absorb binary64 rounding.
+ *
+ *   roles     [B, N] int8 labels in [0, R)  (HOST memory)
+ *   alpha     [R] weights >= 0 with a positive sum (HOST)
+ *   budget    fraction of tokens kept, > 0
+ *   quota_out [B, R] int32 (HOST): prefix tokens kept per bucket
+ *   kept_out  [B] int32 (HOST): W + sum of the sample's quotas
+ *   k_cap_out max over samples of kept_out (HOST, may be NULL)
+ *
+ * Rejects labels outside [0, R), negative alpha, a zero alpha sum, W > N.
+ */
+kve_status_t kve_role_allocate(const int8_t* roles, int B, int N, int R,
+                               const double* alpha, double budget, int W,
+                               int32_t* quota_out, int32_t* kept_out,
+                               int32_t* k_cap_out);
+
+/* ------------------------------------------------------------------------- */
+/* Per-role top-k selection (Algorithm 1, per-bucket top-k).                  */
+/* ------------------------------------------------------------------------- */
+
+/* Workspace bytes kve_topk_select needs for these shapes. */
+size_t kve_topk_workspace_size(int L, int B, int Hkv, int N, int R);
+
+/*
+ * For every (l, b, j) segment: within each bucket r the candidate tokens
+ * t < N-W labelled r are ranked by score descending, ties broken by the lower
+ * index, and the first quota[b, r] are kept.  The window [N-W, N) is always
+ * kept.  The kept indices are written in ascending order.
+ *
+ *   score     [L, B, Hkv, N] float32 (device).  -0.0 ranks equal to +0.0 and
+ *             NaN ranks below every number.
+ *   roles     [B, N] int8 (device); labels outside [0, R) are never kept.
+ *   quota     [B, R] int32 (device); negative values count as 0 and values
+ *             above the bucket's population as the population.
+ *   idx_out   [L, B, Hkv, k_cap] int32 (device): entries [0, count) of each
+ *             segment are written, the rest left untouched.
+ *   count_out [L, B, Hkv] int32 (device, may be NULL): number of kept tokens
+ *             of each segment.  A value above k_cap means the output was
+ *             truncated to its first k_cap indices (the caller's k_cap was too
+ *             small for the quotas it passed).
+ */
+kve_status_t kve_topk_select(const float* score, const int8_t* roles, const int32_t* quota,
+                             int L, int B, int Hkv, int N, int W, int R, int k_cap,
+                             int32_t* idx_out, int32_t* count_out,
+                             void* workspace, size_t workspace_bytes, void* stream);
+
+/* ------------------------------------------------------------------------- */
+/* K/V compaction: the dense cache of a compacting implementation (§6).      */
+/* ------------------------------------------------------------------------- */
+
+/*
+ * k_out[l,b,j,m,:] = k[l,b,j,idx[l,b,j,m],:] and the same for v, bit for bit,
+ * for m < min(count[l,b,j], k_cap).  Rows at or beyond that are not written.
+ * Index values outside [0, N) are skipped (the row is not written).
+ *
+ *   k, v          [L, B, Hkv, N, d] (device, dtype)
+ *   idx           [L, B, Hkv, k_cap] int32 (device)
+ *   count         [L, B, Hkv] int32 (device): valid entries of each idx row
+ *   k_out, v_out  [L, B, Hkv, k_cap, d] (device, dtype)
+ * v and v_out may both be NULL to compact K only.
+ */
+kve_status_t kve_kv_compact(const void* k, const void* v, kve_dtype_t dtype,
+                            const int32_t* idx, const int32_t* count,
+                            int L, int B, int Hkv, int N, int d, int k_cap,
+                            void* k_out, void* v_out, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* KVE_H */

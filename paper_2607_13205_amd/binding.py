@@ -1,0 +1,235 @@
+"""Thin ctypes binding of libkve.so (argument marshalling only).
+
+Every step of the eviction path runs in the HIP library; this module only
+checks tensor shapes against the C ABI, allocates outputs and workspaces with
+torch when the caller does not pass them, and forwards raw device pointers and
+the current HIP stream.  There is no fallback: if the library is missing the
+import fails.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+
+_LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libkve.so")
+
+KVE_OK = 0
+KVE_ERR_INVALID_ARG = 1
+KVE_ERR_UNSUPPORTED = 2
+KVE_ERR_WORKSPACE = 3
+KVE_ERR_HIP = 4
+DTYPE_BF16 = 0
+DTYPE_F32 = 1
+
+#: every symbol include/kve.h declares
+EXPORTED = (
+    "kve_version", "kve_last_error",
+    "kve_snapkv_workspace_size", "kve_snapkv_score",
+    "kve_h2o_workspace_size", "kve_h2o_score",
+    "kve_role_allocate",
+    "kve_topk_workspace_size", "kve_topk_select",
+    "kve_kv_compact",
+)
+
+
+class KveError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(f"kve status {status}: {message}")
+        self.status = status
+
+
+def _load():
+    if not os.path.exists(_LIB_PATH):
+        raise ImportError(
+            f"{_LIB_PATH} is missing: build it with `python -m paper_2607_13205_amd.build` "
+            "(or __graft_entry__.build()); there is no non-HIP fallback")
+    lib = ctypes.CDLL(_LIB_PATH)
+    c_int, c_size, c_void, c_float, c_double = (ctypes.c_int, ctypes.c_size_t, ctypes.c_void_p,
+                                                ctypes.c_float, ctypes.c_double)
+    sig = {
+        "kve_version": (c_int, []),
+        "kve_last_error": (ctypes.c_char_p, []),
+        "kve_snapkv_workspace_size": (c_size, [c_int] * 7),
+        "kve_snapkv_score": (c_int, [c_void, c_void, c_int] + [c_int] * 7 +
+                             [c_float, c_int, c_void, c_void, c_size, c_void]),
+        "kve_h2o_workspace_size": (c_size, [c_int] * 6),
+        "kve_h2o_score": (c_int, [c_void, c_void, c_int] + [c_int] * 6 +
+                          [c_float, c_void, c_void, c_size, c_void]),
+        "kve_role_allocate": (c_int, [c_void, c_int, c_int, c_int, c_void, c_double, c_int,
+                                      c_void, c_void, c_void]),
+        "kve_topk_workspace_size": (c_size, [c_int] * 5),
+        "kve_topk_select": (c_int, [c_void, c_void, c_void] + [c_int] * 7 +
+                            [c_void, c_void, c_void, c_size, c_void]),
+        "kve_kv_compact": (c_int, [c_void, c_void, c_int, c_void, c_void] + [c_int] * 6 +
+                           [c_void, c_void, c_void]),
+    }
+    for name, (res, args) in sig.items():
+        fn = getattr(lib, name)
+        fn.restype = res
+        fn.argtypes = args
+    return lib
+
+
+LIB = _load()
+
+
+def last_error() -> str:
+    return LIB.kve_last_error().decode()
+
+
+def _check(status: int):
+    if status != KVE_OK:
+        raise KveError(status, last_error())
+
+
+# ---------------------------------------------------------------------------
+# torch plumbing
+# ---------------------------------------------------------------------------
+
+def _torch():
+    import torch
+    return torch
+
+
+def _dtype_code(t) -> int:
+    torch = _torch()
+    if t.dtype == torch.bfloat16:
+        return DTYPE_BF16
+    if t.dtype == torch.float32:
+        return DTYPE_F32
+    raise TypeError(f"unsupported dtype {t.dtype} (bfloat16 or float32)")
+
+
+def _dev(t, name):
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a device tensor")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream=None):
+    torch = _torch()
+    s = torch.cuda.current_stream() if stream is None else stream
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def _workspace(nbytes, device, workspace=None):
+    torch = _torch()
+    if nbytes == 0:
+        return None, 0
+    if workspace is not None:
+        return workspace, workspace.numel() * workspace.element_size()
+    return torch.empty(int(nbytes), dtype=torch.uint8, device=device), int(nbytes)
+
+
+def _ptr(t):
+    return ctypes.c_void_p(0 if t is None else t.data_ptr())
+
+
+# ---------------------------------------------------------------------------
+# entry points
+# ---------------------------------------------------------------------------
+
+def snapkv_workspace_size(L, B, Hq, Hkv, N, W, d) -> int:
+    return int(LIB.kve_snapkv_workspace_size(L, B, Hq, Hkv, N, W, d))
+
+
+def snapkv_score(q_win, k, pool_k: int, scale: float = 0.0, score=None, workspace=None,
+                 stream=None):
+    """Pooled SnapKV score [L, B, Hkv, N] (float32) of q_win [L, B, Hq, W, d]
+    and k [L, B, Hkv, N, d]; see kve_snapkv_score in include/kve.h."""
+    torch = _torch()
+    L, B, Hq, W, d = q_win.shape
+    Lk, Bk, Hkv, N, dk = k.shape
+    if (L, B, d) != (Lk, Bk, dk) or q_win.dtype != k.dtype:
+        raise ValueError("q_win and k disagree in L, B, d or dtype")
+    if score is None:
+        score = torch.empty((L, B, Hkv, N), dtype=torch.float32, device=k.device)
+    ws, wsb = _workspace(snapkv_workspace_size(L, B, Hq, Hkv, N, W, d), k.device, workspace)
+    _check(LIB.kve_snapkv_score(_dev(q_win, "q_win"), _dev(k, "k"), _dtype_code(k),
+                                L, B, Hq, Hkv, N, W, d, float(scale), int(pool_k),
+                                _dev(score, "score"), _ptr(ws), wsb, _stream(stream)))
+    return score
+
+
+def h2o_workspace_size(L, B, Hq, Hkv, N, d) -> int:
+    return int(LIB.kve_h2o_workspace_size(L, B, Hq, Hkv, N, d))
+
+
+def h2o_score(q, k, scale: float = 0.0, score=None, workspace=None, stream=None):
+    """H2O score [L, B, Hkv, N] of q [L, B, Hq, N, d] and k [L, B, Hkv, N, d]."""
+    torch = _torch()
+    L, B, Hq, N, d = q.shape
+    Lk, Bk, Hkv, Nk, dk = k.shape
+    if (L, B, N, d) != (Lk, Bk, Nk, dk) or q.dtype != k.dtype:
+        raise ValueError("q and k disagree in L, B, N, d or dtype")
+    if score is None:
+        score = torch.empty((L, B, Hkv, N), dtype=torch.float32, device=k.device)
+    ws, wsb = _workspace(h2o_workspace_size(L, B, Hq, Hkv, N, d), k.device, workspace)
+    _check(LIB.kve_h2o_score(_dev(q, "q"), _dev(k, "k"), _dtype_code(k), L, B, Hq, Hkv, N, d,
+                             float(scale), _dev(score, "score"), _ptr(ws), wsb, _stream(stream)))
+    return score
+
+
+def role_allocate(roles, R: int, alpha, budget: float, W: int):
+    """Host role allocation.  roles: int8 array [B, N] (host).  Returns
+    (quota int32 [B, R], kept int32 [B], k_cap)."""
+    roles = np.ascontiguousarray(np.asarray(roles, dtype=np.int8))
+    if roles.ndim == 1:
+        roles = roles[None]
+    B, N = roles.shape
+    alpha = np.ascontiguousarray(np.asarray(alpha, dtype=np.float64))
+    quota = np.zeros((B, R), dtype=np.int32)
+    kept = np.zeros(B, dtype=np.int32)
+    kcap = ctypes.c_int32(0)
+    _check(LIB.kve_role_allocate(roles.ctypes.data_as(ctypes.c_void_p), B, N, int(R),
+                                 alpha.ctypes.data_as(ctypes.c_void_p), float(budget), int(W),
+                                 quota.ctypes.data_as(ctypes.c_void_p),
+                                 kept.ctypes.data_as(ctypes.c_void_p), ctypes.byref(kcap)))
+    return quota, kept, int(kcap.value)
+
+
+def topk_select(score, roles, quota, W: int, R: int, k_cap: int, idx_out=None, count_out=None,
+                stream=None):
+    """Ascending kept indices [L, B, Hkv, k_cap] and per-segment counts [L, B, Hkv]."""
+    torch = _torch()
+    L, B, Hkv, N = score.shape
+    if tuple(roles.shape) != (B, N) or roles.dtype != torch.int8:
+        raise ValueError("roles must be int8 [B, N]")
+    if tuple(quota.shape) != (B, R) or quota.dtype != torch.int32:
+        raise ValueError("quota must be int32 [B, R]")
+    if idx_out is None:
+        idx_out = torch.full((L, B, Hkv, max(k_cap, 0)), -1, dtype=torch.int32, device=score.device)
+    if count_out is None:
+        count_out = torch.empty((L, B, Hkv), dtype=torch.int32, device=score.device)
+    _check(LIB.kve_topk_select(_dev(score, "score"), _dev(roles, "roles"), _dev(quota, "quota"),
+                               L, B, Hkv, N, int(W), int(R), int(k_cap),
+                               _dev(idx_out, "idx_out"), _dev(count_out, "count_out"),
+                               None, 0, _stream(stream)))
+    return idx_out, count_out
+
+
+def kv_compact(k, v, idx, count, k_out=None, v_out=None, stream=None):
+    """Compacted K (and V) [L, B, Hkv, k_cap, d]."""
+    torch = _torch()
+    L, B, Hkv, N, d = k.shape
+    k_cap = idx.shape[-1]
+    if tuple(idx.shape[:3]) != (L, B, Hkv) or idx.dtype != torch.int32:
+        raise ValueError("idx must be int32 [L, B, Hkv, k_cap]")
+    if tuple(count.shape) != (L, B, Hkv) or count.dtype != torch.int32:
+        raise ValueError("count must be int32 [L, B, Hkv]")
+    if v is not None and (v.shape != k.shape or v.dtype != k.dtype):
+        raise ValueError("v must match k")
+    if k_out is None:
+        k_out = torch.zeros((L, B, Hkv, k_cap, d), dtype=k.dtype, device=k.device)
+    if v is not None and v_out is None:
+        v_out = torch.zeros_like(k_out)
+    _check(LIB.kve_kv_compact(_dev(k, "k"), None if v is None else _dev(v, "v"), _dtype_code(k),
+                              _dev(idx, "idx"), _dev(count, "count"), L, B, Hkv, N, d, int(k_cap),
+                              _dev(k_out, "k_out"), None if v is None else _dev(v_out, "v_out"),
+                              _stream(stream)))
+    return k_out, v_out

@@ -1,0 +1,270 @@
+// C ABI of libkve: argument validation, the host-side role allocation and the
+// dispatch to the HIP launchers.  Declarations and contracts: include/kve.h.
+#include "../../include/kve.h"
+
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <string>
+#include <vector>
+
+#include "kve_internal.h"
+
+namespace {
+
+thread_local std::string g_error;
+
+kve_status_t fail(kve_status_t st, const char* fmt, ...) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof(buf), fmt, ap);
+    va_end(ap);
+    g_error = buf;
+    return st;
+}
+
+kve_status_t ok() {
+    g_error.clear();
+    return KVE_OK;
+}
+
+kve_status_t from_hip(hipError_t e, const char* what) {
+    if (e == hipSuccess) return ok();
+    return fail(KVE_ERR_HIP, "%s: HIP error %d (%s)", what, (int)e, hipGetErrorString(e));
+}
+
+bool aligned(const void* p) { return (reinterpret_cast<uintptr_t>(p) & (kve::kAlign - 1)) == 0; }
+
+constexpr long long kMaxGrid = 2147483647LL;
+constexpr double kCeilGuard = 1e-9;
+
+long long ceil_guarded(double x) { return (long long)std::ceil(x - kCeilGuard); }
+
+kve_status_t check_common(const char* fn, int L, int B, int Hq, int Hkv, int N, int d, int dtype) {
+    if (L <= 0 || B <= 0 || Hq <= 0 || Hkv <= 0 || N <= 0 || d <= 0)
+        return fail(KVE_ERR_INVALID_ARG, "%s: sizes must be positive (L=%d B=%d Hq=%d Hkv=%d N=%d d=%d)",
+                    fn, L, B, Hq, Hkv, N, d);
+    if (Hq % Hkv != 0)
+        return fail(KVE_ERR_INVALID_ARG, "%s: Hq=%d is not a multiple of Hkv=%d", fn, Hq, Hkv);
+    if (dtype != KVE_DTYPE_BF16 && dtype != KVE_DTYPE_F32)
+        return fail(KVE_ERR_UNSUPPORTED, "%s: unknown dtype %d", fn, dtype);
+    if (d != 64 && d != 128)
+        return fail(KVE_ERR_UNSUPPORTED, "%s: head_dim %d not built (64 or 128)", fn, d);
+    if ((long long)L * B * Hq > kMaxGrid / 4 || N > (1 << 30))
+        return fail(KVE_ERR_UNSUPPORTED, "%s: shape too large", fn);
+    return KVE_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int kve_version(void) { return KVE_ABI_VERSION; }
+
+const char* kve_last_error(void) { return g_error.c_str(); }
+
+size_t kve_snapkv_workspace_size(int L, int B, int Hq, int Hkv, int N, int W, int d) {
+    (void)d;
+    if (L <= 0 || B <= 0 || Hq <= 0 || Hkv <= 0 || N <= 0 || W <= 0 || Hq % Hkv != 0) return 0;
+    return kve::snap_plan(L, B, Hq, Hkv, N, W).total;
+}
+
+kve_status_t kve_snapkv_score(const void* q_win, const void* k, kve_dtype_t dtype, int L, int B,
+                              int Hq, int Hkv, int N, int W, int d, float scale, int pool_k,
+                              float* score, void* workspace, size_t workspace_bytes, void* stream) {
+    const char* fn = "kve_snapkv_score";
+    kve_status_t st = check_common(fn, L, B, Hq, Hkv, N, d, (int)dtype);
+    if (st != KVE_OK) return st;
+    if (q_win == nullptr || k == nullptr || score == nullptr)
+        return fail(KVE_ERR_INVALID_ARG, "%s: null tensor pointer", fn);
+    if (W < 1 || W > N) return fail(KVE_ERR_INVALID_ARG, "%s: need 1 <= W <= N (W=%d N=%d)", fn, W, N);
+    if (pool_k < 1 || pool_k % 2 == 0 || pool_k > 255)
+        return fail(KVE_ERR_INVALID_ARG, "%s: pool_k must be odd in [1, 255] (got %d)", fn, pool_k);
+    if (!(std::isfinite(scale) && scale >= 0.0f))
+        return fail(KVE_ERR_INVALID_ARG, "%s: scale must be finite and >= 0", fn);
+    const long long rows = (long long)(Hq / Hkv) * W;
+    if (rows > kve::kSnapMaxRows)
+        return fail(KVE_ERR_UNSUPPORTED, "%s: G*W=%lld exceeds %d", fn, rows, kve::kSnapMaxRows);
+    const kve::SnapPlan p = kve::snap_plan(L, B, Hq, Hkv, N, W);
+    if ((long long)p.segs * p.rgroups * p.nchunks > kMaxGrid)
+        return fail(KVE_ERR_UNSUPPORTED, "%s: shape too large", fn);
+    if (workspace_bytes < p.total || (p.total > 0 && workspace == nullptr))
+        return fail(KVE_ERR_WORKSPACE, "%s: workspace of %zu bytes < %zu needed", fn, workspace_bytes,
+                    p.total);
+    if (!aligned(workspace)) return fail(KVE_ERR_INVALID_ARG, "%s: workspace not 256-byte aligned", fn);
+    if (scale == 0.0f) scale = 1.0f / std::sqrt((float)d);
+    return from_hip(kve::launch_snapkv(q_win, k, (int)dtype, L, B, Hq, Hkv, N, W, d, scale, pool_k,
+                                       score, workspace, static_cast<hipStream_t>(stream)),
+                    fn);
+}
+
+size_t kve_h2o_workspace_size(int L, int B, int Hq, int Hkv, int N, int d) {
+    (void)Hkv;
+    (void)d;
+    if (L <= 0 || B <= 0 || Hq <= 0 || N <= 0) return 0;
+    return kve::h2o_workspace(L, B, Hq, N);
+}
+
+kve_status_t kve_h2o_score(const void* q, const void* k, kve_dtype_t dtype, int L, int B, int Hq,
+                           int Hkv, int N, int d, float scale, float* score, void* workspace,
+                           size_t workspace_bytes, void* stream) {
+    const char* fn = "kve_h2o_score";
+    kve_status_t st = check_common(fn, L, B, Hq, Hkv, N, d, (int)dtype);
+    if (st != KVE_OK) return st;
+    if (q == nullptr || k == nullptr || score == nullptr)
+        return fail(KVE_ERR_INVALID_ARG, "%s: null tensor pointer", fn);
+    if (!(std::isfinite(scale) && scale >= 0.0f))
+        return fail(KVE_ERR_INVALID_ARG, "%s: scale must be finite and >= 0", fn);
+    const long long nrb = (N + kve::kH2oRowBlock - 1) / kve::kH2oRowBlock;
+    if ((long long)L * B * Hq * nrb > kMaxGrid) return fail(KVE_ERR_UNSUPPORTED, "%s: shape too large", fn);
+    const size_t need = kve::h2o_workspace(L, B, Hq, N);
+    if (workspace_bytes < need || workspace == nullptr)
+        return fail(KVE_ERR_WORKSPACE, "%s: workspace of %zu bytes < %zu needed", fn, workspace_bytes, need);
+    if (!aligned(workspace)) return fail(KVE_ERR_INVALID_ARG, "%s: workspace not 256-byte aligned", fn);
+    if (scale == 0.0f) scale = 1.0f / std::sqrt((float)d);
+    return from_hip(kve::launch_h2o(q, k, (int)dtype, L, B, Hq, Hkv, N, d, scale, score, workspace,
+                                    static_cast<hipStream_t>(stream)),
+                    fn);
+}
+
+kve_status_t kve_role_allocate(const int8_t* roles, int B, int N, int R, const double* alpha,
+                               double budget, int W, int32_t* quota_out, int32_t* kept_out,
+                               int32_t* k_cap_out) {
+    const char* fn = "kve_role_allocate";
+    if (roles == nullptr || alpha == nullptr || quota_out == nullptr || kept_out == nullptr)
+        return fail(KVE_ERR_INVALID_ARG, "%s: null pointer", fn);
+    if (B <= 0 || N <= 0) return fail(KVE_ERR_INVALID_ARG, "%s: B and N must be positive", fn);
+    if (R < 1 || R > 8) return fail(KVE_ERR_INVALID_ARG, "%s: R=%d outside [1, 8]", fn, R);
+    if (W < 0 || W > N) return fail(KVE_ERR_INVALID_ARG, "%s: need 0 <= W <= N (W=%d N=%d)", fn, W, N);
+    if (!(std::isfinite(budget) && budget > 0.0))
+        return fail(KVE_ERR_INVALID_ARG, "%s: budget must be finite and > 0", fn);
+    double asum = 0.0;
+    for (int r = 0; r < R; ++r) {
+        if (!(std::isfinite(alpha[r]) && alpha[r] >= 0.0))
+            return fail(KVE_ERR_INVALID_ARG, "%s: alpha[%d] must be finite and >= 0", fn, r);
+        asum += alpha[r];
+    }
+    if (!(asum > 0.0)) return fail(KVE_ERR_INVALID_ARG, "%s: alpha sums to 0", fn);
+    for (size_t i = 0; i < (size_t)B * N; ++i)
+        if (roles[i] < 0 || roles[i] >= R)
+            return fail(KVE_ERR_INVALID_ARG, "%s: role label %d at %zu outside [0, %d)", fn, (int)roles[i],
+                        i, R);
+
+    std::vector<int32_t> quota((size_t)B * R, 0), kept(B, 0);
+    int32_t k_cap = 0;
+    const int P = N - W;
+    for (int b = 0; b < B; ++b) {
+        const int8_t* rb = roles + (size_t)b * N;
+        long long n[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+        for (int t = 0; t < P; ++t) ++n[rb[t]];
+        int32_t* q = quota.data() + (size_t)b * R;
+        if (budget >= 1.0) {
+            // the full-cache baseline keeps every token
+            for (int r = 0; r < R; ++r) q[r] = (int32_t)n[r];
+            kept[b] = N;
+        } else {
+            long long K = ceil_guarded(budget * (double)N);
+            if (K > N) K = N;
+            long long rem = K - W;
+            if (rem < 0) rem = 0;
+            bool open[8];
+            for (int r = 0; r < R; ++r) open[r] = alpha[r] > 0.0 && n[r] > 0;
+            while (rem > 0) {
+                double total = 0.0;
+                int n_open = 0;
+                for (int r = 0; r < R; ++r)
+                    if (open[r]) {
+                        total += alpha[r];
+                        ++n_open;
+                    }
+                if (n_open == 0) break;
+                long long share[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+                bool any_full = false;
+                for (int r = 0; r < R; ++r)
+                    if (open[r]) {
+                        share[r] = ceil_guarded(alpha[r] / total * (double)rem);
+                        if (share[r] > n[r]) any_full = true;
+                    }
+                if (!any_full) {
+                    for (int r = 0; r < R; ++r)
+                        if (open[r]) q[r] = (int32_t)share[r];
+                    break;
+                }
+                // buckets that cannot use their share keep all their tokens; the
+                // budget they leave is re-split over the buckets still open
+                for (int r = 0; r < R; ++r)
+                    if (open[r] && share[r] > n[r]) {
+                        q[r] = (int32_t)n[r];
+                        rem -= n[r];
+                        open[r] = false;
+                    }
+                if (rem < 0) rem = 0;
+            }
+            long long sum = W;
+            for (int r = 0; r < R; ++r) sum += q[r];
+            kept[b] = (int32_t)sum;
+        }
+        if (kept[b] > k_cap) k_cap = kept[b];
+    }
+    for (size_t i = 0; i < quota.size(); ++i) quota_out[i] = quota[i];
+    for (int b = 0; b < B; ++b) kept_out[b] = kept[b];
+    if (k_cap_out != nullptr) *k_cap_out = k_cap;
+    return ok();
+}
+
+size_t kve_topk_workspace_size(int L, int B, int Hkv, int N, int R) {
+    (void)L;
+    (void)B;
+    (void)Hkv;
+    (void)N;
+    (void)R;
+    return 0;
+}
+
+kve_status_t kve_topk_select(const float* score, const int8_t* roles, const int32_t* quota, int L,
+                             int B, int Hkv, int N, int W, int R, int k_cap, int32_t* idx_out,
+                             int32_t* count_out, void* workspace, size_t workspace_bytes,
+                             void* stream) {
+    (void)workspace;
+    (void)workspace_bytes;
+    const char* fn = "kve_topk_select";
+    if (score == nullptr || roles == nullptr || quota == nullptr)
+        return fail(KVE_ERR_INVALID_ARG, "%s: null pointer", fn);
+    if (L <= 0 || B <= 0 || Hkv <= 0 || N <= 0)
+        return fail(KVE_ERR_INVALID_ARG, "%s: sizes must be positive", fn);
+    if (W < 0 || W > N) return fail(KVE_ERR_INVALID_ARG, "%s: need 0 <= W <= N", fn);
+    if (R < 1 || R > 8) return fail(KVE_ERR_INVALID_ARG, "%s: R=%d outside [1, 8]", fn, R);
+    if (k_cap < 0) return fail(KVE_ERR_INVALID_ARG, "%s: k_cap < 0", fn);
+    if (k_cap > 0 && idx_out == nullptr) return fail(KVE_ERR_INVALID_ARG, "%s: null idx_out", fn);
+    if ((long long)L * B * Hkv > kMaxGrid || N > (1 << 30))
+        return fail(KVE_ERR_UNSUPPORTED, "%s: shape too large", fn);
+    return from_hip(kve::launch_topk(score, roles, quota, L, B, Hkv, N, W, R, k_cap, idx_out, count_out,
+                                     static_cast<hipStream_t>(stream)),
+                    fn);
+}
+
+kve_status_t kve_kv_compact(const void* k, const void* v, kve_dtype_t dtype, const int32_t* idx,
+                            const int32_t* count, int L, int B, int Hkv, int N, int d, int k_cap,
+                            void* k_out, void* v_out, void* stream) {
+    const char* fn = "kve_kv_compact";
+    if (k == nullptr || idx == nullptr || count == nullptr || k_out == nullptr)
+        return fail(KVE_ERR_INVALID_ARG, "%s: null pointer", fn);
+    if ((v == nullptr) != (v_out == nullptr))
+        return fail(KVE_ERR_INVALID_ARG, "%s: v and v_out must both be given or both be NULL", fn);
+    if (L <= 0 || B <= 0 || Hkv <= 0 || N <= 0 || k_cap < 0)
+        return fail(KVE_ERR_INVALID_ARG, "%s: invalid sizes", fn);
+    if (dtype != KVE_DTYPE_BF16 && dtype != KVE_DTYPE_F32)
+        return fail(KVE_ERR_UNSUPPORTED, "%s: unknown dtype %d", fn, (int)dtype);
+    if (d != 64 && d != 128) return fail(KVE_ERR_UNSUPPORTED, "%s: head_dim %d not built", fn, d);
+    const long long segs = (long long)L * B * Hkv;
+    if (segs * ((k_cap + 63) / 64) > kMaxGrid) return fail(KVE_ERR_UNSUPPORTED, "%s: shape too large", fn);
+    const int es = dtype == KVE_DTYPE_BF16 ? 2 : 4;
+    return from_hip(kve::launch_compact(k, v, es, idx, count, L, B, Hkv, N, d, k_cap, k_out, v_out,
+                                        static_cast<hipStream_t>(stream)),
+                    fn);
+}
+
+}  // extern "C"

@@ -1,0 +1,83 @@
+"""The whole eviction step (one pass of the hot path) over resident tensors.
+
+score (SnapKV windowed + pooled, or H2O)  ->  role allocation (host)  ->
+per-role top-k  ->  K/V compaction.  Buffers are allocated once by
+``EvictBuffers`` so that repeated steps allocate nothing.
+"""
+
+from __future__ import annotations
+
+from dataclasses import dataclass
+
+import numpy as np
+
+from . import binding as kb
+
+
+@dataclass
+class EvictBuffers:
+    score: object
+    ws_score: object
+    quota_host: object   # pinned int32 [B, R]
+    quota_dev: object
+    idx: object
+    count: object
+    k_out: object
+    v_out: object
+    k_cap: int
+    copy_done: object = None   # event after the last quota upload from quota_host
+
+
+def alloc_buffers(k, n_q_heads: int, W: int, R: int, k_cap: int, scorer: str = "snapkv",
+                  with_v: bool = True) -> EvictBuffers:
+    import torch
+    L, B, Hkv, N, d = k.shape
+    dev = k.device
+    if scorer == "snapkv":
+        wsb = kb.snapkv_workspace_size(L, B, n_q_heads, Hkv, N, W, d)
+    else:
+        wsb = kb.h2o_workspace_size(L, B, n_q_heads, Hkv, N, d)
+    return EvictBuffers(
+        score=torch.empty((L, B, Hkv, N), dtype=torch.float32, device=dev),
+        ws_score=torch.empty(max(wsb, 1), dtype=torch.uint8, device=dev),
+        quota_host=torch.zeros((B, R), dtype=torch.int32).pin_memory(),
+        quota_dev=torch.zeros((B, R), dtype=torch.int32, device=dev),
+        idx=torch.full((L, B, Hkv, k_cap), -1, dtype=torch.int32, device=dev),
+        count=torch.zeros((L, B, Hkv), dtype=torch.int32, device=dev),
+        k_out=torch.zeros((L, B, Hkv, k_cap, d), dtype=k.dtype, device=dev),
+        v_out=torch.zeros((L, B, Hkv, k_cap, d), dtype=k.dtype, device=dev) if with_v else None,
+        k_cap=k_cap,
+    )
+
+
+def evict(q, k, v, roles_host: np.ndarray, roles_dev, alpha, budget: float, W: int,
+          pool_k: int, bufs: EvictBuffers, scorer: str = "snapkv", scale: float = 0.0,
+          score_events=None):
+    """One eviction step; returns (quota [B, R] host, kept [B] host).
+
+    q is the window queries [L, B, Hq, W, d] (SnapKV) or all queries
+    [L, B, Hq, N, d] (H2O, which uses W = 0 and no pool).  ``score_events``,
+    a pair of torch.cuda.Event, brackets the score call on the launch stream."""
+    import torch
+    R = len(alpha)
+    if score_events is not None:
+        score_events[0].record()
+    if scorer == "snapkv":
+        kb.snapkv_score(q, k, pool_k, scale, score=bufs.score, workspace=bufs.ws_score)
+    else:
+        kb.h2o_score(q, k, scale, score=bufs.score, workspace=bufs.ws_score)
+    if score_events is not None:
+        score_events[1].record()
+    quota, kept, k_cap = kb.role_allocate(roles_host, R, alpha, budget, W)
+    if k_cap > bufs.k_cap:
+        raise ValueError(f"buffers hold {bufs.k_cap} rows, the allocation keeps {k_cap}")
+    if bufs.copy_done is None:
+        bufs.copy_done = torch.cuda.Event()
+    bufs.copy_done.synchronize()          # the previous upload has left quota_host
+    bufs.quota_host.numpy()[...] = quota
+    bufs.quota_dev.copy_(bufs.quota_host, non_blocking=True)
+    bufs.copy_done.record()
+    kb.topk_select(bufs.score, roles_dev, bufs.quota_dev, W, R, bufs.k_cap,
+                   idx_out=bufs.idx, count_out=bufs.count)
+    kb.kv_compact(k, v, bufs.idx, bufs.count, k_out=bufs.k_out, v_out=bufs.v_out)
+    return quota, kept

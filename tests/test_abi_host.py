@@ -1,0 +1,112 @@
+"""The C ABI on the CPU: the library loads, exports every declared symbol,
+validates arguments before launching anything, and its host-side role
+allocation agrees with the oracle."""
+
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+import oracle as O
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+@pytest.fixture(scope="module")
+def kve():
+    from paper_2607_13205_amd.build import ensure_built
+    ensure_built()
+    import paper_2607_13205_amd as K
+    return K
+
+
+def _declared():
+    text = open(os.path.join(ROOT, "include", "kve.h")).read()
+    return sorted(set(re.findall(r"\b(kve_[a-z0-9_]+)\s*\(", text)))
+
+
+def test_every_declared_symbol_is_exported(kve):
+    names = _declared()
+    assert len(names) == 10
+    assert sorted(kve.EXPORTED) == names
+    lib = ctypes.CDLL(kve.binding._LIB_PATH)
+    for n in names:
+        assert hasattr(lib, n), n
+    assert kve.binding.LIB.kve_version() == 1
+
+
+@pytest.mark.parametrize("ex_seed", range(3))
+def test_role_allocate_matches_oracle_on_random_grid(kve, ex_seed):
+    r = np.random.default_rng(ex_seed)
+    for _ in range(400):
+        N = int(r.integers(1, 300))
+        W = int(r.integers(0, N + 1))
+        R = int(r.integers(1, 9))
+        B = int(r.integers(1, 4))
+        roles = r.integers(0, R, (B, N)).astype(np.int8)
+        alpha = r.random(R)
+        alpha[r.random(R) < 0.3] = 0.0
+        if alpha.sum() == 0:
+            alpha[-1] = 0.5
+        budget = float(r.choice([0.01, 0.05, 0.07, 0.1, 0.2, 0.33, 0.5, 0.9, 1.0, 1.5]))
+        q, kept, kcap = kve.role_allocate(roles, R, alpha, budget, W)
+        qo, ko, kco = O.role_allocate_batch(roles, R, alpha, budget, W)
+        assert np.array_equal(q, qo) and np.array_equal(kept, ko) and kcap == kco
+
+
+def test_role_allocate_golden_examples(kve):
+    from tests.test_oracle_alloc import _load_examples, _roles_from_counts
+    for name, N, W, B, alpha, n, quota, kept in _load_examples():
+        roles = _roles_from_counts(n, W)
+        q, k, _ = kve.role_allocate(roles, 4, alpha, B, W)
+        assert q[0].tolist() == quota and int(k[0]) == kept, name
+
+
+def test_role_allocate_rejects_bad_input(kve):
+    roles = np.zeros((1, 10), dtype=np.int8)
+    a = [0.25, 0.0, 0.7, 0.05]
+    for args in [(roles, 4, a, 0.0, 2), (roles, 4, a, 0.5, 11), (roles, 9, a * 3, 0.5, 2),
+                 (roles, 4, [0, 0, 0, 0], 0.5, 2), (roles, 4, [0.1, -1, 0.7, 0.05], 0.5, 2),
+                 (roles + 4, 4, a, 0.5, 2), (roles, 4, a, float("nan"), 2)]:
+        with pytest.raises(kve.KveError) as e:
+            kve.role_allocate(*args)
+        assert e.value.status == 1
+        assert kve.last_error()
+
+
+def test_device_entry_points_validate_before_launch(kve):
+    """Invalid arguments return an error code without touching the GPU (no
+    device exists here, so any launch would fail with KVE_ERR_HIP instead)."""
+    L = kve.binding.LIB
+    null = None
+    dummy = ctypes.c_void_p(0x1000)  # never dereferenced: every call below fails validation
+    # snapkv: even pool kernel, W > N, unsupported d, Hq % Hkv, short workspace, null score
+    assert L.kve_snapkv_score(dummy, dummy, 0, 1, 1, 4, 2, 64, 8, 128, 0.0, 4, dummy, dummy, 1 << 30, null) == 1
+    assert L.kve_snapkv_score(dummy, dummy, 0, 1, 1, 4, 2, 64, 65, 128, 0.0, 7, dummy, dummy, 1 << 30, null) == 1
+    assert L.kve_snapkv_score(dummy, dummy, 0, 1, 1, 4, 2, 64, 8, 96, 0.0, 7, dummy, dummy, 1 << 30, null) == 2
+    assert L.kve_snapkv_score(dummy, dummy, 0, 1, 1, 5, 2, 64, 8, 128, 0.0, 7, dummy, dummy, 1 << 30, null) == 1
+    assert L.kve_snapkv_score(dummy, dummy, 0, 1, 1, 4, 2, 64, 8, 128, 0.0, 7, dummy, dummy, 16, null) == 3
+    assert L.kve_snapkv_score(dummy, dummy, 0, 1, 1, 4, 2, 64, 8, 128, 0.0, 7, null, dummy, 1 << 30, null) == 1
+    assert L.kve_snapkv_score(dummy, dummy, 7, 1, 1, 4, 2, 64, 8, 128, 0.0, 7, dummy, dummy, 1 << 30, null) == 2
+    assert L.kve_snapkv_score(dummy, dummy, 0, 1, 1, 64, 1, 64, 32, 128, 0.0, 7, dummy, dummy, 1 << 30, null) == 2
+    assert "pool_k" in kve.last_error() or kve.last_error()
+    # h2o: short workspace, bad dtype
+    assert L.kve_h2o_score(dummy, dummy, 0, 1, 1, 4, 2, 64, 128, 0.0, dummy, dummy, 8, null) == 3
+    assert L.kve_h2o_score(dummy, dummy, 3, 1, 1, 4, 2, 64, 128, 0.0, dummy, dummy, 1 << 30, null) == 2
+    # topk: R out of range, W > N, negative k_cap
+    assert L.kve_topk_select(dummy, dummy, dummy, 1, 1, 2, 64, 8, 9, 10, dummy, dummy, null, 0, null) == 1
+    assert L.kve_topk_select(dummy, dummy, dummy, 1, 1, 2, 64, 65, 4, 10, dummy, dummy, null, 0, null) == 1
+    assert L.kve_topk_select(dummy, dummy, dummy, 1, 1, 2, 64, 8, 4, -1, dummy, dummy, null, 0, null) == 1
+    # compact: v without v_out, bad head_dim
+    assert L.kve_kv_compact(dummy, dummy, 0, dummy, dummy, 1, 1, 2, 64, 128, 10, dummy, null, null) == 1
+    assert L.kve_kv_compact(dummy, null, 0, dummy, dummy, 1, 1, 2, 64, 80, 10, dummy, null, null) == 2
+
+
+def test_workspace_sizes_are_aligned_and_monotone(kve):
+    a = kve.snapkv_workspace_size(1, 1, 32, 8, 8192, 32, 128)
+    b = kve.snapkv_workspace_size(2, 1, 32, 8, 8192, 32, 128)
+    assert a > 0 and a % 256 == 0 and b >= a
+    assert kve.h2o_workspace_size(1, 1, 32, 8, 16384, 128) == 32 * 16384 * 4
+    assert kve.binding.LIB.kve_topk_workspace_size(1, 1, 8, 8192, 4) == 0

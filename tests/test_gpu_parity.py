@@ -1,0 +1,319 @@
+"""Parity of the HIP path (through the C ABI) with the CPU oracle on MI355X.
+
+Every input comes from the seeded generators in ``workload``; the oracle gets
+the exact bits the GPU received (bf16 upcast exactly to float64).
+"""
+
+from __future__ import annotations
+
+import math
+
+import numpy as np
+import pytest
+
+import oracle as O
+import workload as WL
+from tests.parity import check_kept_set, check_scores
+
+pytestmark = pytest.mark.gpu
+torch = pytest.importorskip("torch")
+
+
+@pytest.fixture(scope="module")
+def K():
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    from paper_2607_13205_amd.build import ensure_built
+    ensure_built()
+    import paper_2607_13205_amd as K
+    return K
+
+
+def f64(t):
+    return t.detach().float().cpu().numpy().astype(np.float64)
+
+
+def custom(name, L, B, Hq, Hkv, N, W, d, pool_k, dtype, scorer="snapkv"):
+    return WL.Workload(name, L=L, B=B, Hq=Hq, Hkv=Hkv, N=N, W=W, d=d, pool_k=pool_k, dtype=dtype,
+                       mix=(0.35, 0.20, 0.30, 0.15), budgets=(0.1,), scorer=scorer)
+
+
+def note(msg):
+    print(msg, flush=True)
+
+
+SNAP_CASES = [
+    WL.get_workload("tiny"),
+    custom("ragged", 2, 2, 8, 2, 1000, 24, 128, 7, "bf16"),
+    custom("rowgroups", 1, 1, 8, 2, 700, 64, 64, 3, "bf16"),
+    custom("w1", 1, 1, 4, 4, 300, 1, 128, 7, "bf16"),
+    custom("wfull", 1, 1, 2, 1, 96, 96, 64, 1, "f32"),
+    custom("f32d128", 1, 2, 4, 2, 333, 16, 128, 15, "f32"),
+    custom("bigpool", 1, 1, 4, 1, 450, 8, 128, 31, "bf16"),
+    custom("n1", 1, 1, 2, 1, 1, 1, 64, 5, "bf16"),
+    custom("g8", 1, 1, 16, 2, 513, 20, 128, 7, "bf16"),
+]
+
+
+@pytest.mark.parametrize("wl", SNAP_CASES, ids=lambda w: w.name)
+def test_snapkv_score_matches_oracle(K, wl):
+    note(f"snapkv parity {wl}")
+    inp = WL.make_inputs(wl, device="cuda", with_v=False)
+    score = K.snapkv_score(inp["q"], inp["k"], wl.pool_k)
+    torch.cuda.synchronize()
+    ref = O.snapkv_score(f64(inp["q"]), f64(inp["k"]), wl.Hkv, wl.pool_k)
+    check_scores(f64(score), ref, wl.name)
+
+
+def test_snapkv_score_layer8k_all_segments(K):
+    wl = WL.get_workload("layer8k")
+    note("snapkv parity layer8k (8 segments)")
+    inp = WL.make_inputs(wl, device="cuda", with_v=False)
+    score = K.snapkv_score(inp["q"], inp["k"], wl.pool_k)
+    torch.cuda.synchronize()
+    ref = O.snapkv_score(f64(inp["q"]), f64(inp["k"]), wl.Hkv, wl.pool_k)
+    check_scores(f64(score), ref, wl.name)
+
+
+def test_snapkv_explicit_scale(K):
+    wl = custom("scale", 1, 1, 4, 2, 256, 8, 64, 5, "bf16")
+    inp = WL.make_inputs(wl, device="cuda", with_v=False)
+    score = K.snapkv_score(inp["q"], inp["k"], wl.pool_k, scale=0.05)
+    torch.cuda.synchronize()
+    ref = O.snapkv_score(f64(inp["q"]), f64(inp["k"]), wl.Hkv, wl.pool_k, scale=0.05)
+    check_scores(f64(score), ref, "scale")
+
+
+H2O_CASES = [
+    custom("h2o_small", 1, 1, 4, 2, 300, 0, 128, 1, "bf16", scorer="h2o"),
+    custom("h2o_f32", 1, 1, 2, 1, 200, 0, 64, 1, "f32", scorer="h2o"),
+    custom("h2o_ragged", 2, 1, 8, 2, 513, 0, 128, 1, "bf16", scorer="h2o"),
+    custom("h2o_n1", 1, 1, 2, 2, 1, 0, 64, 1, "bf16", scorer="h2o"),
+]
+
+
+@pytest.mark.parametrize("wl", H2O_CASES, ids=lambda w: w.name)
+def test_h2o_score_matches_oracle(K, wl):
+    note(f"h2o parity {wl}")
+    inp = WL.make_inputs(wl, device="cuda", with_v=False)
+    score = K.h2o_score(inp["q"], inp["k"])
+    torch.cuda.synchronize()
+    ref = O.h2o_score(f64(inp["q"]), f64(inp["k"]), wl.Hkv)
+    check_scores(f64(score), ref, wl.name)
+    # total mass: every query row distributes exactly G*N per KV head in sum
+    tot = f64(score).sum(axis=-1)
+    np.testing.assert_allclose(tot, wl.G * wl.N, rtol=1e-4)
+
+
+def test_h2o_full_size_one_kv_head(K):
+    """The 16k-token H2O workload at its real shape; the oracle recomputes the
+    scores of one KV head (4 query heads x 16384 rows) in float64."""
+    wl = WL.get_workload("h2o16k")
+    note("h2o parity h2o16k (full size, KV head 5 checked)")
+    inp = WL.make_inputs(wl, device="cuda", with_v=False)
+    score = K.h2o_score(inp["q"], inp["k"])
+    torch.cuda.synchronize()
+    j = 5
+    q = f64(inp["q"][0, 0, j * wl.G:(j + 1) * wl.G])
+    k = f64(inp["k"][0, 0, j])
+    ref = O.h2o_mass(q, k, row_block=1024)
+    check_scores(f64(score[0, 0, j]), ref, "h2o16k head 5")
+    np.testing.assert_allclose(f64(score).sum(axis=-1), wl.G * wl.N, rtol=1e-4)
+
+
+def _random_selection_case(rng, N, R_labels, R):
+    s = rng.random(N).astype(np.float32)
+    s[rng.random(N) < 0.2] = 0.5                         # exact ties
+    s[rng.random(N) < 0.05] = -0.0
+    s[rng.random(N) < 0.05] = np.nan
+    roles = rng.integers(-1, R_labels, N).astype(np.int8)
+    return s, roles
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_topk_select_bit_exact_with_oracle(K, seed):
+    rng = np.random.default_rng(seed)
+    L, B, Hkv = 2, 2, 3
+    N = int(rng.choice([7, 300, 1000, 4097]))
+    W = int(rng.integers(0, min(N, 40)))
+    R = int(rng.integers(1, 9))
+    score = np.zeros((L, B, Hkv, N), dtype=np.float32)
+    roles = np.zeros((B, N), dtype=np.int8)
+    for b in range(B):
+        _, roles[b] = _random_selection_case(rng, N, R + 1, R)
+    for l in range(L):
+        for b in range(B):
+            for j in range(Hkv):
+                score[l, b, j], _ = _random_selection_case(rng, N, R, R)
+    quota = rng.integers(-2, N // max(R, 1) + 3, (B, R)).astype(np.int32)
+    kept = [W + sum(min(max(int(quota[b, r]), 0), int(np.sum(roles[b, :N - W] == r)))
+                    for r in range(R)) for b in range(B)]
+    k_cap = max(kept)
+    idx, cnt = K.topk_select(torch.from_numpy(score).cuda(), torch.from_numpy(roles).cuda(),
+                             torch.from_numpy(quota).cuda(), W, R, k_cap)
+    torch.cuda.synchronize()
+    idx, cnt = idx.cpu().numpy(), cnt.cpu().numpy()
+    for l in range(L):
+        for b in range(B):
+            for j in range(Hkv):
+                ref = O.select_keep(score[l, b, j], roles[b], quota[b], W)
+                assert cnt[l, b, j] == len(ref) == kept[b]
+                assert idx[l, b, j, :len(ref)].tolist() == ref.tolist()
+
+
+def test_topk_reports_truncation(K):
+    N, W = 100, 4
+    score = torch.rand((1, 1, 1, N)).cuda()
+    roles = torch.zeros((1, N), dtype=torch.int8).cuda()
+    quota = torch.tensor([[50]], dtype=torch.int32).cuda()
+    idx, cnt = K.topk_select(score, roles, quota, W, 1, 20)
+    torch.cuda.synchronize()
+    assert int(cnt[0, 0, 0]) == 54
+    ref = O.select_keep(score[0, 0, 0].cpu().numpy(), np.zeros(N, dtype=np.int8), [50], W)
+    assert idx[0, 0, 0].cpu().numpy().tolist() == ref[:20].tolist()
+
+
+@pytest.mark.parametrize("dtype,d", [("bf16", 128), ("bf16", 64), ("f32", 64), ("f32", 128)])
+def test_kv_compact_bit_exact(K, dtype, d):
+    rng = np.random.default_rng(3)
+    L, B, Hkv, N, k_cap = 2, 2, 3, 257, 40
+    tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
+    kk = torch.randn((L, B, Hkv, N, d)).to(tdt).cuda()
+    vv = torch.randn((L, B, Hkv, N, d)).to(tdt).cuda()
+    idx = np.full((L, B, Hkv, k_cap), -1, dtype=np.int32)
+    cnt = rng.integers(0, k_cap + 1, (L, B, Hkv)).astype(np.int32)
+    for s in np.ndindex(L, B, Hkv):
+        idx[s][:cnt[s]] = np.sort(rng.choice(N, cnt[s], replace=False))
+    idx[0, 0, 0, 0] = N + 5                 # out-of-range entry: skipped
+    cnt[1, 1, 2] = k_cap + 7                # count above capacity: clamped
+    idx[1, 1, 2] = np.arange(k_cap)
+    ko, vo = K.kv_compact(kk, vv, torch.from_numpy(idx).cuda(), torch.from_numpy(cnt).cuda())
+    torch.cuda.synchronize()
+    bits = torch.int16 if dtype == "bf16" else torch.int32
+    kbits, vbits = kk.view(bits).cpu().numpy(), vv.view(bits).cpu().numpy()
+    kob, vob = ko.view(bits).cpu().numpy(), vo.view(bits).cpu().numpy()
+    for s in np.ndindex(L, B, Hkv):
+        c = min(cnt[s], k_cap)
+        for m in range(k_cap):
+            t = idx[s][m]
+            if m < c and 0 <= t < N:
+                assert np.array_equal(kob[s][m], O.kv_compact(kbits[s], [t])[0])
+                assert np.array_equal(vob[s][m], O.kv_compact(vbits[s], [t])[0])
+            else:
+                assert not kob[s][m].any() and not vob[s][m].any()
+
+
+def _pipeline_check(K, wl, inp, budget, alpha, segs=None):
+    """Run the whole step on the GPU and check scores, kept sets and compacted
+    rows of the given segments against the oracle."""
+    from paper_2607_13205_amd import pipeline
+    W = 0 if wl.scorer == "h2o" else wl.W
+    pool = 1 if wl.scorer == "h2o" else wl.pool_k
+    _, _, k_cap = K.role_allocate(inp["roles"], 4, alpha, budget, W)
+    bufs = pipeline.alloc_buffers(inp["k"], wl.Hq, W, 4, k_cap, scorer=wl.scorer)
+    quota, kept = pipeline.evict(inp["q"], inp["k"], inp["v"], inp["roles"], inp["roles_t"], alpha,
+                                 budget, W, pool, bufs, scorer=wl.scorer)
+    torch.cuda.synchronize()
+    qo, ko, _ = O.role_allocate_batch(inp["roles"], 4, alpha, budget, W)
+    assert np.array_equal(quota, qo) and np.array_equal(kept, ko)
+    if segs is None:
+        segs = list(np.ndindex(len(inp["layers"]), wl.B, wl.Hkv))
+    ties = 0
+    for (l, b, j) in segs:
+        kseg = f64(inp["k"][l, b, j])
+        if wl.scorer == "h2o":
+            s_ref = O.h2o_mass(f64(inp["q"][l, b, j * wl.G:(j + 1) * wl.G]), kseg, row_block=1024)
+        else:
+            s_ref = O.maxpool_prefix(O.snapkv_mass(f64(inp["q"][l, b, j * wl.G:(j + 1) * wl.G]), kseg),
+                                     W, pool)
+        check_scores(f64(bufs.score[l, b, j]), s_ref, f"{wl.name} seg {(l, b, j)}")
+        roles = inp["roles"][b]
+        idx_ref = O.select_keep(s_ref, roles, qo[b], W)
+        n = int(bufs.count[l, b, j])
+        assert n == kept[b]
+        idx_gpu = bufs.idx[l, b, j, :n].cpu().numpy()
+        ties += check_kept_set(idx_gpu, idx_ref, s_ref, roles, W, qo[b])
+        # the oracle's selection on the GPU's own float32 scores is bit-exact
+        idx_same = O.select_keep(bufs.score[l, b, j].cpu().numpy(), roles, qo[b], W)
+        assert np.array_equal(idx_gpu, idx_same)
+        # compaction: row m is the input row idx_gpu[m], bit for bit
+        bits = torch.int16 if inp["k"].dtype == torch.bfloat16 else torch.int32
+        kin = inp["k"][l, b, j].view(bits).cpu().numpy()
+        vin = inp["v"][l, b, j].view(bits).cpu().numpy()
+        assert np.array_equal(bufs.k_out[l, b, j, :n].view(bits).cpu().numpy(), O.kv_compact(kin, idx_gpu))
+        assert np.array_equal(bufs.v_out[l, b, j, :n].view(bits).cpu().numpy(), O.kv_compact(vin, idx_gpu))
+    return ties
+
+
+@pytest.mark.parametrize("name,budget", [("tiny", 0.10), ("layer8k", 0.05), ("layer8k", 0.10),
+                                         ("layer8k", 0.20), ("layer8k", 0.50)])
+def test_pipeline_small_workloads(K, name, budget):
+    wl = WL.get_workload(name)
+    note(f"pipeline {name} B={budget}")
+    inp = WL.make_inputs(wl, device="cuda")
+    ties = _pipeline_check(K, wl, inp, budget, WL.default_alpha(0.0))
+    note(f"  near-tie pairs: {ties}")
+
+
+def test_pipeline_alpha_key_nonzero_and_neutral(K):
+    wl = WL.get_workload("layer8k").with_(Hq=8, Hkv=2)
+    inp = WL.make_inputs(wl, device="cuda")
+    _pipeline_check(K, wl, inp, 0.1, WL.default_alpha(0.02))
+    # neutral policy: one bucket with weight 1 is plain SnapKV at budget B
+    roles1 = np.zeros_like(inp["roles"])
+    inp1 = dict(inp, roles=roles1, roles_t=torch.from_numpy(roles1).cuda())
+    from paper_2607_13205_amd import pipeline
+    _, _, k_cap = K.role_allocate(roles1, 1, [1.0], 0.1, wl.W)
+    bufs = pipeline.alloc_buffers(inp["k"], wl.Hq, wl.W, 1, k_cap)
+    pipeline.evict(inp1["q"], inp1["k"], inp1["v"], roles1, inp1["roles_t"], [1.0], 0.1, wl.W,
+                   wl.pool_k, bufs)
+    torch.cuda.synchronize()
+    for j in range(wl.Hkv):
+        s = bufs.score[0, 0, j].cpu().numpy()
+        K_ = math.ceil(0.1 * wl.N - 1e-9)
+        order = sorted(range(wl.N - wl.W), key=lambda t: (-s[t], t))
+        ref = sorted(order[:K_ - wl.W] + list(range(wl.N - wl.W, wl.N)))
+        n = int(bufs.count[0, 0, j])
+        assert bufs.idx[0, 0, j, :n].cpu().numpy().tolist() == ref
+
+
+def test_pipeline_h2o_small(K):
+    wl = custom("h2o_pipe", 1, 1, 8, 2, 700, 0, 128, 1, "bf16", scorer="h2o")
+    inp = WL.make_inputs(wl, device="cuda")
+    _pipeline_check(K, wl, inp, 0.1, WL.default_alpha(0.0))
+
+
+def test_determinism(K):
+    wl = WL.get_workload("layer8k")
+    inp = WL.make_inputs(wl, device="cuda")
+    from paper_2607_13205_amd import pipeline
+    alpha = WL.default_alpha(0.0)
+    outs = []
+    for _ in range(2):
+        _, _, k_cap = K.role_allocate(inp["roles"], 4, alpha, 0.1, wl.W)
+        bufs = pipeline.alloc_buffers(inp["k"], wl.Hq, wl.W, 4, k_cap)
+        pipeline.evict(inp["q"], inp["k"], inp["v"], inp["roles"], inp["roles_t"], alpha, 0.1,
+                       wl.W, wl.pool_k, bufs)
+        torch.cuda.synchronize()
+        outs.append((bufs.score.clone(), bufs.idx.clone(), bufs.k_out.clone()))
+    assert torch.equal(outs[0][0], outs[1][0])
+    assert torch.equal(outs[0][1], outs[1][1])
+    assert torch.equal(outs[0][2].view(torch.int16), outs[1][2].view(torch.int16))
+
+
+@pytest.mark.parametrize("name,budget,segs", [
+    ("stack32k", 0.05, [(0, 0, 0), (17, 2, 5), (31, 3, 7)]),
+    ("long128k", 0.05, [(0, 0, 0), (31, 0, 7)]),
+    ("long128k", 0.20, [(13, 0, 2)]),
+])
+def test_pipeline_full_size_sampled(K, name, budget, segs):
+    """Real shapes, the launch configuration the benchmark times; the oracle
+    recomputes a few sampled (layer, sample, KV head) segments."""
+    wl = WL.get_workload(name)
+    note(f"pipeline full size {name} B={budget}: generating inputs")
+    inp = WL.make_inputs(wl, device="cuda")
+    torch.cuda.synchronize()
+    note("  running and checking sampled segments")
+    ties = _pipeline_check(K, wl, inp, budget, WL.default_alpha(0.0), segs=segs)
+    note(f"  near-tie pairs: {ties}")
+    del inp
+    torch.cuda.empty_cache()
