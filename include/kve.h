@@ -87,9 +87,14 @@ size_t kve_snapkv_workspace_size(int L, int B, int Hq, int Hkv, int N, int W, in
  *   pool_k odd, >= 1 (1 disables pooling)
  *   score  [L, B, Hkv, N] float32 output (device)
  *
- * Requires 1 <= W <= N, G*W <= 256.  Scores are accumulated in float32 from
- * products of the input type; the two-pass softmax subtracts each row's
- * maximum before exponentiating.
+ * Requires 1 <= W <= N, G*W <= 1024.  Scores are accumulated in float32 from
+ * products of the input type; the softmax subtracts each row's maximum before
+ * exponentiating (per key chunk, merged exactly across chunks).
+ *
+ * The first 4 bytes of the workspace receive a device status word: nonzero
+ * after the call has run means an internal wait of the persistent kernel
+ * timed out (it cannot when the GPU runs nothing else that starves it) and the
+ * scores must not be used.
  */
 kve_status_t kve_snapkv_score(const void* q_win, const void* k, kve_dtype_t dtype,
                               int L, int B, int Hq, int Hkv, int N, int W, int d,

@@ -7,6 +7,8 @@
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
+#include <cstdlib>
+#include <cstring>
 #include <string>
 #include <vector>
 
@@ -67,9 +69,9 @@ int kve_version(void) { return KVE_ABI_VERSION; }
 const char* kve_last_error(void) { return g_error.c_str(); }
 
 size_t kve_snapkv_workspace_size(int L, int B, int Hq, int Hkv, int N, int W, int d) {
-    (void)d;
     if (L <= 0 || B <= 0 || Hq <= 0 || Hkv <= 0 || N <= 0 || W <= 0 || Hq % Hkv != 0) return 0;
-    return kve::snap_plan(L, B, Hq, Hkv, N, W).total;
+    if (d != 64 && d != 128) return 0;
+    return kve::snap_plan(L, B, Hq, Hkv, N, W, d).total;
 }
 
 kve_status_t kve_snapkv_score(const void* q_win, const void* k, kve_dtype_t dtype, int L, int B,
@@ -88,16 +90,21 @@ kve_status_t kve_snapkv_score(const void* q_win, const void* k, kve_dtype_t dtyp
     const long long rows = (long long)(Hq / Hkv) * W;
     if (rows > kve::kSnapMaxRows)
         return fail(KVE_ERR_UNSUPPORTED, "%s: G*W=%lld exceeds %d", fn, rows, kve::kSnapMaxRows);
-    const kve::SnapPlan p = kve::snap_plan(L, B, Hq, Hkv, N, W);
-    if ((long long)p.segs * p.rgroups * p.nchunks > kMaxGrid)
+    const kve::SnapPlan p = kve::snap_plan(L, B, Hq, Hkv, N, W, d);
+    if ((long long)p.n_vsegs * p.nranges > kMaxGrid)
         return fail(KVE_ERR_UNSUPPORTED, "%s: shape too large", fn);
     if (workspace_bytes < p.total || (p.total > 0 && workspace == nullptr))
         return fail(KVE_ERR_WORKSPACE, "%s: workspace of %zu bytes < %zu needed", fn, workspace_bytes,
                     p.total);
     if (!aligned(workspace)) return fail(KVE_ERR_INVALID_ARG, "%s: workspace not 256-byte aligned", fn);
     if (scale == 0.0f) scale = 1.0f / std::sqrt((float)d);
+    // KVE_SNAPKV_PATH=persistent selects the persistent single-read kernel
+    // (when the shape fits one cooperative grid); the default is the streaming
+    // two-pass kernels, which measure faster.
+    const char* path = std::getenv("KVE_SNAPKV_PATH");
+    const bool persistent = path != nullptr && std::strcmp(path, "persistent") == 0;
     return from_hip(kve::launch_snapkv(q_win, k, (int)dtype, L, B, Hq, Hkv, N, W, d, scale, pool_k,
-                                       score, workspace, static_cast<hipStream_t>(stream)),
+                                       score, workspace, persistent, static_cast<hipStream_t>(stream)),
                     fn);
 }
 

@@ -1,248 +1,247 @@
-// SnapKV windowed score with fused GQA sum and prefix max-pool.
+// SnapKV windowed score with fused GQA sum and prefix max-pool: streaming
+// two-pass kernels.
 //
 // Paper: §2 (SnapKV: windowed mass over the last W queries, 1-D max-pool over
 // the KV axis), §4 "SnapKV mechanism" (pool kernel 7) and Algorithm 1
 // (windowed-mass and pooling steps).
 //
-// Work decomposition.  A segment is one (layer, sample, KV head).  Its rows are
-// the G*W window queries of the group (head-major), taken in row groups of 128
-// rows: one workgroup of four waves owns a row group and a chunk of keys; each
-// wave owns a 32-row block whose query fragments stay in registers for the whole
-// chunk.  Keys are streamed through LDS in tiles of 64 with 16-byte coalesced
-// loads and multiplied on the matrix cores (bf16: 32x32x16, fp32: 32x32x2).
+// A segment is one (layer, sample, KV head); its rows are the G*W window
+// queries of the group (head-major), taken in row groups of 128 (a virtual
+// segment, vseg, is one segment and one row group).  A workgroup of four waves
+// owns a vseg and a contiguous range of its keys; each wave owns a 32-row
+// block whose query fragments stay in registers.  Keys stream through a
+// four-slot LDS ring in chunks of 64 with direct-to-LDS loads issued three
+// chunks ahead, so every wave keeps HBM requests in flight while it multiplies
+// on the matrix cores (bf16 32x32x16, fp32 32x32x2).  No workgroup waits on
+// another one.
 //
-//   pass 1  snap_stats   per (chunk, row): running max m and sum of exp2(x - m)
-//   combine snap_lse     per row: lse2 = m + log2(sum) over the chunks
-//   pass 2  snap_colsum  per key: sum over the row group of exp2(x - lse2)
-//   pool    snap_pool    adds the row groups and max-pools the prefix
+//   pass 1   snap_pass1    S^T = K Q^T: each lane holds one row and 16 keys per
+//                          block, so the running row max and sum of
+//                          exp2(x - max) stay in the lane; one log-sum-exp
+//                          per (vseg, range, row) is written.
+//   combine  snap_combine  per row: lse2 over the ranges (+inf for padding rows).
+//   pass 2   snap_pass2    S = Q K^T: each lane holds one key and 16 rows, so
+//                          the column sum of exp2(x - lse2) is a lane sum plus
+//                          one shuffle; the four row blocks add through LDS.
+//   pool     snap_pool     adds the row groups and max-pools the prefix.
 //
 // Logits are kept in log2 units (x = scale * log2(e) * <q, k>) so that every
 // exponential is a single v_exp_f32.
 #include "kve_device.h"
 #include "kve_internal.h"
+#include "kve_stream.h"
 
 namespace kve {
 namespace {
 
-constexpr int kThreads = 256;
+constexpr int kThreads = 256;  // four waves
+constexpr int kWaves = 4;
+constexpr int kRing = 4;       // LDS chunk slots: the chunk in use and three ahead
 constexpr int kPoolTile = 256;
 constexpr int kMaxPoolHalf = 127;
 
-template <typename T, int D>
-struct SnapShape {
-    static constexpr int ES = (int)sizeof(T);
-    static constexpr int ROW_BYTES = D * ES;
-    static constexpr int ROWB = ROW_BYTES + 16;  // padded LDS row: spreads banks
-    static constexpr int TILE_BYTES = kSnapTileKeys * ROW_BYTES;
-    static constexpr int NSTEP = D / Mma<T>::KSTEP;
+// Wait until this wave's loads of the current chunk have landed, while the
+// loads of up to `ahead` later chunks stay in flight.
+template <int LPW>
+__device__ __forceinline__ void wait_chunk(int ahead) {
+    if (ahead >= 2)
+        wait_vmcnt<2 * LPW>();
+    else if (ahead == 1)
+        wait_vmcnt<LPW>();
+    else
+        wait_vmcnt<0>();
+}
+
+struct Span {
+    int vseg, seg, rg, range, t_begin, t_end, nsub;
 };
 
-template <typename T, int D>
-using FragArr = typename Mma<T>::frag[SnapShape<T, D>::NSTEP];
-
-
-// Copy rows [t0, t0 + kSnapTileKeys) of a [*, D] matrix into LDS; rows at or
-// beyond t_end are zero-filled.  All threads of the block take part.
-template <typename T, int D>
-__device__ __forceinline__ void stage_rows(char* dst, const T* src, int t0, int t_end) {
-    using S = SnapShape<T, D>;
-    for (int o = threadIdx.x * 16; o < S::TILE_BYTES; o += kThreads * 16) {
-        const int key = o / S::ROW_BYTES;
-        const int within = o - key * S::ROW_BYTES;
-        const int t = t0 + key;
-        u32x4 v = zero16();
-        if (t < t_end)
-            v = ld16(reinterpret_cast<const char*>(src) + (size_t)t * S::ROW_BYTES + within);
-        st16(dst + key * S::ROWB + within, v);
-    }
-}
-
-// Query fragments of this lane's row (A operand) for every k step.
-template <typename T, int D>
-__device__ __forceinline__ void load_row_frags(FragArr<T, D>& fr,
-                                               const T* base, int row, int nrows) {
-    using M = Mma<T>;
-    const int lane = threadIdx.x & 63;
-#pragma unroll
-    for (int s = 0; s < SnapShape<T, D>::NSTEP; ++s) {
-        const int kb = s * M::KSTEP + (lane >> 5) * M::KPL;
-        fr[s] = row < nrows ? M::load(base + (size_t)row * D, kb) : M::zero();
-    }
-}
-
-// 32 rows x 32 keys block: A fragments in registers, B rows in LDS.
-template <typename T, int D>
-__device__ __forceinline__ f32x16 block_logits(const FragArr<T, D>& qa,
-                                               const char* krow) {
-    using M = Mma<T>;
-    const int lane = threadIdx.x & 63;
-    f32x16 acc = {};
-#pragma unroll
-    for (int s = 0; s < SnapShape<T, D>::NSTEP; ++s)
-        acc = M::mma(qa[s], M::load(krow, s * M::KSTEP + (lane >> 5) * M::KPL), acc);
-    return acc;
-}
-
-struct SegIdx {
-    int c, rg, seg;
-};
-__device__ __forceinline__ SegIdx seg_index(int nchunks, int rgroups) {
-    int bid = blockIdx.x;
-    SegIdx s;
-    s.c = bid % nchunks;
-    bid /= nchunks;
-    s.rg = bid % rgroups;
-    s.seg = bid / rgroups;
+__device__ __forceinline__ Span span_of(int nranges, int rgroups, int range_keys, int N) {
+    Span s;
+    s.vseg = blockIdx.x / nranges;
+    s.range = blockIdx.x - s.vseg * nranges;
+    s.seg = s.vseg / rgroups;
+    s.rg = s.vseg - s.seg * rgroups;
+    s.t_begin = s.range * range_keys;
+    s.t_end = min(N, s.t_begin + range_keys);
+    s.nsub = (s.t_end - s.t_begin + kChunkKeys - 1) / kChunkKeys;
     return s;
 }
 
 template <typename T, int D>
-__global__ __launch_bounds__(kThreads) void snap_stats(const T* __restrict__ q, const T* __restrict__ k,
-                                                       int N, int W, int rows, int rgroups,
-                                                       int rows_pad, int chunk, int nchunks, float sl2,
-                                                       float2* __restrict__ stats) {
-    using S = SnapShape<T, D>;
-    __shared__ __align__(16) char sk[kSnapTileKeys * S::ROWB];
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    const SegIdx ix = seg_index(nchunks, rgroups);
-    const int row0 = ix.rg * kSnapRowsPerGroup + wave * 32;
-    const T* qseg = q + (size_t)ix.seg * rows * D;
-    const T* kseg = k + (size_t)ix.seg * N * D;
-
-    typename Mma<T>::frag qa[S::NSTEP];
-    load_row_frags<T, D>(qa, qseg, row0 + (lane & 31), rows);
-
-    float m[16], l[16];
-    int lim[16];  // last key each of this lane's rows may see (causal), -1 for padding rows
+__device__ __forceinline__ void load_q(QFrag<T, D>& qf, const T* q, int seg, int rows, int row) {
+    using M = Mma<T>;
+    const int lane = threadIdx.x & 63;
+    const T* base = q + ((size_t)seg * rows + row) * D;
 #pragma unroll
-    for (int i = 0; i < 16; ++i) {
-        const int r = row0 + c_row(i, lane);
-        m[i] = -INFINITY;
-        l[i] = 0.0f;
-        lim[i] = r < rows ? N - W + (r % W) : -1;
-    }
-    const int t_begin = ix.c * chunk;
-    const int t_end = min(N, t_begin + chunk);
-    for (int t0 = t_begin; t0 < t_end; t0 += kSnapTileKeys) {
-        __syncthreads();
-        stage_rows<T, D>(sk, kseg, t0, t_end);
-        __syncthreads();
-        if (row0 >= rows) continue;
-#pragma unroll
-        for (int cb = 0; cb < kSnapTileKeys / 32; ++cb) {
-            const f32x16 acc = block_logits<T, D>(qa, sk + (cb * 32 + (lane & 31)) * S::ROWB);
-            const int t = t0 + cb * 32 + (lane & 31);
-#pragma unroll
-            for (int i = 0; i < 16; ++i) {
-                const bool valid = t < t_end && t <= lim[i];
-                const float x = valid ? acc[i] * sl2 : -INFINITY;
-                const float mn = fmaxf(m[i], x);
-                if (mn != -INFINITY) {
-                    l[i] = l[i] * fast_exp2(m[i] - mn) + fast_exp2(x - mn);
-                    m[i] = mn;
-                }
-            }
-        }
-    }
-    // combine the 32 lanes that hold the same rows
-#pragma unroll
-    for (int off = 1; off < 32; off <<= 1) {
-#pragma unroll
-        for (int i = 0; i < 16; ++i) {
-            const float mo = __shfl_xor(m[i], off);
-            const float lo = __shfl_xor(l[i], off);
-            lse2_merge(m[i], l[i], mo, lo);
-        }
-    }
-    if ((lane & 31) == 0) {
-#pragma unroll
-        for (int i = 0; i < 16; ++i) {
-            const int r = row0 + c_row(i, lane);
-            if (r < rows)
-                stats[((size_t)ix.seg * nchunks + ix.c) * rows_pad + r] = make_float2(m[i], l[i]);
-        }
-    }
-}
-
-__global__ __launch_bounds__(kThreads) void snap_lse(const float2* __restrict__ stats, int nchunks,
-                                                     int rows, int rows_pad, float* __restrict__ lse) {
-    const int seg = blockIdx.x;
-    for (int r = threadIdx.x; r < rows; r += blockDim.x) {
-        float m = -INFINITY, l = 0.0f;
-        for (int c = 0; c < nchunks; ++c) {
-            const float2 v = stats[((size_t)seg * nchunks + c) * rows_pad + r];
-            lse2_merge(m, l, v.x, v.y);
-        }
-        lse[(size_t)seg * rows_pad + r] = l > 0.0f ? m + log2f(l) : -INFINITY;
-    }
+    for (int s = 0; s < KChunk<T, D>::NSTEP; ++s)
+        qf[s] = row < rows ? M::load(base, s * M::KSTEP + (lane >> 5) * M::KPL) : M::zero();
 }
 
 template <typename T, int D>
-__global__ __launch_bounds__(kThreads) void snap_colsum(const T* __restrict__ q, const T* __restrict__ k,
-                                                        int N, int W, int rows, int rgroups,
-                                                        int rows_pad, int chunk, int nchunks, float sl2,
-                                                        const float* __restrict__ lse, int segs,
-                                                        float* __restrict__ raw) {
-    using S = SnapShape<T, D>;
-    __shared__ __align__(16) char sk[kSnapTileKeys * S::ROWB];
-    __shared__ float scol[kThreads / kWave][kSnapTileKeys];
+__device__ __forceinline__ void issue_chunk(char* ring, const char* kseg, const Span& sp, int s) {
+    const int t0 = sp.t_begin + s * kChunkKeys;
+    chunk_stream<T, D, kWaves>(ring + (s % kRing) * KChunk<T, D>::BYTES, kseg + (size_t)t0 * KChunk<T, D>::ROW,
+                               sp.t_end - t0, threadIdx.x >> 6, threadIdx.x & 63);
+}
+
+template <typename T, int D>
+__global__ __launch_bounds__(kThreads, 2) void snap_pass1(const T* __restrict__ q, const T* __restrict__ k,
+                                                          int N, int W, int rows, int rgroups, int nranges,
+                                                          int range_keys, float sl2,
+                                                          float* __restrict__ stats) {
+    using C = KChunk<T, D>;
+    using M = Mma<T>;
+    constexpr int LPW = chunk_loads_per_wave<T, D, kWaves>();
+    __shared__ __align__(16) char ring[kRing][C::BYTES];
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    const SegIdx ix = seg_index(nchunks, rgroups);
-    const int row0 = ix.rg * kSnapRowsPerGroup + wave * 32;
-    const T* qseg = q + (size_t)ix.seg * rows * D;
-    const T* kseg = k + (size_t)ix.seg * N * D;
+    const Span sp = span_of(nranges, rgroups, range_keys, N);
+    const int P_rows = N - W;
+    const char* kseg = reinterpret_cast<const char*>(k) + (size_t)sp.seg * N * C::ROW;
 
-    typename Mma<T>::frag qa[S::NSTEP];
-    load_row_frags<T, D>(qa, qseg, row0 + (lane & 31), rows);
+    QFrag<T, D> qf;
+    const int qr = sp.rg * 128 + wave * 32 + (lane & 31);  // this lane's query row
+    load_q<T, D>(qf, q, sp.seg, rows, qr);
+    const int lim = qr < rows ? P_rows + (qr % W) : -1;
+    drain_loads();
 
-    float lr[16];
-    int lim[16];
+    for (int s = 0; s < min(kRing - 1, sp.nsub); ++s) issue_chunk<T, D>(&ring[0][0], kseg, sp, s);
+
+    float m2 = -INFINITY, l = 0.0f;  // running max (log2 units) and sum of this lane's keys
+    for (int s = 0; s < sp.nsub; ++s) {
+        wait_chunk<LPW>(min(kRing - 2, sp.nsub - 1 - s));
+        lds_barrier();
+        if (s + kRing - 1 < sp.nsub) issue_chunk<T, D>(&ring[0][0], kseg, sp, s + kRing - 1);
+        const char* buf = ring[s % kRing];
+        const int t0 = sp.t_begin + s * kChunkKeys;
+        float x[2][16];
 #pragma unroll
-    for (int i = 0; i < 16; ++i) {
-        const int r = row0 + c_row(i, lane);
-        lim[i] = r < rows ? N - W + (r % W) : -1;
-        lr[i] = r < rows ? lse[(size_t)ix.seg * rows_pad + r] : 0.0f;
-    }
-    float* out = raw + ((size_t)ix.rg * segs + ix.seg) * N;
-    const int t_begin = ix.c * chunk;
-    const int t_end = min(N, t_begin + chunk);
-    for (int t0 = t_begin; t0 < t_end; t0 += kSnapTileKeys) {
-        __syncthreads();
-        stage_rows<T, D>(sk, kseg, t0, t_end);
-        __syncthreads();
-        float col[kSnapTileKeys / 32];
+        for (int j = 0; j < 2; ++j) {
+            f32x16 acc = {};
+            const int r = 32 * j + (lane & 31);
 #pragma unroll
-        for (int cb = 0; cb < kSnapTileKeys / 32; ++cb) col[cb] = 0.0f;
-        if (row0 < rows) {
+            for (int st = 0; st < C::NSTEP; ++st)
+                acc = M::mma(chunk_frag<T, D>(buf, r, st * M::KSTEP + (lane >> 5) * M::KPL), qf[st], acc);
 #pragma unroll
-            for (int cb = 0; cb < kSnapTileKeys / 32; ++cb) {
-                const f32x16 acc = block_logits<T, D>(qa, sk + (cb * 32 + (lane & 31)) * S::ROWB);
-                const int t = t0 + cb * 32 + (lane & 31);
-                float sum = 0.0f;
+            for (int i = 0; i < 16; ++i) x[j][i] = acc[i];
+        }
+        if (t0 + kChunkKeys > P_rows) {  // keys past N or inside the causal window
+#pragma unroll
+            for (int j = 0; j < 2; ++j)
 #pragma unroll
                 for (int i = 0; i < 16; ++i) {
-                    const bool valid = t < t_end && t <= lim[i];
-                    sum += valid ? fast_exp2(acc[i] * sl2 - lr[i]) : 0.0f;
+                    const int t = t0 + 32 * j + c_row(i, lane);
+                    if (!(t < sp.t_end && t <= lim)) x[j][i] = -INFINITY;
                 }
-                col[cb] = sum;
-            }
         }
+        float mx = -INFINITY;
 #pragma unroll
-        for (int cb = 0; cb < kSnapTileKeys / 32; ++cb) {
-            col[cb] += __shfl_xor(col[cb], 32);
-            if (lane < 32) scol[wave][cb * 32 + lane] = col[cb];
-        }
-        __syncthreads();
-        if (threadIdx.x < kSnapTileKeys) {
-            const int t = t0 + threadIdx.x;
-            if (t < t_end) {
-                float s = 0.0f;
+        for (int j = 0; j < 2; ++j)
 #pragma unroll
-                for (int w = 0; w < kThreads / kWave; ++w) s += scol[w][threadIdx.x];
-                out[t] = s;
-            }
+            for (int i = 0; i < 16; i += 2) mx = fmaxf(mx, fmaxf(x[j][i], x[j][i + 1]));
+        const float mn = fmaxf(m2, mx * sl2);
+        if (mn != -INFINITY) {
+            float acc = l * fast_exp2(m2 - mn);
+#pragma unroll
+            for (int j = 0; j < 2; ++j)
+#pragma unroll
+                for (int i = 0; i < 16; ++i) acc += fast_exp2(fmaf(x[j][i], sl2, -mn));
+            l = acc;
+            m2 = mn;
         }
     }
+    // the two lane halves hold the same row and different keys
+    lse2_merge(m2, l, __shfl_xor(m2, 32), __shfl_xor(l, 32));
+    if (lane < 32)
+        stats[((size_t)sp.vseg * nranges + sp.range) * 128 + wave * 32 + lane] =
+            (m2 != -INFINITY && l > 0.0f) ? m2 + log2f(l) : -INFINITY;
+}
+
+__global__ __launch_bounds__(128) void snap_combine(const float* __restrict__ stats, int nranges, int rows,
+                                                    int rgroups, float* __restrict__ lse) {
+    const int vseg = blockIdx.x, r = threadIdx.x;
+    const int row = (vseg % rgroups) * 128 + r;
+    float a = -INFINITY, b = 0.0f;
+    for (int c = 0; c < nranges; ++c) {
+        const float v = stats[((size_t)vseg * nranges + c) * 128 + r];
+        lse2_merge(a, b, v, v == -INFINITY ? 0.0f : 1.0f);
+    }
+    // rows past the window rows contribute nothing to the column sums
+    lse[(size_t)vseg * 128 + r] = (row < rows && b > 0.0f) ? a + log2f(b) : INFINITY;
+}
+
+template <typename T, int D>
+__global__ __launch_bounds__(kThreads, 2) void snap_pass2(const T* __restrict__ q, const T* __restrict__ k,
+                                                          int N, int W, int rows, int rgroups, int nranges,
+                                                          int range_keys, float sl2,
+                                                          const float* __restrict__ lse, int segs,
+                                                          float* __restrict__ raw) {
+    using C = KChunk<T, D>;
+    using M = Mma<T>;
+    constexpr int LPW = chunk_loads_per_wave<T, D, kWaves>();
+    __shared__ __align__(16) char ring[kRing][C::BYTES];
+    __shared__ float scol[2][kWaves][kChunkKeys];
+    __shared__ float sraw[kSnapMaxRange];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const Span sp = span_of(nranges, rgroups, range_keys, N);
+    const int P_rows = N - W;
+    const char* kseg = reinterpret_cast<const char*>(k) + (size_t)sp.seg * N * C::ROW;
+
+    QFrag<T, D> qf;
+    const int row0 = sp.rg * 128 + wave * 32;
+    load_q<T, D>(qf, q, sp.seg, rows, row0 + (lane & 31));
+    float l2[16];
+#pragma unroll
+    for (int i = 0; i < 16; ++i) l2[i] = lse[(size_t)sp.vseg * 128 + wave * 32 + c_row(i, lane)];
+    drain_loads();
+
+    for (int s = 0; s < min(kRing - 1, sp.nsub); ++s) issue_chunk<T, D>(&ring[0][0], kseg, sp, s);
+
+    for (int s = 0; s < sp.nsub; ++s) {
+        wait_chunk<LPW>(min(kRing - 2, sp.nsub - 1 - s));
+        lds_barrier();
+        if (s + kRing - 1 < sp.nsub) issue_chunk<T, D>(&ring[0][0], kseg, sp, s + kRing - 1);
+        if (s >= 1 && tid < kChunkKeys) {
+            const float* c = &scol[(s - 1) & 1][0][tid];
+            sraw[(s - 1) * kChunkKeys + tid] =
+                (c[0] + c[kChunkKeys]) + (c[2 * kChunkKeys] + c[3 * kChunkKeys]);
+        }
+        const char* buf = ring[s % kRing];
+        const int t0 = sp.t_begin + s * kChunkKeys;
+        const bool full = t0 + kChunkKeys <= P_rows;
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+            f32x16 acc = {};
+            const int r = 32 * j + (lane & 31);
+#pragma unroll
+            for (int st = 0; st < C::NSTEP; ++st)
+                acc = M::mma(qf[st], chunk_frag<T, D>(buf, r, st * M::KSTEP + (lane >> 5) * M::KPL), acc);
+            float col = 0.0f;
+            if (full) {
+#pragma unroll
+                for (int i = 0; i < 16; ++i) col += fast_exp2(fmaf(acc[i], sl2, -l2[i]));
+            } else {
+                const int t = t0 + r;
+#pragma unroll
+                for (int i = 0; i < 16; ++i) {
+                    const int row = row0 + c_row(i, lane);
+                    const bool ok = t < sp.t_end && row < rows && t <= P_rows + (row % W);
+                    col += ok ? fast_exp2(fmaf(acc[i], sl2, -l2[i])) : 0.0f;
+                }
+            }
+            col += __shfl_xor(col, 32);
+            if (lane < 32) scol[s & 1][wave][32 * j + lane] = col;
+        }
+    }
+    __syncthreads();
+    if (tid < kChunkKeys) {
+        const int s = sp.nsub - 1;
+        const float* c = &scol[s & 1][0][tid];
+        sraw[s * kChunkKeys + tid] = (c[0] + c[kChunkKeys]) + (c[2 * kChunkKeys] + c[3 * kChunkKeys]);
+    }
+    __syncthreads();
+    float* out = raw + ((size_t)sp.rg * segs + sp.seg) * N + sp.t_begin;
+    for (int e = tid; e < sp.t_end - sp.t_begin; e += kThreads) out[e] = sraw[e];
 }
 
 __global__ __launch_bounds__(kPoolTile) void snap_pool(const float* __restrict__ raw, int rgroups,
@@ -279,22 +278,30 @@ __global__ __launch_bounds__(kPoolTile) void snap_pool(const float* __restrict__
 
 template <typename T, int D>
 hipError_t run_snapkv(const void* q, const void* k, int L, int B, int Hq, int Hkv, int N, int W,
-                      float scale, int pool_k, float* score, void* ws, hipStream_t st) {
-    const SnapPlan p = snap_plan(L, B, Hq, Hkv, N, W);
+                      float scale, int pool_k, float* score, void* ws, bool persistent, hipStream_t st) {
+    const SnapPlan p = snap_plan(L, B, Hq, Hkv, N, W, D);
     char* w = static_cast<char*>(ws);
-    float2* stats = reinterpret_cast<float2*>(w + p.off_stats);
+    float* stats = reinterpret_cast<float*>(w + p.off_stats);
     float* lse = reinterpret_cast<float*>(w + p.off_lse);
     float* raw = reinterpret_cast<float*>(w + p.off_raw);
     const float sl2 = scale * kLog2e;
     const T* qt = static_cast<const T*>(q);
     const T* kt = static_cast<const T*>(k);
-    const dim3 grid((unsigned)(p.segs * p.rgroups * p.nchunks));
-    hipLaunchKernelGGL((snap_stats<T, D>), grid, dim3(kThreads), 0, st, qt, kt, N, W, p.rows,
-                       p.rgroups, p.rows_pad, p.chunk, p.nchunks, sl2, stats);
-    hipLaunchKernelGGL(snap_lse, dim3(p.segs), dim3(kThreads), 0, st, stats, p.nchunks, p.rows,
-                       p.rows_pad, lse);
-    hipLaunchKernelGGL((snap_colsum<T, D>), grid, dim3(kThreads), 0, st, qt, kt, N, W, p.rows,
-                       p.rgroups, p.rows_pad, p.chunk, p.nchunks, sl2, lse, p.segs, raw);
+    bool used = false;
+    if (persistent) {
+        const hipError_t e = launch_snapkv_fused(q, k, sizeof(T) == 2 ? 0 : 1, L, B, Hq, Hkv, N, W, D, scale,
+                                                 raw, ws, st, &used);
+        if (e != hipSuccess) return e;
+    }
+    if (!used) {
+        const dim3 grid((unsigned)((size_t)p.n_vsegs * p.nranges));
+        hipLaunchKernelGGL((snap_pass1<T, D>), grid, dim3(kThreads), 0, st, qt, kt, N, W, p.rows, p.rgroups,
+                           p.nranges, p.range_keys, sl2, stats);
+        hipLaunchKernelGGL(snap_combine, dim3((unsigned)p.n_vsegs), dim3(128), 0, st, stats, p.nranges, p.rows,
+                           p.rgroups, lse);
+        hipLaunchKernelGGL((snap_pass2<T, D>), grid, dim3(kThreads), 0, st, qt, kt, N, W, p.rows, p.rgroups,
+                           p.nranges, p.range_keys, sl2, lse, p.segs, raw);
+    }
     const int tiles = (N + kPoolTile - 1) / kPoolTile;
     hipLaunchKernelGGL(snap_pool, dim3((unsigned)(p.segs * tiles)), dim3(kPoolTile), 0, st, raw,
                        p.rgroups, p.segs, N, W, pool_k, tiles, score);
@@ -305,13 +312,15 @@ hipError_t run_snapkv(const void* q, const void* k, int L, int B, int Hq, int Hk
 
 hipError_t launch_snapkv(const void* q, const void* k, int dtype, int L, int B, int Hq, int Hkv,
                          int N, int W, int d, float scale, int pool_k, float* score, void* ws,
-                         hipStream_t st) {
+                         bool persistent, hipStream_t st) {
     if (dtype == 0) {
-        if (d == 128) return run_snapkv<__bf16, 128>(q, k, L, B, Hq, Hkv, N, W, scale, pool_k, score, ws, st);
-        return run_snapkv<__bf16, 64>(q, k, L, B, Hq, Hkv, N, W, scale, pool_k, score, ws, st);
+        if (d == 128)
+            return run_snapkv<__bf16, 128>(q, k, L, B, Hq, Hkv, N, W, scale, pool_k, score, ws, persistent, st);
+        return run_snapkv<__bf16, 64>(q, k, L, B, Hq, Hkv, N, W, scale, pool_k, score, ws, persistent, st);
     }
-    if (d == 128) return run_snapkv<float, 128>(q, k, L, B, Hq, Hkv, N, W, scale, pool_k, score, ws, st);
-    return run_snapkv<float, 64>(q, k, L, B, Hq, Hkv, N, W, scale, pool_k, score, ws, st);
+    if (d == 128)
+        return run_snapkv<float, 128>(q, k, L, B, Hq, Hkv, N, W, scale, pool_k, score, ws, persistent, st);
+    return run_snapkv<float, 64>(q, k, L, B, Hq, Hkv, N, W, scale, pool_k, score, ws, persistent, st);
 }
 
 }  // namespace kve
