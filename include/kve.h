@@ -88,13 +88,17 @@ size_t kve_snapkv_workspace_size(int L, int B, int Hq, int Hkv, int N, int W, in
  *   score  [L, B, Hkv, N] float32 output (device)
  *
  * Requires 1 <= W <= N, G*W <= 1024.  Scores are accumulated in float32 from
- * products of the input type; the softmax subtracts each row's maximum before
- * exponentiating (per key chunk, merged exactly across chunks).
+ * products of the input type; each row's softmax is taken relative to a
+ * running reference that is raised to the largest logit seen whenever a
+ * partial sum would leave [0, 2^64], so no exponential overflows and the
+ * per-chunk sums merge exactly.
  *
- * The first 4 bytes of the workspace receive a device status word: nonzero
- * after the call has run means an internal wait of the persistent kernel
- * timed out (it cannot when the GPU runs nothing else that starves it) and the
- * scores must not be used.
+ * The workspace (kve_snapkv_workspace_size bytes, 256-byte aligned, owned by
+ * the caller) holds per-row statistics and per-key partial sums; its contents
+ * on entry do not matter.  Errors: KVE_ERR_INVALID_ARG (null pointers, bad
+ * shapes, even pool_k, negative or non-finite scale), KVE_ERR_UNSUPPORTED
+ * (d not 64/128, G*W > 1024, grid too large), KVE_ERR_WORKSPACE (too small),
+ * KVE_ERR_HIP (launch failure).  Kernels run asynchronously on `stream`.
  */
 kve_status_t kve_snapkv_score(const void* q_win, const void* k, kve_dtype_t dtype,
                               int L, int B, int Hq, int Hkv, int N, int W, int d,

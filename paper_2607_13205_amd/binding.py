@@ -3,8 +3,10 @@
 Every step of the eviction path runs in the HIP library; this module only
 checks tensor shapes against the C ABI, allocates outputs and workspaces with
 torch when the caller does not pass them, and forwards raw device pointers and
-the current HIP stream.  There is no fallback: if the library is missing the
-import fails.
+the current HIP stream.  There is no fallback: the first call into the
+library (any entry point below) raises ImportError if libkve.so is missing.
+The library is opened on first use, so that the package (and its build
+module) can be imported before the library is built.
 """
 
 from __future__ import annotations
@@ -73,7 +75,18 @@ def _load():
     return lib
 
 
-LIB = _load()
+class _Lib:
+    """libkve.so, opened on first attribute access."""
+
+    _cdll = None
+
+    def __getattr__(self, name):
+        if _Lib._cdll is None:
+            _Lib._cdll = _load()
+        return getattr(_Lib._cdll, name)
+
+
+LIB = _Lib()
 
 
 def last_error() -> str:

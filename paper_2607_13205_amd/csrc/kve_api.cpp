@@ -98,13 +98,8 @@ kve_status_t kve_snapkv_score(const void* q_win, const void* k, kve_dtype_t dtyp
                     p.total);
     if (!aligned(workspace)) return fail(KVE_ERR_INVALID_ARG, "%s: workspace not 256-byte aligned", fn);
     if (scale == 0.0f) scale = 1.0f / std::sqrt((float)d);
-    // KVE_SNAPKV_PATH=persistent selects the persistent single-read kernel
-    // (when the shape fits one cooperative grid); the default is the streaming
-    // two-pass kernels, which measure faster.
-    const char* path = std::getenv("KVE_SNAPKV_PATH");
-    const bool persistent = path != nullptr && std::strcmp(path, "persistent") == 0;
-    return from_hip(kve::launch_snapkv(q_win, k, (int)dtype, L, B, Hq, Hkv, N, W, d, scale, pool_k,
-                                       score, workspace, persistent, static_cast<hipStream_t>(stream)),
+    return from_hip(kve::launch_snapkv(q_win, k, (int)dtype, L, B, Hq, Hkv, N, W, d, scale, pool_k, score,
+                                       workspace, static_cast<hipStream_t>(stream)),
                     fn);
 }
 

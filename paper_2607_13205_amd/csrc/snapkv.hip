@@ -13,16 +13,18 @@
 // four-slot LDS ring in chunks of 64 with direct-to-LDS loads issued three
 // chunks ahead, so every wave keeps HBM requests in flight while it multiplies
 // on the matrix cores (bf16 32x32x16, fp32 32x32x2).  No workgroup waits on
-// another one.
+// another one; two workgroups share a compute unit, so that one's matrix-core
+// work overlaps the other's exponentials.
 //
 //   pass 1   snap_pass1    S^T = K Q^T: each lane holds one row and 16 keys per
-//                          block, so the running row max and sum of
-//                          exp2(x - max) stay in the lane; one log-sum-exp
-//                          per (vseg, range, row) is written.
+//                          32-key block, so the running row sum of
+//                          exp2(x - ref) stays in the lane; one log-sum-exp per
+//                          (vseg, range, row) is written.
 //   combine  snap_combine  per row: lse2 over the ranges (+inf for padding rows).
-//   pass 2   snap_pass2    S = Q K^T: each lane holds one key and 16 rows, so
-//                          the column sum of exp2(x - lse2) is a lane sum plus
-//                          one shuffle; the four row blocks add through LDS.
+//   pass 2   snap_pass2    S = Q K^T: each lane holds one key and 16 rows per
+//                          block, so the column sum of exp2(x - lse2) is a lane
+//                          sum plus one shuffle; the four row blocks (waves)
+//                          add through LDS and each chunk's 64 sums go out.
 //   pool     snap_pool     adds the row groups and max-pools the prefix.
 //
 // Logits are kept in log2 units (x = scale * log2(e) * <q, k>) so that every
@@ -34,26 +36,22 @@
 namespace kve {
 namespace {
 
-constexpr int kThreads = 256;  // four waves
 constexpr int kWaves = 4;
-constexpr int kRing = 4;       // LDS chunk slots: the chunk in use and three ahead
+constexpr int kThreads = kWaves * 64;
+constexpr int kKeys = kSnapChunkKeys;  // keys per chunk
+constexpr int kRing = 4;               // LDS slots: the chunk in use and three ahead
 constexpr int kPoolTile = 256;
 constexpr int kMaxPoolHalf = 127;
 
-// Wait until this wave's loads of the current chunk have landed, while the
-// loads of up to `ahead` later chunks stay in flight.
-template <int LPW>
-__device__ __forceinline__ void wait_chunk(int ahead) {
-    if (ahead >= 2)
-        wait_vmcnt<2 * LPW>();
-    else if (ahead == 1)
-        wait_vmcnt<LPW>();
-    else
-        wait_vmcnt<0>();
-}
+template <typename T, int D>
+struct Geo {
+    using C = KChunk<T, D, kKeys>;
+    using Rd = ChunkReader<T, D, kKeys>;
+    using Wr = ChunkWriter<T, D, kKeys, kWaves>;
+};
 
 struct Span {
-    int vseg, seg, rg, range, t_begin, t_end, nsub;
+    int vseg, seg, rg, range, t_begin, t_end, nch;
 };
 
 __device__ __forceinline__ Span span_of(int nranges, int rgroups, int range_keys, int N) {
@@ -64,25 +62,97 @@ __device__ __forceinline__ Span span_of(int nranges, int rgroups, int range_keys
     s.rg = s.vseg - s.seg * rgroups;
     s.t_begin = s.range * range_keys;
     s.t_end = min(N, s.t_begin + range_keys);
-    s.nsub = (s.t_end - s.t_begin + kChunkKeys - 1) / kChunkKeys;
+    s.nch = (s.t_end - s.t_begin + kKeys - 1) / kKeys;
     return s;
 }
 
+// Query fragments of this wave's 32-row block (zero for padding rows).
 template <typename T, int D>
-__device__ __forceinline__ void load_q(QFrag<T, D>& qf, const T* q, int seg, int rows, int row) {
+using QRows = typename Mma<T>::frag[Geo<T, D>::C::NSTEP];
+
+template <typename T, int D>
+__device__ __forceinline__ void load_q(QRows<T, D>& qf, const T* q, int seg, int rows, int row, int lane) {
     using M = Mma<T>;
-    const int lane = threadIdx.x & 63;
     const T* base = q + ((size_t)seg * rows + row) * D;
 #pragma unroll
-    for (int s = 0; s < KChunk<T, D>::NSTEP; ++s)
-        qf[s] = row < rows ? M::load(base, s * M::KSTEP + (lane >> 5) * M::KPL) : M::zero();
+    for (int st = 0; st < Geo<T, D>::C::NSTEP; ++st) {
+        qf[st] = row < rows ? M::load(base, st * M::KSTEP + (lane >> 5) * M::KPL) : M::zero();
+        pin(qf[st]);
+    }
 }
 
 template <typename T, int D>
-__device__ __forceinline__ void issue_chunk(char* ring, const char* kseg, const Span& sp, int s) {
-    const int t0 = sp.t_begin + s * kChunkKeys;
-    chunk_stream<T, D, kWaves>(ring + (s % kRing) * KChunk<T, D>::BYTES, kseg + (size_t)t0 * KChunk<T, D>::ROW,
-                               sp.t_end - t0, threadIdx.x >> 6, threadIdx.x & 63);
+struct Stream {
+    using G = Geo<T, D>;
+    typename G::Wr wr;
+    const char* kseg;
+    int t_begin, t_end, nch;
+
+    __device__ __forceinline__ void open(const T* k, const Span& sp, int N, int wave, int lane) {
+        wr.init(wave, lane);
+        kseg = reinterpret_cast<const char*>(k) + (size_t)sp.seg * N * G::C::ROW;
+        t_begin = sp.t_begin;
+        t_end = sp.t_end;
+        nch = sp.nch;
+    }
+    __device__ __forceinline__ void issue(char* ring, int c, int slot) const {
+        const int t0 = t_begin + c * kKeys;
+        wr.issue(ring + slot * G::C::BYTES, kseg + (size_t)t0 * G::C::ROW, t_end - t0);
+    }
+    __device__ __forceinline__ void prologue(char* ring) const {
+        for (int c = 0; c < min(kRing - 1, nch); ++c) issue(ring, c, c);
+    }
+    // Before step s (slot u = s % kRing): wait for this wave's loads of chunk
+    // s, publish it with the barrier, then refill the slot of chunk s - 1
+    // (read by every wave before the barrier) with chunk s + kRing - 1.
+    __device__ __forceinline__ void advance(char* ring, int s, int u) const {
+        wait_chunk<G::Wr::LPW, kRing - 2>(min(kRing - 2, nch - 1 - s));
+        lds_barrier();
+        if (s + kRing - 1 < nch) issue(ring, s + kRing - 1, (u + kRing - 1) % kRing);
+    }
+};
+
+// Products of one chunk with this wave's 32 query rows: two 32-key blocks,
+// two independent accumulation chains.  KEYS_A: keys are the A operand
+// (S^T = K Q^T, lane = query row); otherwise the query rows are (S = Q K^T,
+// lane = key).  The accumulators start at zero or, with `init` (Q K^T only),
+// at init[c_row(i)] for element i: rows c_row(4 a .. 4 a + 3) are consecutive.
+template <typename T, int D, bool KEYS_A>
+__device__ __forceinline__ void chunk_mma(f32x16 (&acc)[2], const typename Geo<T, D>::Rd& rd, const char* slot,
+                                          const QRows<T, D>& qf, const float* init, int lane) {
+    using M = Mma<T>;
+    f32x16 c0;
+    if (init == nullptr) {
+        c0 = f32x16{};
+    } else {
+#pragma unroll
+        for (int a = 0; a < 4; ++a) {
+            const float4 v = *reinterpret_cast<const float4*>(init + c_row(4 * a, lane));
+            c0[4 * a] = v.x;
+            c0[4 * a + 1] = v.y;
+            c0[4 * a + 2] = v.z;
+            c0[4 * a + 3] = v.w;
+        }
+    }
+#pragma unroll
+    for (int st = 0; st < Geo<T, D>::C::NSTEP; ++st) {
+        const typename M::frag kf[2] = {rd.get(slot, 0, st), rd.get(slot, 1, st)};
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb) {
+            const f32x16 c = st == 0 ? c0 : acc[kb];
+            acc[kb] = KEYS_A ? M::mma(kf[kb], qf[st], c) : M::mma(qf[st], kf[kb], c);
+        }
+    }
+    if constexpr (Geo<T, D>::Rd::kTable) {
+        // keep the fragment reads two k-steps ahead of the products
+        constexpr int NS = Geo<T, D>::C::NSTEP;
+        __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);  // LDS reads of steps 0, 1
+#pragma unroll
+        for (int st = 0; st < NS; ++st) {
+            __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);  // products of step st
+            if (st + 2 < NS) __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);  // reads of step st + 2
+        }
+    }
 }
 
 template <typename T, int D>
@@ -90,84 +160,97 @@ __global__ __launch_bounds__(kThreads, 2) void snap_pass1(const T* __restrict__ 
                                                           int N, int W, int rows, int rgroups, int nranges,
                                                           int range_keys, float sl2,
                                                           float* __restrict__ stats) {
-    using C = KChunk<T, D>;
-    using M = Mma<T>;
-    constexpr int LPW = chunk_loads_per_wave<T, D, kWaves>();
-    __shared__ __align__(16) char ring[kRing][C::BYTES];
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    using G = Geo<T, D>;
+    __shared__ __align__(16) char ring[kRing * G::C::BYTES];
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const Span sp = span_of(nranges, rgroups, range_keys, N);
     const int P_rows = N - W;
-    const char* kseg = reinterpret_cast<const char*>(k) + (size_t)sp.seg * N * C::ROW;
 
-    QFrag<T, D> qf;
-    const int qr = sp.rg * 128 + wave * 32 + (lane & 31);  // this lane's query row
-    load_q<T, D>(qf, q, sp.seg, rows, qr);
-    const int lim = qr < rows ? P_rows + (qr % W) : -1;
-    drain_loads();
+    QRows<T, D> qf;
+    const int qr = sp.rg * kSnapRowsPerGroup + wave * 32 + (lane & 31);  // this lane's query row
+    load_q<T, D>(qf, q, sp.seg, rows, qr, lane);
+    const int lim = qr < rows ? P_rows + qr % W : -1;  // last key the row sees
+    typename G::Rd rd;
+    rd.init(lane, 0);
+    Stream<T, D> str;
+    str.open(k, sp, N, wave, lane);
+    str.prologue(ring);
 
-    for (int s = 0; s < min(kRing - 1, sp.nsub); ++s) issue_chunk<T, D>(&ring[0][0], kseg, sp, s);
-
-    float m2 = -INFINITY, l = 0.0f;  // running max (log2 units) and sum of this lane's keys
-    for (int s = 0; s < sp.nsub; ++s) {
-        wait_chunk<LPW>(min(kRing - 2, sp.nsub - 1 - s));
-        lds_barrier();
-        if (s + kRing - 1 < sp.nsub) issue_chunk<T, D>(&ring[0][0], kseg, sp, s + kRing - 1);
-        const char* buf = ring[s % kRing];
-        const int t0 = sp.t_begin + s * kChunkKeys;
-        float x[2][16];
+    // Reference m (log2 units) and sum l of exp2(x - m) over this lane's keys.
+    // m is raised only when a chunk's partial sum leaves [0, 2^64] (a key more
+    // than 64 above m, no reference yet, or masked keys before the first
+    // one); m is then the largest logit seen so far, so nothing overflows or
+    // loses precision.
+    float m = -INFINITY, l = 0.0f;
+    for (int s0 = 0; s0 < sp.nch; s0 += kRing) {
 #pragma unroll
-        for (int j = 0; j < 2; ++j) {
-            f32x16 acc = {};
-            const int r = 32 * j + (lane & 31);
+        for (int u = 0; u < kRing; ++u) {
+            const int s = s0 + u;
+            if (s >= sp.nch) break;
+            str.advance(ring, s, u);
+            f32x16 acc[2];
+            chunk_mma<T, D, true>(acc, rd, ring + u * G::C::BYTES, qf, nullptr, lane);
+            if (sp.t_begin + (s + 1) * kKeys > P_rows) {  // keys past the range end or inside the causal window
+                // key of element (kb, i) = base + 32 kb + 8 (i / 4) + i % 4
+                const int last = min(lim, sp.t_end - 1) - (sp.t_begin + s * kKeys + 4 * (lane >> 5));
 #pragma unroll
-            for (int st = 0; st < C::NSTEP; ++st)
-                acc = M::mma(chunk_frag<T, D>(buf, r, st * M::KSTEP + (lane >> 5) * M::KPL), qf[st], acc);
+                for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-            for (int i = 0; i < 16; ++i) x[j][i] = acc[i];
-        }
-        if (t0 + kChunkKeys > P_rows) {  // keys past N or inside the causal window
+                    for (int i = 0; i < 16; ++i)
+                        if (32 * kb + 8 * (i >> 2) + (i & 3) > last) acc[kb][i] = -INFINITY;
+            }
+            // exponentials side by side, then a tree of sums
+            f32x16 ex[2];
 #pragma unroll
-            for (int j = 0; j < 2; ++j)
+            for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-                for (int i = 0; i < 16; ++i) {
-                    const int t = t0 + 32 * j + c_row(i, lane);
-                    if (!(t < sp.t_end && t <= lim)) x[j][i] = -INFINITY;
+                for (int i = 0; i < 16; ++i) ex[kb][i] = fast_exp2(fmaf(acc[kb][i], sl2, -m));
+            float part[4];
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+                part[e] = (ex[0][e] + ex[0][e + 4]) + (ex[0][e + 8] + ex[0][e + 12]) +
+                          ((ex[1][e] + ex[1][e + 4]) + (ex[1][e + 8] + ex[1][e + 12]));
+            const float ln = l + ((part[0] + part[1]) + (part[2] + part[3]));
+            if (ln <= 0x1p64f) {  // false for inf and NaN
+                l = ln;
+            } else {  // new reference: the largest logit so far
+                float mx = -INFINITY;
+#pragma unroll
+                for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+                    for (int i = 0; i < 16; ++i) mx = fmaxf(mx, acc[kb][i]);
+                const float mn = fmaxf(m, mx * sl2);
+                if (mn != -INFINITY) {
+                    float a = l * fast_exp2(m - mn);
+#pragma unroll
+                    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+                        for (int i = 0; i < 16; ++i) a += fast_exp2(fmaf(acc[kb][i], sl2, -mn));
+                    l = a;
+                    m = mn;
                 }
-        }
-        float mx = -INFINITY;
-#pragma unroll
-        for (int j = 0; j < 2; ++j)
-#pragma unroll
-            for (int i = 0; i < 16; i += 2) mx = fmaxf(mx, fmaxf(x[j][i], x[j][i + 1]));
-        const float mn = fmaxf(m2, mx * sl2);
-        if (mn != -INFINITY) {
-            float acc = l * fast_exp2(m2 - mn);
-#pragma unroll
-            for (int j = 0; j < 2; ++j)
-#pragma unroll
-                for (int i = 0; i < 16; ++i) acc += fast_exp2(fmaf(x[j][i], sl2, -mn));
-            l = acc;
-            m2 = mn;
+            }
         }
     }
     // the two lane halves hold the same row and different keys
-    lse2_merge(m2, l, __shfl_xor(m2, 32), __shfl_xor(l, 32));
+    lse2_merge(m, l, __shfl_xor(m, 32), __shfl_xor(l, 32));
     if (lane < 32)
-        stats[((size_t)sp.vseg * nranges + sp.range) * 128 + wave * 32 + lane] =
-            (m2 != -INFINITY && l > 0.0f) ? m2 + log2f(l) : -INFINITY;
+        stats[((size_t)sp.vseg * nranges + sp.range) * kSnapRowsPerGroup + wave * 32 + lane] =
+            (m != -INFINITY && l > 0.0f) ? m + log2f(l) : -INFINITY;
 }
 
-__global__ __launch_bounds__(128) void snap_combine(const float* __restrict__ stats, int nranges, int rows,
-                                                    int rgroups, float* __restrict__ lse) {
+__global__ __launch_bounds__(kSnapRowsPerGroup) void snap_combine(const float* __restrict__ stats, int nranges,
+                                                                  int rows, int rgroups, float* __restrict__ lse) {
     const int vseg = blockIdx.x, r = threadIdx.x;
-    const int row = (vseg % rgroups) * 128 + r;
+    const int row = (vseg % rgroups) * kSnapRowsPerGroup + r;
     float a = -INFINITY, b = 0.0f;
     for (int c = 0; c < nranges; ++c) {
-        const float v = stats[((size_t)vseg * nranges + c) * 128 + r];
+        const float v = stats[((size_t)vseg * nranges + c) * kSnapRowsPerGroup + r];
         lse2_merge(a, b, v, v == -INFINITY ? 0.0f : 1.0f);
     }
     // rows past the window rows contribute nothing to the column sums
-    lse[(size_t)vseg * 128 + r] = (row < rows && b > 0.0f) ? a + log2f(b) : INFINITY;
+    lse[(size_t)vseg * kSnapRowsPerGroup + r] = (row < rows && b > 0.0f) ? a + log2f(b) : INFINITY;
 }
 
 template <typename T, int D>
@@ -176,75 +259,90 @@ __global__ __launch_bounds__(kThreads, 2) void snap_pass2(const T* __restrict__ 
                                                           int range_keys, float sl2,
                                                           const float* __restrict__ lse, int segs,
                                                           float* __restrict__ raw) {
-    using C = KChunk<T, D>;
-    using M = Mma<T>;
-    constexpr int LPW = chunk_loads_per_wave<T, D, kWaves>();
-    __shared__ __align__(16) char ring[kRing][C::BYTES];
-    __shared__ float scol[2][kWaves][kChunkKeys];
-    __shared__ float sraw[kSnapMaxRange];
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    using G = Geo<T, D>;
+    __shared__ __align__(16) char ring[kRing * G::C::BYTES];
+    __shared__ float scol[2][kWaves][kKeys];                   // column sums per row block, two chunks
+    __shared__ __align__(16) float sinit[kSnapRowsPerGroup];  // -lse / sl2 of each row
+    __shared__ __align__(16) int swin[kSnapRowsPerGroup];     // window index (row % W) of each row
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const Span sp = span_of(nranges, rgroups, range_keys, N);
     const int P_rows = N - W;
-    const char* kseg = reinterpret_cast<const char*>(k) + (size_t)sp.seg * N * C::ROW;
 
-    QFrag<T, D> qf;
-    const int row0 = sp.rg * 128 + wave * 32;
-    load_q<T, D>(qf, q, sp.seg, rows, row0 + (lane & 31));
-    float l2[16];
-#pragma unroll
-    for (int i = 0; i < 16; ++i) l2[i] = lse[(size_t)sp.vseg * 128 + wave * 32 + c_row(i, lane)];
-    drain_loads();
+    // The products start from -lse / sl2 of their row, so that sl2 * acc is
+    // x - lse2 directly (the accumulator is float32: the offset costs no
+    // precision that matters); padding rows (lse = +inf) start at -inf and add
+    // exactly 0.  Per-row values live in LDS: as registers they would stay
+    // live across the whole loop.
+    if (threadIdx.x < kSnapRowsPerGroup) {
+        sinit[threadIdx.x] = -lse[(size_t)sp.vseg * kSnapRowsPerGroup + threadIdx.x] / sl2;
+        swin[threadIdx.x] = (sp.rg * kSnapRowsPerGroup + (int)threadIdx.x) % W;
+    }
+    QRows<T, D> qf;
+    load_q<T, D>(qf, q, sp.seg, rows, sp.rg * kSnapRowsPerGroup + wave * 32 + (lane & 31), lane);
+    typename G::Rd rd;
+    rd.init(lane, 0);
+    Stream<T, D> str;
+    str.open(k, sp, N, wave, lane);
+    str.prologue(ring);
+    float* out = raw + ((size_t)sp.rg * segs + sp.seg) * N;
 
-    for (int s = 0; s < min(kRing - 1, sp.nsub); ++s) issue_chunk<T, D>(&ring[0][0], kseg, sp, s);
-
-    for (int s = 0; s < sp.nsub; ++s) {
-        wait_chunk<LPW>(min(kRing - 2, sp.nsub - 1 - s));
-        lds_barrier();
-        if (s + kRing - 1 < sp.nsub) issue_chunk<T, D>(&ring[0][0], kseg, sp, s + kRing - 1);
-        if (s >= 1 && tid < kChunkKeys) {
-            const float* c = &scol[(s - 1) & 1][0][tid];
-            sraw[(s - 1) * kChunkKeys + tid] =
-                (c[0] + c[kChunkKeys]) + (c[2 * kChunkKeys] + c[3 * kChunkKeys]);
+    // add the four row blocks of chunk s (every wave has written it); each wave
+    // adds 16 of the 64 keys and writes them out
+    auto reduce = [&](int s) {
+        if (lane < kKeys / kWaves) {
+            const int key = wave * (kKeys / kWaves) + lane;
+            const int t = sp.t_begin + s * kKeys + key;
+            const float* c = &scol[s & 1][0][key];
+            if (t < sp.t_end) out[t] = (c[0] + c[kKeys]) + (c[2 * kKeys] + c[3 * kKeys]);
         }
-        const char* buf = ring[s % kRing];
-        const int t0 = sp.t_begin + s * kChunkKeys;
-        const bool full = t0 + kChunkKeys <= P_rows;
+    };
+    for (int s0 = 0; s0 < sp.nch; s0 += kRing) {
 #pragma unroll
-        for (int j = 0; j < 2; ++j) {
-            f32x16 acc = {};
-            const int r = 32 * j + (lane & 31);
+        for (int u = 0; u < kRing; ++u) {
+            const int s = s0 + u;
+            if (s >= sp.nch) break;
+            // the barrier inside also orders the scol writes of chunk s - 1
+            // before their sum, and that sum before chunk s + 1 reuses the buffer
+            str.advance(ring, s, u);
+            if (s >= 1) reduce(s - 1);
+            f32x16 acc[2];
+            chunk_mma<T, D, false>(acc, rd, ring + u * G::C::BYTES, qf, sinit + wave * 32, lane);
+            if (sp.t_begin + (s + 1) * kKeys > P_rows) {  // keys past the range end or inside the causal window
+                // key t is visible to window query i (position P_rows + i) iff t - P_rows <= i
 #pragma unroll
-            for (int st = 0; st < C::NSTEP; ++st)
-                acc = M::mma(qf[st], chunk_frag<T, D>(buf, r, st * M::KSTEP + (lane >> 5) * M::KPL), acc);
-            float col = 0.0f;
-            if (full) {
+                for (int a = 0; a < 4; ++a) {
+                    const int4 w4 = *reinterpret_cast<const int4*>(&swin[wave * 32 + c_row(4 * a, lane)]);
+                    const int wv[4] = {w4.x, w4.y, w4.z, w4.w};
 #pragma unroll
-                for (int i = 0; i < 16; ++i) col += fast_exp2(fmaf(acc[i], sl2, -l2[i]));
-            } else {
-                const int t = t0 + r;
+                    for (int kb = 0; kb < 2; ++kb) {
+                        const int t = sp.t_begin + s * kKeys + 32 * kb + (lane & 31);
 #pragma unroll
-                for (int i = 0; i < 16; ++i) {
-                    const int row = row0 + c_row(i, lane);
-                    const bool ok = t < sp.t_end && row < rows && t <= P_rows + (row % W);
-                    col += ok ? fast_exp2(fmaf(acc[i], sl2, -l2[i])) : 0.0f;
+                        for (int e = 0; e < 4; ++e)
+                            if (!(t < sp.t_end && t - P_rows <= wv[e])) acc[kb][4 * a + e] = -INFINITY;
+                    }
                 }
             }
-            col += __shfl_xor(col, 32);
-            if (lane < 32) scol[s & 1][wave][32 * j + lane] = col;
+            // exponentials in place (the logits are not needed again), then a
+            // tree of sums over the lane's 16 rows and one shuffle for the other 16
+#pragma unroll
+            for (int kb = 0; kb < 2; ++kb) {
+#pragma unroll
+                for (int i = 0; i < 16; ++i) acc[kb][i] = fast_exp2(acc[kb][i] * sl2);
+                const float c = ((acc[kb][0] + acc[kb][1]) + (acc[kb][2] + acc[kb][3]) +
+                                 ((acc[kb][4] + acc[kb][5]) + (acc[kb][6] + acc[kb][7]))) +
+                                (((acc[kb][8] + acc[kb][9]) + (acc[kb][10] + acc[kb][11])) +
+                                 ((acc[kb][12] + acc[kb][13]) + (acc[kb][14] + acc[kb][15])));
+                const float v = c + __shfl_xor(c, 32);
+                if (lane < 32) scol[s & 1][wave][32 * kb + lane] = v;
+            }
         }
     }
     __syncthreads();
-    if (tid < kChunkKeys) {
-        const int s = sp.nsub - 1;
-        const float* c = &scol[s & 1][0][tid];
-        sraw[s * kChunkKeys + tid] = (c[0] + c[kChunkKeys]) + (c[2 * kChunkKeys] + c[3 * kChunkKeys]);
-    }
-    __syncthreads();
-    float* out = raw + ((size_t)sp.rg * segs + sp.seg) * N + sp.t_begin;
-    for (int e = tid; e < sp.t_end - sp.t_begin; e += kThreads) out[e] = sraw[e];
+    reduce(sp.nch - 1);
 }
 
-__global__ __launch_bounds__(kPoolTile) void snap_pool(const float* __restrict__ raw, int rgroups,
+__global__ __launch_bounds__(kPoolTile) void snap_pool(const float* __restrict__ raw, int planes,
                                                        int segs, int N, int W, int pool_k, int tiles,
                                                        float* __restrict__ score) {
     __shared__ float ss[kPoolTile + 2 * kMaxPoolHalf];
@@ -258,7 +356,7 @@ __global__ __launch_bounds__(kPoolTile) void snap_pool(const float* __restrict__
         float s = -INFINITY;
         if (u >= 0 && u < N) {
             s = 0.0f;
-            for (int rg = 0; rg < rgroups; ++rg) s += raw[((size_t)rg * segs + seg) * N + u];
+            for (int pl = 0; pl < planes; ++pl) s += raw[((size_t)pl * segs + seg) * N + u];
         }
         ss[e] = s;
     }
@@ -278,7 +376,7 @@ __global__ __launch_bounds__(kPoolTile) void snap_pool(const float* __restrict__
 
 template <typename T, int D>
 hipError_t run_snapkv(const void* q, const void* k, int L, int B, int Hq, int Hkv, int N, int W,
-                      float scale, int pool_k, float* score, void* ws, bool persistent, hipStream_t st) {
+                      float scale, int pool_k, float* score, void* ws, hipStream_t st) {
     const SnapPlan p = snap_plan(L, B, Hq, Hkv, N, W, D);
     char* w = static_cast<char*>(ws);
     float* stats = reinterpret_cast<float*>(w + p.off_stats);
@@ -287,24 +385,16 @@ hipError_t run_snapkv(const void* q, const void* k, int L, int B, int Hq, int Hk
     const float sl2 = scale * kLog2e;
     const T* qt = static_cast<const T*>(q);
     const T* kt = static_cast<const T*>(k);
-    bool used = false;
-    if (persistent) {
-        const hipError_t e = launch_snapkv_fused(q, k, sizeof(T) == 2 ? 0 : 1, L, B, Hq, Hkv, N, W, D, scale,
-                                                 raw, ws, st, &used);
-        if (e != hipSuccess) return e;
-    }
-    if (!used) {
-        const dim3 grid((unsigned)((size_t)p.n_vsegs * p.nranges));
-        hipLaunchKernelGGL((snap_pass1<T, D>), grid, dim3(kThreads), 0, st, qt, kt, N, W, p.rows, p.rgroups,
-                           p.nranges, p.range_keys, sl2, stats);
-        hipLaunchKernelGGL(snap_combine, dim3((unsigned)p.n_vsegs), dim3(128), 0, st, stats, p.nranges, p.rows,
-                           p.rgroups, lse);
-        hipLaunchKernelGGL((snap_pass2<T, D>), grid, dim3(kThreads), 0, st, qt, kt, N, W, p.rows, p.rgroups,
-                           p.nranges, p.range_keys, sl2, lse, p.segs, raw);
-    }
+    const dim3 grid((unsigned)((size_t)p.n_vsegs * p.nranges));
+    hipLaunchKernelGGL((snap_pass1<T, D>), grid, dim3(kThreads), 0, st, qt, kt, N, W, p.rows, p.rgroups,
+                       p.nranges, p.range_keys, sl2, stats);
+    hipLaunchKernelGGL(snap_combine, dim3((unsigned)p.n_vsegs), dim3(kSnapRowsPerGroup), 0, st, stats,
+                       p.nranges, p.rows, p.rgroups, lse);
+    hipLaunchKernelGGL((snap_pass2<T, D>), grid, dim3(kThreads), 0, st, qt, kt, N, W, p.rows, p.rgroups,
+                       p.nranges, p.range_keys, sl2, lse, p.segs, raw);
     const int tiles = (N + kPoolTile - 1) / kPoolTile;
-    hipLaunchKernelGGL(snap_pool, dim3((unsigned)(p.segs * tiles)), dim3(kPoolTile), 0, st, raw,
-                       p.rgroups, p.segs, N, W, pool_k, tiles, score);
+    hipLaunchKernelGGL(snap_pool, dim3((unsigned)(p.segs * tiles)), dim3(kPoolTile), 0, st, raw, p.planes,
+                       p.segs, N, W, pool_k, tiles, score);
     return hipGetLastError();
 }
 
@@ -312,15 +402,13 @@ hipError_t run_snapkv(const void* q, const void* k, int L, int B, int Hq, int Hk
 
 hipError_t launch_snapkv(const void* q, const void* k, int dtype, int L, int B, int Hq, int Hkv,
                          int N, int W, int d, float scale, int pool_k, float* score, void* ws,
-                         bool persistent, hipStream_t st) {
+                         hipStream_t st) {
     if (dtype == 0) {
-        if (d == 128)
-            return run_snapkv<__bf16, 128>(q, k, L, B, Hq, Hkv, N, W, scale, pool_k, score, ws, persistent, st);
-        return run_snapkv<__bf16, 64>(q, k, L, B, Hq, Hkv, N, W, scale, pool_k, score, ws, persistent, st);
+        if (d == 128) return run_snapkv<__bf16, 128>(q, k, L, B, Hq, Hkv, N, W, scale, pool_k, score, ws, st);
+        return run_snapkv<__bf16, 64>(q, k, L, B, Hq, Hkv, N, W, scale, pool_k, score, ws, st);
     }
-    if (d == 128)
-        return run_snapkv<float, 128>(q, k, L, B, Hq, Hkv, N, W, scale, pool_k, score, ws, persistent, st);
-    return run_snapkv<float, 64>(q, k, L, B, Hq, Hkv, N, W, scale, pool_k, score, ws, persistent, st);
+    if (d == 128) return run_snapkv<float, 128>(q, k, L, B, Hq, Hkv, N, W, scale, pool_k, score, ws, st);
+    return run_snapkv<float, 64>(q, k, L, B, Hq, Hkv, N, W, scale, pool_k, score, ws, st);
 }
 
 }  // namespace kve
