@@ -13,11 +13,18 @@ second (a token counts once it has passed through all layers and KV heads);
 ``roofline`` refers to the SnapKV score call, timed with HIP events on the
 stream it is launched on; ``cpu_baseline`` times the float64 CPU oracle on a
 bounded sample of the same workload.
+
+``roofline.traffic`` is the measured HBM traffic of one score call, read from
+the counter summary in profiles/ (rocprofv3 FETCH_SIZE and WRITE_SIZE,
+scaled by what the same counters read for a plain device copy of known
+size); it is null when the kernel sources differ from the ones that summary
+was taken on.  ``python bench.py --calibrate-copy`` runs only that copy.
 """
 
 from __future__ import annotations
 
 import argparse
+import hashlib
 import json
 import math
 import os
@@ -29,6 +36,11 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 METRIC = "prefill tokens scored+compressed/s per GPU; % HBM peak (SnapKV), % MFMA (H2O)"
+TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "snapkv_score_stack32k_traffic.md")
+# sources of the kernels one score call launches
+SCORE_SOURCES = ("paper_2607_13205_amd/csrc/snapkv.hip", "paper_2607_13205_amd/csrc/kve_stream.h",
+                 "paper_2607_13205_amd/csrc/kve_device.h", "paper_2607_13205_amd/csrc/kve_internal.h")
+COPY_BYTES = 1 << 30
 HBM_PEAK_GBS = 8000.0
 BF16_MFMA_PEAK_TFLOPS = 2500.0
 
@@ -45,7 +57,50 @@ def parse():
                     help="target CPU time of the oracle baseline sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-h2o", action="store_true", help="skip the H2O scorer leg")
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="only run a plain device copy of 1 GiB (5 times), for counter calibration")
     return ap.parse_args()
+
+
+def score_sources_sha() -> str:
+    h = hashlib.sha256()
+    for rel in SCORE_SOURCES:
+        with open(os.path.join(ROOT, rel), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
+
+
+def measured_traffic(wl_name: str):
+    """HBM bytes per score call from the committed counter summary, or None when
+    it is missing, covers another workload, or was taken on other sources."""
+    try:
+        with open(TRAFFIC_SUMMARY) as f:
+            text = f.read()
+    except OSError:
+        return None
+    fields = {}
+    for line in text.splitlines():
+        line = line.strip().strip("`")
+        if line.startswith("- ") and ":" in line:
+            key, val = line[2:].split(":", 1)
+            fields[key.strip()] = val.strip().strip("`")
+    if fields.get("workload") != wl_name or fields.get("sources_sha256") != score_sources_sha():
+        return None
+    try:
+        return int(fields["traffic_bytes_per_call"])
+    except (KeyError, ValueError):
+        return None
+
+
+def calibrate_copy():
+    import torch
+    src = torch.ones(COPY_BYTES // 4, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    for _ in range(5):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"calibrate_copy_bytes_read": COPY_BYTES, "bytes_written": COPY_BYTES, "repeats": 5}))
 
 
 def snapkv_algorithmic_bytes(wl, elem=2):
@@ -143,6 +198,9 @@ def main():
         sys.exit(2)
     import torch
 
+    if args.calibrate_copy:
+        calibrate_copy()
+        return
     import workload as WL
     from paper_2607_13205_amd.build import ensure_built
     ensure_built()
@@ -215,7 +273,7 @@ def main():
         "roofline": {
             "kernel": "kve_snapkv_score (score passes + pool)",
             "bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-            "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+            "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": measured_traffic(wl.name),
             "ms": round(ms_score, 4), "algorithmic_bytes": score_bytes,
         },
     }
