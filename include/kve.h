@@ -121,7 +121,13 @@ size_t kve_h2o_workspace_size(int L, int B, int Hq, int Hkv, int N, int d);
  *   scale  0 selects 1/sqrt(d)
  *   score  [L, B, Hkv, N] float32 output (device)
  *
- * Two passes: per-row log-sum-exp over the causal row, then column sums.
+ * Two passes on the matrix cores: per-row log-sum-exp over the causal row,
+ * then column sums.  Requires Hq/Hkv <= 128.  The workspace
+ * (kve_h2o_workspace_size bytes, 256-byte aligned, owned by the caller) holds
+ * one float per (layer, sample, query head, row); its contents on entry do not
+ * matter.  Errors: KVE_ERR_INVALID_ARG (null pointers, bad shapes, negative or
+ * non-finite scale), KVE_ERR_UNSUPPORTED (d not 64/128, Hq/Hkv > 128, grid
+ * too large), KVE_ERR_WORKSPACE (too small), KVE_ERR_HIP (launch failure).
  */
 kve_status_t kve_h2o_score(const void* q, const void* k, kve_dtype_t dtype,
                            int L, int B, int Hq, int Hkv, int N, int d, float scale,

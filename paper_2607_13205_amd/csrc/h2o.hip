@@ -1,212 +1,225 @@
 // H2O accumulated attention score, the baseline scorer.
 //
-// Paper §2 (H2O family): s(t) = sum over prefill queries q of p_t(q), kept per
-// (layer, head); here summed over the G query heads of each KV head.
+// Paper §2 (H2O family): s(t) = sum over prefill queries i >= t of the causal
+// softmax weight p_i(t), kept per (layer, head); here summed over the G query
+// heads of each KV head.
 //
-// The causal QK^T is a dense contraction, so both passes run on the matrix
-// cores (bf16 32x32x16, fp32 32x32x2):
-//   h2o_rows  one workgroup per (query head, 128-row block): four waves own 32
-//             rows each (query fragments in registers) and stream the causal
-//             keys through LDS; per row m + log2(sum exp2(x - m)).
-//   h2o_cols  one workgroup per (KV head, 128-key block): four waves own 32 keys
-//             each (key fragments in registers) and stream every later query
-//             row of the G heads, with its log-sum-exp, through LDS; per key
-//             sum of exp2(x - lse2).
+// Both passes are the causal QK^T on the matrix cores (bf16 32x32x16, fp32
+// 32x32x2) with operands streamed through a four-slot LDS ring by direct-to-LDS
+// loads, as in the SnapKV kernels:
+//   h2o_pass1  one workgroup per (KV group, block of positions): its 128 rows
+//              are the G heads of the group at 128/G consecutive positions
+//              (position-major), query fragments in registers; the keys up to
+//              the block's last position stream through LDS and each lane
+//              keeps one row's running softmax denominator.  Writes
+//              -lse2/sl2 per row, the start value pass 2 needs, into rows of
+//              pitch NP = N rounded up to 64 floats per head.
+//   h2o_pass2  one workgroup per (KV group, 128-key block): four waves own 32
+//              keys each (key fragments in registers); every later query row
+//              of the G heads streams through LDS in 64-row chunks together
+//              with its -lse2/sl2, which starts the products, so that
+//              sl2 * acc = x - lse2 and each lane sums exp2 over its key's
+//              column directly.
 // Logits are in log2 units, x = scale * log2(e) * <q, k>.
 #include "kve_device.h"
 #include "kve_internal.h"
+#include "kve_stream.h"
 
 namespace kve {
 namespace {
 
-constexpr int kThreads = 256;
-constexpr int kTile = 64;  // keys (rows pass) or query rows (cols pass) per LDS tile
+constexpr int kWaves = 4;
+constexpr int kThreads = kWaves * 64;
+constexpr int kKeys = 64;  // rows per chunk (keys in pass 1, query rows in pass 2)
+constexpr int kRing = 4;
+constexpr int kKeyBlock = 128;  // keys per pass-2 workgroup
 
 template <typename T, int D>
-struct H2oShape {
-    static constexpr int ES = (int)sizeof(T);
-    static constexpr int ROW_BYTES = D * ES;
-    static constexpr int ROWB = ROW_BYTES + 16;
-    static constexpr int TILE_BYTES = kTile * ROW_BYTES;
-    static constexpr int NSTEP = D / Mma<T>::KSTEP;
+struct Geo {
+    using C = KChunk<T, D, kKeys>;
+    using Rd = ChunkReader<T, D, kKeys>;
+    using Wr = ChunkWriter<T, D, kKeys, kWaves>;
+    using Ring = ChunkRing<T, D, kKeys, kWaves, kRing>;
+    using Frags = typename Mma<T>::frag[C::NSTEP];
+};
+
+// Fragments of one row (key or query) of length D, zero when !valid.
+template <typename T, int D>
+__device__ __forceinline__ void load_row_frags(typename Geo<T, D>::Frags& f, const T* row, bool valid, int lane) {
+    using M = Mma<T>;
+#pragma unroll
+    for (int st = 0; st < Geo<T, D>::C::NSTEP; ++st) {
+        f[st] = valid ? M::load(row, st * M::KSTEP + (lane >> 5) * M::KPL) : M::zero();
+        pin(f[st]);
+    }
+}
+
+// Chunks of consecutive rows of one [N, D] matrix, from `first`.
+template <typename T, int D>
+struct RowChunks {
+    const char* base;
+    int first, end;
+    __device__ __forceinline__ void operator()(int c, const char** rows, int* valid) const {
+        const int r0 = first + c * kKeys;
+        *rows = base + (size_t)r0 * Geo<T, D>::C::ROW;
+        *valid = end - r0;
+    }
 };
 
 template <typename T, int D>
-using FragArr = typename Mma<T>::frag[H2oShape<T, D>::NSTEP];
-
-
-template <typename T, int D>
-__device__ __forceinline__ void stage_tile(char* dst, const T* src, int t0, int t_end) {
-    using S = H2oShape<T, D>;
-    for (int o = threadIdx.x * 16; o < S::TILE_BYTES; o += kThreads * 16) {
-        const int row = o / S::ROW_BYTES;
-        const int within = o - row * S::ROW_BYTES;
-        const int t = t0 + row;
-        u32x4 v = zero16();
-        if (t < t_end)
-            v = ld16(reinterpret_cast<const char*>(src) + (size_t)t * S::ROW_BYTES + within);
-        st16(dst + row * S::ROWB + within, v);
-    }
-}
-
-template <typename T, int D>
-__device__ __forceinline__ void load_frags(FragArr<T, D>& fr,
-                                           const T* base, int row, int nrows) {
-    using M = Mma<T>;
+__global__ __launch_bounds__(kThreads, 2) void h2o_pass1(const T* __restrict__ q, const T* __restrict__ k,
+                                                         int Hq, int Hkv, int N, int NP, int npos, int nblk,
+                                                         float sl2, float* __restrict__ linit) {
+    using G = Geo<T, D>;
+    __shared__ __align__(16) char ring[kRing * G::C::BYTES];
     const int lane = threadIdx.x & 63;
-#pragma unroll
-    for (int s = 0; s < H2oShape<T, D>::NSTEP; ++s) {
-        const int kb = s * M::KSTEP + (lane >> 5) * M::KPL;
-        fr[s] = row < nrows ? M::load(base + (size_t)row * D, kb) : M::zero();
-    }
-}
-
-template <typename T, int D>
-__global__ __launch_bounds__(kThreads) void h2o_rows(const T* __restrict__ q, const T* __restrict__ k,
-                                                     int Hq, int Hkv, int N, int nrb, float sl2,
-                                                     float* __restrict__ lse) {
-    using S = H2oShape<T, D>;
-    using M = Mma<T>;
-    __shared__ __align__(16) char sk[kTile * S::ROWB];
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int Gh = Hq / Hkv;
     int bid = blockIdx.x;
-    const int rb = nrb - 1 - bid % nrb;  // longest causal rows first
-    bid /= nrb;
-    const int hq = bid % Hq;
-    const int lb = bid / Hq;
-    const int G = Hq / Hkv;
-    const int j = hq / G;
-    const int row0 = rb * kH2oRowBlock + wave * 32;
-    const T* qh = q + ((size_t)lb * Hq + hq) * N * D;
-    const T* kj = k + ((size_t)lb * Hkv + j) * N * D;
+    const int pb = nblk - 1 - bid % nblk;  // longest causal rows first
+    bid /= nblk;
+    const int j = bid % Hkv;
+    const int lb = bid / Hkv;
+    const int p0 = pb * npos;
+    // this lane's row: head g of the group at position pos (position-major)
+    const int r = wave * 32 + (lane & 31);
+    const int g = r % Gh;
+    const int pos = p0 + r / Gh;
+    const bool valid = r < npos * Gh && pos < N;
+    const size_t head = (size_t)lb * Hq + (size_t)j * Gh + g;
 
-    typename M::frag qa[S::NSTEP];
-    load_frags<T, D>(qa, qh, row0 + (lane & 31), N);
-    float m[16], l[16];
+    typename G::Frags qf;
+    load_row_frags<T, D>(qf, q + (head * N + (valid ? pos : 0)) * D, valid, lane);
+    const int t_end = min(N, p0 + npos);  // keys up to the block's last position
+    const int nch = (t_end + kKeys - 1) / kKeys;
+    typename G::Rd rd;
+    rd.init(lane, 0);
+    typename G::Ring ring_io;
+    ring_io.open(nch, wave, lane);
+    const RowChunks<T, D> src{reinterpret_cast<const char*>(k) + ((size_t)lb * Hkv + j) * N * G::C::ROW, 0, t_end};
+    ring_io.prologue(ring, src);
+
+    const int lim = valid ? pos : -1;  // last key the row sees
+    RowSum rs;
+    for (int s0 = 0; s0 < nch; s0 += kRing) {
 #pragma unroll
-    for (int i = 0; i < 16; ++i) {
-        m[i] = -INFINITY;
-        l[i] = 0.0f;
-    }
-    const int t_end = min(N, rb * kH2oRowBlock + kH2oRowBlock);
-    for (int t0 = 0; t0 < t_end; t0 += kTile) {
-        __syncthreads();
-        stage_tile<T, D>(sk, kj, t0, t_end);
-        __syncthreads();
-        if (row0 >= N) continue;
+        for (int u = 0; u < kRing; ++u) {
+            const int s = s0 + u;
+            if (s >= nch) break;
+            ring_io.advance(ring, s, u, src);
+            f32x16 acc[2];
+            chunk_mma<T, D, kKeys, true>(acc, rd, ring + u * G::C::BYTES, qf, nullptr, lane);
+            if ((s + 1) * kKeys > p0) {  // a key of the chunk lies after some row of the block
+                // key of element (kb, i) = base + 32 kb + 8 (i / 4) + i % 4
+                const int last = lim - (s * kKeys + 4 * (lane >> 5));
 #pragma unroll
-        for (int cb = 0; cb < kTile / 32; ++cb) {
-            if (t0 + cb * 32 > row0 + 31) continue;  // every key of the block is after every row
-            f32x16 acc = {};
-            const char* krow = sk + (cb * 32 + (lane & 31)) * S::ROWB;
+                for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-            for (int s = 0; s < S::NSTEP; ++s)
-                acc = M::mma(qa[s], M::load(krow, s * M::KSTEP + (lane >> 5) * M::KPL), acc);
-            const int t = t0 + cb * 32 + (lane & 31);
-#pragma unroll
-            for (int i = 0; i < 16; ++i) {
-                const int r = row0 + c_row(i, lane);
-                const bool valid = r < N && t <= r;
-                const float x = valid ? acc[i] * sl2 : -INFINITY;
-                const float mn = fmaxf(m[i], x);
-                if (mn != -INFINITY) {
-                    l[i] = l[i] * fast_exp2(m[i] - mn) + fast_exp2(x - mn);
-                    m[i] = mn;
-                }
+                    for (int i = 0; i < 16; ++i)
+                        if (32 * kb + 8 * (i >> 2) + (i & 3) > last) acc[kb][i] = -INFINITY;
             }
+            rs.add(acc, sl2);
         }
     }
-#pragma unroll
-    for (int off = 1; off < 32; off <<= 1) {
-#pragma unroll
-        for (int i = 0; i < 16; ++i) {
-            const float mo = __shfl_xor(m[i], off);
-            const float lo = __shfl_xor(l[i], off);
-            lse2_merge(m[i], l[i], mo, lo);
-        }
-    }
-    if ((lane & 31) == 0) {
-        float* out = lse + ((size_t)lb * Hq + hq) * N;
-#pragma unroll
-        for (int i = 0; i < 16; ++i) {
-            const int r = row0 + c_row(i, lane);
-            if (r < N) out[r] = l[i] > 0.0f ? m[i] + log2f(l[i]) : -INFINITY;
-        }
-    }
+    // the two lane halves hold the same row and different keys
+    lse2_merge(rs.m, rs.l, __shfl_xor(rs.m, 32), __shfl_xor(rs.l, 32));
+    if (lane < 32 && valid) linit[head * NP + pos] = -rs.lse2() / sl2;
 }
 
 template <typename T, int D>
-__global__ __launch_bounds__(kThreads) void h2o_cols(const T* __restrict__ q, const T* __restrict__ k,
-                                                     const float* __restrict__ lse, int Hq, int Hkv,
-                                                     int N, int nkb, float sl2,
-                                                     float* __restrict__ score) {
-    using S = H2oShape<T, D>;
-    using M = Mma<T>;
-    __shared__ __align__(16) char sq[kTile * S::ROWB];
-    __shared__ float slse[kTile];
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+__global__ __launch_bounds__(kThreads, 2) void h2o_pass2(const T* __restrict__ q, const T* __restrict__ k,
+                                                         const float* __restrict__ linit, int Hq, int Hkv,
+                                                         int N, int NP, int nkb, float sl2,
+                                                         float* __restrict__ score) {
+    using G = Geo<T, D>;
+    __shared__ __align__(16) char ring[kRing * G::C::BYTES];
+    __shared__ __align__(16) float sli[kRing][kKeys];  // -lse2/sl2 of each chunk row
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int Gh = Hq / Hkv;
     int bid = blockIdx.x;
-    const int kb = bid % nkb;
+    const int kb = bid % nkb;  // key blocks near 0 have the most rows
     bid /= nkb;
     const int j = bid % Hkv;
     const int lb = bid / Hkv;
-    const int G = Hq / Hkv;
-    const int key0 = kb * kH2oKeyBlock + wave * 32;
-    const int my_key = key0 + (lane & 31);
-    const T* kj = k + ((size_t)lb * Hkv + j) * N * D;
+    const int kb0 = kb * kKeyBlock;
+    const int key = kb0 + wave * 32 + (lane & 31);
+    const size_t head0 = (size_t)lb * Hq + (size_t)j * Gh;
 
-    typename M::frag kf[S::NSTEP];
-    load_frags<T, D>(kf, kj, my_key, N);
+    typename G::Frags kf;
+    load_row_frags<T, D>(kf, k + (((size_t)lb * Hkv + j) * N + (key < N ? key : 0)) * D, key < N, lane);
+    // rows kb0 .. N - 1 of every head of the group, head by head
+    const int cph = (N - kb0 + kKeys - 1) / kKeys;
+    const int nch = Gh * cph;
+    typename G::Rd rd;
+    rd.init(lane, 0);
+    typename G::Wr wr;
+    wr.init(wave, lane);
+    // chunk c: head c / cph, rows from kb0 + 64 (c % cph); with its 64 start
+    // values (256 bytes: four 16-byte pieces per wave, lanes 0..3).  r0 is a
+    // multiple of 64 below N, so the 64 values lie inside the head's row of
+    // pitch NP and start 256-byte aligned; rows past N are masked.
+    auto issue = [&](int c, int slot) {
+        const int h = c / cph;
+        const int r0 = kb0 + (c - h * cph) * kKeys;
+        const char* rows = reinterpret_cast<const char*>(q) + ((head0 + h) * N + r0) * G::C::ROW;
+        wr.issue(ring + slot * G::C::BYTES, rows, N - r0);
+        if (lane < 4)
+            lds_dma16(reinterpret_cast<const char*>(linit + (head0 + h) * NP + r0), (unsigned)(wave * 64 + lane * 16),
+                      reinterpret_cast<const char*>(&sli[slot][wave * 16]));
+    };
+    for (int c = 0; c < min(kRing - 1, nch); ++c) issue(c, c);
+
     float col = 0.0f;
-    const int r_start = (kb * kH2oKeyBlock) / kTile * kTile;
-    for (int h = 0; h < G; ++h) {
-        const size_t head = (size_t)lb * Hq + (size_t)j * G + h;
-        const T* qh = q + head * N * D;
-        const float* lh = lse + head * N;
-        for (int r0 = r_start; r0 < N; r0 += kTile) {
-            __syncthreads();
-            stage_tile<T, D>(sq, qh, r0, N);
-            if (threadIdx.x < kTile) {
-                const int r = r0 + threadIdx.x;
-                slse[threadIdx.x] = r < N ? lh[r] : 0.0f;
+    for (int s0 = 0; s0 < nch; s0 += kRing) {
+#pragma unroll
+        for (int u = 0; u < kRing; ++u) {
+            const int s = s0 + u;
+            if (s >= nch) break;
+            wait_chunk<G::Wr::LPW + 1, kRing - 2>(min(kRing - 2, nch - 1 - s));
+            lds_barrier();
+            if (s + kRing - 1 < nch) issue(s + kRing - 1, (u + kRing - 1) % kRing);
+            f32x16 acc[2];
+            chunk_mma<T, D, kKeys, true>(acc, rd, ring + u * G::C::BYTES, kf, &sli[u][0], lane);
+            const int h = s / cph;
+            const int r0 = kb0 + (s - h * cph) * kKeys;
+            if (r0 < kb0 + kKeyBlock || r0 + kKeys > N) {  // rows before some key, or past N
+                // row of element (b, i) = r0 + 32 b + 8 (i / 4) + 4 (lane / 32) + i % 4; it
+                // counts iff key <= row < N
+                const int lo = key - (r0 + 4 * (lane >> 5));
+                const int hi = N - (r0 + 4 * (lane >> 5));
+#pragma unroll
+                for (int b = 0; b < 2; ++b)
+#pragma unroll
+                    for (int i = 0; i < 16; ++i) {
+                        const int off = 32 * b + 8 * (i >> 2) + (i & 3);
+                        if (off < lo || off >= hi) acc[b][i] = -INFINITY;
+                    }
             }
-            __syncthreads();
-            if (key0 >= N || r0 + kTile - 1 < key0) continue;
-#pragma unroll
-            for (int rbk = 0; rbk < kTile / 32; ++rbk) {
-                if (r0 + rbk * 32 + 31 < key0) continue;  // every row of the block is before every key
-                f32x16 acc = {};
-                const char* qrow = sq + (rbk * 32 + (lane & 31)) * S::ROWB;
-#pragma unroll
-                for (int s = 0; s < S::NSTEP; ++s)
-                    acc = M::mma(M::load(qrow, s * M::KSTEP + (lane >> 5) * M::KPL), kf[s], acc);
-#pragma unroll
-                for (int i = 0; i < 16; ++i) {
-                    const int rr = rbk * 32 + c_row(i, lane);
-                    const int r = r0 + rr;
-                    const bool valid = r < N && r >= my_key;
-                    col += valid ? fast_exp2(acc[i] * sl2 - slse[rr]) : 0.0f;
-                }
-            }
+            col += exp2_sum(acc, sl2);
         }
     }
+    // the two lane halves hold the same key and different rows
     col += __shfl_xor(col, 32);
-    if (lane < 32 && my_key < N) score[((size_t)lb * Hkv + j) * N + my_key] = col;
+    if (lane < 32 && key < N) score[((size_t)lb * Hkv + j) * N + key] = col;
 }
 
 template <typename T, int D>
 hipError_t run_h2o(const void* q, const void* k, int L, int B, int Hq, int Hkv, int N, float scale,
                    float* score, void* ws, hipStream_t st) {
-    float* lse = static_cast<float*>(ws);
+    float* linit = static_cast<float*>(ws);
     const float sl2 = scale * kLog2e;
     const T* qt = static_cast<const T*>(q);
     const T* kt = static_cast<const T*>(k);
-    const int nrb = (N + kH2oRowBlock - 1) / kH2oRowBlock;
-    const int nkb = (N + kH2oKeyBlock - 1) / kH2oKeyBlock;
-    hipLaunchKernelGGL((h2o_rows<T, D>), dim3((unsigned)((size_t)L * B * Hq * nrb)), dim3(kThreads), 0,
-                       st, qt, kt, Hq, Hkv, N, nrb, sl2, lse);
-    hipLaunchKernelGGL((h2o_cols<T, D>), dim3((unsigned)((size_t)L * B * Hkv * nkb)), dim3(kThreads), 0,
-                       st, qt, kt, lse, Hq, Hkv, N, nkb, sl2, score);
+    const int Gh = Hq / Hkv;
+    const int npos = kH2oRowsPerGroup / Gh;  // positions per pass-1 workgroup
+    const int nblk = (N + npos - 1) / npos;
+    const int nkb = (N + kKeyBlock - 1) / kKeyBlock;
+    const int NP = h2o_pitch(N);
+    hipLaunchKernelGGL((h2o_pass1<T, D>), dim3((unsigned)((size_t)L * B * Hkv * nblk)), dim3(kThreads), 0, st, qt,
+                       kt, Hq, Hkv, N, NP, npos, nblk, sl2, linit);
+    hipLaunchKernelGGL((h2o_pass2<T, D>), dim3((unsigned)((size_t)L * B * Hkv * nkb)), dim3(kThreads), 0, st, qt,
+                       kt, linit, Hq, Hkv, N, NP, nkb, sl2, score);
     return hipGetLastError();
 }
 

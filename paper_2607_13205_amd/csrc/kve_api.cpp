@@ -120,8 +120,11 @@ kve_status_t kve_h2o_score(const void* q, const void* k, kve_dtype_t dtype, int 
         return fail(KVE_ERR_INVALID_ARG, "%s: null tensor pointer", fn);
     if (!(std::isfinite(scale) && scale >= 0.0f))
         return fail(KVE_ERR_INVALID_ARG, "%s: scale must be finite and >= 0", fn);
-    const long long nrb = (N + kve::kH2oRowBlock - 1) / kve::kH2oRowBlock;
-    if ((long long)L * B * Hq * nrb > kMaxGrid) return fail(KVE_ERR_UNSUPPORTED, "%s: shape too large", fn);
+    const int G = Hq / Hkv;
+    if (G > kve::kH2oRowsPerGroup)
+        return fail(KVE_ERR_UNSUPPORTED, "%s: Hq/Hkv=%d exceeds %d", fn, G, kve::kH2oRowsPerGroup);
+    const long long nblk = (N + kve::kH2oRowsPerGroup / G - 1) / (kve::kH2oRowsPerGroup / G);
+    if ((long long)L * B * Hkv * nblk > kMaxGrid) return fail(KVE_ERR_UNSUPPORTED, "%s: shape too large", fn);
     const size_t need = kve::h2o_workspace(L, B, Hq, N);
     if (workspace_bytes < need || workspace == nullptr)
         return fail(KVE_ERR_WORKSPACE, "%s: workspace of %zu bytes < %zu needed", fn, workspace_bytes, need);

@@ -58,14 +58,17 @@ inline SnapPlan snap_plan(int L, int B, int Hq, int Hkv, int N, int W, int d = 1
 }
 
 // ---------------------------------------------------------------------------
-// H2O score: pass 1 one log-sum-exp per (layer, sample, query head, row);
-// pass 2 column sums over the group's heads.
+// H2O score: pass 1 one start value (-lse2 / sl2) per (layer, sample, query
+// head, row), in rows of pitch h2o_pitch(N) floats; pass 2 the column sums
+// over the group's heads.  A pass-1 workgroup covers kH2oRowsPerGroup rows:
+// the G heads of a KV group at kH2oRowsPerGroup / G positions.
 // ---------------------------------------------------------------------------
-constexpr int kH2oRowBlock = 128;
-constexpr int kH2oKeyBlock = 128;
+constexpr int kH2oRowsPerGroup = 128;
+
+inline int h2o_pitch(int N) { return (N + 63) / 64 * 64; }
 
 inline size_t h2o_workspace(int L, int B, int Hq, int N) {
-    return align_up((size_t)L * B * Hq * N * sizeof(float));
+    return align_up((size_t)L * B * Hq * h2o_pitch(N) * sizeof(float));
 }
 
 hipError_t launch_snapkv(const void* q, const void* k, int dtype, int L, int B, int Hq, int Hkv,

@@ -175,4 +175,152 @@ __device__ __forceinline__ void lds_barrier() {
     __atomic_signal_fence(__ATOMIC_SEQ_CST);
 }
 
+
+// ---------------------------------------------------------------------------
+// A ring of RING chunk slots in LDS, filled RING - 1 chunks ahead by all
+// NWAVES waves of a workgroup.  The caller names each chunk's first row and
+// its number of valid rows with src(c, &rows, &valid).
+// ---------------------------------------------------------------------------
+template <typename T, int D, int KEYS, int NWAVES, int RING>
+struct ChunkRing {
+    using C = KChunk<T, D, KEYS>;
+    using Wr = ChunkWriter<T, D, KEYS, NWAVES>;
+    Wr wr;
+    int nch;
+
+    __device__ __forceinline__ void open(int nchunks, int wave_uniform, int lane) {
+        wr.init(wave_uniform, lane);
+        nch = nchunks;
+    }
+    template <typename Src>
+    __device__ __forceinline__ void issue(char* ring, int c, int slot, const Src& src) const {
+        const char* rows;
+        int valid;
+        src(c, &rows, &valid);
+        wr.issue(ring + slot * C::BYTES, rows, valid);
+    }
+    template <typename Src>
+    __device__ __forceinline__ void prologue(char* ring, const Src& src) const {
+        for (int c = 0; c < min(RING - 1, nch); ++c) issue(ring, c, c, src);
+    }
+    // Before step s (slot u = s % RING): wait for this wave's loads of chunk
+    // s, publish it with the barrier, then refill the slot of chunk s - 1
+    // (read by every wave before the barrier) with chunk s + RING - 1.
+    template <typename Src>
+    __device__ __forceinline__ void advance(char* ring, int s, int u, const Src& src) const {
+        wait_chunk<Wr::LPW, RING - 2>(min(RING - 2, nch - 1 - s));
+        lds_barrier();
+        if (s + RING - 1 < nch) issue(ring, s + RING - 1, (u + RING - 1) % RING, src);
+    }
+};
+
+// Products of one chunk's first 64 rows (two 32-row blocks b, fragments from
+// LDS) with 32 rows held in registers (reg[st]).  LDS_A: the chunk rows are the
+// A operand (element i of acc[b] belongs to chunk row 32 b + c_row(i, lane),
+// the lane to register row lane % 32); otherwise the register rows are
+// (element i belongs to register row c_row(i, lane) in both blocks, the lane
+// to chunk row 32 b + lane % 32).  acc[b] starts at zero or, given `init`, at
+// the init value of the A-operand row of each element: init[32 b + c_row(i)]
+// with LDS_A, init[c_row(i)] otherwise (rows c_row(4 a .. 4 a + 3) are four
+// consecutive floats).
+template <typename T, int D, int KEYS, bool LDS_A>
+__device__ __forceinline__ void chunk_mma(f32x16 (&acc)[2], const ChunkReader<T, D, KEYS>& rd, const char* slot,
+                                          const typename Mma<T>::frag (&reg)[KChunk<T, D, KEYS>::NSTEP],
+                                          const float* init, int lane) {
+    using M = Mma<T>;
+    constexpr int NS = KChunk<T, D, KEYS>::NSTEP;
+    f32x16 c0[2];
+#pragma unroll
+    for (int b = 0; b < 2; ++b) {
+        if (init == nullptr) {
+            c0[b] = f32x16{};
+        } else {
+#pragma unroll
+            for (int a = 0; a < 4; ++a) {
+                const float4 v = *reinterpret_cast<const float4*>(init + (LDS_A ? 32 * b : 0) + c_row(4 * a, lane));
+                c0[b][4 * a] = v.x;
+                c0[b][4 * a + 1] = v.y;
+                c0[b][4 * a + 2] = v.z;
+                c0[b][4 * a + 3] = v.w;
+            }
+        }
+    }
+#pragma unroll
+    for (int st = 0; st < NS; ++st) {
+        const typename M::frag f[2] = {rd.get(slot, 0, st), rd.get(slot, 1, st)};
+#pragma unroll
+        for (int b = 0; b < 2; ++b) {
+            const f32x16 c = st == 0 ? c0[b] : acc[b];
+            acc[b] = LDS_A ? M::mma(f[b], reg[st], c) : M::mma(reg[st], f[b], c);
+        }
+    }
+    if constexpr (ChunkReader<T, D, KEYS>::kTable) {
+        // keep the fragment reads two k-steps ahead of the products
+        __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);  // LDS reads of steps 0, 1
+#pragma unroll
+        for (int st = 0; st < NS; ++st) {
+            __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);  // products of step st
+            if (st + 2 < NS) __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);  // reads of step st + 2
+        }
+    }
+}
+
+// Running softmax denominator of one row over chunks of 32 logits per lane
+// (x in acc units; sl2 turns them into log2 units).  The reference m is raised
+// only when a chunk's partial sum leaves [0, 2^64] (a logit more than 64 above
+// m, no reference yet, or masked logits before the first one); m is then the
+// largest logit seen so far, so nothing overflows or loses precision.
+struct RowSum {
+    float m = -INFINITY, l = 0.0f;
+
+    __device__ __forceinline__ void add(const f32x16 (&x)[2], float sl2) {
+        f32x16 ex[2];  // the logits stay in x for a possible new reference
+#pragma unroll
+        for (int b = 0; b < 2; ++b)
+#pragma unroll
+            for (int i = 0; i < 16; ++i) ex[b][i] = fast_exp2(fmaf(x[b][i], sl2, -m));
+        float part[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+            part[e] = (ex[0][e] + ex[0][e + 4]) + (ex[0][e + 8] + ex[0][e + 12]) +
+                      ((ex[1][e] + ex[1][e + 4]) + (ex[1][e + 8] + ex[1][e + 12]));
+        const float ln = l + ((part[0] + part[1]) + (part[2] + part[3]));
+        if (ln <= 0x1p64f) {  // false for inf and NaN
+            l = ln;
+            return;
+        }
+        float mx = -INFINITY;
+#pragma unroll
+        for (int b = 0; b < 2; ++b)
+#pragma unroll
+            for (int i = 0; i < 16; ++i) mx = fmaxf(mx, x[b][i]);
+        const float mn = fmaxf(m, mx * sl2);
+        if (mn == -INFINITY) return;
+        float a = l * fast_exp2(m - mn);
+#pragma unroll
+        for (int b = 0; b < 2; ++b)
+#pragma unroll
+            for (int i = 0; i < 16; ++i) a += fast_exp2(fmaf(x[b][i], sl2, -mn));
+        l = a;
+        m = mn;
+    }
+    // log2 of the sum, -inf when empty
+    __device__ __forceinline__ float lse2() const { return (m != -INFINITY && l > 0.0f) ? m + log2f(l) : -INFINITY; }
+};
+
+// Sum of exp2(sl2 * x) over the 32 values a lane holds in x (in place: the
+// logits are not needed again), as a tree.
+__device__ __forceinline__ float exp2_sum(f32x16 (&x)[2], float sl2) {
+#pragma unroll
+    for (int b = 0; b < 2; ++b)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) x[b][i] = fast_exp2(x[b][i] * sl2);
+    float part[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+        part[e] = (x[0][e] + x[0][e + 4]) + (x[0][e + 8] + x[0][e + 12]) +
+                  ((x[1][e] + x[1][e + 4]) + (x[1][e + 8] + x[1][e + 12]));
+    return (part[0] + part[1]) + (part[2] + part[3]);
+}
+
 }  // namespace kve

@@ -47,7 +47,7 @@ template <typename T, int D>
 struct Geo {
     using C = KChunk<T, D, kKeys>;
     using Rd = ChunkReader<T, D, kKeys>;
-    using Wr = ChunkWriter<T, D, kKeys, kWaves>;
+    using Ring = ChunkRing<T, D, kKeys, kWaves, kRing>;
 };
 
 struct Span {
@@ -81,79 +81,17 @@ __device__ __forceinline__ void load_q(QRows<T, D>& qf, const T* q, int seg, int
     }
 }
 
+// Chunks of a key range of one segment: chunk c starts at key t_begin + 64 c.
 template <typename T, int D>
-struct Stream {
-    using G = Geo<T, D>;
-    typename G::Wr wr;
+struct KeyChunks {
     const char* kseg;
-    int t_begin, t_end, nch;
-
-    __device__ __forceinline__ void open(const T* k, const Span& sp, int N, int wave, int lane) {
-        wr.init(wave, lane);
-        kseg = reinterpret_cast<const char*>(k) + (size_t)sp.seg * N * G::C::ROW;
-        t_begin = sp.t_begin;
-        t_end = sp.t_end;
-        nch = sp.nch;
-    }
-    __device__ __forceinline__ void issue(char* ring, int c, int slot) const {
+    int t_begin, t_end;
+    __device__ __forceinline__ void operator()(int c, const char** rows, int* valid) const {
         const int t0 = t_begin + c * kKeys;
-        wr.issue(ring + slot * G::C::BYTES, kseg + (size_t)t0 * G::C::ROW, t_end - t0);
-    }
-    __device__ __forceinline__ void prologue(char* ring) const {
-        for (int c = 0; c < min(kRing - 1, nch); ++c) issue(ring, c, c);
-    }
-    // Before step s (slot u = s % kRing): wait for this wave's loads of chunk
-    // s, publish it with the barrier, then refill the slot of chunk s - 1
-    // (read by every wave before the barrier) with chunk s + kRing - 1.
-    __device__ __forceinline__ void advance(char* ring, int s, int u) const {
-        wait_chunk<G::Wr::LPW, kRing - 2>(min(kRing - 2, nch - 1 - s));
-        lds_barrier();
-        if (s + kRing - 1 < nch) issue(ring, s + kRing - 1, (u + kRing - 1) % kRing);
+        *rows = kseg + (size_t)t0 * Geo<T, D>::C::ROW;
+        *valid = t_end - t0;
     }
 };
-
-// Products of one chunk with this wave's 32 query rows: two 32-key blocks,
-// two independent accumulation chains.  KEYS_A: keys are the A operand
-// (S^T = K Q^T, lane = query row); otherwise the query rows are (S = Q K^T,
-// lane = key).  The accumulators start at zero or, with `init` (Q K^T only),
-// at init[c_row(i)] for element i: rows c_row(4 a .. 4 a + 3) are consecutive.
-template <typename T, int D, bool KEYS_A>
-__device__ __forceinline__ void chunk_mma(f32x16 (&acc)[2], const typename Geo<T, D>::Rd& rd, const char* slot,
-                                          const QRows<T, D>& qf, const float* init, int lane) {
-    using M = Mma<T>;
-    f32x16 c0;
-    if (init == nullptr) {
-        c0 = f32x16{};
-    } else {
-#pragma unroll
-        for (int a = 0; a < 4; ++a) {
-            const float4 v = *reinterpret_cast<const float4*>(init + c_row(4 * a, lane));
-            c0[4 * a] = v.x;
-            c0[4 * a + 1] = v.y;
-            c0[4 * a + 2] = v.z;
-            c0[4 * a + 3] = v.w;
-        }
-    }
-#pragma unroll
-    for (int st = 0; st < Geo<T, D>::C::NSTEP; ++st) {
-        const typename M::frag kf[2] = {rd.get(slot, 0, st), rd.get(slot, 1, st)};
-#pragma unroll
-        for (int kb = 0; kb < 2; ++kb) {
-            const f32x16 c = st == 0 ? c0 : acc[kb];
-            acc[kb] = KEYS_A ? M::mma(kf[kb], qf[st], c) : M::mma(qf[st], kf[kb], c);
-        }
-    }
-    if constexpr (Geo<T, D>::Rd::kTable) {
-        // keep the fragment reads two k-steps ahead of the products
-        constexpr int NS = Geo<T, D>::C::NSTEP;
-        __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);  // LDS reads of steps 0, 1
-#pragma unroll
-        for (int st = 0; st < NS; ++st) {
-            __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);  // products of step st
-            if (st + 2 < NS) __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);  // reads of step st + 2
-        }
-    }
-}
 
 template <typename T, int D>
 __global__ __launch_bounds__(kThreads, 2) void snap_pass1(const T* __restrict__ q, const T* __restrict__ k,
@@ -173,24 +111,21 @@ __global__ __launch_bounds__(kThreads, 2) void snap_pass1(const T* __restrict__ 
     const int lim = qr < rows ? P_rows + qr % W : -1;  // last key the row sees
     typename G::Rd rd;
     rd.init(lane, 0);
-    Stream<T, D> str;
-    str.open(k, sp, N, wave, lane);
-    str.prologue(ring);
+    typename G::Ring ring_io;
+    ring_io.open(sp.nch, wave, lane);
+    const KeyChunks<T, D> src{reinterpret_cast<const char*>(k) + (size_t)sp.seg * N * G::C::ROW, sp.t_begin,
+                              sp.t_end};
+    ring_io.prologue(ring, src);
 
-    // Reference m (log2 units) and sum l of exp2(x - m) over this lane's keys.
-    // m is raised only when a chunk's partial sum leaves [0, 2^64] (a key more
-    // than 64 above m, no reference yet, or masked keys before the first
-    // one); m is then the largest logit seen so far, so nothing overflows or
-    // loses precision.
-    float m = -INFINITY, l = 0.0f;
+    RowSum rs;
     for (int s0 = 0; s0 < sp.nch; s0 += kRing) {
 #pragma unroll
         for (int u = 0; u < kRing; ++u) {
             const int s = s0 + u;
             if (s >= sp.nch) break;
-            str.advance(ring, s, u);
+            ring_io.advance(ring, s, u, src);
             f32x16 acc[2];
-            chunk_mma<T, D, true>(acc, rd, ring + u * G::C::BYTES, qf, nullptr, lane);
+            chunk_mma<T, D, kKeys, true>(acc, rd, ring + u * G::C::BYTES, qf, nullptr, lane);
             if (sp.t_begin + (s + 1) * kKeys > P_rows) {  // keys past the range end or inside the causal window
                 // key of element (kb, i) = base + 32 kb + 8 (i / 4) + i % 4
                 const int last = min(lim, sp.t_end - 1) - (sp.t_begin + s * kKeys + 4 * (lane >> 5));
@@ -200,44 +135,12 @@ __global__ __launch_bounds__(kThreads, 2) void snap_pass1(const T* __restrict__ 
                     for (int i = 0; i < 16; ++i)
                         if (32 * kb + 8 * (i >> 2) + (i & 3) > last) acc[kb][i] = -INFINITY;
             }
-            // exponentials side by side, then a tree of sums
-            f32x16 ex[2];
-#pragma unroll
-            for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-                for (int i = 0; i < 16; ++i) ex[kb][i] = fast_exp2(fmaf(acc[kb][i], sl2, -m));
-            float part[4];
-#pragma unroll
-            for (int e = 0; e < 4; ++e)
-                part[e] = (ex[0][e] + ex[0][e + 4]) + (ex[0][e + 8] + ex[0][e + 12]) +
-                          ((ex[1][e] + ex[1][e + 4]) + (ex[1][e + 8] + ex[1][e + 12]));
-            const float ln = l + ((part[0] + part[1]) + (part[2] + part[3]));
-            if (ln <= 0x1p64f) {  // false for inf and NaN
-                l = ln;
-            } else {  // new reference: the largest logit so far
-                float mx = -INFINITY;
-#pragma unroll
-                for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-                    for (int i = 0; i < 16; ++i) mx = fmaxf(mx, acc[kb][i]);
-                const float mn = fmaxf(m, mx * sl2);
-                if (mn != -INFINITY) {
-                    float a = l * fast_exp2(m - mn);
-#pragma unroll
-                    for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-                        for (int i = 0; i < 16; ++i) a += fast_exp2(fmaf(acc[kb][i], sl2, -mn));
-                    l = a;
-                    m = mn;
-                }
-            }
+            rs.add(acc, sl2);
         }
     }
     // the two lane halves hold the same row and different keys
-    lse2_merge(m, l, __shfl_xor(m, 32), __shfl_xor(l, 32));
-    if (lane < 32)
-        stats[((size_t)sp.vseg * nranges + sp.range) * kSnapRowsPerGroup + wave * 32 + lane] =
-            (m != -INFINITY && l > 0.0f) ? m + log2f(l) : -INFINITY;
+    lse2_merge(rs.m, rs.l, __shfl_xor(rs.m, 32), __shfl_xor(rs.l, 32));
+    if (lane < 32) stats[((size_t)sp.vseg * nranges + sp.range) * kSnapRowsPerGroup + wave * 32 + lane] = rs.lse2();
 }
 
 __global__ __launch_bounds__(kSnapRowsPerGroup) void snap_combine(const float* __restrict__ stats, int nranges,
@@ -282,9 +185,11 @@ __global__ __launch_bounds__(kThreads, 2) void snap_pass2(const T* __restrict__ 
     load_q<T, D>(qf, q, sp.seg, rows, sp.rg * kSnapRowsPerGroup + wave * 32 + (lane & 31), lane);
     typename G::Rd rd;
     rd.init(lane, 0);
-    Stream<T, D> str;
-    str.open(k, sp, N, wave, lane);
-    str.prologue(ring);
+    typename G::Ring ring_io;
+    ring_io.open(sp.nch, wave, lane);
+    const KeyChunks<T, D> src{reinterpret_cast<const char*>(k) + (size_t)sp.seg * N * G::C::ROW, sp.t_begin,
+                              sp.t_end};
+    ring_io.prologue(ring, src);
     float* out = raw + ((size_t)sp.rg * segs + sp.seg) * N;
 
     // add the four row blocks of chunk s (every wave has written it); each wave
@@ -304,10 +209,10 @@ __global__ __launch_bounds__(kThreads, 2) void snap_pass2(const T* __restrict__ 
             if (s >= sp.nch) break;
             // the barrier inside also orders the scol writes of chunk s - 1
             // before their sum, and that sum before chunk s + 1 reuses the buffer
-            str.advance(ring, s, u);
+            ring_io.advance(ring, s, u, src);
             if (s >= 1) reduce(s - 1);
             f32x16 acc[2];
-            chunk_mma<T, D, false>(acc, rd, ring + u * G::C::BYTES, qf, sinit + wave * 32, lane);
+            chunk_mma<T, D, kKeys, false>(acc, rd, ring + u * G::C::BYTES, qf, sinit + wave * 32, lane);
             if (sp.t_begin + (s + 1) * kKeys > P_rows) {  // keys past the range end or inside the causal window
                 // key t is visible to window query i (position P_rows + i) iff t - P_rows <= i
 #pragma unroll
@@ -323,8 +228,8 @@ __global__ __launch_bounds__(kThreads, 2) void snap_pass2(const T* __restrict__ 
                     }
                 }
             }
-            // exponentials in place (the logits are not needed again), then a
-            // tree of sums over the lane's 16 rows and one shuffle for the other 16
+            // exponentials of each key block: a lane sum over its 16 rows and
+            // one shuffle for the other 16
 #pragma unroll
             for (int kb = 0; kb < 2; ++kb) {
 #pragma unroll

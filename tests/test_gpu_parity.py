@@ -101,6 +101,10 @@ H2O_CASES = [
     custom("h2o_f32", 1, 1, 2, 1, 200, 0, 64, 1, "f32", scorer="h2o"),
     custom("h2o_ragged", 2, 1, 8, 2, 513, 0, 128, 1, "bf16", scorer="h2o"),
     custom("h2o_n1", 1, 1, 2, 2, 1, 0, 64, 1, "bf16", scorer="h2o"),
+    # G = 8: 16 positions per row block; G = 3: 42 positions and 2 padding rows
+    custom("h2o_g8", 1, 1, 16, 2, 700, 0, 128, 1, "bf16", scorer="h2o"),
+    custom("h2o_g3", 1, 2, 6, 2, 333, 0, 64, 1, "bf16", scorer="h2o"),
+    custom("h2o_g1_f32", 1, 1, 2, 2, 260, 0, 128, 1, "f32", scorer="h2o"),
 ]
 
 
