@@ -3,12 +3,24 @@
 // dense cache of a compacting implementation).
 //
 // topk_select: one workgroup per (layer, sample, KV head) segment.  Scores are
-// mapped to order-preserving 32-bit keys (-0 -> +0, NaN lowest) and, for every
-// role bucket at once, a most-significant-digit radix select (4 passes of 8
-// bits, one LDS histogram of 256 bins per bucket) finds the key of the
-// quota-th largest candidate.  A final ordered pass keeps every key above the
-// threshold and, among keys equal to it, the lowest indices first, and writes
-// the kept positions in ascending order (ballot + prefix count per chunk).
+// mapped to order-preserving 32-bit keys (-0 -> +0, NaN lowest).
+//   1. Three most-significant-digit passes (11, 11 and 10 bits), all buckets
+//      at once with one LDS histogram per bucket, fix the key of the quota-th
+//      largest candidate (the threshold) and how many candidates equal to it
+//      stay.  The first digit holds the sign and all exponent bits, so float
+//      scores spread over its bins; the first histogram also gives each
+//      bucket's population, which decides whether the bucket is kept whole,
+//      skipped, or selected.  The digit is found by all threads at once (a
+//      scan over groups of bins).
+//   2. Each wave owns a contiguous quarter of the positions and walks it 64
+//      positions at a time: per-lane counts give what each wave run keeps
+//      (keys above the threshold, the window, whole buckets, and keys equal to
+//      the threshold lowest index first); ballots then rank the kept positions
+//      so that they come out in ascending order.
+// The sweeps read 16 positions per thread before they use any, so that the
+// memory latency is paid once per group and not once per key; the loads are
+// unconditional (clamped to a valid position) so that none waits behind a
+// branch.
 #include "kve_device.h"
 #include "kve_internal.h"
 
@@ -17,143 +29,247 @@ namespace {
 
 constexpr int kThreads = 256;
 constexpr int kWaves = kThreads / kWave;
-constexpr int kMaxR = 8;
-constexpr int kDigits = 256;
+constexpr int kMaxR = 8;  // buckets supported (one kernel instantiation each)
+constexpr int kDigitBits = 11;
+constexpr int kDigits = 1 << kDigitBits;
+constexpr int kBatch = 16;
 
 enum : int { kModeNone = 0, kModeSelect = 1, kModeAll = 2 };
 
+template <int R>
+struct TopkShared {
+    uint32_t hist[R][kDigits];
+    uint32_t pref[R];  // key bits fixed so far (bits lo .. 31)
+    int lo[R];         // lowest fixed bit; 0 once the threshold is known
+    int need[R];       // still to take among keys matching the prefix
+    int mode[R];
+    int wave_eq[kWaves][R];  // equal-to-threshold candidates per wave run
+    int wave_keep[kWaves];       // kept positions per wave run
+    int scan[kWaves];
+};
+
+// Exclusive prefix sum over the workgroup of one value per thread (in thread
+// order); every thread also gets the total.  `tmp` holds kWaves ints.
+__device__ __forceinline__ int block_exclusive_scan(int v, int* tmp, int& total) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    int incl = v;
+#pragma unroll
+    for (int off = 1; off < kWave; off <<= 1) {
+        const int o = __shfl_up(incl, off);
+        if (lane >= off) incl += o;
+    }
+    if (lane == kWave - 1) tmp[wave] = incl;
+    __syncthreads();
+    int before = 0;
+    total = 0;
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w) {
+        const int t = tmp[w];
+        if (w < wave) before += t;
+        total += t;
+    }
+    __syncthreads();
+    return before + incl - v;
+}
+
+template <int R>
 __global__ __launch_bounds__(kThreads) void topk_kernel(const float* __restrict__ score,
                                                         const int8_t* __restrict__ roles,
                                                         const int32_t* __restrict__ quota, int B,
-                                                        int Hkv, int N, int W, int R, int k_cap,
+                                                        int Hkv, int N, int W, int k_cap,
                                                         int32_t* __restrict__ idx_out,
                                                         int32_t* __restrict__ count_out) {
-    __shared__ uint32_t hist[kMaxR][kDigits];
-    __shared__ uint32_t s_prefix[kMaxR];  // key bits fixed so far
-    __shared__ int s_need[kMaxR];         // still to take among keys matching the prefix
-    __shared__ int s_mode[kMaxR];
-    __shared__ int s_wcnt[kWaves][kMaxR + 1];
-    __shared__ int s_eq_seen[kMaxR];
-    __shared__ int s_base;
-
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    __shared__ TopkShared<R> sh;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int seg = blockIdx.x;
     const int b = (seg / Hkv) % B;
     const float* sc = score + (size_t)seg * N;
     const int8_t* ro = roles + (size_t)b * N;
     const int P = N - W;
-    const uint64_t lt_mask = (1ull << lane) - 1ull;
 
     if (tid < R) {
-        s_prefix[tid] = 0u;
-        s_mode[tid] = kModeSelect;
-        s_need[tid] = 0;
-        s_eq_seen[tid] = 0;
+        sh.mode[tid] = kModeSelect;  // decided after the first histogram
+        sh.pref[tid] = 0u;
+        sh.lo[tid] = 32;
+        sh.need[tid] = 0;
     }
-    if (tid == 0) s_base = 0;
     __syncthreads();
 
-    for (int pass = 0; pass < 4; ++pass) {
-        const int shift = 24 - 8 * pass;
-        const uint32_t himask = pass == 0 ? 0u : (0xFFFFFFFFu << (shift + 8));
-        for (int e = tid; e < R * kDigits; e += kThreads) hist[e / kDigits][e % kDigits] = 0u;
+    // 1. radix passes over the keys, all buckets at once: digits of 11, 11 and
+    //    10 bits from the top; the first covers the sign and exponent bits
+    for (int pass = 0; pass < (32 + kDigitBits - 1) / kDigitBits; ++pass) {
+        bool any = false;
+#pragma unroll
+        for (int r = 0; r < R; ++r) any |= sh.mode[r] == kModeSelect && sh.lo[r] > 0;
+        if (!any) break;  // uniform: every thread reads the same LDS values
+        for (int e = tid; e < R * kDigits; e += kThreads) (&sh.hist[0][0])[e] = 0u;
         __syncthreads();
-        for (int t = tid; t < P; t += kThreads) {
-            const int r = ro[t];
-            if (r < 0 || r >= R || s_mode[r] != kModeSelect) continue;
-            const uint32_t key = score_key(sc[t]);
-            if ((key & himask) != s_prefix[r]) continue;
-            atomicAdd(&hist[r][(key >> shift) & (kDigits - 1)], 1u);
+        for (int t00 = tid; t00 < P; t00 += kThreads * kBatch) {
+            int rv[kBatch];
+            float sv[kBatch];
+#pragma unroll
+            for (int e = 0; e < kBatch; ++e) {  // unconditional loads (clamped index), then the bound
+                const int t = t00 + e * kThreads;
+                const int tc = min(t, P - 1);
+                const int r = ro[tc];
+                sv[e] = sc[tc];
+                rv[e] = t < P ? r : -1;
+            }
+#pragma unroll
+            for (int e = 0; e < kBatch; ++e) {
+                const int r = rv[e];
+                if (r < 0 || r >= R || sh.mode[r] != kModeSelect) continue;
+                const int lo = sh.lo[r];
+                if (lo == 0) continue;
+                const uint32_t key = score_key(sv[e]);
+                if (lo < 32 && (key >> lo) != sh.pref[r]) continue;
+                const int w = min(kDigitBits, lo);
+                atomicAdd(&sh.hist[r][(key >> (lo - w)) & ((1u << w) - 1u)], 1u);
+            }
         }
         __syncthreads();
-        if (tid < R && s_mode[tid] == kModeSelect) {
-            const int r = tid;
+        // Digit search, every thread at once: thread tid holds the kPerThread
+        // bins from the top going down; a scan gives the count of keys in all
+        // higher bins, and the thread whose bins reach `want` finds the digit.
+        // After the first histogram (the bucket's whole population) the bucket
+        // is kept whole, skipped, or selected.
+#pragma unroll 1
+        for (int r = 0; r < R; ++r) {
+            if (!(sh.mode[r] == kModeSelect && sh.lo[r] > 0)) continue;  // uniform
+            constexpr int kPerThread = kDigits / kThreads;
+            const int hi = kDigits - kPerThread * tid;  // bins [hi - kPerThread, hi)
+            int mine = 0;
+#pragma unroll
+            for (int e = 1; e <= kPerThread; ++e) mine += (int)sh.hist[r][hi - e];
+            int total;
+            const int above = block_exclusive_scan(mine, sh.scan, total);
+            int want = sh.need[r];
             if (pass == 0) {
-                int n = 0;
-                for (int dgt = 0; dgt < kDigits; ++dgt) n += (int)hist[r][dgt];
                 const int q = max(quota[(size_t)b * R + r], 0);
-                if (q == 0)
-                    s_mode[r] = kModeNone;
-                else if (q >= n)
-                    s_mode[r] = kModeAll;
-                else
-                    s_need[r] = q;
-            }
-            if (s_mode[r] == kModeSelect) {
-                const int want = s_need[r];
-                int cum = 0, dgt = kDigits - 1;
-                for (; dgt > 0; --dgt) {
-                    const int hcount = (int)hist[r][dgt];
-                    if (cum + hcount >= want) break;
-                    cum += hcount;
+                if (q == 0 || q >= total) {
+                    if (tid == 0) sh.mode[r] = q == 0 ? kModeNone : kModeAll;
+                    __syncthreads();
+                    continue;
                 }
-                s_prefix[r] |= (uint32_t)dgt << shift;
-                s_need[r] = want - cum;
+                want = q;
             }
+            if (above < want && above + mine >= want) {  // exactly one thread
+                const int lo = sh.lo[r], w = min(kDigitBits, lo);
+                int cum = above, dgt = hi - 1;
+                for (; dgt > hi - kPerThread; --dgt) {
+                    const int h = (int)sh.hist[r][dgt];
+                    if (cum + h >= want) break;
+                    cum += h;
+                }
+                sh.pref[r] = (lo < 32 ? sh.pref[r] << w : 0u) | (uint32_t)dgt;
+                sh.need[r] = want - cum;
+                sh.lo[r] = lo - w;
+            }
+            __syncthreads();
         }
-        __syncthreads();
     }
 
-    // Ordered output pass: s_prefix[r] is the threshold key, s_need[r] >= 1 the
-    // number of candidates equal to it that stay (lowest index first).
-    for (int c0 = 0; c0 < N; c0 += kThreads) {
-        const int t = c0 + tid;
-        bool keep = false, eq = false;
-        int r = -1;
-        if (t < N) {
-            if (t >= P) {
-                keep = true;
-            } else {
-                r = ro[t];
-                if (r >= 0 && r < R) {
-                    const int mode = s_mode[r];
-                    if (mode == kModeAll) {
-                        keep = true;
-                    } else if (mode == kModeSelect) {
-                        const uint32_t key = score_key(sc[t]);
-                        if (key > s_prefix[r])
-                            keep = true;
-                        else if (key == s_prefix[r])
-                            eq = true;
-                    }
+    // 2. ordered output over wave runs [w0, w1), 64 positions per step
+    int mode[R], need[R];
+    uint32_t th[R];  // threshold key of each selecting bucket
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+        mode[r] = sh.mode[r];
+        th[r] = sh.pref[r];
+        need[r] = mode[r] == kModeSelect ? sh.need[r] : 0;
+    }
+    const int run = (N + kWaves * kWave - 1) / (kWaves * kWave) * kWave;  // positions per wave, whole steps
+    const int w0 = min(N, wave * run), w1 = min(N, w0 + run);
+    // class of position t: 1 kept, 2 + r equal to the threshold of bucket r, 0 dropped
+    auto classify = [&](int t, int r, float x) {
+        if (t >= P) return 1;
+        int c = 0;
+#pragma unroll
+        for (int q = 0; q < R; ++q)
+            if (r == q) {
+                if (mode[q] == kModeAll) {
+                    c = 1;
+                } else if (mode[q] == kModeSelect) {
+                    const uint32_t key = score_key(x);
+                    c = key > th[q] ? 1 : (key == th[q] ? 2 + q : 0);
                 }
             }
+        return c;
+    };
+    // visit(t, c) for every position of this wave's run, 64 consecutive per step
+    auto sweep = [&](auto&& visit) {
+        for (int s00 = w0; s00 < w1; s00 += kWave * kBatch) {
+            int rv[kBatch];
+            float sv[kBatch];
+#pragma unroll
+            for (int e = 0; e < kBatch; ++e) {  // unconditional loads (clamped index), then the bound
+                const int t = s00 + e * kWave + lane;
+                const int tc = max(0, min(t, min(w1, P) - 1));
+                const int r = ro[tc];
+                sv[e] = sc[tc];
+                rv[e] = t < min(w1, P) ? r : -1;
+            }
+#pragma unroll
+            for (int e = 0; e < kBatch; ++e) {
+                const int t = s00 + e * kWave + lane;
+                visit(t, t < w1 ? classify(t, rv[e], sv[e]) : 0);
+            }
         }
-        int rank_w = 0;
-        for (int rr = 0; rr < R; ++rr) {
-            const bool mine = eq && r == rr;
-            const uint64_t mask = __ballot(mine);
-            if (mine) rank_w = __popcll(mask & lt_mask);
-            if (lane == 0) s_wcnt[wave][rr] = __popcll(mask);
-        }
-        __syncthreads();
-        if (eq) {
-            int rank = s_eq_seen[r] + rank_w;
-            for (int w = 0; w < wave; ++w) rank += s_wcnt[w][r];
-            keep = rank < s_need[r];
-        }
-        const uint64_t km = __ballot(keep);
-        if (lane == 0) s_wcnt[wave][kMaxR] = __popcll(km);
-        __syncthreads();
-        if (keep) {
-            int pos = s_base + __popcll(km & lt_mask);
-            for (int w = 0; w < wave; ++w) pos += s_wcnt[w][kMaxR];
-            if (pos < k_cap) idx_out[(size_t)seg * k_cap + pos] = t;
-        }
-        __syncthreads();
-        if (tid == 0) {
-            int tot = 0;
-            for (int w = 0; w < kWaves; ++w) tot += s_wcnt[w][kMaxR];
-            s_base += tot;
-        }
-        if (tid < R) {
-            int tot = 0;
-            for (int w = 0; w < kWaves; ++w) tot += s_wcnt[w][tid];
-            s_eq_seen[tid] += tot;
-        }
-        __syncthreads();
+    };
+    const uint64_t lt = (1ull << lane) - 1ull;
+    // count this run's kept positions and its equal keys per bucket, per lane,
+    // then over the wave
+    int keep = 0, eq[R];
+#pragma unroll
+    for (int r = 0; r < R; ++r) eq[r] = 0;
+    sweep([&](int, int c) {
+        keep += c == 1;
+#pragma unroll
+        for (int r = 0; r < R; ++r) eq[r] += c == 2 + r;
+    });
+#pragma unroll
+    for (int off = 1; off < kWave; off <<= 1) {
+        keep += __shfl_xor(keep, off);
+#pragma unroll
+        for (int r = 0; r < R; ++r) eq[r] += __shfl_xor(eq[r], off);
     }
-    if (tid == 0 && count_out != nullptr) count_out[seg] = s_base;
+    if (lane == 0) {
+#pragma unroll
+        for (int r = 0; r < R; ++r) sh.wave_eq[wave][r] = eq[r];
+    }
+    __syncthreads();
+    // equal keys are kept lowest index first: the earlier runs' equal keys come first
+    int eq_seen[R];
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+        eq_seen[r] = 0;
+        for (int w = 0; w < wave; ++w) eq_seen[r] += sh.wave_eq[w][r];
+        keep += max(0, min(eq[r], need[r] - eq_seen[r]));
+    }
+    if (lane == 0) sh.wave_keep[wave] = keep;
+    __syncthreads();
+    int pos = 0, total = 0;
+    for (int w = 0; w < kWaves; ++w) {
+        if (w < wave) pos += sh.wave_keep[w];
+        total += sh.wave_keep[w];
+    }
+    sweep([&](int t, int c) {
+        bool k = c == 1;
+        if (__ballot(c >= 2) != 0ull) {  // rare: keys equal to a threshold in this step
+#pragma unroll
+            for (int r = 0; r < R; ++r) {
+                const uint64_t m = __ballot(c == 2 + r);
+                if (c == 2 + r) k = eq_seen[r] + __popcll(m & lt) < need[r];
+                eq_seen[r] += __popcll(m);
+            }
+        }
+        const uint64_t km = __ballot(k);
+        const int at = pos + __popcll(km & lt);
+        if (k && at < k_cap) idx_out[(size_t)seg * k_cap + at] = t;
+        pos += __popcll(km);
+    });
+    if (tid == 0 && count_out != nullptr) count_out[seg] = total;
 }
 
 constexpr int kCompactRows = 64;
@@ -191,8 +307,25 @@ hipError_t launch_topk(const float* score, const int8_t* roles, const int32_t* q
                        int Hkv, int N, int W, int R, int k_cap, int32_t* idx_out, int32_t* count_out,
                        hipStream_t st) {
     const size_t segs = (size_t)L * B * Hkv;
-    hipLaunchKernelGGL(topk_kernel, dim3((unsigned)segs), dim3(kThreads), 0, st, score, roles, quota, B,
-                       Hkv, N, W, R, k_cap, idx_out, count_out);
+    const dim3 grid((unsigned)segs), block(kThreads);
+    switch (R) {
+#define KVE_TOPK_CASE(RR)                                                                                  \
+    case RR:                                                                                               \
+        hipLaunchKernelGGL(topk_kernel<RR>, grid, block, 0, st, score, roles, quota, B, Hkv, N, W, k_cap, \
+                           idx_out, count_out);                                                            \
+        break;
+        KVE_TOPK_CASE(1)
+        KVE_TOPK_CASE(2)
+        KVE_TOPK_CASE(3)
+        KVE_TOPK_CASE(4)
+        KVE_TOPK_CASE(5)
+        KVE_TOPK_CASE(6)
+        KVE_TOPK_CASE(7)
+        KVE_TOPK_CASE(8)
+#undef KVE_TOPK_CASE
+        default:
+            return hipErrorInvalidValue;
+    }
     return hipGetLastError();
 }
 
