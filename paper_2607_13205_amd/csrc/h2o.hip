@@ -14,13 +14,17 @@
 //              keeps one row's running softmax denominator.  Writes
 //              -lse2/sl2 per row, the start value pass 2 needs, into rows of
 //              pitch NP = N rounded up to 64 floats per head.
-//   h2o_pass2  one workgroup per (KV group, 128-key block): four waves own 32
-//              keys each (key fragments in registers); every later query row
-//              of the G heads streams through LDS in 64-row chunks together
-//              with its -lse2/sl2, which starts the products, so that
-//              sl2 * acc = x - lse2 and each lane sums exp2 over its key's
-//              column directly.
+//   h2o_pass2  one workgroup per (query head, 128-key block), key blocks near
+//              0 (the most rows) first: four waves own 32 keys each (key
+//              fragments in registers); every later query row of the head
+//              streams through LDS in 64-row chunks together with its
+//              -lse2/sl2, which starts the products, so that sl2 * acc =
+//              x - lse2 and each lane sums exp2 over its key's column
+//              directly.  One column sum per (query head, key).
+//   h2o_heads  adds the G heads of each KV group, in head order.
 // Logits are in log2 units, x = scale * log2(e) * <q, k>.
+#include <algorithm>
+
 #include "kve_device.h"
 #include "kve_internal.h"
 #include "kve_stream.h"
@@ -128,44 +132,39 @@ __global__ __launch_bounds__(kThreads, 2) void h2o_pass1(const T* __restrict__ q
 
 template <typename T, int D>
 __global__ __launch_bounds__(kThreads, 2) void h2o_pass2(const T* __restrict__ q, const T* __restrict__ k,
-                                                         const float* __restrict__ linit, int Hq, int Hkv,
-                                                         int N, int NP, int nkb, float sl2,
-                                                         float* __restrict__ score) {
+                                                         const float* __restrict__ linit, int heads, int Hq,
+                                                         int Hkv, int N, int NP, float sl2,
+                                                         float* __restrict__ colsum) {
     using G = Geo<T, D>;
     __shared__ __align__(16) char ring[kRing * G::C::BYTES];
     __shared__ __align__(16) float sli[kRing][kKeys];  // -lse2/sl2 of each chunk row
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int Gh = Hq / Hkv;
-    int bid = blockIdx.x;
-    const int kb = bid % nkb;  // key blocks near 0 have the most rows
-    bid /= nkb;
-    const int j = bid % Hkv;
-    const int lb = bid / Hkv;
+    const int kb = blockIdx.x / heads;  // key blocks near 0 (the most rows) first
+    const size_t head = (size_t)(blockIdx.x - kb * heads);  // over all layers and samples
+    const size_t lbj = head / Gh;                            // (layer, sample, KV head)
     const int kb0 = kb * kKeyBlock;
     const int key = kb0 + wave * 32 + (lane & 31);
-    const size_t head0 = (size_t)lb * Hq + (size_t)j * Gh;
 
     typename G::Frags kf;
-    load_row_frags<T, D>(kf, k + (((size_t)lb * Hkv + j) * N + (key < N ? key : 0)) * D, key < N, lane);
-    // rows kb0 .. N - 1 of every head of the group, head by head
-    const int cph = (N - kb0 + kKeys - 1) / kKeys;
-    const int nch = Gh * cph;
+    load_row_frags<T, D>(kf, k + (lbj * N + (key < N ? key : 0)) * D, key < N, lane);
+    // rows kb0 .. N - 1 of this head
+    const int nch = (N - kb0 + kKeys - 1) / kKeys;
     typename G::Rd rd;
     rd.init(lane, 0);
     typename G::Wr wr;
     wr.init(wave, lane);
-    // chunk c: head c / cph, rows from kb0 + 64 (c % cph); with its 64 start
-    // values (256 bytes: four 16-byte pieces per wave, lanes 0..3).  r0 is a
-    // multiple of 64 below N, so the 64 values lie inside the head's row of
-    // pitch NP and start 256-byte aligned; rows past N are masked.
+    // chunk c: rows from kb0 + 64 c, with their 64 start values (256 bytes:
+    // four 16-byte pieces per wave, lanes 0..3).  r0 is a multiple of 64 below
+    // N, so the 64 values lie inside the head's row of pitch NP and start
+    // 256-byte aligned; rows past N are masked.
     auto issue = [&](int c, int slot) {
-        const int h = c / cph;
-        const int r0 = kb0 + (c - h * cph) * kKeys;
-        const char* rows = reinterpret_cast<const char*>(q) + ((head0 + h) * N + r0) * G::C::ROW;
+        const int r0 = kb0 + c * kKeys;
+        const char* rows = reinterpret_cast<const char*>(q) + (head * N + r0) * G::C::ROW;
         wr.issue(ring + slot * G::C::BYTES, rows, N - r0);
         if (lane < 4)
-            lds_dma16(reinterpret_cast<const char*>(linit + (head0 + h) * NP + r0), (unsigned)(wave * 64 + lane * 16),
+            lds_dma16(reinterpret_cast<const char*>(linit + head * NP + r0), (unsigned)(wave * 64 + lane * 16),
                       reinterpret_cast<const char*>(&sli[slot][wave * 16]));
     };
     for (int c = 0; c < min(kRing - 1, nch); ++c) issue(c, c);
@@ -181,8 +180,7 @@ __global__ __launch_bounds__(kThreads, 2) void h2o_pass2(const T* __restrict__ q
             if (s + kRing - 1 < nch) issue(s + kRing - 1, (u + kRing - 1) % kRing);
             f32x16 acc[2];
             chunk_mma<T, D, kKeys, true>(acc, rd, ring + u * G::C::BYTES, kf, &sli[u][0], lane);
-            const int h = s / cph;
-            const int r0 = kb0 + (s - h * cph) * kKeys;
+            const int r0 = kb0 + s * kKeys;
             if (r0 < kb0 + kKeyBlock || r0 + kKeys > N) {  // rows before some key, or past N
                 // row of element (b, i) = r0 + 32 b + 8 (i / 4) + 4 (lane / 32) + i % 4; it
                 // counts iff key <= row < N
@@ -201,13 +199,26 @@ __global__ __launch_bounds__(kThreads, 2) void h2o_pass2(const T* __restrict__ q
     }
     // the two lane halves hold the same key and different rows
     col += __shfl_xor(col, 32);
-    if (lane < 32 && key < N) score[((size_t)lb * Hkv + j) * N + key] = col;
+    if (lane < 32 && key < N) colsum[head * N + key] = col;
+}
+
+// score of (layer, sample, KV head j) = sum of its G heads' column sums, in head order
+__global__ __launch_bounds__(kThreads) void h2o_heads(const float* __restrict__ colsum, int Gh, int N,
+                                                      size_t total, float* __restrict__ score) {
+    for (size_t e = (size_t)blockIdx.x * kThreads + threadIdx.x; e < total; e += (size_t)gridDim.x * kThreads) {
+        const size_t lbj = e / N, t = e - lbj * N;
+        const float* c = colsum + lbj * Gh * N + t;
+        float v = 0.0f;
+        for (int g = 0; g < Gh; ++g) v += c[(size_t)g * N];
+        score[e] = v;
+    }
 }
 
 template <typename T, int D>
 hipError_t run_h2o(const void* q, const void* k, int L, int B, int Hq, int Hkv, int N, float scale,
                    float* score, void* ws, hipStream_t st) {
     float* linit = static_cast<float*>(ws);
+    float* colsum = linit + h2o_colsum_offset(L, B, Hq, N);
     const float sl2 = scale * kLog2e;
     const T* qt = static_cast<const T*>(q);
     const T* kt = static_cast<const T*>(k);
@@ -218,8 +229,12 @@ hipError_t run_h2o(const void* q, const void* k, int L, int B, int Hq, int Hkv, 
     const int NP = h2o_pitch(N);
     hipLaunchKernelGGL((h2o_pass1<T, D>), dim3((unsigned)((size_t)L * B * Hkv * nblk)), dim3(kThreads), 0, st, qt,
                        kt, Hq, Hkv, N, NP, npos, nblk, sl2, linit);
-    hipLaunchKernelGGL((h2o_pass2<T, D>), dim3((unsigned)((size_t)L * B * Hkv * nkb)), dim3(kThreads), 0, st, qt,
-                       kt, linit, Hq, Hkv, N, NP, nkb, sl2, score);
+    const int heads = L * B * Hq;
+    hipLaunchKernelGGL((h2o_pass2<T, D>), dim3((unsigned)((size_t)heads * nkb)), dim3(kThreads), 0, st, qt, kt,
+                       linit, heads, Hq, Hkv, N, NP, sl2, colsum);
+    const size_t total = (size_t)L * B * Hkv * N;
+    hipLaunchKernelGGL(h2o_heads, dim3((unsigned)std::min<size_t>((total + kThreads - 1) / kThreads, 4096)),
+                       dim3(kThreads), 0, st, colsum, Gh, N, total, score);
     return hipGetLastError();
 }
 

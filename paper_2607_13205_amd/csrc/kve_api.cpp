@@ -124,7 +124,9 @@ kve_status_t kve_h2o_score(const void* q, const void* k, kve_dtype_t dtype, int 
     if (G > kve::kH2oRowsPerGroup)
         return fail(KVE_ERR_UNSUPPORTED, "%s: Hq/Hkv=%d exceeds %d", fn, G, kve::kH2oRowsPerGroup);
     const long long nblk = (N + kve::kH2oRowsPerGroup / G - 1) / (kve::kH2oRowsPerGroup / G);
-    if ((long long)L * B * Hkv * nblk > kMaxGrid) return fail(KVE_ERR_UNSUPPORTED, "%s: shape too large", fn);
+    const long long nkb = (N + 127) / 128;  // pass-2 key blocks
+    if ((long long)L * B * Hkv * nblk > kMaxGrid || (long long)L * B * Hq * nkb > kMaxGrid)
+        return fail(KVE_ERR_UNSUPPORTED, "%s: shape too large", fn);
     const size_t need = kve::h2o_workspace(L, B, Hq, N);
     if (workspace_bytes < need || workspace == nullptr)
         return fail(KVE_ERR_WORKSPACE, "%s: workspace of %zu bytes < %zu needed", fn, workspace_bytes, need);

@@ -59,16 +59,21 @@ inline SnapPlan snap_plan(int L, int B, int Hq, int Hkv, int N, int W, int d = 1
 
 // ---------------------------------------------------------------------------
 // H2O score: pass 1 one start value (-lse2 / sl2) per (layer, sample, query
-// head, row), in rows of pitch h2o_pitch(N) floats; pass 2 the column sums
-// over the group's heads.  A pass-1 workgroup covers kH2oRowsPerGroup rows:
+// head, row), in rows of pitch h2o_pitch(N) floats; pass 2 one column sum per
+// (query head, key), added over the group's heads by a last step.  A pass-1 workgroup covers kH2oRowsPerGroup rows:
 // the G heads of a KV group at kH2oRowsPerGroup / G positions.
 // ---------------------------------------------------------------------------
 constexpr int kH2oRowsPerGroup = 128;
 
 inline int h2o_pitch(int N) { return (N + 63) / 64 * 64; }
 
+// floats before the per-(query head, key) column sums
+inline size_t h2o_colsum_offset(int L, int B, int Hq, int N) {
+    return align_up((size_t)L * B * Hq * h2o_pitch(N) * sizeof(float)) / sizeof(float);
+}
+
 inline size_t h2o_workspace(int L, int B, int Hq, int N) {
-    return align_up((size_t)L * B * Hq * h2o_pitch(N) * sizeof(float));
+    return h2o_colsum_offset(L, B, Hq, N) * sizeof(float) + align_up((size_t)L * B * Hq * N * sizeof(float));
 }
 
 hipError_t launch_snapkv(const void* q, const void* k, int dtype, int L, int B, int Hq, int Hkv,

@@ -223,16 +223,21 @@ struct ChunkRing {
 // the init value of the A-operand row of each element: init[32 b + c_row(i)]
 // with LDS_A, init[c_row(i)] otherwise (rows c_row(4 a .. 4 a + 3) are four
 // consecutive floats).
+//
+// c_init, when given, replaces `init`: acc[b] starts at c_init[LDS_A ? b : 0]
+// (values already in registers).
 template <typename T, int D, int KEYS, bool LDS_A>
 __device__ __forceinline__ void chunk_mma(f32x16 (&acc)[2], const ChunkReader<T, D, KEYS>& rd, const char* slot,
                                           const typename Mma<T>::frag (&reg)[KChunk<T, D, KEYS>::NSTEP],
-                                          const float* init, int lane) {
+                                          const float* init, int lane, const f32x16* c_init = nullptr) {
     using M = Mma<T>;
     constexpr int NS = KChunk<T, D, KEYS>::NSTEP;
     f32x16 c0[2];
 #pragma unroll
     for (int b = 0; b < 2; ++b) {
-        if (init == nullptr) {
+        if (c_init != nullptr) {
+            c0[b] = c_init[LDS_A ? b : 0];
+        } else if (init == nullptr) {
             c0[b] = f32x16{};
         } else {
 #pragma unroll

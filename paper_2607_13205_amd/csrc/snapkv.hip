@@ -40,7 +40,7 @@ constexpr int kWaves = 4;
 constexpr int kThreads = kWaves * 64;
 constexpr int kKeys = kSnapChunkKeys;  // keys per chunk
 constexpr int kRing = 4;               // LDS slots: the chunk in use and three ahead
-constexpr int kPoolTile = 256;
+constexpr int kPoolTile = 4096;  // keys per pool workgroup
 constexpr int kMaxPoolHalf = 127;
 
 template <typename T, int D>
@@ -175,14 +175,27 @@ __global__ __launch_bounds__(kThreads, 2) void snap_pass2(const T* __restrict__ 
     // The products start from -lse / sl2 of their row, so that sl2 * acc is
     // x - lse2 directly (the accumulator is float32: the offset costs no
     // precision that matters); padding rows (lse = +inf) start at -inf and add
-    // exactly 0.  Per-row values live in LDS: as registers they would stay
-    // live across the whole loop.
+    // exactly 0.  The window index of each row stays in LDS for the masked
+    // path: as registers the 32 loop-invariant bounds would stay live across
+    // the whole loop.
     if (threadIdx.x < kSnapRowsPerGroup) {
         sinit[threadIdx.x] = -lse[(size_t)sp.vseg * kSnapRowsPerGroup + threadIdx.x] / sl2;
         swin[threadIdx.x] = (sp.rg * kSnapRowsPerGroup + (int)threadIdx.x) % W;
     }
     QRows<T, D> qf;
     load_q<T, D>(qf, q, sp.seg, rows, sp.rg * kSnapRowsPerGroup + wave * 32 + (lane & 31), lane);
+    __syncthreads();  // sinit, swin written (nothing streams yet)
+    // start values of this lane's 16 rows, the same for every chunk
+    f32x16 c_init;
+#pragma unroll
+    for (int a = 0; a < 4; ++a) {
+        const float4 v = *reinterpret_cast<const float4*>(&sinit[wave * 32 + c_row(4 * a, lane)]);
+        c_init[4 * a] = v.x;
+        c_init[4 * a + 1] = v.y;
+        c_init[4 * a + 2] = v.z;
+        c_init[4 * a + 3] = v.w;
+    }
+    pin(c_init);
     typename G::Rd rd;
     rd.init(lane, 0);
     typename G::Ring ring_io;
@@ -212,7 +225,7 @@ __global__ __launch_bounds__(kThreads, 2) void snap_pass2(const T* __restrict__ 
             ring_io.advance(ring, s, u, src);
             if (s >= 1) reduce(s - 1);
             f32x16 acc[2];
-            chunk_mma<T, D, kKeys, false>(acc, rd, ring + u * G::C::BYTES, qf, sinit + wave * 32, lane);
+            chunk_mma<T, D, kKeys, false>(acc, rd, ring + u * G::C::BYTES, qf, nullptr, lane, &c_init);
             if (sp.t_begin + (s + 1) * kKeys > P_rows) {  // keys past the range end or inside the causal window
                 // key t is visible to window query i (position P_rows + i) iff t - P_rows <= i
 #pragma unroll
@@ -247,36 +260,51 @@ __global__ __launch_bounds__(kThreads, 2) void snap_pass2(const T* __restrict__ 
     reduce(sp.nch - 1);
 }
 
-__global__ __launch_bounds__(kPoolTile) void snap_pool(const float* __restrict__ raw, int planes,
-                                                       int segs, int N, int W, int pool_k, int tiles,
-                                                       float* __restrict__ score) {
+// Pool: one workgroup per (segment, tile of kPoolTile keys).  The tile and its
+// halo of h keys on each side are summed over the planes into LDS (16 keys per
+// thread, loads first), then each key takes the max over its window, which
+// stops at the end of the candidate prefix; window keys keep their raw score.
+__global__ __launch_bounds__(kThreads) void snap_pool(const float* __restrict__ raw, int planes, int segs,
+                                                      int N, int W, int pool_k, int tiles,
+                                                      float* __restrict__ score) {
     __shared__ float ss[kPoolTile + 2 * kMaxPoolHalf];
     const int tile = blockIdx.x % tiles;
     const int seg = blockIdx.x / tiles;
     const int h = pool_k / 2;
     const int P = N - W;
     const int t0 = tile * kPoolTile;
-    for (int e = threadIdx.x; e < kPoolTile + 2 * h; e += kPoolTile) {
-        const int u = t0 - h + e;
-        float s = -INFINITY;
-        if (u >= 0 && u < N) {
-            s = 0.0f;
-            for (int pl = 0; pl < planes; ++pl) s += raw[((size_t)pl * segs + seg) * N + u];
+    const int n = min(kPoolTile, N - t0) + 2 * h;  // staged keys t0 - h .. t0 + n - h - 1
+    constexpr int kPer = (kPoolTile + 2 * kMaxPoolHalf + kThreads - 1) / kThreads;
+    float v[kPer];
+#pragma unroll
+    for (int i = 0; i < kPer; ++i) v[i] = 0.0f;
+    for (int pl = 0; pl < planes; ++pl) {
+        const float* row = raw + ((size_t)pl * segs + seg) * N;
+#pragma unroll
+        for (int i = 0; i < kPer; ++i) {  // unconditional loads (clamped index), then the bound
+            const int u = t0 - h + i * kThreads + (int)threadIdx.x;
+            v[i] += row[min(max(u, 0), N - 1)];
         }
-        ss[e] = s;
+    }
+#pragma unroll
+    for (int i = 0; i < kPer; ++i) {
+        const int e = i * kThreads + (int)threadIdx.x;
+        const int u = t0 - h + e;
+        if (e < n) ss[e] = (u >= 0 && u < N) ? v[i] : -INFINITY;
     }
     __syncthreads();
-    const int t = t0 + threadIdx.x;
-    if (t >= N) return;
-    float v;
-    if (t < P) {
-        const int lo = max(0, t - h), hi = min(P - 1, t + h);
-        v = -INFINITY;
-        for (int u = lo; u <= hi; ++u) v = fmaxf(v, ss[u - t0 + h]);
-    } else {
-        v = ss[threadIdx.x + h];
+    for (int e = threadIdx.x; e < min(kPoolTile, N - t0); e += kThreads) {
+        const int t = t0 + e;
+        float m;
+        if (t < P) {
+            const int lo = max(0, t - h), hi = min(P - 1, t + h);
+            m = -INFINITY;
+            for (int u = lo; u <= hi; ++u) m = fmaxf(m, ss[u - t0 + h]);
+        } else {
+            m = ss[e + h];
+        }
+        score[(size_t)seg * N + t] = m;
     }
-    score[(size_t)seg * N + t] = v;
 }
 
 template <typename T, int D>
@@ -298,7 +326,7 @@ hipError_t run_snapkv(const void* q, const void* k, int L, int B, int Hq, int Hk
     hipLaunchKernelGGL((snap_pass2<T, D>), grid, dim3(kThreads), 0, st, qt, kt, N, W, p.rows, p.rgroups,
                        p.nranges, p.range_keys, sl2, lse, p.segs, raw);
     const int tiles = (N + kPoolTile - 1) / kPoolTile;
-    hipLaunchKernelGGL(snap_pool, dim3((unsigned)(p.segs * tiles)), dim3(kPoolTile), 0, st, raw, p.planes,
+    hipLaunchKernelGGL(snap_pool, dim3((unsigned)(p.segs * tiles)), dim3(kThreads), 0, st, raw, p.planes,
                        p.segs, N, W, pool_k, tiles, score);
     return hipGetLastError();
 }

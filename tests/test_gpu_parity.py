@@ -146,13 +146,12 @@ def _random_selection_case(rng, N, R_labels, R):
     return s, roles
 
 
-@pytest.mark.parametrize("seed", range(6))
-def test_topk_select_bit_exact_with_oracle(K, seed):
-    rng = np.random.default_rng(seed)
+@pytest.mark.parametrize("R", range(1, 9))  # the kernel is instantiated per bucket count
+def test_topk_select_bit_exact_with_oracle(K, R):
+    rng = np.random.default_rng(R)
     L, B, Hkv = 2, 2, 3
-    N = int(rng.choice([7, 300, 1000, 4097]))
+    N = [7, 300, 1000, 4097, 70000, 33, 2049, 65][R - 1]
     W = int(rng.integers(0, min(N, 40)))
-    R = int(rng.integers(1, 9))
     score = np.zeros((L, B, Hkv, N), dtype=np.float32)
     roles = np.zeros((B, N), dtype=np.int8)
     for b in range(B):
