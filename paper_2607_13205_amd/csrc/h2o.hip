@@ -5,8 +5,8 @@
 // heads of each KV head.
 //
 // Both passes are the causal QK^T on the matrix cores (bf16 32x32x16, fp32
-// 32x32x2) with operands streamed through a four-slot LDS ring by direct-to-LDS
-// loads, as in the SnapKV kernels:
+// 32x32x2) with operands streamed through a three-slot LDS ring by
+// direct-to-LDS loads, as in the SnapKV kernels:
 //   h2o_pass1  one workgroup per (KV group, block of positions): its 128 rows
 //              are the G heads of the group at 128/G consecutive positions
 //              (position-major), query fragments in registers; the keys up to
@@ -35,7 +35,7 @@ namespace {
 constexpr int kWaves = 4;
 constexpr int kThreads = kWaves * 64;
 constexpr int kKeys = 64;  // rows per chunk (keys in pass 1, query rows in pass 2)
-constexpr int kRing = 4;
+constexpr int kRing = 3;  // the operands are L2-resident: two chunks ahead suffice
 constexpr int kKeyBlock = 128;  // keys per pass-2 workgroup
 
 template <typename T, int D>
