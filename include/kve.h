@@ -124,8 +124,10 @@ size_t kve_h2o_workspace_size(int L, int B, int Hq, int Hkv, int N, int d);
  * Two passes on the matrix cores: per-row log-sum-exp over the causal row,
  * then column sums per query head, added over the G heads in head order.
  * Requires Hq/Hkv <= 128.  The workspace (kve_h2o_workspace_size bytes,
- * 256-byte aligned, owned by the caller) holds two floats per (layer, sample,
- * query head, row); its contents on entry do not matter.  Errors: KVE_ERR_INVALID_ARG (null pointers, bad shapes, negative or
+ * 256-byte aligned, owned by the caller) holds, per (layer, sample, query
+ * head), one start value per query row (rows padded to a multiple of 64
+ * floats) and one column sum per key; its contents on entry do not matter.
+ * Errors: KVE_ERR_INVALID_ARG (null pointers, bad shapes, negative or
  * non-finite scale), KVE_ERR_UNSUPPORTED (d not 64/128, Hq/Hkv > 128, grid
  * too large), KVE_ERR_WORKSPACE (too small), KVE_ERR_HIP (launch failure).
  */

@@ -108,5 +108,9 @@ def test_workspace_sizes_are_aligned_and_monotone(kve):
     a = kve.snapkv_workspace_size(1, 1, 32, 8, 8192, 32, 128)
     b = kve.snapkv_workspace_size(2, 1, 32, 8, 8192, 32, 128)
     assert a > 0 and a % 256 == 0 and b >= a
-    assert kve.h2o_workspace_size(1, 1, 32, 8, 16384, 128) == 32 * 16384 * 4
+    # one start value per query row (rows padded to 64 floats) and one column sum
+    # per (query head, key)
+    assert kve.h2o_workspace_size(1, 1, 32, 8, 16384, 128) == 2 * 32 * 16384 * 4
+    h = kve.h2o_workspace_size(2, 1, 32, 8, 1000, 128)
+    assert h % 256 == 0 and h >= 2 * 32 * 1024 * 4 + 2 * 32 * 1000 * 4
     assert kve.binding.LIB.kve_topk_workspace_size(1, 1, 8, 8192, 4) == 0
