@@ -5,7 +5,7 @@
 // heads of each KV head.
 //
 // Both passes are the causal QK^T on the matrix cores (bf16 32x32x16, fp32
-// 32x32x2) with operands streamed through a three-slot LDS ring by
+// 32x32x2) with operands streamed through a two-slot LDS ring by
 // direct-to-LDS loads, as in the SnapKV kernels:
 //   h2o_pass1  one workgroup per (KV group, block of positions): its 128 rows
 //              are the G heads of the group at 128/G consecutive positions
@@ -35,7 +35,9 @@ namespace {
 constexpr int kWaves = 4;
 constexpr int kThreads = kWaves * 64;
 constexpr int kKeys = 64;  // rows per chunk (keys in pass 1, query rows in pass 2)
-constexpr int kRing = 3;  // the operands are L2-resident: two chunks ahead suffice
+// The operands are L2-resident: one chunk ahead suffices, and the smaller ring
+// lets four workgroups share a compute unit.
+constexpr int kRing = 2;
 constexpr int kKeyBlock = 128;  // keys per pass-2 workgroup
 
 template <typename T, int D>

@@ -9,12 +9,12 @@
 // queries of the group (head-major), taken in row groups of 128 (a virtual
 // segment, vseg, is one segment and one row group).  A workgroup of four waves
 // owns a vseg and a contiguous range of its keys; each wave owns a 32-row
-// block whose query fragments stay in registers.  Keys stream through a
-// four-slot LDS ring in chunks of 64 with direct-to-LDS loads issued three
-// chunks ahead, so every wave keeps HBM requests in flight while it multiplies
-// on the matrix cores (bf16 32x32x16, fp32 32x32x2).  No workgroup waits on
-// another one; two workgroups share a compute unit, so that one's matrix-core
-// work overlaps the other's exponentials.
+// block whose query fragments stay in registers.  Keys stream through an LDS
+// ring in chunks of 64 with direct-to-LDS loads issued one to three chunks
+// ahead, so every wave keeps HBM requests in flight while it multiplies on the
+// matrix cores (bf16 32x32x16, fp32 32x32x2).  No workgroup waits on another
+// one; two to four workgroups share a compute unit, so that one's matrix-core
+// work overlaps another's exponentials.
 //
 //   pass 1   snap_pass1    S^T = K Q^T: each lane holds one row and 16 keys per
 //                          32-key block, so the running row sum of
@@ -39,15 +39,28 @@ namespace {
 constexpr int kWaves = 4;
 constexpr int kThreads = kWaves * 64;
 constexpr int kKeys = kSnapChunkKeys;  // keys per chunk
-constexpr int kRing = 4;               // LDS slots: the chunk in use and three ahead
 constexpr int kPoolTile = 4096;  // keys per pool workgroup
 constexpr int kMaxPoolHalf = 127;
 
-template <typename T, int D>
+// LDS ring depth and workgroups per compute unit of each pass.  bf16: pass 1
+// keeps two chunks in flight at three workgroups per CU, pass 2 one chunk at
+// four (its longer per-chunk work hides the shorter prefetch, and the extra
+// workgroup overlaps more of one wave's exponentials with another's products).
+// fp32 fragments need twice the registers: two workgroups, three chunks ahead.
+template <typename T>
+struct Tune {
+    static constexpr int kRing1 = 4, kOcc1 = 2, kRing2 = 4, kOcc2 = 2;
+};
+template <>
+struct Tune<__bf16> {
+    static constexpr int kRing1 = 3, kOcc1 = 3, kRing2 = 2, kOcc2 = 4;
+};
+
+template <typename T, int D, int RING>
 struct Geo {
     using C = KChunk<T, D, kKeys>;
     using Rd = ChunkReader<T, D, kKeys>;
-    using Ring = ChunkRing<T, D, kKeys, kWaves, kRing>;
+    using Ring = ChunkRing<T, D, kKeys, kWaves, RING>;
 };
 
 struct Span {
@@ -68,14 +81,14 @@ __device__ __forceinline__ Span span_of(int nranges, int rgroups, int range_keys
 
 // Query fragments of this wave's 32-row block (zero for padding rows).
 template <typename T, int D>
-using QRows = typename Mma<T>::frag[Geo<T, D>::C::NSTEP];
+using QRows = typename Mma<T>::frag[KChunk<T, D, kKeys>::NSTEP];
 
 template <typename T, int D>
 __device__ __forceinline__ void load_q(QRows<T, D>& qf, const T* q, int seg, int rows, int row, int lane) {
     using M = Mma<T>;
     const T* base = q + ((size_t)seg * rows + row) * D;
 #pragma unroll
-    for (int st = 0; st < Geo<T, D>::C::NSTEP; ++st) {
+    for (int st = 0; st < KChunk<T, D, kKeys>::NSTEP; ++st) {
         qf[st] = row < rows ? M::load(base, st * M::KSTEP + (lane >> 5) * M::KPL) : M::zero();
         pin(qf[st]);
     }
@@ -88,17 +101,18 @@ struct KeyChunks {
     int t_begin, t_end;
     __device__ __forceinline__ void operator()(int c, const char** rows, int* valid) const {
         const int t0 = t_begin + c * kKeys;
-        *rows = kseg + (size_t)t0 * Geo<T, D>::C::ROW;
+        *rows = kseg + (size_t)t0 * KChunk<T, D, kKeys>::ROW;
         *valid = t_end - t0;
     }
 };
 
 template <typename T, int D>
-__global__ __launch_bounds__(kThreads, 2) void snap_pass1(const T* __restrict__ q, const T* __restrict__ k,
+__global__ __launch_bounds__(kThreads, Tune<T>::kOcc1) void snap_pass1(const T* __restrict__ q, const T* __restrict__ k,
                                                           int N, int W, int rows, int rgroups, int nranges,
                                                           int range_keys, float sl2,
                                                           float* __restrict__ stats) {
-    using G = Geo<T, D>;
+    constexpr int kRing = Tune<T>::kRing1;
+    using G = Geo<T, D, kRing>;
     __shared__ __align__(16) char ring[kRing * G::C::BYTES];
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -157,12 +171,13 @@ __global__ __launch_bounds__(kSnapRowsPerGroup) void snap_combine(const float* _
 }
 
 template <typename T, int D>
-__global__ __launch_bounds__(kThreads, 2) void snap_pass2(const T* __restrict__ q, const T* __restrict__ k,
+__global__ __launch_bounds__(kThreads, Tune<T>::kOcc2) void snap_pass2(const T* __restrict__ q, const T* __restrict__ k,
                                                           int N, int W, int rows, int rgroups, int nranges,
                                                           int range_keys, float sl2,
                                                           const float* __restrict__ lse, int segs,
                                                           float* __restrict__ raw) {
-    using G = Geo<T, D>;
+    constexpr int kRing = Tune<T>::kRing2;
+    using G = Geo<T, D, kRing>;
     __shared__ __align__(16) char ring[kRing * G::C::BYTES];
     __shared__ float scol[2][kWaves][kKeys];                   // column sums per row block, two chunks
     __shared__ __align__(16) float sinit[kSnapRowsPerGroup];  // -lse / sl2 of each row
