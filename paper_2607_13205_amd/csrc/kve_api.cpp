@@ -98,16 +98,6 @@ kve_status_t kve_snapkv_score(const void* q_win, const void* k, kve_dtype_t dtyp
                     p.total);
     if (!aligned(workspace)) return fail(KVE_ERR_INVALID_ARG, "%s: workspace not 256-byte aligned", fn);
     if (scale == 0.0f) scale = 1.0f / std::sqrt((float)d);
-    // The single-read kernel where it applies (bf16, every vseg's items fit
-    // twice over in the resident workgroups), else the two-pass kernels.
-    // KVE_SNAPKV_PATH=two_pass selects the two-pass kernels for every input.
-    const char* path = std::getenv("KVE_SNAPKV_PATH");
-    const bool two_pass = path != nullptr && std::strcmp(path, "two_pass") == 0;
-    if (!two_pass && (long long)p.n_vsegs * p.nitems1 <= kMaxGrid &&
-        kve::snapkv_onepass_fits((int)dtype, d, p.nitems1))
-        return from_hip(kve::launch_snapkv_onepass(q_win, k, L, B, Hq, Hkv, N, W, d, scale, pool_k, score,
-                                                   workspace, static_cast<hipStream_t>(stream)),
-                        fn);
     return from_hip(kve::launch_snapkv(q_win, k, (int)dtype, L, B, Hq, Hkv, N, W, d, scale, pool_k, score,
                                        workspace, static_cast<hipStream_t>(stream)),
                     fn);

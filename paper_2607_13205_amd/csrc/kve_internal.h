@@ -24,15 +24,9 @@ constexpr int kSnapChunkKeys = 64;
 constexpr int kSnapTargetGroups = 4096;  // workgroups per pass the range size aims at
 constexpr int kSnapMaxRangeChunks = 32;  // at most 2048 keys per range
 
-// The single-read kernel (bf16) takes items of kSnap1ItemKeys keys of one
-// vseg; it writes one log-sum-exp per (vseg, item, row) and keeps a ticket, an
-// error word, and per-vseg arrival counters and ready flags in the workspace.
-constexpr int kSnap1ItemKeys = 256;
-constexpr int kSnap1CtlHead = 64;  // words before the per-vseg counters
-
 struct SnapPlan {
-    int segs, rows, rgroups, n_vsegs, range_keys, nranges, planes, nitems1;
-    size_t off_stats, off_lse, off_raw, off_part1, off_ctl, total;
+    int segs, rows, rgroups, n_vsegs, range_keys, nranges, planes;
+    size_t off_stats, off_lse, off_raw, total;
 };
 
 inline SnapPlan snap_plan(int L, int B, int Hq, int Hkv, int N, int W, int d = 128) {
@@ -59,11 +53,6 @@ inline SnapPlan snap_plan(int L, int B, int Hq, int Hkv, int N, int W, int d = 1
     off = align_up(off + (size_t)p.n_vsegs * kSnapRowsPerGroup * sizeof(float));
     p.off_raw = off;
     off = align_up(off + (size_t)p.planes * p.segs * N * sizeof(float));
-    p.nitems1 = (N + kSnap1ItemKeys - 1) / kSnap1ItemKeys;
-    p.off_part1 = off;
-    off = align_up(off + (size_t)p.n_vsegs * p.nitems1 * kSnapRowsPerGroup * sizeof(float));
-    p.off_ctl = off;
-    off = align_up(off + (size_t)(kSnap1CtlHead + 2 * p.n_vsegs) * sizeof(unsigned));
     p.total = off;
     return p;
 }
@@ -90,18 +79,6 @@ inline size_t h2o_workspace(int L, int B, int Hq, int N) {
 hipError_t launch_snapkv(const void* q, const void* k, int dtype, int L, int B, int Hq, int Hkv,
                          int N, int W, int d, float scale, int pool_k, float* score, void* ws,
                          hipStream_t st);
-
-// Pool step of the SnapKV score: adds the planes of raw column sums and
-// max-pools the candidate prefix into score.
-hipError_t launch_snap_pool(const float* raw, int planes, int segs, int N, int W, int pool_k, float* score,
-                            hipStream_t st);
-
-// Single-read SnapKV score (bf16 only): whether it applies to these shapes on
-// the current device (every vseg's items fit twice over in the resident
-// workgroups), and its launcher (same arguments and workspace as launch_snapkv).
-bool snapkv_onepass_fits(int dtype, int d, int nitems);
-hipError_t launch_snapkv_onepass(const void* q, const void* k, int L, int B, int Hq, int Hkv, int N, int W,
-                                 int d, float scale, int pool_k, float* score, void* ws, hipStream_t st);
 
 hipError_t launch_h2o(const void* q, const void* k, int dtype, int L, int B, int Hq, int Hkv,
                       int N, int d, float scale, float* score, void* ws, hipStream_t st);

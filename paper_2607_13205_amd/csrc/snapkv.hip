@@ -340,18 +340,13 @@ hipError_t run_snapkv(const void* q, const void* k, int L, int B, int Hq, int Hk
                        p.nranges, p.rows, p.rgroups, lse);
     hipLaunchKernelGGL((snap_pass2<T, D>), grid, dim3(kThreads), 0, st, qt, kt, N, W, p.rows, p.rgroups,
                        p.nranges, p.range_keys, sl2, lse, p.segs, raw);
-    return launch_snap_pool(raw, p.planes, p.segs, N, W, pool_k, score, st);
+    const int tiles = (N + kPoolTile - 1) / kPoolTile;
+    hipLaunchKernelGGL(snap_pool, dim3((unsigned)(p.segs * tiles)), dim3(kThreads), 0, st, raw, p.planes,
+                       p.segs, N, W, pool_k, tiles, score);
+    return hipGetLastError();
 }
 
 }  // namespace
-
-hipError_t launch_snap_pool(const float* raw, int planes, int segs, int N, int W, int pool_k, float* score,
-                            hipStream_t st) {
-    const int tiles = (N + kPoolTile - 1) / kPoolTile;
-    hipLaunchKernelGGL(snap_pool, dim3((unsigned)(segs * tiles)), dim3(kThreads), 0, st, raw, planes, segs, N,
-                       W, pool_k, tiles, score);
-    return hipGetLastError();
-}
 
 hipError_t launch_snapkv(const void* q, const void* k, int dtype, int L, int B, int Hq, int Hkv,
                          int N, int W, int d, float scale, int pool_k, float* score, void* ws,

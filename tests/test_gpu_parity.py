@@ -70,14 +70,9 @@ SNAP_CASES = [
 ]
 
 
-# bf16 inputs take the single-read kernel unless KVE_SNAPKV_PATH=two_pass
-# selects the two-pass kernels (fp32 inputs always take those)
-@pytest.mark.parametrize("path", ["default", "two_pass"])
 @pytest.mark.parametrize("wl", SNAP_CASES, ids=lambda w: w.name)
-def test_snapkv_score_matches_oracle(K, wl, path, monkeypatch):
-    if path == "two_pass":
-        monkeypatch.setenv("KVE_SNAPKV_PATH", "two_pass")
-    note(f"snapkv parity {wl} path={path}")
+def test_snapkv_score_matches_oracle(K, wl):
+    note(f"snapkv parity {wl}")
     inp = WL.make_inputs(wl, device="cuda", with_v=False)
     score = run_snapkv(K, inp["q"], inp["k"], wl.pool_k)
     ref = O.snapkv_score(f64(inp["q"]), f64(inp["k"]), wl.Hkv, wl.pool_k)
