@@ -35,13 +35,21 @@ __device__ __forceinline__ int chunk_swz(int r, int c) {
 // chunks kept in flight.  Callers wait with explicit vmcnt counts instead;
 // loads the compiler does not know of can only make its own waits stricter
 // (memory operations complete in order per wave), never too lenient.
+//
+// NT marks the load non-temporal: for data read once (streamed keys), so that
+// its lines are the first the caches give up.
+template <bool NT = false>
 __device__ __forceinline__ void lds_dma16(const char* base, unsigned voff, const char* lds_dst) {
     const unsigned m0 = __builtin_amdgcn_readfirstlane(
         (unsigned)(size_t)(const __attribute__((address_space(3))) char*)lds_dst);
     // the LDS base goes in M0; one wait state must separate its write from the
     // direct-to-LDS load that reads it
-    asm volatile("s_nop 0\n\tglobal_load_lds_dwordx4 %0, %1"
-                 :: "v"(voff), "s"(base), "{m0}"(m0) : "memory");
+    if constexpr (NT)
+        asm volatile("s_nop 0\n\tglobal_load_lds_dwordx4 %0, %1 nt"
+                     :: "v"(voff), "s"(base), "{m0}"(m0) : "memory");
+    else
+        asm volatile("s_nop 0\n\tglobal_load_lds_dwordx4 %0, %1"
+                     :: "v"(voff), "s"(base), "{m0}"(m0) : "memory");
 }
 
 // Matrix-core fragments of a chunk, read from LDS with per-lane byte offsets
@@ -87,8 +95,8 @@ struct ChunkReader {
 // per chunk; load j lands at byte (j * NWAVES + wv) * 1024 of the slot.  A
 // chunk with fewer than KEYS valid rows reads row 0 in place of the missing
 // rows (never outside the segment), so the number of loads per chunk stays
-// fixed; callers mask those keys.
-template <typename T, int D, int KEYS, int NWAVES>
+// fixed; callers mask those keys.  NT: non-temporal loads (see lds_dma16).
+template <typename T, int D, int KEYS, int NWAVES, bool NT = false>
 struct ChunkWriter {
     using C = KChunk<T, D, KEYS>;
     static constexpr int LPW = C::BYTES / (NWAVES * 1024);
@@ -110,12 +118,12 @@ struct ChunkWriter {
     __device__ __forceinline__ void issue(char* slot, const char* rows, int valid) const {
         if (valid >= KEYS) {
 #pragma unroll
-            for (int j = 0; j < LPW; ++j) lds_dma16(rows, goff[j], slot + (j * NWAVES + wv) * 1024);
+            for (int j = 0; j < LPW; ++j) lds_dma16<NT>(rows, goff[j], slot + (j * NWAVES + wv) * 1024);
         } else {
 #pragma unroll
             for (int j = 0; j < LPW; ++j) {
                 const int r = (int)(goff[j] / C::ROW);
-                lds_dma16(rows, r < valid ? goff[j] : goff[j] - (unsigned)(r * C::ROW),
+                lds_dma16<NT>(rows, r < valid ? goff[j] : goff[j] - (unsigned)(r * C::ROW),
                           slot + (j * NWAVES + wv) * 1024);
             }
         }
@@ -181,10 +189,10 @@ __device__ __forceinline__ void lds_barrier() {
 // NWAVES waves of a workgroup.  The caller names each chunk's first row and
 // its number of valid rows with src(c, &rows, &valid).
 // ---------------------------------------------------------------------------
-template <typename T, int D, int KEYS, int NWAVES, int RING>
+template <typename T, int D, int KEYS, int NWAVES, int RING, bool NT = false>
 struct ChunkRing {
     using C = KChunk<T, D, KEYS>;
-    using Wr = ChunkWriter<T, D, KEYS, NWAVES>;
+    using Wr = ChunkWriter<T, D, KEYS, NWAVES, NT>;
     Wr wr;
     int nch;
 
