@@ -67,6 +67,11 @@ SNAP_CASES = [
     # 32 vsegs x 71 chunks: ranges of three 128-key chunks, the last one ragged
     custom("multirange", 2, 2, 8, 8, 9000, 16, 128, 7, "bf16"),
     custom("f32multirange", 2, 2, 8, 4, 9000, 8, 64, 5, "f32"),
+    # wide pools across many ranges of 256 keys (half-widths 64 and 65)
+    custom("pool129", 1, 2, 8, 4, 5000, 16, 128, 129, "bf16"),
+    custom("pool131", 1, 2, 8, 4, 5000, 16, 128, 131, "bf16"),
+    # a last range of 6 keys, shorter than the half-width 7
+    custom("shorttail", 1, 1, 4, 2, 1030, 8, 64, 15, "bf16"),
 ]
 
 
