@@ -17,15 +17,21 @@ struct KChunk {
     static constexpr int NSTEP = D / Mma<T>::KSTEP;
 };
 
-// Byte offset of 16-byte piece c of key row r inside a chunk buffer.  The XOR
-// swizzle puts the eight consecutive rows that one LDS read cycle of a
-// matrix-core operand touches (same piece) on distinct 16-byte bank groups.
-// It changes only the low three bits of the piece index, so pieces c and
-// c + 8 of a row stay 128 bytes apart.
+// Byte offset of 16-byte piece c of key row r inside a chunk buffer.  A
+// matrix-core operand read (ds_read_b128) serves sixteen lanes, i.e. sixteen
+// consecutive rows at the same piece, per LDS cycle; the XOR swizzle of the
+// piece index puts them on sixteen distinct 16-byte bank groups.  Rows of
+// sixteen or more pieces: piece ^ (r % 16).  Rows of eight pieces (two rows per
+// 256-byte bank cycle): piece ^ ((r / 2) % 8).  Rows r and r + 32 share the
+// swizzle, so a second 32-row block is an immediate offset away.
+template <int ROW>
+__device__ __forceinline__ int chunk_swz_bits(int r) {
+    static_assert(ROW >= 128, "rows of at least eight 16-byte pieces");
+    return ROW >= 256 ? (r & 15) : ((r >> 1) & 7);
+}
 template <int ROW>
 __device__ __forceinline__ int chunk_swz(int r, int c) {
-    static_assert(ROW >= 128, "rows of at least eight 16-byte pieces");
-    return r * ROW + ((c ^ (r & 7)) << 4);
+    return r * ROW + ((c ^ chunk_swz_bits<ROW>(r)) << 4);
 }
 
 // One direct-to-LDS load: lane i's 16 bytes at base + voff (bytes) land in LDS
@@ -56,17 +62,15 @@ __device__ __forceinline__ void lds_dma16(const char* base, unsigned voff, const
 // worked out once per kernel.  Fragment (kb, st) of lane l is key row
 // 32 kb + l%32 (counted from the wave's first key row, `base` bytes into the
 // chunk) at k-step st.  With bf16 the swizzled offset of each k-step is
-// kept in a register, so that a read is one ds_read_b128 whose slot and
-// key-block parts are immediate offsets; fp32 chunks (D/2 k-steps) work the
-// offset out at each read.
+// kept in a register (k-step st reads piece 2 st + lane / 32), so that a read
+// is one ds_read_b128 whose slot and key-block parts are immediate offsets;
+// fp32 chunks (D/2 k-steps) work the offset out at each read.
 template <typename T, int D, int KEYS>
 struct ChunkReader {
     using C = KChunk<T, D, KEYS>;
     using M = Mma<T>;
     static constexpr bool kTable = sizeof(T) == 2;
-    // bf16: k-step st reads piece 2 st + (lane / 32); steps st and st + 4 are
-    // 128 bytes apart, so four offsets cover all steps
-    static constexpr int NOFF = kTable ? (C::NSTEP < 4 ? C::NSTEP : 4) : 1;
+    static constexpr int NOFF = kTable ? C::NSTEP : 1;
     int off[NOFF];
     int lane, base;
 
@@ -84,7 +88,7 @@ struct ChunkReader {
     }
     __device__ __forceinline__ typename M::frag get(const char* slot, int kb, int st) const {
         if constexpr (kTable)
-            return M::load(slot + kb * 32 * C::ROW + (st / 4) * 128 + off[st % 4], 0);
+            return M::load(slot + kb * 32 * C::ROW + off[st], 0);
         else
             return M::load(slot + kb * 32 * C::ROW + offset(st), 0);
     }
@@ -110,7 +114,7 @@ struct ChunkWriter {
         for (int j = 0; j < LPW; ++j) {
             const int o = (j * NWAVES + wv) * 1024 + lane * 16;
             const int r = o / C::ROW;
-            const int c = ((o - r * C::ROW) >> 4) ^ (r & 7);  // inverse of chunk_swz
+            const int c = ((o - r * C::ROW) >> 4) ^ chunk_swz_bits<C::ROW>(r);  // inverse of chunk_swz
             goff[j] = (unsigned)(r * C::ROW + c * 16);
         }
     }
