@@ -12,7 +12,9 @@ Prints one JSON line.  ``value`` is prefill tokens scored and compressed per
 second (a token counts once it has passed through all layers and KV heads);
 ``roofline`` refers to the SnapKV score call, timed with HIP events on the
 stream it is launched on; ``cpu_baseline`` times the float64 CPU oracle on a
-bounded sample of the same workload.
+bounded sample of the same workload; ``policies`` gives the step time of the
+same workload under fair eviction and the No-KEY counterfactual, which reuse
+every kernel with other quotas.
 
 ``roofline.traffic`` is the measured HBM traffic of one score call, read from
 the counter summary in profiles/ (rocprofv3 FETCH_SIZE and WRITE_SIZE,
@@ -57,6 +59,8 @@ def parse():
                     help="target CPU time of the oracle baseline sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-h2o", action="store_true", help="skip the H2O scorer leg")
+    ap.add_argument("--no-policies", action="store_true",
+                    help="skip the fair-eviction and No-KEY step timings")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a plain device copy of 1 GiB (5 times), for counter calibration")
     return ap.parse_args()
@@ -189,6 +193,38 @@ def h2o_leg(K, WL, steps):
             "mfma_frac_1pass": round(tf2 / 2 / BF16_MFMA_PEAK_TFLOPS, 4)}
 
 
+def policy_leg(WL, pipeline, wl, inp, budget, W, pool, steps):
+    """Step time (HIP events) of the same workload under fair eviction and the
+    No-KEY counterfactual: same kernels, other bucket labels and quotas."""
+    import torch
+    Policy = pipeline.Policy
+    out = {}
+    for name, pol in (("fair", Policy.fair(4)), ("no_key", Policy.no_role(WL.KEY, 4))):
+        buckets = pol.buckets(inp["roles"])
+        buckets_t = torch.from_numpy(buckets).to(inp["k"].device)
+        _, kept, k_cap = pol.allocate(buckets, budget, W)
+        bufs = pipeline.alloc_buffers(inp["k"], wl.Hq, W, pol.R, k_cap, scorer=wl.scorer)
+
+        def step():
+            pipeline.evict(inp["q"], inp["k"], inp["v"], buckets, buckets_t, pol, budget, W, pool,
+                           bufs, scorer=wl.scorer)
+
+        for _ in range(2):
+            step()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(steps):
+            step()
+        e1.record()
+        torch.cuda.synchronize()
+        out[name] = {"ms_per_step": round(e0.elapsed_time(e1) / steps, 4), "k_cap": k_cap,
+                     "kept_mean": round(float(kept.mean()), 1)}
+        del bufs
+        torch.cuda.empty_cache()
+    return out
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -277,9 +313,12 @@ def main():
             "ms": round(ms_score, 4), "algorithmic_bytes": score_bytes,
         },
     }
+    del bufs
+    torch.cuda.empty_cache()
+    if not args.no_policies:
+        print("[bench] fair-eviction and No-KEY steps", file=sys.stderr, flush=True)
+        out["policies"] = policy_leg(WL, pipeline, wl, inp, budget, W, pool, max(3, args.steps // 2))
     if not args.no_h2o and wl.name != "h2o16k":
-        del bufs
-        torch.cuda.empty_cache()
         print("[bench] H2O leg", file=sys.stderr, flush=True)
         out["h2o"] = h2o_leg(K, WL, max(3, args.steps // 2))
     if not args.no_cpu_baseline:

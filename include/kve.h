@@ -167,6 +167,38 @@ kve_status_t kve_role_allocate(const int8_t* roles, int B, int N, int R,
                                int32_t* quota_out, int32_t* kept_out,
                                int32_t* k_cap_out);
 
+/*
+ * Fair-eviction quotas (§5 "Fair-eviction baseline": the same retention rate
+ * for every bucket).  kve_role_allocate with each sample's own bucket
+ * populations as the weights, alpha_r = n_r: with P = N - W candidates and
+ * K_p as above, bucket r keeps ceil(n_r * K_p / P) of its n_r candidates (no
+ * bucket overflows, so there is no redistribution; the quotas may exceed K_p
+ * by fewer than R tokens through the ceilings).  A sample with no candidate
+ * prefix (W = N) keeps the window only; budget >= 1 keeps every token.
+ * Arguments, ownership and errors as for kve_role_allocate, without alpha.
+ */
+kve_status_t kve_role_allocate_fair(const int8_t* roles, int B, int N, int R,
+                                    double budget, int W, int32_t* quota_out,
+                                    int32_t* kept_out, int32_t* k_cap_out);
+
+/*
+ * Bucket relabelling: out[i] = map[roles[i]] for i < n.  With it the same
+ * allocator and top-k express policies over a coarser partition than the
+ * labels, e.g. the No-X counterfactual of §3 ("Counterfactual", Table 2):
+ * map role X to bucket 1 and every other role to bucket 0, then allocate with
+ * alpha = (1, 0), so that the K_p prefix slots go to the best-scoring tokens
+ * of any role but X.
+ *
+ *   roles [n] int8 labels in [0, R_in) (HOST)
+ *   map   [R_in] int8 buckets in [0, 8) (HOST)
+ *   out   [n] int8 (HOST, may alias roles)
+ *
+ * Rejects R_in outside [1, 127], map entries outside [0, 8) and labels outside
+ * [0, R_in); out is untouched on error.
+ */
+kve_status_t kve_role_map(const int8_t* roles, size_t n, const int8_t* map, int R_in,
+                          int8_t* out);
+
 /* ------------------------------------------------------------------------- */
 /* Per-role top-k selection (Algorithm 1, per-bucket top-k).                  */
 /* ------------------------------------------------------------------------- */

@@ -33,7 +33,14 @@ that uses it):
   R10 budget left once every positive-weight bucket is full stays unspent; a
       budget B >= 1 is the full-cache baseline and keeps all N tokens;
   R12 equal scores: the lower token index wins;
-  R13 -0.0 ranks equal to +0.0 and NaN ranks below every number.
+  R13 -0.0 ranks equal to +0.0 and NaN ranks below every number;
+  R17 the No-X counterfactual (§3 "Counterfactual", Table 2) keeps the same
+      K_p prefix slots as the other policies, filled by score from the prefix
+      tokens whose role is not X; when fewer such tokens exist the slots left
+      stay empty;
+  R18 fair eviction (§5 "Fair-eviction baseline") retains every bucket at the
+      same rate: bucket r keeps ceil(n_r * K_p / P) of its n_r candidates, the
+      ceiling of R7 as for the role policy.
 """
 
 from __future__ import annotations
@@ -55,6 +62,11 @@ __all__ = [
     "role_counts",
     "role_allocate",
     "role_allocate_batch",
+    "role_map",
+    "no_role_policy",
+    "no_role_keep",
+    "fair_allocate",
+    "fair_allocate_batch",
     "rank_key",
     "select_keep",
     "topk_select",
@@ -266,6 +278,81 @@ def role_allocate_batch(roles: np.ndarray, R: int, alpha, budget: float, W: int)
     kept = np.zeros(Bt, dtype=np.int64)
     for b in range(Bt):
         quota[b], kept[b] = role_allocate(roles[b], R, alpha, budget, W)
+    return quota, kept, int(kept.max()) if Bt else 0
+
+
+# ---------------------------------------------------------------------------
+# Other policies over the same partition-and-allocate container: the No-X
+# counterfactual (§3 "Counterfactual", Table 2) and fair eviction (§5)
+# ---------------------------------------------------------------------------
+
+def role_map(roles: np.ndarray, bucket_of) -> np.ndarray:
+    """Bucket labels: token t goes to bucket bucket_of[roles[t]]."""
+    roles = np.asarray(roles)
+    bucket_of = [int(x) for x in bucket_of]
+    if np.any(roles < 0) or np.any(roles >= len(bucket_of)):
+        raise ValueError("role label outside the map")
+    out = np.empty(roles.shape, dtype=np.int8)
+    for r, b in enumerate(bucket_of):
+        out[roles == r] = b
+    return out
+
+
+def no_role_policy(x: int, n_roles: int):
+    """No-X as a two-bucket policy: role x alone in bucket 1 with weight 0,
+    every other role in bucket 0 with weight 1.  Returns (bucket_of, alpha)."""
+    if not 0 <= x < n_roles:
+        raise ValueError("banned role outside [0, n_roles)")
+    bucket_of = [1 if r == x else 0 for r in range(n_roles)]
+    return bucket_of, [1.0, 0.0]
+
+
+def no_role_keep(score: np.ndarray, roles: np.ndarray, x: int, budget: float,
+                 W: int) -> np.ndarray:
+    """Kept indices of one segment under No-X, from the definition (R17): the
+    window, plus the K_p best-scoring prefix tokens whose role is not x (score
+    descending, index ascending; NaN last), ascending."""
+    score = np.asarray(score, dtype=np.float64)
+    roles = np.asarray(roles)
+    N = score.shape[0]
+    if budget >= 1.0:
+        return np.arange(N, dtype=np.int64)
+    K = min(N, ceil_guarded(budget * N))
+    K_p = max(0, K - W)
+    key = np.where(np.isnan(score), -np.inf, score)
+    allowed = [t for t in range(N - W) if roles[t] != x]
+    allowed.sort(key=lambda t: (-key[t], t))
+    kept = allowed[:K_p] + list(range(N - W, N))
+    return np.array(sorted(kept), dtype=np.int64)
+
+
+def fair_allocate(roles: np.ndarray, R: int, budget: float, W: int):
+    """Fair-eviction quotas of one sample (R18): (quota[R], kept)."""
+    roles = np.asarray(roles)
+    N = int(roles.shape[0])
+    if not (0 <= W <= N):
+        raise ValueError("need 0 <= W <= N")
+    if budget <= 0:
+        raise ValueError("budget must be > 0")
+    if np.any(roles < 0) or np.any(roles >= R):
+        raise ValueError("role label outside [0, R)")
+    n = role_counts(roles, R, W)
+    if budget >= 1.0:
+        return n.copy(), N
+    if n.sum() == 0:                       # no candidate prefix: the window alone
+        return np.zeros(R, dtype=np.int64), W
+    # the weight of a bucket is its own population: the same rate everywhere
+    return role_allocate(roles, R, [float(c) for c in n], budget, W)
+
+
+def fair_allocate_batch(roles: np.ndarray, R: int, budget: float, W: int):
+    """fair_allocate for every sample of roles [B, N]: (quota[B, R], kept[B], k_cap)."""
+    roles = np.asarray(roles)
+    Bt = roles.shape[0]
+    quota = np.zeros((Bt, R), dtype=np.int64)
+    kept = np.zeros(Bt, dtype=np.int64)
+    for b in range(Bt):
+        quota[b], kept[b] = fair_allocate(roles[b], R, budget, W)
     return quota, kept, int(kept.max()) if Bt else 0
 
 

@@ -5,14 +5,18 @@ The hot path runs in libkve.so (HIP); this package is its thin Python binding:
   snapkv_score   SnapKV windowed score + GQA sum + prefix max-pool
   h2o_score      H2O accumulated score (baseline scorer)
   role_allocate  per-bucket quotas with redistribution (host)
+  role_allocate_fair  equal retention rate per bucket (host)
+  role_map       relabel roles into buckets, e.g. the No-X counterfactual (host)
   topk_select    per-role top-k with the window kept, ascending indices
   kv_compact     dense K/V cache of the kept rows
   pipeline.evict the whole step over resident tensors
 """
 
 from .binding import (EXPORTED, KveError, h2o_score, h2o_workspace_size, kv_compact,  # noqa: F401
-                      last_error, role_allocate, snapkv_score, snapkv_workspace_size, topk_select)
+                      last_error, role_allocate, role_allocate_fair, role_map, snapkv_score,
+                      snapkv_workspace_size, topk_select)
 from . import pipeline  # noqa: F401
 
-__all__ = ["snapkv_score", "h2o_score", "role_allocate", "topk_select", "kv_compact",
-           "snapkv_workspace_size", "h2o_workspace_size", "KveError", "last_error", "pipeline"]
+__all__ = ["snapkv_score", "h2o_score", "role_allocate", "role_allocate_fair", "role_map",
+           "topk_select", "kv_compact", "snapkv_workspace_size", "h2o_workspace_size", "KveError",
+           "last_error", "pipeline"]

@@ -31,7 +31,7 @@ EXPORTED = (
     "kve_version", "kve_last_error",
     "kve_snapkv_workspace_size", "kve_snapkv_score",
     "kve_h2o_workspace_size", "kve_h2o_score",
-    "kve_role_allocate",
+    "kve_role_allocate", "kve_role_allocate_fair", "kve_role_map",
     "kve_topk_workspace_size", "kve_topk_select",
     "kve_kv_compact",
 )
@@ -62,6 +62,9 @@ def _load():
                           [c_float, c_void, c_void, c_size, c_void]),
         "kve_role_allocate": (c_int, [c_void, c_int, c_int, c_int, c_void, c_double, c_int,
                                       c_void, c_void, c_void]),
+        "kve_role_allocate_fair": (c_int, [c_void, c_int, c_int, c_int, c_double, c_int,
+                                           c_void, c_void, c_void]),
+        "kve_role_map": (c_int, [c_void, c_size, c_void, c_int, c_void]),
         "kve_topk_workspace_size": (c_size, [c_int] * 5),
         "kve_topk_select": (c_int, [c_void, c_void, c_void] + [c_int] * 7 +
                             [c_void, c_void, c_void, c_size, c_void]),
@@ -204,6 +207,36 @@ def role_allocate(roles, R: int, alpha, budget: float, W: int):
                                  quota.ctypes.data_as(ctypes.c_void_p),
                                  kept.ctypes.data_as(ctypes.c_void_p), ctypes.byref(kcap)))
     return quota, kept, int(kcap.value)
+
+
+def role_allocate_fair(roles, R: int, budget: float, W: int):
+    """Fair-eviction quotas (every bucket kept at the same rate), host.
+    roles: int8 array [B, N] (host).  Returns (quota int32 [B, R], kept int32 [B], k_cap)."""
+    roles = np.ascontiguousarray(np.asarray(roles, dtype=np.int8))
+    if roles.ndim == 1:
+        roles = roles[None]
+    B, N = roles.shape
+    quota = np.zeros((B, R), dtype=np.int32)
+    kept = np.zeros(B, dtype=np.int32)
+    kcap = ctypes.c_int32(0)
+    _check(LIB.kve_role_allocate_fair(roles.ctypes.data_as(ctypes.c_void_p), B, N, int(R),
+                                      float(budget), int(W),
+                                      quota.ctypes.data_as(ctypes.c_void_p),
+                                      kept.ctypes.data_as(ctypes.c_void_p), ctypes.byref(kcap)))
+    return quota, kept, int(kcap.value)
+
+
+def role_map(roles, bucket_of):
+    """Bucket labels out[i] = bucket_of[roles[i]] (host int8 arrays of any shape)."""
+    roles = np.ascontiguousarray(np.asarray(roles, dtype=np.int8))
+    bmap = np.ascontiguousarray(np.asarray(bucket_of, dtype=np.int8))
+    if bmap.ndim != 1 or bmap.size == 0:
+        raise ValueError("bucket_of must be a non-empty 1-D sequence")
+    out = np.empty_like(roles)
+    _check(LIB.kve_role_map(roles.ctypes.data_as(ctypes.c_void_p), roles.size,
+                            bmap.ctypes.data_as(ctypes.c_void_p), int(bmap.size),
+                            out.ctypes.data_as(ctypes.c_void_p)))
+    return out
 
 
 def topk_select(score, roles, quota, W: int, R: int, k_cap: int, idx_out=None, count_out=None,

@@ -60,6 +60,82 @@ kve_status_t check_common(const char* fn, int L, int B, int Hq, int Hkv, int N, 
     return KVE_OK;
 }
 
+// Checks shared by the allocators: sizes, budget, window and labels.
+kve_status_t check_allocation(const char* fn, const int8_t* roles, int B, int N, int R, double budget, int W) {
+    if (B <= 0 || N <= 0) return fail(KVE_ERR_INVALID_ARG, "%s: B and N must be positive", fn);
+    if (R < 1 || R > 8) return fail(KVE_ERR_INVALID_ARG, "%s: R=%d outside [1, 8]", fn, R);
+    if (W < 0 || W > N) return fail(KVE_ERR_INVALID_ARG, "%s: need 0 <= W <= N (W=%d N=%d)", fn, W, N);
+    if (!(std::isfinite(budget) && budget > 0.0))
+        return fail(KVE_ERR_INVALID_ARG, "%s: budget must be finite and > 0", fn);
+    for (size_t i = 0; i < (size_t)B * N; ++i)
+        if (roles[i] < 0 || roles[i] >= R)
+            return fail(KVE_ERR_INVALID_ARG, "%s: role label %d at %zu outside [0, %d)", fn, (int)roles[i], i,
+                        R);
+    return KVE_OK;
+}
+
+// n[r]: candidate-prefix tokens (t < N - W) of one sample carrying label r.
+void bucket_counts(const int8_t* rb, int N, int W, int R, long long* n) {
+    for (int r = 0; r < R; ++r) n[r] = 0;
+    for (int t = 0; t < N - W; ++t) ++n[rb[t]];
+}
+
+// Quotas of one sample (§4.1 role policy, Algorithm 1): the prefix budget
+// K - W split in proportion to alpha over the buckets with alpha > 0 and
+// tokens; a bucket whose ceiling share exceeds its population keeps its whole
+// population and the rest is re-split over the buckets still open.  Returns
+// the kept count W + sum(q).  alpha may sum to 0 (no bucket open: nothing of
+// the prefix is kept).
+int32_t allocate_sample(const long long* n, const double* alpha, int R, double budget, int N, int W,
+                        int32_t* q) {
+    for (int r = 0; r < R; ++r) q[r] = 0;
+    if (budget >= 1.0) {
+        // the full-cache baseline keeps every token
+        for (int r = 0; r < R; ++r) q[r] = (int32_t)n[r];
+        return N;
+    }
+    long long K = ceil_guarded(budget * (double)N);
+    if (K > N) K = N;
+    long long rem = K - W;
+    if (rem < 0) rem = 0;
+    bool open[8];
+    for (int r = 0; r < R; ++r) open[r] = alpha[r] > 0.0 && n[r] > 0;
+    while (rem > 0) {
+        double total = 0.0;
+        int n_open = 0;
+        for (int r = 0; r < R; ++r)
+            if (open[r]) {
+                total += alpha[r];
+                ++n_open;
+            }
+        if (n_open == 0) break;
+        long long share[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+        bool any_full = false;
+        for (int r = 0; r < R; ++r)
+            if (open[r]) {
+                share[r] = ceil_guarded(alpha[r] / total * (double)rem);
+                if (share[r] > n[r]) any_full = true;
+            }
+        if (!any_full) {
+            for (int r = 0; r < R; ++r)
+                if (open[r]) q[r] = (int32_t)share[r];
+            break;
+        }
+        // buckets that cannot use their share keep all their tokens; the
+        // budget they leave is re-split over the buckets still open
+        for (int r = 0; r < R; ++r)
+            if (open[r] && share[r] > n[r]) {
+                q[r] = (int32_t)n[r];
+                rem -= n[r];
+                open[r] = false;
+            }
+        if (rem < 0) rem = 0;
+    }
+    long long sum = W;
+    for (int r = 0; r < R; ++r) sum += q[r];
+    return (int32_t)sum;
+}
+
 }  // namespace
 
 extern "C" {
@@ -143,11 +219,8 @@ kve_status_t kve_role_allocate(const int8_t* roles, int B, int N, int R, const d
     const char* fn = "kve_role_allocate";
     if (roles == nullptr || alpha == nullptr || quota_out == nullptr || kept_out == nullptr)
         return fail(KVE_ERR_INVALID_ARG, "%s: null pointer", fn);
-    if (B <= 0 || N <= 0) return fail(KVE_ERR_INVALID_ARG, "%s: B and N must be positive", fn);
-    if (R < 1 || R > 8) return fail(KVE_ERR_INVALID_ARG, "%s: R=%d outside [1, 8]", fn, R);
-    if (W < 0 || W > N) return fail(KVE_ERR_INVALID_ARG, "%s: need 0 <= W <= N (W=%d N=%d)", fn, W, N);
-    if (!(std::isfinite(budget) && budget > 0.0))
-        return fail(KVE_ERR_INVALID_ARG, "%s: budget must be finite and > 0", fn);
+    kve_status_t st = check_allocation(fn, roles, B, N, R, budget, W);
+    if (st != KVE_OK) return st;
     double asum = 0.0;
     for (int r = 0; r < R; ++r) {
         if (!(std::isfinite(alpha[r]) && alpha[r] >= 0.0))
@@ -155,70 +228,57 @@ kve_status_t kve_role_allocate(const int8_t* roles, int B, int N, int R, const d
         asum += alpha[r];
     }
     if (!(asum > 0.0)) return fail(KVE_ERR_INVALID_ARG, "%s: alpha sums to 0", fn);
-    for (size_t i = 0; i < (size_t)B * N; ++i)
-        if (roles[i] < 0 || roles[i] >= R)
-            return fail(KVE_ERR_INVALID_ARG, "%s: role label %d at %zu outside [0, %d)", fn, (int)roles[i],
-                        i, R);
-
     std::vector<int32_t> quota((size_t)B * R, 0), kept(B, 0);
     int32_t k_cap = 0;
-    const int P = N - W;
     for (int b = 0; b < B; ++b) {
-        const int8_t* rb = roles + (size_t)b * N;
-        long long n[8] = {0, 0, 0, 0, 0, 0, 0, 0};
-        for (int t = 0; t < P; ++t) ++n[rb[t]];
-        int32_t* q = quota.data() + (size_t)b * R;
-        if (budget >= 1.0) {
-            // the full-cache baseline keeps every token
-            for (int r = 0; r < R; ++r) q[r] = (int32_t)n[r];
-            kept[b] = N;
-        } else {
-            long long K = ceil_guarded(budget * (double)N);
-            if (K > N) K = N;
-            long long rem = K - W;
-            if (rem < 0) rem = 0;
-            bool open[8];
-            for (int r = 0; r < R; ++r) open[r] = alpha[r] > 0.0 && n[r] > 0;
-            while (rem > 0) {
-                double total = 0.0;
-                int n_open = 0;
-                for (int r = 0; r < R; ++r)
-                    if (open[r]) {
-                        total += alpha[r];
-                        ++n_open;
-                    }
-                if (n_open == 0) break;
-                long long share[8] = {0, 0, 0, 0, 0, 0, 0, 0};
-                bool any_full = false;
-                for (int r = 0; r < R; ++r)
-                    if (open[r]) {
-                        share[r] = ceil_guarded(alpha[r] / total * (double)rem);
-                        if (share[r] > n[r]) any_full = true;
-                    }
-                if (!any_full) {
-                    for (int r = 0; r < R; ++r)
-                        if (open[r]) q[r] = (int32_t)share[r];
-                    break;
-                }
-                // buckets that cannot use their share keep all their tokens; the
-                // budget they leave is re-split over the buckets still open
-                for (int r = 0; r < R; ++r)
-                    if (open[r] && share[r] > n[r]) {
-                        q[r] = (int32_t)n[r];
-                        rem -= n[r];
-                        open[r] = false;
-                    }
-                if (rem < 0) rem = 0;
-            }
-            long long sum = W;
-            for (int r = 0; r < R; ++r) sum += q[r];
-            kept[b] = (int32_t)sum;
-        }
+        long long n[8];
+        bucket_counts(roles + (size_t)b * N, N, W, R, n);
+        kept[b] = allocate_sample(n, alpha, R, budget, N, W, quota.data() + (size_t)b * R);
         if (kept[b] > k_cap) k_cap = kept[b];
     }
     for (size_t i = 0; i < quota.size(); ++i) quota_out[i] = quota[i];
     for (int b = 0; b < B; ++b) kept_out[b] = kept[b];
     if (k_cap_out != nullptr) *k_cap_out = k_cap;
+    return ok();
+}
+
+kve_status_t kve_role_allocate_fair(const int8_t* roles, int B, int N, int R, double budget, int W,
+                                    int32_t* quota_out, int32_t* kept_out, int32_t* k_cap_out) {
+    const char* fn = "kve_role_allocate_fair";
+    if (roles == nullptr || quota_out == nullptr || kept_out == nullptr)
+        return fail(KVE_ERR_INVALID_ARG, "%s: null pointer", fn);
+    kve_status_t st = check_allocation(fn, roles, B, N, R, budget, W);
+    if (st != KVE_OK) return st;
+    std::vector<int32_t> quota((size_t)B * R, 0), kept(B, 0);
+    int32_t k_cap = 0;
+    for (int b = 0; b < B; ++b) {
+        long long n[8];
+        bucket_counts(roles + (size_t)b * N, N, W, R, n);
+        // each bucket weighted by its own population: the same share of every bucket
+        double alpha[8];
+        for (int r = 0; r < R; ++r) alpha[r] = (double)n[r];
+        kept[b] = allocate_sample(n, alpha, R, budget, N, W, quota.data() + (size_t)b * R);
+        if (kept[b] > k_cap) k_cap = kept[b];
+    }
+    for (size_t i = 0; i < quota.size(); ++i) quota_out[i] = quota[i];
+    for (int b = 0; b < B; ++b) kept_out[b] = kept[b];
+    if (k_cap_out != nullptr) *k_cap_out = k_cap;
+    return ok();
+}
+
+kve_status_t kve_role_map(const int8_t* roles, size_t n, const int8_t* map, int R_in, int8_t* out) {
+    const char* fn = "kve_role_map";
+    if ((n > 0 && (roles == nullptr || out == nullptr)) || map == nullptr)
+        return fail(KVE_ERR_INVALID_ARG, "%s: null pointer", fn);
+    if (R_in < 1 || R_in > 127) return fail(KVE_ERR_INVALID_ARG, "%s: R_in=%d outside [1, 127]", fn, R_in);
+    for (int r = 0; r < R_in; ++r)
+        if (map[r] < 0 || map[r] >= 8)
+            return fail(KVE_ERR_INVALID_ARG, "%s: map[%d]=%d outside [0, 8)", fn, r, (int)map[r]);
+    for (size_t i = 0; i < n; ++i)
+        if (roles[i] < 0 || roles[i] >= R_in)
+            return fail(KVE_ERR_INVALID_ARG, "%s: role label %d at %zu outside [0, %d)", fn, (int)roles[i], i,
+                        R_in);
+    for (size_t i = 0; i < n; ++i) out[i] = map[roles[i]];
     return ok();
 }
 

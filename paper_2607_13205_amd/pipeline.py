@@ -3,6 +3,10 @@
 score (SnapKV windowed + pooled, or H2O)  ->  role allocation (host)  ->
 per-role top-k  ->  K/V compaction.  Buffers are allocated once by
 ``EvictBuffers`` so that repeated steps allocate nothing.
+
+``Policy`` names how the budget is split over buckets: the role-conditional
+weights of §4.1, fair eviction (§5, the same rate for every bucket) or the
+No-X counterfactual of §3 (one role banned from the prefix).
 """
 
 from __future__ import annotations
@@ -12,6 +16,55 @@ from dataclasses import dataclass
 import numpy as np
 
 from . import binding as kb
+
+
+@dataclass(frozen=True)
+class Policy:
+    """A split of the prefix budget over R buckets.
+
+    alpha      per-bucket weights (role-conditional policy), or None for fair
+               eviction, where every sample weights each bucket by its own
+               candidate count.
+    bucket_of  map from role label to bucket, or None when the role labels are
+               the buckets.  The step itself takes bucket labels: relabel the
+               roles once with ``buckets`` and keep the result resident.
+    """
+    R: int
+    alpha: tuple | None = None
+    bucket_of: tuple | None = None
+
+    @staticmethod
+    def role(alpha) -> "Policy":
+        a = tuple(float(x) for x in alpha)
+        return Policy(len(a), a)
+
+    @staticmethod
+    def fair(R: int) -> "Policy":
+        return Policy(int(R), None)
+
+    @staticmethod
+    def no_role(x: int, n_roles: int) -> "Policy":
+        """No-X: role x alone in bucket 1 with weight 0, the rest in bucket 0."""
+        if not 0 <= x < n_roles:
+            raise ValueError("banned role outside [0, n_roles)")
+        return Policy(2, (1.0, 0.0), tuple(1 if r == x else 0 for r in range(n_roles)))
+
+    def buckets(self, roles_host: np.ndarray) -> np.ndarray:
+        """Bucket labels of roles [B, N] (host int8)."""
+        if self.bucket_of is None:
+            return np.asarray(roles_host, dtype=np.int8)
+        return kb.role_map(roles_host, self.bucket_of)
+
+    def allocate(self, buckets_host: np.ndarray, budget: float, W: int):
+        """(quota [B, R], kept [B], k_cap) for bucket labels [B, N]."""
+        if self.alpha is None:
+            return kb.role_allocate_fair(buckets_host, self.R, budget, W)
+        return kb.role_allocate(buckets_host, self.R, self.alpha, budget, W)
+
+
+def as_policy(policy) -> Policy:
+    """A Policy, or a plain weight sequence read as the role-conditional policy."""
+    return policy if isinstance(policy, Policy) else Policy.role(policy)
 
 
 @dataclass
@@ -50,16 +103,19 @@ def alloc_buffers(k, n_q_heads: int, W: int, R: int, k_cap: int, scorer: str = "
     )
 
 
-def evict(q, k, v, roles_host: np.ndarray, roles_dev, alpha, budget: float, W: int,
+def evict(q, k, v, roles_host: np.ndarray, roles_dev, policy, budget: float, W: int,
           pool_k: int, bufs: EvictBuffers, scorer: str = "snapkv", scale: float = 0.0,
           score_events=None):
     """One eviction step; returns (quota [B, R] host, kept [B] host).
 
     q is the window queries [L, B, Hq, W, d] (SnapKV) or all queries
-    [L, B, Hq, N, d] (H2O, which uses W = 0 and no pool).  ``score_events``,
-    a pair of torch.cuda.Event, brackets the score call on the launch stream."""
+    [L, B, Hq, N, d] (H2O, which uses W = 0 and no pool).  roles_host /
+    roles_dev are the bucket labels [B, N] of ``policy`` (a Policy, or the
+    weights of the role-conditional policy).  ``score_events``, a pair of
+    torch.cuda.Event, brackets the score call on the launch stream."""
     import torch
-    R = len(alpha)
+    policy = as_policy(policy)
+    R = policy.R
     if score_events is not None:
         score_events[0].record()
     if scorer == "snapkv":
@@ -68,7 +124,7 @@ def evict(q, k, v, roles_host: np.ndarray, roles_dev, alpha, budget: float, W: i
         kb.h2o_score(q, k, scale, score=bufs.score, workspace=bufs.ws_score)
     if score_events is not None:
         score_events[1].record()
-    quota, kept, k_cap = kb.role_allocate(roles_host, R, alpha, budget, W)
+    quota, kept, k_cap = policy.allocate(roles_host, budget, W)
     if k_cap > bufs.k_cap:
         raise ValueError(f"buffers hold {bufs.k_cap} rows, the allocation keeps {k_cap}")
     if bufs.copy_done is None:

@@ -29,7 +29,7 @@ def _declared():
 
 def test_every_declared_symbol_is_exported(kve):
     names = _declared()
-    assert len(names) == 10
+    assert len(names) == 12
     assert sorted(kve.EXPORTED) == names
     lib = ctypes.CDLL(kve.binding._LIB_PATH)
     for n in names:
@@ -74,6 +74,58 @@ def test_role_allocate_rejects_bad_input(kve):
             kve.role_allocate(*args)
         assert e.value.status == 1
         assert kve.last_error()
+
+
+@pytest.mark.parametrize("ex_seed", range(3))
+def test_fair_allocate_matches_oracle_on_random_grid(kve, ex_seed):
+    r = np.random.default_rng(50 + ex_seed)
+    for _ in range(400):
+        N = int(r.integers(1, 300))
+        W = int(r.integers(0, N + 1))
+        R = int(r.integers(1, 9))
+        B = int(r.integers(1, 4))
+        p = r.dirichlet(np.full(R, 0.5))
+        roles = r.choice(R, (B, N), p=p).astype(np.int8)
+        budget = float(r.choice([0.01, 0.05, 0.07, 0.1, 0.2, 0.33, 0.5, 0.9, 1.0, 1.5]))
+        q, kept, kcap = kve.role_allocate_fair(roles, R, budget, W)
+        qo, ko, kco = O.fair_allocate_batch(roles, R, budget, W)
+        assert np.array_equal(q, qo) and np.array_equal(kept, ko) and kcap == kco
+
+
+def test_role_map_and_no_role_allocation_match_oracle(kve):
+    r = np.random.default_rng(60)
+    for _ in range(200):
+        n_roles = int(r.integers(2, 6))
+        B, N = int(r.integers(1, 4)), int(r.integers(1, 300))
+        W = int(r.integers(0, N + 1))
+        roles = r.integers(0, n_roles, (B, N)).astype(np.int8)
+        x = int(r.integers(0, n_roles))
+        bucket_of, alpha = O.no_role_policy(x, n_roles)
+        buckets = kve.role_map(roles, bucket_of)
+        assert np.array_equal(buckets, O.role_map(roles, bucket_of))
+        budget = float(r.choice([0.05, 0.1, 0.3, 0.5, 1.0]))
+        q, kept, kcap = kve.role_allocate(buckets, 2, alpha, budget, W)
+        qo, ko, kco = O.role_allocate_batch(O.role_map(roles, bucket_of), 2, alpha, budget, W)
+        assert np.array_equal(q, qo) and np.array_equal(kept, ko) and kcap == kco
+    # an arbitrary many-to-one map
+    roles = r.integers(0, 7, (2, 100)).astype(np.int8)
+    bmap = [3, 0, 7, 7, 1, 0, 2]
+    assert np.array_equal(kve.role_map(roles, bmap), O.role_map(roles, bmap))
+
+
+def test_fair_and_map_reject_bad_input(kve):
+    roles = np.zeros((1, 10), dtype=np.int8)
+    for args in [(roles, 4, 0.0, 2), (roles, 4, 0.5, 11), (roles, 9, 0.5, 2), (roles + 4, 4, 0.5, 2),
+                 (roles, 4, float("inf"), 2)]:
+        with pytest.raises(kve.KveError) as e:
+            kve.role_allocate_fair(*args)
+        assert e.value.status == 1
+    for rl, bmap in [(roles + 3, [0, 1, 0]), (roles, [8, 0]), (roles, [-1]),
+                     (roles, [0] * 128)]:
+        out_before = rl.copy()
+        with pytest.raises(kve.KveError) as e:
+            kve.role_map(rl, bmap)
+        assert e.value.status == 1 and np.array_equal(rl, out_before)
 
 
 def test_device_entry_points_validate_before_launch(kve):

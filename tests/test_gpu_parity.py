@@ -223,18 +223,28 @@ def test_kv_compact_bit_exact(K, dtype, d):
                 assert not kob[s][m].any() and not vob[s][m].any()
 
 
-def _pipeline_check(K, wl, inp, budget, alpha, segs=None):
+def _pipeline_check(K, wl, inp, budget, policy, segs=None):
     """Run the whole step on the GPU and check scores, kept sets and compacted
-    rows of the given segments against the oracle."""
+    rows of the given segments against the oracle.  ``policy`` is a Policy or
+    the weights of the role-conditional policy."""
     from paper_2607_13205_amd import pipeline
+    policy = pipeline.as_policy(policy)
     W = 0 if wl.scorer == "h2o" else wl.W
     pool = 1 if wl.scorer == "h2o" else wl.pool_k
-    _, _, k_cap = K.role_allocate(inp["roles"], 4, alpha, budget, W)
-    bufs = pipeline.alloc_buffers(inp["k"], wl.Hq, W, 4, k_cap, scorer=wl.scorer)
-    quota, kept = pipeline.evict(inp["q"], inp["k"], inp["v"], inp["roles"], inp["roles_t"], alpha,
+    R = policy.R
+    buckets = policy.buckets(inp["roles"])
+    buckets_t = inp["roles_t"] if policy.bucket_of is None else torch.from_numpy(buckets).cuda()
+    _, _, k_cap = policy.allocate(buckets, budget, W)
+    bufs = pipeline.alloc_buffers(inp["k"], wl.Hq, W, R, k_cap, scorer=wl.scorer)
+    quota, kept = pipeline.evict(inp["q"], inp["k"], inp["v"], buckets, buckets_t, policy,
                                  budget, W, pool, bufs, scorer=wl.scorer)
     torch.cuda.synchronize()
-    qo, ko, _ = O.role_allocate_batch(inp["roles"], 4, alpha, budget, W)
+    ob = inp["roles"] if policy.bucket_of is None else O.role_map(inp["roles"], policy.bucket_of)
+    assert np.array_equal(buckets, ob)
+    if policy.alpha is None:
+        qo, ko, _ = O.fair_allocate_batch(ob, R, budget, W)
+    else:
+        qo, ko, _ = O.role_allocate_batch(ob, R, list(policy.alpha), budget, W)
     assert np.array_equal(quota, qo) and np.array_equal(kept, ko)
     if segs is None:
         segs = list(np.ndindex(len(inp["layers"]), wl.B, wl.Hkv))
@@ -247,8 +257,12 @@ def _pipeline_check(K, wl, inp, budget, alpha, segs=None):
             s_ref = O.maxpool_prefix(O.snapkv_mass(f64(inp["q"][l, b, j * wl.G:(j + 1) * wl.G]), kseg),
                                      W, pool)
         check_scores(f64(bufs.score[l, b, j]), s_ref, f"{wl.name} seg {(l, b, j)}")
-        roles = inp["roles"][b]
+        roles = ob[b]
         idx_ref = O.select_keep(s_ref, roles, qo[b], W)
+        if policy.bucket_of is not None and policy.alpha == (1.0, 0.0) and sum(policy.bucket_of) == 1:
+            # No-X: the bucket composition is the definition's kept set
+            x = list(policy.bucket_of).index(1)
+            assert np.array_equal(idx_ref, O.no_role_keep(s_ref, inp["roles"][b], x, budget, W))
         n = int(bufs.count[l, b, j])
         assert n == kept[b]
         idx_gpu = bufs.idx[l, b, j, :n].cpu().numpy()
@@ -303,6 +317,31 @@ def test_pipeline_h2o_small(K):
     _pipeline_check(K, wl, inp, 0.1, WL.default_alpha(0.0))
 
 
+def _policy(name):
+    from paper_2607_13205_amd.pipeline import Policy
+    return {"fair": Policy.fair(4), "no_key": Policy.no_role(WL.KEY, 4),
+            "no_sink": Policy.no_role(WL.SINK, 4), "no_value": Policy.no_role(WL.VALUE, 4)}[name]
+
+
+@pytest.mark.parametrize("pol,budget", [("no_key", 0.1), ("no_key", 0.5), ("no_sink", 0.3),
+                                        ("no_value", 0.75), ("fair", 0.1)])
+def test_pipeline_h2o_policies(K, pol, budget):
+    """The counterfactual No-X conditions over the H2O score (§3), and fair
+    eviction, through the same allocator, top-k and compaction."""
+    wl = custom("h2o_pol", 1, 2, 8, 2, 1500, 0, 128, 1, "bf16", scorer="h2o")
+    note(f"pipeline h2o {pol} B={budget}")
+    inp = WL.make_inputs(wl, device="cuda")
+    _pipeline_check(K, wl, inp, budget, _policy(pol))
+
+
+@pytest.mark.parametrize("pol,budget", [("fair", 0.05), ("fair", 0.2), ("no_key", 0.1)])
+def test_pipeline_snapkv_policies(K, pol, budget):
+    wl = WL.get_workload("layer8k")
+    note(f"pipeline layer8k {pol} B={budget}")
+    inp = WL.make_inputs(wl, device="cuda")
+    _pipeline_check(K, wl, inp, budget, _policy(pol))
+
+
 def test_determinism(K):
     wl = WL.get_workload("layer8k")
     inp = WL.make_inputs(wl, device="cuda")
@@ -321,20 +360,23 @@ def test_determinism(K):
     assert torch.equal(outs[0][2].view(torch.int16), outs[1][2].view(torch.int16))
 
 
-@pytest.mark.parametrize("name,budget,segs", [
-    ("stack32k", 0.05, [(0, 0, 0), (17, 2, 5), (31, 3, 7)]),
-    ("long128k", 0.05, [(0, 0, 0), (31, 0, 7)]),
-    ("long128k", 0.20, [(13, 0, 2)]),
+@pytest.mark.parametrize("name,budget,segs,pol", [
+    ("stack32k", 0.05, [(0, 0, 0), (17, 2, 5), (31, 3, 7)], "role"),
+    ("stack32k", 0.05, [(9, 1, 4)], "fair"),
+    ("long128k", 0.05, [(0, 0, 0), (31, 0, 7)], "role"),
+    ("long128k", 0.20, [(13, 0, 2)], "role"),
+    ("h2o16k", 0.10, [(0, 0, 3)], "no_key"),
 ])
-def test_pipeline_full_size_sampled(K, name, budget, segs):
+def test_pipeline_full_size_sampled(K, name, budget, segs, pol):
     """Real shapes, the launch configuration the benchmark times; the oracle
     recomputes a few sampled (layer, sample, KV head) segments."""
     wl = WL.get_workload(name)
-    note(f"pipeline full size {name} B={budget}: generating inputs")
+    note(f"pipeline full size {name} B={budget} {pol}: generating inputs")
     inp = WL.make_inputs(wl, device="cuda")
     torch.cuda.synchronize()
     note("  running and checking sampled segments")
-    ties = _pipeline_check(K, wl, inp, budget, WL.default_alpha(0.0), segs=segs)
+    policy = WL.default_alpha(0.0) if pol == "role" else _policy(pol)
+    ties = _pipeline_check(K, wl, inp, budget, policy, segs=segs)
     note(f"  near-tie pairs: {ties}")
     del inp
     torch.cuda.empty_cache()
