@@ -9,8 +9,9 @@ definitions in NumPy float64 so that a reader can check each step by eye.
 Modules
 -------
 ``reference``  NumPy float64 definitions: causal softmax, H2O and SnapKV mass,
-               max-pool, role allocation, per-role selection, compaction and the
-               per-role mass diagnostics.
+               max-pool, role allocation (role-conditional, fair, No-X),
+               per-role selection, compaction, decoding through the keep-set
+               and the per-role mass diagnostics.
 ``brute``      pure-Python loops over tiny inputs (an independent second
                reading used to pin ``reference``).
 

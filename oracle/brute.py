@@ -100,3 +100,24 @@ def _lex_better(a, b, score):
             continue
         return _better(score[x], x, score[y], y)
     return False
+
+
+def decode_loops(q_heads, k, v, keep, scale=None):
+    """Decode through a keep-set with loops: for each head, the softmax of the
+    scaled dot products over the kept positions only, then the weighted sum of
+    their value rows (Algorithm 1, last step)."""
+    d = len(q_heads[0])
+    if scale is None:
+        scale = 1.0 / math.sqrt(d)
+    keep = sorted(set(int(t) for t in keep))
+    out = []
+    for q in q_heads:
+        if not keep:
+            out.append([0.0] * d)
+            continue
+        logits = [scale * _dot(q, k[t]) for t in keep]
+        m = max(logits)
+        w = [math.exp(x - m) for x in logits]
+        z = sum(w)
+        out.append([sum(w[i] * float(v[t][c]) for i, t in enumerate(keep)) / z for c in range(d)])
+    return out

@@ -71,6 +71,9 @@ __all__ = [
     "select_keep",
     "topk_select",
     "kv_compact",
+    "decode_attention",
+    "masked_decode_attention",
+    "decode_attention_batch",
     "per_role_mean_mass",
     "retention_rate",
     "retained_snr_db",
@@ -403,6 +406,77 @@ def kv_compact(kv: np.ndarray, idx: np.ndarray) -> np.ndarray:
     """Compacted rows kv[idx] of one (layer, batch, KV head): a pure copy,
     the dense cache a compacting implementation keeps (§6, systems cost)."""
     return np.asarray(kv)[np.asarray(idx)]
+
+
+# ---------------------------------------------------------------------------
+# Decoding through the keep-set (Algorithm 1, last step; §3 "Setup"; §6
+# "Systems cost": a compacting implementation attends over the kept rows only)
+# ---------------------------------------------------------------------------
+
+def _softmax_rows(x: np.ndarray) -> np.ndarray:
+    """Row softmax; a row whose entries are all -inf gets probability 0 everywhere."""
+    m = np.max(x, axis=1, keepdims=True)
+    m = np.where(np.isneginf(m), 0.0, m)
+    e = np.exp(x - m)
+    z = np.sum(e, axis=1, keepdims=True)
+    return np.divide(e, z, out=np.zeros_like(e), where=z > 0)
+
+
+def decode_attention(q: np.ndarray, k: np.ndarray, v: np.ndarray,
+                     scale: float | None = None) -> np.ndarray:
+    """One decode query per head over the rows of a cache (one KV head).
+
+    q [G, d] (the G query heads of the group), k, v [n, d]; returns [G, d]
+    with o_h = sum_t softmax_t(scale <q_h, k_t>) v_t.  An empty cache (n = 0)
+    gives zeros.  Applied to the compacted rows K[idx], V[idx] this is the
+    decode of a compacting implementation.
+    """
+    q = np.asarray(q, dtype=np.float64)
+    k = np.asarray(k, dtype=np.float64)
+    v = np.asarray(v, dtype=np.float64)
+    G, d = q.shape
+    if k.shape[0] == 0:
+        return np.zeros((G, d), dtype=np.float64)
+    if scale is None:
+        scale = 1.0 / math.sqrt(d)
+    x = scale * (q @ k.T)
+    return _softmax_rows(x) @ v
+
+
+def masked_decode_attention(q: np.ndarray, k: np.ndarray, v: np.ndarray, keep,
+                            scale: float | None = None) -> np.ndarray:
+    """Decode through a keep-mask over the full cache, the form the paper's
+    harness uses: the logit of every position outside ``keep`` is set to -inf
+    and the softmax runs over all N positions.  q [G, d], k, v [N, d]."""
+    q = np.asarray(q, dtype=np.float64)
+    k = np.asarray(k, dtype=np.float64)
+    v = np.asarray(v, dtype=np.float64)
+    d = q.shape[1]
+    if scale is None:
+        scale = 1.0 / math.sqrt(d)
+    mask = np.zeros(k.shape[0], dtype=bool)
+    mask[np.asarray(keep, dtype=np.int64)] = True
+    x = scale * (q @ k.T)
+    x[:, ~mask] = -np.inf
+    return _softmax_rows(x) @ v
+
+
+def decode_attention_batch(q: np.ndarray, k_c: np.ndarray, v_c: np.ndarray,
+                           count: np.ndarray, scale: float | None = None) -> np.ndarray:
+    """decode_attention for whole tensors: q [L, B, Hq, d], k_c, v_c
+    [L, B, Hkv, k_cap, d], count [L, B, Hkv] (rows in use, clamped to
+    [0, k_cap]) -> [L, B, Hq, d].  Query head h reads KV head h // G (R2)."""
+    L, Bt, Hq, d = q.shape
+    Hkv, k_cap = k_c.shape[2], k_c.shape[3]
+    G = Hq // Hkv
+    out = np.zeros((L, Bt, Hq, d), dtype=np.float64)
+    for l in range(L):
+        for b in range(Bt):
+            for j in range(Hkv):
+                n = int(min(max(int(count[l, b, j]), 0), k_cap))
+                out[l, b, j * G:(j + 1) * G] = decode_attention(
+                    q[l, b, j * G:(j + 1) * G], k_c[l, b, j, :n], v_c[l, b, j, :n], scale)
+    return out
 
 
 # ---------------------------------------------------------------------------
