@@ -14,7 +14,9 @@ second (a token counts once it has passed through all layers and KV heads);
 stream it is launched on; ``cpu_baseline`` times the float64 CPU oracle on a
 bounded sample of the same workload; ``policies`` gives the step time of the
 same workload under fair eviction and the No-KEY counterfactual, which reuse
-every kernel with other quotas.
+every kernel with other quotas; ``decode`` times one decode query per head over
+the compacted cache of every layer against the same kernel over the full
+cache.
 
 ``roofline.traffic`` is the measured HBM traffic of one score call, read from
 the counter summary in profiles/ (rocprofv3 FETCH_SIZE and WRITE_SIZE,
@@ -41,7 +43,7 @@ METRIC = "prefill tokens scored+compressed/s per GPU; % HBM peak (SnapKV), % MFM
 TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "snapkv_score_stack32k_traffic.md")
 # sources of the kernels one score call launches
 SCORE_SOURCES = ("paper_2607_13205_amd/csrc/snapkv.hip", "paper_2607_13205_amd/csrc/kve_stream.h",
-                 "paper_2607_13205_amd/csrc/kve_device.h", "paper_2607_13205_amd/csrc/kve_internal.h")
+                 "paper_2607_13205_amd/csrc/kve_device.h", "paper_2607_13205_amd/csrc/kve_snap_plan.h")
 COPY_BYTES = 1 << 30
 HBM_PEAK_GBS = 8000.0
 BF16_MFMA_PEAK_TFLOPS = 2500.0
@@ -59,6 +61,8 @@ def parse():
                     help="target CPU time of the oracle baseline sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-h2o", action="store_true", help="skip the H2O scorer leg")
+    ap.add_argument("--no-decode", action="store_true",
+                    help="skip the decode timings over the compacted and the full cache")
     ap.add_argument("--no-policies", action="store_true",
                     help="skip the fair-eviction and No-KEY step timings")
     ap.add_argument("--calibrate-copy", action="store_true",
@@ -225,6 +229,53 @@ def policy_leg(WL, pipeline, wl, inp, budget, W, pool, steps):
     return out
 
 
+def _time_calls(fn, steps):
+    import torch
+    for _ in range(2):
+        fn()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(steps):
+        fn()
+    e1.record()
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) / steps
+
+
+def decode_leg(K, wl, inp, bufs, steps):
+    """One decode query per head over the compacted cache of every layer
+    (HIP events around the decode call), and the same kernel over the full,
+    uncompressed cache: the 1 - B saving of a compacting implementation."""
+    import torch
+    L, B, Hkv, N, d = inp["k"].shape
+    elem = inp["k"].element_size()
+    g = torch.Generator(device="cuda")
+    g.manual_seed(2024)
+    q = (3.0 * torch.randn((L, B, wl.Hq, d), generator=g, device="cuda")).to(inp["k"].dtype)
+    out = torch.empty((L, B, wl.Hq, d), dtype=torch.float32, device="cuda")
+    ws = torch.empty(K.decode_workspace_size(L, B, wl.Hq, Hkv, bufs.k_cap, d), dtype=torch.uint8,
+                     device="cuda")
+    ms_c = _time_calls(lambda: K.decode_attention(q, bufs.k_out, bufs.v_out, bufs.count, out=out,
+                                                  workspace=ws), steps)
+    rows = int(torch.clamp(bufs.count, 0, bufs.k_cap).sum().item())
+    small = L * B * wl.Hq * d * (elem + 4)                     # q read, out written
+    bytes_c = rows * d * elem * 2 + small
+    full = torch.full((L, B, Hkv), N, dtype=torch.int32, device="cuda")
+    ws_f = torch.empty(K.decode_workspace_size(L, B, wl.Hq, Hkv, N, d), dtype=torch.uint8, device="cuda")
+    ms_f = _time_calls(lambda: K.decode_attention(q, inp["k"], inp["v"], full, out=out, workspace=ws_f),
+                       steps)
+    bytes_f = L * B * Hkv * N * d * elem * 2 + small
+    gbs_c = bytes_c / (ms_c * 1e-3) / 1e9
+    gbs_f = bytes_f / (ms_f * 1e-3) / 1e9
+    return {"kernel": "kve_decode_attention (split + combine), all layers in one call",
+            "ms": round(ms_c, 4), "kept_rows": rows, "algorithmic_bytes": bytes_c,
+            "achieved_GBs": round(gbs_c, 1), "hbm_frac": round(gbs_c / HBM_PEAK_GBS, 4),
+            "ms_full_cache": round(ms_f, 4), "full_cache_GBs": round(gbs_f, 1),
+            "full_cache_hbm_frac": round(gbs_f / HBM_PEAK_GBS, 4),
+            "speedup_vs_full_cache": round(ms_f / ms_c, 2)}
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -313,6 +364,9 @@ def main():
             "ms": round(ms_score, 4), "algorithmic_bytes": score_bytes,
         },
     }
+    if not args.no_decode and scorer == "snapkv":
+        print("[bench] decode over the compacted and the full cache", file=sys.stderr, flush=True)
+        out["decode"] = decode_leg(K, wl, inp, bufs, max(3, args.steps // 2))
     del bufs
     torch.cuda.empty_cache()
     if not args.no_policies:

@@ -249,6 +249,43 @@ kve_status_t kve_kv_compact(const void* k, const void* v, kve_dtype_t dtype,
                             int L, int B, int Hkv, int N, int d, int k_cap,
                             void* k_out, void* v_out, void* stream);
 
+/* ------------------------------------------------------------------------- */
+/* Decode through the keep-set (Algorithm 1, last step; §3 "Setup"; §6        */
+/* "Systems cost": a compacting implementation attends over the kept rows).   */
+/* ------------------------------------------------------------------------- */
+
+/* Workspace bytes kve_decode_attention needs for these shapes (0 if invalid). */
+size_t kve_decode_workspace_size(int L, int B, int Hq, int Hkv, int k_cap, int d);
+
+/*
+ * One decode query per head over the first count rows of a compacted cache:
+ *   out[l, b, h] = sum_t softmax_t(scale * <q[l, b, h], k_c[l, b, j, t]>) v_c[l, b, j, t]
+ * over t < n = min(max(count[l, b, j], 0), k_cap), with j = h / (Hq/Hkv)
+ * (contiguous groups).  This equals decoding through the keep-mask over the
+ * full cache, with evicted positions masked out; a segment with n = 0 gives
+ * zeros.  To attend to the new token as well, append its key and value row
+ * at position count and pass count + 1.
+ *
+ *   q         [L, B, Hq, d] bf16 or fp32 (device)
+ *   k_c, v_c  [L, B, Hkv, k_cap, d], same dtype (device), e.g. the output of
+ *             kve_kv_compact; rows at and beyond n are never used
+ *   count     [L, B, Hkv] int32 (device); kve_topk_select's count_out fits
+ *   scale     softmax scale; 0 means 1/sqrt(d)
+ *   out       [L, B, Hq, d] float32 (device)
+ *   workspace kve_decode_workspace_size bytes, 256-byte aligned, owned by the
+ *             caller: per (segment, split, head) a partial output row and a
+ *             (reference, denominator) pair; contents on entry do not matter.
+ *
+ * Requires Hq/Hkv <= 8.  Enqueued on `stream`, no host synchronisation.
+ * Errors: KVE_ERR_INVALID_ARG (null pointers, bad shapes, negative or
+ * non-finite scale, misaligned workspace), KVE_ERR_UNSUPPORTED (d not 64/128,
+ * Hq/Hkv > 8, grid too large), KVE_ERR_WORKSPACE, KVE_ERR_HIP.
+ */
+kve_status_t kve_decode_attention(const void* q, const void* k_c, const void* v_c,
+                                  const int32_t* count, kve_dtype_t dtype, int L, int B,
+                                  int Hq, int Hkv, int k_cap, int d, float scale, float* out,
+                                  void* workspace, size_t workspace_bytes, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

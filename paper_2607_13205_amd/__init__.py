@@ -9,14 +9,15 @@ The hot path runs in libkve.so (HIP); this package is its thin Python binding:
   role_map       relabel roles into buckets, e.g. the No-X counterfactual (host)
   topk_select    per-role top-k with the window kept, ascending indices
   kv_compact     dense K/V cache of the kept rows
+  decode_attention  one decode query per head over the compacted cache
   pipeline.evict the whole step over resident tensors
 """
 
-from .binding import (EXPORTED, KveError, h2o_score, h2o_workspace_size, kv_compact,  # noqa: F401
-                      last_error, role_allocate, role_allocate_fair, role_map, snapkv_score,
-                      snapkv_workspace_size, topk_select)
+from .binding import (EXPORTED, KveError, decode_attention, decode_workspace_size,  # noqa: F401
+                      h2o_score, h2o_workspace_size, kv_compact, last_error, role_allocate,
+                      role_allocate_fair, role_map, snapkv_score, snapkv_workspace_size, topk_select)
 from . import pipeline  # noqa: F401
 
 __all__ = ["snapkv_score", "h2o_score", "role_allocate", "role_allocate_fair", "role_map",
            "topk_select", "kv_compact", "snapkv_workspace_size", "h2o_workspace_size", "KveError",
-           "last_error", "pipeline"]
+           "last_error", "pipeline", "decode_attention", "decode_workspace_size"]

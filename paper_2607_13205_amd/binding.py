@@ -34,6 +34,7 @@ EXPORTED = (
     "kve_role_allocate", "kve_role_allocate_fair", "kve_role_map",
     "kve_topk_workspace_size", "kve_topk_select",
     "kve_kv_compact",
+    "kve_decode_workspace_size", "kve_decode_attention",
 )
 
 
@@ -70,6 +71,9 @@ def _load():
                             [c_void, c_void, c_void, c_size, c_void]),
         "kve_kv_compact": (c_int, [c_void, c_void, c_int, c_void, c_void] + [c_int] * 6 +
                            [c_void, c_void, c_void]),
+        "kve_decode_workspace_size": (c_size, [c_int] * 6),
+        "kve_decode_attention": (c_int, [c_void, c_void, c_void, c_void, c_int] + [c_int] * 6 +
+                                 [c_float, c_void, c_void, c_size, c_void]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -279,3 +283,26 @@ def kv_compact(k, v, idx, count, k_out=None, v_out=None, stream=None):
                               _dev(k_out, "k_out"), None if v is None else _dev(v_out, "v_out"),
                               _stream(stream)))
     return k_out, v_out
+
+
+def decode_workspace_size(L, B, Hq, Hkv, k_cap, d) -> int:
+    return int(LIB.kve_decode_workspace_size(L, B, Hq, Hkv, k_cap, d))
+
+
+def decode_attention(q, k_c, v_c, count, scale: float = 0.0, out=None, workspace=None, stream=None):
+    """Decode over the first count rows of a compacted cache: q [L, B, Hq, d],
+    k_c, v_c [L, B, Hkv, k_cap, d], count int32 [L, B, Hkv] -> float32 [L, B, Hq, d]."""
+    torch = _torch()
+    L, B, Hq, d = q.shape
+    Lk, Bk, Hkv, k_cap, dk = k_c.shape
+    if (L, B, d) != (Lk, Bk, dk) or v_c.shape != k_c.shape or q.dtype != k_c.dtype or v_c.dtype != k_c.dtype:
+        raise ValueError("q, k_c and v_c disagree in L, B, d, shape or dtype")
+    if tuple(count.shape) != (L, B, Hkv) or count.dtype != torch.int32:
+        raise ValueError("count must be int32 [L, B, Hkv]")
+    if out is None:
+        out = torch.empty((L, B, Hq, d), dtype=torch.float32, device=k_c.device)
+    ws, wsb = _workspace(decode_workspace_size(L, B, Hq, Hkv, k_cap, d), k_c.device, workspace)
+    _check(LIB.kve_decode_attention(_dev(q, "q"), _dev(k_c, "k_c"), _dev(v_c, "v_c"), _dev(count, "count"),
+                                    _dtype_code(k_c), L, B, Hq, Hkv, k_cap, d, float(scale),
+                                    _dev(out, "out"), _ptr(ws), wsb, _stream(stream)))
+    return out

@@ -282,6 +282,38 @@ kve_status_t kve_role_map(const int8_t* roles, size_t n, const int8_t* map, int 
     return ok();
 }
 
+size_t kve_decode_workspace_size(int L, int B, int Hq, int Hkv, int k_cap, int d) {
+    if (L <= 0 || B <= 0 || Hq <= 0 || Hkv <= 0 || k_cap <= 0 || Hq % Hkv != 0) return 0;
+    if (d != 64 && d != 128) return 0;
+    return kve::decode_plan(L, B, Hq, Hkv, k_cap, d).total;
+}
+
+kve_status_t kve_decode_attention(const void* q, const void* k_c, const void* v_c, const int32_t* count,
+                                  kve_dtype_t dtype, int L, int B, int Hq, int Hkv, int k_cap, int d,
+                                  float scale, float* out, void* workspace, size_t workspace_bytes,
+                                  void* stream) {
+    const char* fn = "kve_decode_attention";
+    kve_status_t st = check_common(fn, L, B, Hq, Hkv, k_cap, d, (int)dtype);
+    if (st != KVE_OK) return st;
+    if (q == nullptr || k_c == nullptr || v_c == nullptr || count == nullptr || out == nullptr)
+        return fail(KVE_ERR_INVALID_ARG, "%s: null tensor pointer", fn);
+    if (!(std::isfinite(scale) && scale >= 0.0f))
+        return fail(KVE_ERR_INVALID_ARG, "%s: scale must be finite and >= 0", fn);
+    if (Hq / Hkv > kve::kDecodeMaxGroup)
+        return fail(KVE_ERR_UNSUPPORTED, "%s: Hq/Hkv=%d exceeds %d", fn, Hq / Hkv, kve::kDecodeMaxGroup);
+    const kve::DecodePlan p = kve::decode_plan(L, B, Hq, Hkv, k_cap, d);
+    if ((long long)p.segs * p.nsplit > kMaxGrid)
+        return fail(KVE_ERR_UNSUPPORTED, "%s: shape too large", fn);
+    if (workspace_bytes < p.total || workspace == nullptr)
+        return fail(KVE_ERR_WORKSPACE, "%s: workspace of %zu bytes < %zu needed", fn, workspace_bytes,
+                    p.total);
+    if (!aligned(workspace)) return fail(KVE_ERR_INVALID_ARG, "%s: workspace not 256-byte aligned", fn);
+    if (scale == 0.0f) scale = 1.0f / std::sqrt((float)d);
+    return from_hip(kve::launch_decode(q, k_c, v_c, count, (int)dtype, L, B, Hq, Hkv, k_cap, d, scale, out,
+                                       workspace, static_cast<hipStream_t>(stream)),
+                    fn);
+}
+
 size_t kve_topk_workspace_size(int L, int B, int Hkv, int N, int R) {
     (void)L;
     (void)B;

@@ -5,57 +5,9 @@
 #include <stddef.h>
 #include <stdint.h>
 
+#include "kve_snap_plan.h"
+
 namespace kve {
-
-constexpr size_t kAlign = 256;
-inline size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
-
-// ---------------------------------------------------------------------------
-// SnapKV score: rows of one segment are the G*W window queries (head-major),
-// taken in row groups of 128 (a segment and a row group form a vseg).  Each
-// vseg's keys are split into ranges of whole 64-key chunks, one workgroup each;
-// pass 1 writes one log-sum-exp per (vseg, range, row), a combine step reduces
-// them to one per row, pass 2 writes the column sums of each row group (a
-// plane), and the pool step adds the planes and max-pools the prefix.
-// ---------------------------------------------------------------------------
-constexpr int kSnapRowsPerGroup = 128;
-constexpr int kSnapMaxRows = 1024;
-constexpr int kSnapChunkKeys = 64;
-constexpr int kSnapTargetGroups = 4096;  // workgroups per pass the range size aims at
-constexpr int kSnapMaxRangeChunks = 32;  // at most 2048 keys per range
-
-struct SnapPlan {
-    int segs, rows, rgroups, n_vsegs, range_keys, nranges, planes;
-    size_t off_stats, off_lse, off_raw, total;
-};
-
-inline SnapPlan snap_plan(int L, int B, int Hq, int Hkv, int N, int W, int d = 128) {
-    (void)d;
-    SnapPlan p{};
-    p.segs = L * B * Hkv;
-    p.rows = (Hq / Hkv) * W;
-    p.rgroups = (p.rows + kSnapRowsPerGroup - 1) / kSnapRowsPerGroup;
-    p.n_vsegs = p.segs * p.rgroups;
-    p.planes = p.rgroups;
-    // whole chunks per range: about kSnapTargetGroups workgroups per pass (two
-    // per compute unit at a time), 4 .. 32 chunks each (fewer when N is short)
-    const long long chunks = (N + kSnapChunkKeys - 1) / kSnapChunkKeys;
-    long long per = (chunks * p.n_vsegs + kSnapTargetGroups - 1) / kSnapTargetGroups;
-    if (per < 4) per = 4;
-    if (per > kSnapMaxRangeChunks) per = kSnapMaxRangeChunks;
-    if (per > chunks) per = chunks;
-    p.range_keys = (int)(per * kSnapChunkKeys);
-    p.nranges = (int)((chunks + per - 1) / per);
-    size_t off = 0;
-    p.off_stats = off;
-    off = align_up(off + (size_t)p.n_vsegs * p.nranges * kSnapRowsPerGroup * sizeof(float));
-    p.off_lse = off;
-    off = align_up(off + (size_t)p.n_vsegs * kSnapRowsPerGroup * sizeof(float));
-    p.off_raw = off;
-    off = align_up(off + (size_t)p.planes * p.segs * N * sizeof(float));
-    p.total = off;
-    return p;
-}
 
 // ---------------------------------------------------------------------------
 // H2O score: pass 1 one start value (-lse2 / sl2) per (layer, sample, query
@@ -76,6 +28,39 @@ inline size_t h2o_workspace(int L, int B, int Hq, int N) {
     return h2o_colsum_offset(L, B, Hq, N) * sizeof(float) + align_up((size_t)L * B * Hq * N * sizeof(float));
 }
 
+// ---------------------------------------------------------------------------
+// Decode over a compacted cache: the k_cap rows of a segment are cut into
+// splits of whole kDecodeQuantum-row quanta, one workgroup each (about
+// kDecodeTargetGroups workgroups in all); each writes per head the partial
+// output o[d] and its (reference, denominator) pair, merged by a last step.
+// ---------------------------------------------------------------------------
+constexpr int kDecodeQuantum = 128;
+constexpr int kDecodeTargetGroups = 2048;
+constexpr int kDecodeMaxGroup = 8;  // query heads per KV head
+
+struct DecodePlan {
+    int segs, G, nsplit, split_keys;
+    size_t off_o, off_ml, total;
+};
+
+inline DecodePlan decode_plan(int L, int B, int Hq, int Hkv, int k_cap, int d) {
+    DecodePlan p{};
+    p.segs = L * B * Hkv;
+    p.G = Hq / Hkv;
+    const long long quanta = (k_cap + kDecodeQuantum - 1) / kDecodeQuantum;
+    long long ns = (kDecodeTargetGroups + p.segs - 1) / p.segs;
+    if (ns > quanta) ns = quanta;
+    if (ns < 1) ns = 1;
+    const long long per = (quanta + ns - 1) / ns;
+    p.split_keys = (int)(per * kDecodeQuantum);
+    p.nsplit = (int)((quanta + per - 1) / per);
+    const size_t parts = (size_t)p.segs * p.nsplit * p.G;
+    p.off_o = 0;
+    p.off_ml = align_up(parts * d * sizeof(float));
+    p.total = p.off_ml + align_up(parts * 2 * sizeof(float));
+    return p;
+}
+
 hipError_t launch_snapkv(const void* q, const void* k, int dtype, int L, int B, int Hq, int Hkv,
                          int N, int W, int d, float scale, int pool_k, float* score, void* ws,
                          hipStream_t st);
@@ -86,6 +71,10 @@ hipError_t launch_h2o(const void* q, const void* k, int dtype, int L, int B, int
 hipError_t launch_topk(const float* score, const int8_t* roles, const int32_t* quota, int L,
                        int B, int Hkv, int N, int W, int R, int k_cap, int32_t* idx_out,
                        int32_t* count_out, hipStream_t st);
+
+hipError_t launch_decode(const void* q, const void* kc, const void* vc, const int32_t* count, int dtype, int L,
+                         int B, int Hq, int Hkv, int k_cap, int d, float scale, float* out, void* ws,
+                         hipStream_t st);
 
 hipError_t launch_compact(const void* k, const void* v, int elem_bytes, const int32_t* idx,
                           const int32_t* count, int L, int B, int Hkv, int N, int d, int k_cap,

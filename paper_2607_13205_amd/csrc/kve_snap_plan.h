@@ -1,0 +1,58 @@
+// Workspace plan of the SnapKV score (shared by its kernels and the C ABI).
+#pragma once
+
+#include <stddef.h>
+
+namespace kve {
+
+constexpr size_t kAlign = 256;
+inline size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+// ---------------------------------------------------------------------------
+// SnapKV score: rows of one segment are the G*W window queries (head-major),
+// taken in row groups of 128 (a segment and a row group form a vseg).  Each
+// vseg's keys are split into ranges of whole 64-key chunks, one workgroup each;
+// pass 1 writes one log-sum-exp per (vseg, range, row), a combine step reduces
+// them to one per row, pass 2 writes the column sums of each row group (a
+// plane), and the pool step adds the planes and max-pools the prefix.
+// ---------------------------------------------------------------------------
+constexpr int kSnapRowsPerGroup = 128;
+constexpr int kSnapMaxRows = 1024;
+constexpr int kSnapChunkKeys = 64;
+constexpr int kSnapTargetGroups = 4096;  // workgroups per pass the range size aims at
+constexpr int kSnapMaxRangeChunks = 32;  // at most 2048 keys per range
+
+struct SnapPlan {
+    int segs, rows, rgroups, n_vsegs, range_keys, nranges, planes;
+    size_t off_stats, off_lse, off_raw, total;
+};
+
+inline SnapPlan snap_plan(int L, int B, int Hq, int Hkv, int N, int W, int d = 128) {
+    (void)d;
+    SnapPlan p{};
+    p.segs = L * B * Hkv;
+    p.rows = (Hq / Hkv) * W;
+    p.rgroups = (p.rows + kSnapRowsPerGroup - 1) / kSnapRowsPerGroup;
+    p.n_vsegs = p.segs * p.rgroups;
+    p.planes = p.rgroups;
+    // whole chunks per range: about kSnapTargetGroups workgroups per pass (two
+    // per compute unit at a time), 4 .. 32 chunks each (fewer when N is short)
+    const long long chunks = (N + kSnapChunkKeys - 1) / kSnapChunkKeys;
+    long long per = (chunks * p.n_vsegs + kSnapTargetGroups - 1) / kSnapTargetGroups;
+    if (per < 4) per = 4;
+    if (per > kSnapMaxRangeChunks) per = kSnapMaxRangeChunks;
+    if (per > chunks) per = chunks;
+    p.range_keys = (int)(per * kSnapChunkKeys);
+    p.nranges = (int)((chunks + per - 1) / per);
+    size_t off = 0;
+    p.off_stats = off;
+    off = align_up(off + (size_t)p.n_vsegs * p.nranges * kSnapRowsPerGroup * sizeof(float));
+    p.off_lse = off;
+    off = align_up(off + (size_t)p.n_vsegs * kSnapRowsPerGroup * sizeof(float));
+    p.off_raw = off;
+    off = align_up(off + (size_t)p.planes * p.segs * N * sizeof(float));
+    p.total = off;
+    return p;
+}
+
+}  // namespace kve

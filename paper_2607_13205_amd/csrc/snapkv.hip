@@ -30,7 +30,7 @@
 // Logits are kept in log2 units (x = scale * log2(e) * <q, k>) so that every
 // exponential is a single v_exp_f32.
 #include "kve_device.h"
-#include "kve_internal.h"
+#include "kve_snap_plan.h"
 #include "kve_stream.h"
 
 namespace kve {

@@ -65,3 +65,28 @@ def check_kept_set(idx_gpu, idx_orc, score_orc, roles, W: int, quota):
                 f"boundary {boundary!r}")
         ties += len(a)
     return ties
+
+
+# Decode outputs: o = sum_t p_t v_t is checked against the oracle entry by
+# entry with a bound proportional to sum_t p_t |v_t| (the magnitude the float32
+# sums actually carry, not |o|, which cancels).  Float32 logits of bfloat16
+# products are off by about 1e-6 of their magnitude; the factor (1 + xmax / 16)
+# widens the bound for large logits x (natural-log units), whose absolute
+# rounding error, and hence the relative error of exp(x), grows with |x|.
+DEC_RTOL = 1e-4
+
+
+def check_decode(gpu: np.ndarray, orc: np.ndarray, orc_abs: np.ndarray, xmax: float,
+                 what: str = "decode"):
+    gpu = np.asarray(gpu, dtype=np.float64)
+    orc = np.asarray(orc, dtype=np.float64)
+    assert gpu.shape == orc.shape, (gpu.shape, orc.shape)
+    assert np.all(np.isfinite(gpu)), f"{what}: non-finite values"
+    bound = DEC_RTOL * (1.0 + xmax / 16.0) * np.asarray(orc_abs, dtype=np.float64) + 1e-30
+    err = np.abs(gpu - orc)
+    bad = err > bound
+    if np.any(bad):
+        i = np.unravel_index(np.argmax(err / bound), err.shape)
+        raise AssertionError(f"{what}: {int(bad.sum())} of {bad.size} entries out of tolerance; "
+                             f"worst at {i}: gpu={gpu[i]!r} oracle={orc[i]!r} bound={bound[i]!r}")
+    return float(np.max(err / bound))

@@ -29,7 +29,7 @@ def _declared():
 
 def test_every_declared_symbol_is_exported(kve):
     names = _declared()
-    assert len(names) == 12
+    assert len(names) == 14
     assert sorted(kve.EXPORTED) == names
     lib = ctypes.CDLL(kve.binding._LIB_PATH)
     for n in names:
@@ -154,6 +154,15 @@ def test_device_entry_points_validate_before_launch(kve):
     # compact: v without v_out, bad head_dim
     assert L.kve_kv_compact(dummy, dummy, 0, dummy, dummy, 1, 1, 2, 64, 128, 10, dummy, null, null) == 1
     assert L.kve_kv_compact(dummy, null, 0, dummy, dummy, 1, 1, 2, 64, 80, 10, dummy, null, null) == 2
+    # decode: G > 8, null count, short workspace, negative scale, k_cap 0, misaligned workspace
+    big = 1 << 30
+    assert L.kve_decode_attention(dummy, dummy, dummy, dummy, 0, 1, 1, 18, 2, 64, 128, 0.0, dummy, dummy, big, null) == 2
+    assert L.kve_decode_attention(dummy, dummy, dummy, null, 0, 1, 1, 8, 2, 64, 128, 0.0, dummy, dummy, big, null) == 1
+    assert L.kve_decode_attention(dummy, dummy, dummy, dummy, 0, 1, 1, 8, 2, 64, 128, 0.0, dummy, dummy, 8, null) == 3
+    assert L.kve_decode_attention(dummy, dummy, dummy, dummy, 0, 1, 1, 8, 2, 64, 128, -1.0, dummy, dummy, big, null) == 1
+    assert L.kve_decode_attention(dummy, dummy, dummy, dummy, 0, 1, 1, 8, 2, 0, 128, 0.0, dummy, dummy, big, null) == 1
+    assert L.kve_decode_attention(dummy, dummy, dummy, dummy, 0, 1, 1, 8, 2, 64, 128, 0.0, dummy,
+                                  ctypes.c_void_p(0x1010), big, null) == 1
 
 
 def test_workspace_sizes_are_aligned_and_monotone(kve):
@@ -166,3 +175,7 @@ def test_workspace_sizes_are_aligned_and_monotone(kve):
     h = kve.h2o_workspace_size(2, 1, 32, 8, 1000, 128)
     assert h % 256 == 0 and h >= 2 * 32 * 1024 * 4 + 2 * 32 * 1000 * 4
     assert kve.binding.LIB.kve_topk_workspace_size(1, 1, 8, 8192, 4) == 0
+    # decode: per (segment, split, head) a partial output row and a pair of floats
+    w = kve.decode_workspace_size(32, 4, 32, 8, 1640, 128)
+    assert w % 256 == 0 and w >= 1024 * 32 * (128 + 2) * 4 // 8
+    assert kve.decode_workspace_size(1, 1, 32, 8, 0, 128) == 0

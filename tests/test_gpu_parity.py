@@ -13,7 +13,7 @@ import pytest
 
 import oracle as O
 import workload as WL
-from tests.parity import check_kept_set, check_scores
+from tests.parity import check_decode, check_kept_set, check_scores
 
 pytestmark = pytest.mark.gpu
 torch = pytest.importorskip("torch")
@@ -378,5 +378,139 @@ def test_pipeline_full_size_sampled(K, name, budget, segs, pol):
     policy = WL.default_alpha(0.0) if pol == "role" else _policy(pol)
     ties = _pipeline_check(K, wl, inp, budget, policy, segs=segs)
     note(f"  near-tie pairs: {ties}")
+    if pol == "role" and wl.scorer == "snapkv":
+        note("  decode over the compacted cache of the sampled segments")
+        _decode_after_eviction(K, wl, inp, budget, segs)
     del inp
     torch.cuda.empty_cache()
+
+
+# ---------------------------------------------------------------------------
+# Decode through the keep-set over the compacted cache
+# ---------------------------------------------------------------------------
+
+def _decode_ref(q, kc, vc, count, scale=None):
+    """Oracle output, the same with |v| (the bound's magnitude) and the largest
+    |logit| in natural-log units, for q [L, B, Hq, d], caches [L, B, Hkv, k_cap, d]."""
+    ref = O.decode_attention_batch(q, kc, vc, count, scale)
+    ref_abs = O.decode_attention_batch(q, kc, np.abs(vc), count, scale)
+    L, B, Hq, d = q.shape
+    Hkv, k_cap = kc.shape[2], kc.shape[3]
+    G = Hq // Hkv
+    s = 1.0 / math.sqrt(d) if scale is None else scale
+    xmax = 0.0
+    for l, b, j in np.ndindex(L, B, Hkv):
+        n = int(min(max(int(count[l, b, j]), 0), k_cap))
+        if n:
+            xmax = max(xmax, float(np.max(np.abs(s * q[l, b, j * G:(j + 1) * G] @ kc[l, b, j, :n].T))))
+    return ref, ref_abs, xmax
+
+
+DECODE_CASES = [
+    # name, L, B, Hq, Hkv, k_cap, d, dtype, q gain
+    ("g4", 2, 2, 8, 2, 300, 128, "bf16", 3.0),
+    ("g1", 1, 2, 4, 4, 77, 128, "bf16", 3.0),
+    ("g8", 1, 1, 16, 2, 513, 128, "bf16", 3.0),
+    ("g3", 1, 2, 6, 2, 129, 128, "bf16", 3.0),
+    ("g6d64", 2, 1, 12, 2, 1000, 64, "bf16", 3.0),
+    ("kcap1", 1, 1, 8, 2, 1, 128, "bf16", 3.0),
+    ("splits", 1, 2, 8, 1, 7000, 128, "bf16", 3.0),
+    ("hot", 1, 2, 8, 2, 2000, 128, "bf16", 25.0),
+    ("f32", 1, 2, 8, 2, 260, 128, "f32", 3.0),
+    ("f32d64g8", 1, 1, 8, 1, 333, 64, "f32", 3.0),
+]
+
+
+@pytest.mark.parametrize("case", DECODE_CASES, ids=lambda c: c[0])
+def test_decode_matches_oracle(K, case):
+    """Ragged counts (0, 1, k_cap, above k_cap, in between), rows at and beyond
+    the count filled with NaN (they must never be read into the result), and a
+    workspace filled with NaN bytes."""
+    name, L, B, Hq, Hkv, k_cap, d, dt, gain = case
+    note(f"decode {name}")
+    tdt = torch.bfloat16 if dt == "bf16" else torch.float32
+    g = torch.Generator(device="cpu")
+    g.manual_seed(1234 + len(name))
+    q = (gain * torch.randn((L, B, Hq, d), generator=g)).to(tdt)
+    kc = torch.randn((L, B, Hkv, k_cap, d), generator=g).to(tdt)
+    vc = torch.randn((L, B, Hkv, k_cap, d), generator=g).to(tdt)
+    r = np.random.default_rng(77)
+    count = r.integers(0, k_cap + 1, (L, B, Hkv)).astype(np.int32)
+    flat = count.reshape(-1)
+    specials = [0, 1, k_cap, k_cap + 5, -3]
+    for i in range(min(len(flat), len(specials))):
+        flat[i] = specials[i]
+    count = flat.reshape(count.shape)
+    for idx in np.ndindex(L, B, Hkv):
+        n = int(min(max(int(count[idx]), 0), k_cap))
+        kc[idx][n:] = float("nan")
+        vc[idx][n:] = float("nan")
+    qd, kd, vd = q.cuda(), kc.cuda(), vc.cuda()
+    cd = torch.from_numpy(count).cuda()
+    ws = torch.full((K.decode_workspace_size(L, B, Hq, Hkv, k_cap, d),), 0xFF, dtype=torch.uint8, device="cuda")
+    out = K.decode_attention(qd, kd, vd, cd, workspace=ws)
+    torch.cuda.synchronize()
+    kc64, vc64 = f64(kc), f64(vc)
+    kc64 = np.nan_to_num(kc64, nan=0.0)
+    vc64 = np.nan_to_num(vc64, nan=0.0)
+    ref, ref_abs, xmax = _decode_ref(f64(q), kc64, vc64, count)
+    check_decode(out.cpu().numpy(), ref, ref_abs, xmax, f"decode {name}")
+    # empty segments give zeros
+    for idx in np.ndindex(L, B, Hkv):
+        if min(max(int(count[idx]), 0), k_cap) == 0:
+            G = Hq // Hkv
+            assert not out[idx[0], idx[1], idx[2] * G:(idx[2] + 1) * G].any()
+
+
+def test_decode_explicit_scale_and_repeat(K):
+    L, B, Hq, Hkv, k_cap, d = 1, 2, 8, 2, 400, 128
+    g = torch.Generator(device="cpu")
+    g.manual_seed(99)
+    q = torch.randn((L, B, Hq, d), generator=g).to(torch.bfloat16)
+    kc = torch.randn((L, B, Hkv, k_cap, d), generator=g).to(torch.bfloat16)
+    vc = torch.randn((L, B, Hkv, k_cap, d), generator=g).to(torch.bfloat16)
+    count = np.full((L, B, Hkv), k_cap, dtype=np.int32)
+    cd = torch.from_numpy(count).cuda()
+    out1 = K.decode_attention(q.cuda(), kc.cuda(), vc.cuda(), cd, scale=0.3)
+    out2 = K.decode_attention(q.cuda(), kc.cuda(), vc.cuda(), cd, scale=0.3)
+    torch.cuda.synchronize()
+    assert torch.equal(out1, out2)
+    ref, ref_abs, xmax = _decode_ref(f64(q), f64(kc), f64(vc), count, scale=0.3)
+    check_decode(out1.cpu().numpy(), ref, ref_abs, xmax, "decode scale 0.3")
+
+
+def _decode_after_eviction(K, wl, inp, budget, segs):
+    """Evict with the role policy, decode one new query per head over the
+    compacted cache, and compare with decoding through the keep-mask over the
+    full cache (the paper's harness form) for the sampled segments."""
+    from paper_2607_13205_amd import pipeline
+    W = wl.W
+    alpha = WL.default_alpha(0.0)
+    _, _, k_cap = K.role_allocate(inp["roles"], 4, alpha, budget, W)
+    bufs = pipeline.alloc_buffers(inp["k"], wl.Hq, W, 4, k_cap)
+    pipeline.evict(inp["q"], inp["k"], inp["v"], inp["roles"], inp["roles_t"], alpha, budget, W,
+                   wl.pool_k, bufs)
+    g = torch.Generator(device="cuda")
+    g.manual_seed(4321)
+    L = inp["k"].shape[0]
+    qd = (3.0 * torch.randn((L, wl.B, wl.Hq, wl.d), generator=g, device="cuda")).to(inp["k"].dtype)
+    out = K.decode_attention(qd, bufs.k_out, bufs.v_out, bufs.count)
+    torch.cuda.synchronize()
+    G = wl.G
+    for (l, b, j) in segs:
+        n = int(bufs.count[l, b, j])
+        idx = bufs.idx[l, b, j, :n].cpu().numpy()
+        qs = f64(qd[l, b, j * G:(j + 1) * G])
+        kf, vf = f64(inp["k"][l, b, j]), f64(inp["v"][l, b, j])
+        ref = O.masked_decode_attention(qs, kf, vf, idx)
+        ref_abs = O.masked_decode_attention(qs, kf, np.abs(vf), idx)
+        xmax = float(np.max(np.abs(qs @ kf[idx].T))) / math.sqrt(wl.d)
+        check_decode(out[l, b, j * G:(j + 1) * G].cpu().numpy(), ref, ref_abs, xmax,
+                     f"{wl.name} decode seg {(l, b, j)}")
+    return bufs, out
+
+
+def test_decode_after_eviction_layer8k(K):
+    wl = WL.get_workload("layer8k")
+    inp = WL.make_inputs(wl, device="cuda")
+    _decode_after_eviction(K, wl, inp, 0.1, list(np.ndindex(len(inp["layers"]), wl.B, wl.Hkv)))
