@@ -121,3 +121,25 @@ def decode_loops(q_heads, k, v, keep, scale=None):
         z = sum(w)
         out.append([sum(w[i] * float(v[t][c]) for i, t in enumerate(keep)) / z for c in range(d)])
     return out
+
+
+def quest_loops(q_win, k, page):
+    """Page bounds of the one-shot Quest analogue with loops (§5 "Query-aware
+    baseline"): q_win[h][i] window rows of head h, k the key rows; returns the
+    score of every position (window positions: +inf)."""
+    G, W, d = len(q_win), len(q_win[0]), len(k[0])
+    N = len(k)
+    P = N - W
+    qbar = [[sum(float(q_win[h][i][c]) for i in range(W)) / W for c in range(d)] for h in range(G)]
+    out = [math.inf] * N
+    for start in range(0, P, page):
+        rows = list(range(start, min(start + page, P)))
+        bound = 0.0
+        for h in range(G):
+            for c in range(d):
+                lo = min(float(k[t][c]) for t in rows)
+                hi = max(float(k[t][c]) for t in rows)
+                bound += max(qbar[h][c] * lo, qbar[h][c] * hi)
+        for t in rows:
+            out[t] = bound
+    return out

@@ -40,7 +40,14 @@ that uses it):
       stay empty;
   R18 fair eviction (§5 "Fair-eviction baseline") retains every bucket at the
       same rate: bucket r keeps ceil(n_r * K_p / P) of its n_r candidates, the
-      ceiling of R7 as for the role policy.
+      ceiling of R7 as for the role policy;
+  R20 the one-shot Quest analogue (§5 "Query-aware baseline") scores pages of
+      16 consecutive prefix tokens (the last one ragged; the window belongs to
+      no page) by Quest's per-channel key bound against each head's mean
+      window query, summed over the G heads of the group (as R2 sums their
+      mass); every token carries its page's bound, window tokens +inf, and the
+      same per-bucket top-k then keeps whole pages in bound order (the lower
+      index first on ties), the last one cut at the budget.
 """
 
 from __future__ import annotations
@@ -58,6 +65,9 @@ __all__ = [
     "h2o_mass",
     "maxpool_prefix",
     "snapkv_score",
+    "quest_page_bounds",
+    "quest_mass",
+    "quest_score",
     "h2o_score",
     "role_counts",
     "role_allocate",
@@ -214,6 +224,56 @@ def h2o_score(q: np.ndarray, k: np.ndarray, n_kv_heads: int,
         for b in range(Bt):
             for j in range(n_kv_heads):
                 out[l, b, j] = h2o_mass(q[l, b, j * G:(j + 1) * G], k[l, b, j], scale)
+    return out
+
+
+def quest_page_bounds(q_mean: np.ndarray, k: np.ndarray, page: int) -> np.ndarray:
+    """Quest's page bound (§5 "Query-aware baseline"; R20) for the pages of
+    the key rows k [P, d]: page j covers rows [j*page, min((j+1)*page, P)).
+    For each head h, sum_c max(qbar_h[c] * kmin_j[c], qbar_h[c] * kmax_j[c])
+    with kmin/kmax the per-channel minimum and maximum of the page's keys,
+    summed over the heads.  q_mean [G, d].  No score of a key of the page,
+    sum_h <qbar_h, k_t>, exceeds its page's bound."""
+    q_mean = np.asarray(q_mean, dtype=np.float64)
+    k = np.asarray(k, dtype=np.float64)
+    P = k.shape[0]
+    n_pages = (P + page - 1) // page
+    out = np.zeros(n_pages, dtype=np.float64)
+    for j in range(n_pages):
+        rows = k[j * page:min((j + 1) * page, P)]
+        kmin = rows.min(axis=0)
+        kmax = rows.max(axis=0)
+        out[j] = float(np.sum(np.maximum(q_mean * kmin[None, :], q_mean * kmax[None, :])))
+    return out
+
+
+def quest_mass(q_win: np.ndarray, k: np.ndarray, page: int = 16) -> np.ndarray:
+    """Token scores of the one-shot Quest analogue for one KV head (R20):
+    q_win [G, W, d] window queries, k [N, d].  Prefix token t gets the bound
+    of page t // page; window tokens get +inf (always kept)."""
+    q_win = np.asarray(q_win, dtype=np.float64)
+    N = np.asarray(k).shape[0]
+    W = q_win.shape[1]
+    P = N - W
+    q_mean = q_win.mean(axis=1)                       # each head's mean window query
+    s = np.full(N, np.inf, dtype=np.float64)
+    if P > 0:
+        bounds = quest_page_bounds(q_mean, np.asarray(k)[:P], page)
+        s[:P] = bounds[np.arange(P) // page]
+    return s
+
+
+def quest_score(q_win: np.ndarray, k: np.ndarray, n_kv_heads: int, page: int = 16) -> np.ndarray:
+    """quest_mass for whole tensors: q_win [L, B, Hq, W, d], k [L, B, Hkv, N, d]
+    -> [L, B, Hkv, N]."""
+    L, Bt, Hq, W, d = q_win.shape
+    N = k.shape[3]
+    G = Hq // n_kv_heads
+    out = np.zeros((L, Bt, n_kv_heads, N), dtype=np.float64)
+    for l in range(L):
+        for b in range(Bt):
+            for j in range(n_kv_heads):
+                out[l, b, j] = quest_mass(q_win[l, b, j * G:(j + 1) * G], k[l, b, j], page)
     return out
 
 
