@@ -16,7 +16,8 @@ bounded sample of the same workload; ``policies`` gives the step time of the
 same workload under fair eviction and the No-KEY counterfactual, which reuse
 every kernel with other quotas; ``decode`` times one decode query per head over
 the compacted cache of every layer against the same kernel over the full
-cache.
+cache; ``quest`` times the one-shot Quest page-bound scorer on the same
+inputs, alone and as the score of the whole step.
 
 ``roofline.traffic`` is the measured HBM traffic of one score call, read from
 the counter summary in profiles/ (rocprofv3 FETCH_SIZE and WRITE_SIZE,
@@ -61,6 +62,7 @@ def parse():
                     help="target CPU time of the oracle baseline sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-h2o", action="store_true", help="skip the H2O scorer leg")
+    ap.add_argument("--no-quest", action="store_true", help="skip the Quest scorer timings")
     ap.add_argument("--no-decode", action="store_true",
                     help="skip the decode timings over the compacted and the full cache")
     ap.add_argument("--no-policies", action="store_true",
@@ -276,6 +278,32 @@ def decode_leg(K, wl, inp, bufs, steps):
             "speedup_vs_full_cache": round(ms_f / ms_c, 2)}
 
 
+def quest_leg(K, pipeline, wl, inp, budget, alpha, steps):
+    """The one-shot Quest page-bound score (pages of 16) on the same inputs:
+    the score call alone (HBM-bound: K read once, one float per token written)
+    and the whole step with it as the score."""
+    import torch
+    L, B, Hkv, N, d = inp["k"].shape
+    elem = inp["k"].element_size()
+    score = torch.empty((L, B, Hkv, N), dtype=torch.float32, device="cuda")
+    ws = torch.empty(K.quest_workspace_size(L, B, wl.Hq, Hkv, d), dtype=torch.uint8, device="cuda")
+    ms = _time_calls(lambda: K.quest_score(inp["q"], inp["k"], 16, score=score, workspace=ws), steps)
+    qbytes = L * B * wl.Hq * wl.W * d * elem
+    nbytes = L * B * Hkv * (N - wl.W) * d * elem + qbytes + L * B * Hkv * N * 4
+    gbs = nbytes / (ms * 1e-3) / 1e9
+    del score, ws
+    _, _, k_cap = K.role_allocate(inp["roles"], 4, alpha, budget, wl.W)
+    bufs = pipeline.alloc_buffers(inp["k"], wl.Hq, wl.W, 4, k_cap, scorer="quest")
+    ms_step = _time_calls(lambda: pipeline.evict(inp["q"], inp["k"], inp["v"], inp["roles"], inp["roles_t"],
+                                                 alpha, budget, wl.W, 1, bufs, scorer="quest"), steps)
+    del bufs
+    torch.cuda.empty_cache()
+    return {"kernel": "kve_quest_score (mean query + page bounds), page 16", "ms": round(ms, 4),
+            "algorithmic_bytes": nbytes, "achieved_GBs": round(gbs, 1),
+            "hbm_frac": round(gbs / HBM_PEAK_GBS, 4), "ms_per_step": round(ms_step, 4),
+            "tokens_per_s": round(B * N / (ms_step * 1e-3), 1)}
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -369,6 +397,9 @@ def main():
         out["decode"] = decode_leg(K, wl, inp, bufs, max(3, args.steps // 2))
     del bufs
     torch.cuda.empty_cache()
+    if not args.no_quest and scorer == "snapkv":
+        print("[bench] Quest scorer", file=sys.stderr, flush=True)
+        out["quest"] = quest_leg(K, pipeline, wl, inp, budget, alpha, max(3, args.steps // 2))
     if not args.no_policies:
         print("[bench] fair-eviction and No-KEY steps", file=sys.stderr, flush=True)
         out["policies"] = policy_leg(WL, pipeline, wl, inp, budget, W, pool, max(3, args.steps // 2))

@@ -137,6 +137,47 @@ kve_status_t kve_h2o_score(const void* q, const void* k, kve_dtype_t dtype,
                            void* stream);
 
 /* ------------------------------------------------------------------------- */
+/* One-shot Quest analogue (paper §5 "Query-aware baseline"): page key bounds  */
+/* against the mean window query, a second scorer for the same selection.     */
+/* ------------------------------------------------------------------------- */
+
+/* Workspace bytes kve_quest_score needs (0 if invalid). */
+size_t kve_quest_workspace_size(int L, int B, int Hq, int Hkv, int d);
+
+/*
+ * Per (layer l, sample b, KV head j): the candidate prefix [0, N-W) is cut
+ * into pages of `page` consecutive tokens, page i = [i*page, min((i+1)*page,
+ * N-W)).  With qbar_h the mean of the W window queries of query head h and
+ * kmin, kmax the per-channel minimum and maximum of a page's keys, the page
+ * score is
+ *   sum over the G heads h of group j, sum over channels c of
+ *   max(qbar_h[c] * kmin[c], qbar_h[c] * kmax[c]),
+ * an upper bound of sum_h <qbar_h, k_t> for every key t of the page (Quest's
+ * criterion, made once after prefill).  score[l, b, j, t] is the score of
+ * token t's page for t < N-W and +inf for the window.  Fed to
+ * kve_topk_select, one bucket keeps whole pages in bound order (ties: the
+ * lower page), the last one cut at the budget; role buckets compose as with
+ * the other scores.
+ *
+ *   q_win     [L, B, Hq, W, d] bf16 or fp32 (device), as for kve_snapkv_score
+ *   k         [L, B, Hkv, N, d] same dtype (device)
+ *   page      tokens per page, 1 .. 1024 (16 is Quest's usual size)
+ *   score     [L, B, Hkv, N] float32 (device)
+ *   workspace kve_quest_workspace_size bytes, 256-byte aligned, owned by the
+ *             caller: the mean window query of every head, [L, B, Hq, d]
+ *             float32; contents on entry do not matter.
+ *
+ * Requires Hq/Hkv <= 8.  Enqueued on `stream`.  Errors: KVE_ERR_INVALID_ARG
+ * (null pointers, bad shapes, W outside [1, N], page outside [1, 1024],
+ * misaligned workspace), KVE_ERR_UNSUPPORTED (d not 64/128, Hq/Hkv > 8, grid
+ * too large), KVE_ERR_WORKSPACE, KVE_ERR_HIP.
+ */
+kve_status_t kve_quest_score(const void* q_win, const void* k, kve_dtype_t dtype,
+                             int L, int B, int Hq, int Hkv, int N, int W, int d, int page,
+                             float* score, void* workspace, size_t workspace_bytes,
+                             void* stream);
+
+/* ------------------------------------------------------------------------- */
 /* Role-conditional allocation (paper §4.1 role policy; Algorithm 1,          */
 /* per-bucket top-k and redistribution steps).  HOST function.                */
 /* ------------------------------------------------------------------------- */

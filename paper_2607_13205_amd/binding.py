@@ -35,6 +35,7 @@ EXPORTED = (
     "kve_topk_workspace_size", "kve_topk_select",
     "kve_kv_compact",
     "kve_decode_workspace_size", "kve_decode_attention",
+    "kve_quest_workspace_size", "kve_quest_score",
 )
 
 
@@ -72,6 +73,8 @@ def _load():
         "kve_kv_compact": (c_int, [c_void, c_void, c_int, c_void, c_void] + [c_int] * 6 +
                            [c_void, c_void, c_void]),
         "kve_decode_workspace_size": (c_size, [c_int] * 6),
+        "kve_quest_workspace_size": (c_size, [c_int] * 5),
+        "kve_quest_score": (c_int, [c_void, c_void, c_int] + [c_int] * 8 + [c_void, c_void, c_size, c_void]),
         "kve_decode_attention": (c_int, [c_void, c_void, c_void, c_void, c_int] + [c_int] * 6 +
                                  [c_float, c_void, c_void, c_size, c_void]),
     }
@@ -192,6 +195,25 @@ def h2o_score(q, k, scale: float = 0.0, score=None, workspace=None, stream=None)
     ws, wsb = _workspace(h2o_workspace_size(L, B, Hq, Hkv, N, d), k.device, workspace)
     _check(LIB.kve_h2o_score(_dev(q, "q"), _dev(k, "k"), _dtype_code(k), L, B, Hq, Hkv, N, d,
                              float(scale), _dev(score, "score"), _ptr(ws), wsb, _stream(stream)))
+    return score
+
+
+def quest_workspace_size(L, B, Hq, Hkv, d) -> int:
+    return int(LIB.kve_quest_workspace_size(L, B, Hq, Hkv, d))
+
+
+def quest_score(q_win, k, page: int = 16, score=None, workspace=None, stream=None):
+    """One-shot Quest page-bound scores [L, B, Hkv, N] (window tokens +inf)."""
+    torch = _torch()
+    L, B, Hq, W, d = q_win.shape
+    Lk, Bk, Hkv, N, dk = k.shape
+    if (L, B, d) != (Lk, Bk, dk) or q_win.dtype != k.dtype:
+        raise ValueError("q_win and k disagree in L, B, d or dtype")
+    if score is None:
+        score = torch.empty((L, B, Hkv, N), dtype=torch.float32, device=k.device)
+    ws, wsb = _workspace(quest_workspace_size(L, B, Hq, Hkv, d), k.device, workspace)
+    _check(LIB.kve_quest_score(_dev(q_win, "q_win"), _dev(k, "k"), _dtype_code(k), L, B, Hq, Hkv, N, W, d,
+                               int(page), _dev(score, "score"), _ptr(ws), wsb, _stream(stream)))
     return score
 
 

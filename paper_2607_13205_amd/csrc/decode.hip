@@ -64,31 +64,6 @@ struct QKFrag<float, D> {
     }
 };
 
-// 16 bytes of a value row as CW floats.
-template <typename T>
-struct VPiece;
-
-template <>
-struct VPiece<__bf16> {
-    static constexpr int CW = 8;
-    __device__ __forceinline__ static void to_f(u32x4 v, float (&f)[CW]) {
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-            f[2 * e] = __uint_as_float(v[e] << 16);
-            f[2 * e + 1] = __uint_as_float(v[e] & 0xffff0000u);
-        }
-    }
-};
-
-template <>
-struct VPiece<float> {
-    static constexpr int CW = 4;
-    __device__ __forceinline__ static void to_f(u32x4 v, float (&f)[CW]) {
-#pragma unroll
-        for (int e = 0; e < 4; ++e) f[e] = __uint_as_float(v[e]);
-    }
-};
-
 __device__ __forceinline__ float xor_max32(float v) {
 #pragma unroll
     for (int s = 1; s < 32; s <<= 1) v = fmaxf(v, __shfl_xor(v, s));

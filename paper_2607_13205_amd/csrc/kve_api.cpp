@@ -282,6 +282,36 @@ kve_status_t kve_role_map(const int8_t* roles, size_t n, const int8_t* map, int 
     return ok();
 }
 
+size_t kve_quest_workspace_size(int L, int B, int Hq, int Hkv, int d) {
+    if (L <= 0 || B <= 0 || Hq <= 0 || Hkv <= 0 || Hq % Hkv != 0) return 0;
+    if (d != 64 && d != 128) return 0;
+    return kve::align_up((size_t)L * B * Hq * d * sizeof(float));
+}
+
+kve_status_t kve_quest_score(const void* q_win, const void* k, kve_dtype_t dtype, int L, int B, int Hq,
+                             int Hkv, int N, int W, int d, int page, float* score, void* workspace,
+                             size_t workspace_bytes, void* stream) {
+    const char* fn = "kve_quest_score";
+    kve_status_t st = check_common(fn, L, B, Hq, Hkv, N, d, (int)dtype);
+    if (st != KVE_OK) return st;
+    if (q_win == nullptr || k == nullptr || score == nullptr)
+        return fail(KVE_ERR_INVALID_ARG, "%s: null tensor pointer", fn);
+    if (W < 1 || W > N) return fail(KVE_ERR_INVALID_ARG, "%s: need 1 <= W <= N (W=%d N=%d)", fn, W, N);
+    if (page < 1 || page > kve::kQuestMaxPage)
+        return fail(KVE_ERR_INVALID_ARG, "%s: page must be in [1, %d] (got %d)", fn, kve::kQuestMaxPage, page);
+    if (Hq / Hkv > kve::kQuestMaxGroup)
+        return fail(KVE_ERR_UNSUPPORTED, "%s: Hq/Hkv=%d exceeds %d", fn, Hq / Hkv, kve::kQuestMaxGroup);
+    const kve::QuestPlan p = kve::quest_plan(L, B, Hq, Hkv, N, W, d, dtype == KVE_DTYPE_BF16 ? 2 : 4, page);
+    if ((long long)p.segs * p.nranges > kMaxGrid) return fail(KVE_ERR_UNSUPPORTED, "%s: shape too large", fn);
+    if (workspace_bytes < p.total || workspace == nullptr)
+        return fail(KVE_ERR_WORKSPACE, "%s: workspace of %zu bytes < %zu needed", fn, workspace_bytes,
+                    p.total);
+    if (!aligned(workspace)) return fail(KVE_ERR_INVALID_ARG, "%s: workspace not 256-byte aligned", fn);
+    return from_hip(kve::launch_quest(q_win, k, (int)dtype, L, B, Hq, Hkv, N, W, d, page, score, workspace,
+                                      static_cast<hipStream_t>(stream)),
+                    fn);
+}
+
 size_t kve_decode_workspace_size(int L, int B, int Hq, int Hkv, int k_cap, int d) {
     if (L <= 0 || B <= 0 || Hq <= 0 || Hkv <= 0 || k_cap <= 0 || Hq % Hkv != 0) return 0;
     if (d != 64 && d != 128) return 0;

@@ -67,6 +67,31 @@ template <> struct Mma<float> {
     }
 };
 
+// 16 bytes of a key or value row as CW floats.
+template <typename T>
+struct VPiece;
+
+template <>
+struct VPiece<__bf16> {
+    static constexpr int CW = 8;
+    __device__ __forceinline__ static void to_f(u32x4 v, float (&f)[CW]) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            f[2 * e] = __uint_as_float(v[e] << 16);
+            f[2 * e + 1] = __uint_as_float(v[e] & 0xffff0000u);
+        }
+    }
+};
+
+template <>
+struct VPiece<float> {
+    static constexpr int CW = 4;
+    __device__ __forceinline__ static void to_f(u32x4 v, float (&f)[CW]) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) f[e] = __uint_as_float(v[e]);
+    }
+};
+
 // Row of output register i held by lane l in a 32x32 block (see Mma).
 __device__ __forceinline__ int c_row(int i, int lane) {
     return 8 * (i >> 2) + 4 * (lane >> 5) + (i & 3);

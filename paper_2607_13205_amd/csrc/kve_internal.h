@@ -61,6 +61,37 @@ inline DecodePlan decode_plan(int L, int B, int Hq, int Hkv, int k_cap, int d) {
     return p;
 }
 
+// ---------------------------------------------------------------------------
+// One-shot Quest analogue: a first step writes each head's mean window query
+// (the workspace, [segs, G, d] float32); the page step cuts the prefix of a
+// segment into pages and gives each workgroup a range of whole wave steps of
+// pages (about kQuestTargetGroups workgroups in all).
+// ---------------------------------------------------------------------------
+constexpr int kQuestTargetGroups = 4096;
+constexpr int kQuestMaxGroup = 8;  // query heads per KV head
+constexpr int kQuestMaxPage = 1024;
+
+struct QuestPlan {
+    int segs, G, n_pages, range_pages, nranges;
+    size_t total;
+};
+
+inline QuestPlan quest_plan(int L, int B, int Hq, int Hkv, int N, int W, int d, int elem, int page) {
+    QuestPlan p{};
+    p.segs = L * B * Hkv;
+    p.G = Hq / Hkv;
+    const int P = N - W;
+    p.n_pages = (P + page - 1) / page;
+    const int step = 4 * (64 / (d * elem / 16));  // pages per workgroup step: 4 waves
+    const long long steps = (p.n_pages + step - 1) / step;
+    long long per = (steps * p.segs + kQuestTargetGroups - 1) / kQuestTargetGroups;
+    if (per < 1) per = 1;
+    p.range_pages = (int)(per * step);
+    p.nranges = p.n_pages > 0 ? (int)((p.n_pages + p.range_pages - 1) / p.range_pages) : 1;
+    p.total = align_up((size_t)p.segs * p.G * d * sizeof(float));
+    return p;
+}
+
 hipError_t launch_snapkv(const void* q, const void* k, int dtype, int L, int B, int Hq, int Hkv,
                          int N, int W, int d, float scale, int pool_k, float* score, void* ws,
                          hipStream_t st);
@@ -75,6 +106,9 @@ hipError_t launch_topk(const float* score, const int8_t* roles, const int32_t* q
 hipError_t launch_decode(const void* q, const void* kc, const void* vc, const int32_t* count, int dtype, int L,
                          int B, int Hq, int Hkv, int k_cap, int d, float scale, float* out, void* ws,
                          hipStream_t st);
+
+hipError_t launch_quest(const void* q, const void* k, int dtype, int L, int B, int Hq, int Hkv, int N, int W,
+                        int d, int page, float* score, void* ws, hipStream_t st);
 
 hipError_t launch_compact(const void* k, const void* v, int elem_bytes, const int32_t* idx,
                           const int32_t* count, int L, int B, int Hkv, int N, int d, int k_cap,

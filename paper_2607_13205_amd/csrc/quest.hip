@@ -1,0 +1,146 @@
+// One-shot Quest analogue (§5 "Query-aware baseline"): the candidate prefix
+// of every segment (layer, sample, KV head) is cut into pages of `page`
+// consecutive tokens (the last one ragged; the window belongs to no page).
+// A page's score is Quest's key bound: per head h of the group, the sum over
+// channels of max(qbar_h[c] kmin[c], qbar_h[c] kmax[c]), with kmin and kmax the
+// per-channel extremes of the page's keys and qbar_h the mean of head h's
+// window queries, summed over the group's heads.  Every prefix token gets its
+// page's score and the window +inf, so that the per-bucket top-k keeps whole
+// pages in bound order.
+//
+// One pass over K: a group of lanes covers one key row (16 bytes each), so a
+// wave streams several pages side by side, keeping running per-channel minima
+// and maxima in registers; the bound is then a short reduction over the group.
+// HBM-bound: K is read once, one float written per token.
+#include "kve_device.h"
+#include "kve_internal.h"
+
+namespace kve {
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int kWaves = kThreads / kWave;
+constexpr int kRowBatch = 16;  // key rows loaded before any is used
+
+// qbar[seg, h, c] = mean over the W window rows of head h (float32)
+template <typename T>
+__global__ __launch_bounds__(kThreads) void quest_qmean(const T* __restrict__ q, int W, int G, int D,
+                                                        float* __restrict__ qbar) {
+    const int seg = blockIdx.x;
+    const float inv = 1.0f / (float)W;
+    for (int e = threadIdx.x; e < G * D; e += kThreads) {
+        const int h = e / D, c = e - (e / D) * D;
+        const T* rows = q + ((size_t)seg * G + h) * W * D + c;
+        float acc = 0.0f;
+        for (int i = 0; i < W; ++i) acc += (float)rows[(size_t)i * D];
+        qbar[(size_t)seg * G * D + e] = acc * inv;
+    }
+}
+
+// One workgroup per (segment, range of pages).  NH: heads per KV head padded
+// to 4 or 8 (the padded heads have a zero mean query and add nothing).
+template <typename T, int D, int NH>
+__global__ __launch_bounds__(kThreads) void quest_pages(const T* __restrict__ k, const float* __restrict__ qbar,
+                                                        int N, int W, int G, int page, int n_pages, int nranges,
+                                                        int range_pages, float* __restrict__ score) {
+    using VP = VPiece<T>;
+    constexpr int CW = VP::CW;        // channels per lane
+    constexpr int CPL = D / CW;       // lanes per key row
+    constexpr int PPW = kWave / CPL;  // pages per wave step
+    static_assert(NH == 4 || NH == 8, "4 or 8 padded heads");
+
+    const int seg = blockIdx.x / nranges;
+    const int rg = blockIdx.x - seg * nranges;
+    const int lane = threadIdx.x & (kWave - 1);
+    const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+    const int grp = lane / CPL, cg = lane - (lane / CPL) * CPL;
+    const int P = N - W;
+    float* srow = score + (size_t)seg * N;
+
+    if (rg == 0)
+        for (int e = threadIdx.x; e < W; e += kThreads) srow[P + e] = INFINITY;
+
+    // this lane's channels of every head's mean query
+    float qv[NH][CW];
+#pragma unroll
+    for (int h = 0; h < NH; ++h)
+#pragma unroll
+        for (int c = 0; c < CW; ++c) qv[h][c] = h < G ? qbar[((size_t)seg * G + h) * D + cg * CW + c] : 0.0f;
+
+    const T* ks = k + (size_t)seg * N * D + cg * CW;
+    const int p0 = rg * range_pages, p1 = min(n_pages, p0 + range_pages);
+    for (int base = p0 + wv * PPW; base < p1; base += kWaves * PPW) {
+        const int pg = min(base + grp, p1 - 1);  // groups past the range redo the last page, unwritten
+        const int t0 = pg * page, t1 = min(t0 + page, P);
+        float kmin[CW], kmax[CW];
+#pragma unroll
+        for (int c = 0; c < CW; ++c) {
+            kmin[c] = INFINITY;
+            kmax[c] = -INFINITY;
+        }
+        // rows past a ragged last page repeat its last row: extremes unchanged
+        const T* pbase = ks + (size_t)t0 * D;
+        const int last = t1 - t0 - 1;
+        for (int r0 = 0; r0 < page; r0 += kRowBatch) {
+            // every load of the batch in flight before the first is used;
+            // non-temporal: each key row is read once
+            u32x4 raw[kRowBatch];
+#pragma unroll
+            for (int i = 0; i < kRowBatch; ++i)
+                raw[i] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(pbase + (size_t)min(r0 + i, last) * D));
+#pragma unroll
+            for (int i = 0; i < kRowBatch; i += 2) {
+                float fa[CW], fb[CW];
+                VP::to_f(raw[i], fa);
+                VP::to_f(raw[i + 1], fb);
+#pragma unroll
+                for (int c = 0; c < CW; ++c) {  // three-input minimum and maximum: two rows per step
+                    kmin[c] = fminf(fminf(kmin[c], fa[c]), fb[c]);
+                    kmax[c] = fmaxf(fmaxf(kmax[c], fa[c]), fb[c]);
+                }
+            }
+        }
+        float s = 0.0f;
+#pragma unroll
+        for (int h = 0; h < NH; ++h)
+#pragma unroll
+            for (int c = 0; c < CW; ++c) s += fmaxf(qv[h][c] * kmin[c], qv[h][c] * kmax[c]);
+#pragma unroll
+        for (int m = 1; m < CPL; m <<= 1) s += __shfl_xor(s, m);
+        if (base + grp < p1)
+            for (int e = cg; e < t1 - t0; e += CPL) srow[t0 + e] = s;
+    }
+}
+
+template <typename T, int D, int NH>
+hipError_t run_quest(const void* q, const void* k, int L, int B, int Hq, int Hkv, int N, int W, int page,
+                     float* score, void* ws, hipStream_t st) {
+    const QuestPlan p = quest_plan(L, B, Hq, Hkv, N, W, D, (int)sizeof(T), page);
+    float* qbar = static_cast<float*>(ws);
+    hipLaunchKernelGGL((quest_qmean<T>), dim3((unsigned)p.segs), dim3(kThreads), 0, st, static_cast<const T*>(q), W,
+                       p.G, D, qbar);
+    hipLaunchKernelGGL((quest_pages<T, D, NH>), dim3((unsigned)((size_t)p.segs * p.nranges)), dim3(kThreads), 0, st,
+                       static_cast<const T*>(k), qbar, N, W, p.G, page, p.n_pages, p.nranges, p.range_pages, score);
+    return hipGetLastError();
+}
+
+template <typename T, int D>
+hipError_t run_quest_g(const void* q, const void* k, int L, int B, int Hq, int Hkv, int N, int W, int page,
+                       float* score, void* ws, hipStream_t st) {
+    if (Hq / Hkv <= 4) return run_quest<T, D, 4>(q, k, L, B, Hq, Hkv, N, W, page, score, ws, st);
+    return run_quest<T, D, 8>(q, k, L, B, Hq, Hkv, N, W, page, score, ws, st);
+}
+
+}  // namespace
+
+hipError_t launch_quest(const void* q, const void* k, int dtype, int L, int B, int Hq, int Hkv, int N, int W,
+                        int d, int page, float* score, void* ws, hipStream_t st) {
+    if (dtype == 0) {
+        if (d == 128) return run_quest_g<__bf16, 128>(q, k, L, B, Hq, Hkv, N, W, page, score, ws, st);
+        return run_quest_g<__bf16, 64>(q, k, L, B, Hq, Hkv, N, W, page, score, ws, st);
+    }
+    if (d == 128) return run_quest_g<float, 128>(q, k, L, B, Hq, Hkv, N, W, page, score, ws, st);
+    return run_quest_g<float, 64>(q, k, L, B, Hq, Hkv, N, W, page, score, ws, st);
+}
+
+}  // namespace kve

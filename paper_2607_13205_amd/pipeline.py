@@ -1,6 +1,7 @@
 """The whole eviction step (one pass of the hot path) over resident tensors.
 
-score (SnapKV windowed + pooled, or H2O)  ->  role allocation (host)  ->
+score (SnapKV windowed + pooled, H2O, or the one-shot Quest page bound)  ->
+role allocation (host)  ->
 per-role top-k  ->  K/V compaction.  Buffers are allocated once by
 ``EvictBuffers`` so that repeated steps allocate nothing.
 
@@ -88,6 +89,8 @@ def alloc_buffers(k, n_q_heads: int, W: int, R: int, k_cap: int, scorer: str = "
     dev = k.device
     if scorer == "snapkv":
         wsb = kb.snapkv_workspace_size(L, B, n_q_heads, Hkv, N, W, d)
+    elif scorer == "quest":
+        wsb = kb.quest_workspace_size(L, B, n_q_heads, Hkv, d)
     else:
         wsb = kb.h2o_workspace_size(L, B, n_q_heads, Hkv, N, d)
     return EvictBuffers(
@@ -105,11 +108,12 @@ def alloc_buffers(k, n_q_heads: int, W: int, R: int, k_cap: int, scorer: str = "
 
 def evict(q, k, v, roles_host: np.ndarray, roles_dev, policy, budget: float, W: int,
           pool_k: int, bufs: EvictBuffers, scorer: str = "snapkv", scale: float = 0.0,
-          score_events=None):
+          score_events=None, page: int = 16):
     """One eviction step; returns (quota [B, R] host, kept [B] host).
 
-    q is the window queries [L, B, Hq, W, d] (SnapKV) or all queries
-    [L, B, Hq, N, d] (H2O, which uses W = 0 and no pool).  roles_host /
+    q is the window queries [L, B, Hq, W, d] (SnapKV; Quest, which scores
+    pages of ``page`` tokens and ignores pool_k) or all queries [L, B, Hq, N, d]
+    (H2O, which uses W = 0 and no pool).  roles_host /
     roles_dev are the bucket labels [B, N] of ``policy`` (a Policy, or the
     weights of the role-conditional policy).  ``score_events``, a pair of
     torch.cuda.Event, brackets the score call on the launch stream."""
@@ -120,6 +124,8 @@ def evict(q, k, v, roles_host: np.ndarray, roles_dev, policy, budget: float, W: 
         score_events[0].record()
     if scorer == "snapkv":
         kb.snapkv_score(q, k, pool_k, scale, score=bufs.score, workspace=bufs.ws_score)
+    elif scorer == "quest":
+        kb.quest_score(q, k, page, score=bufs.score, workspace=bufs.ws_score)
     else:
         kb.h2o_score(q, k, scale, score=bufs.score, workspace=bufs.ws_score)
     if score_events is not None:

@@ -29,7 +29,7 @@ def _declared():
 
 def test_every_declared_symbol_is_exported(kve):
     names = _declared()
-    assert len(names) == 14
+    assert len(names) == 16
     assert sorted(kve.EXPORTED) == names
     lib = ctypes.CDLL(kve.binding._LIB_PATH)
     for n in names:
@@ -154,8 +154,14 @@ def test_device_entry_points_validate_before_launch(kve):
     # compact: v without v_out, bad head_dim
     assert L.kve_kv_compact(dummy, dummy, 0, dummy, dummy, 1, 1, 2, 64, 128, 10, dummy, null, null) == 1
     assert L.kve_kv_compact(dummy, null, 0, dummy, dummy, 1, 1, 2, 64, 80, 10, dummy, null, null) == 2
-    # decode: G > 8, null count, short workspace, negative scale, k_cap 0, misaligned workspace
     big = 1 << 30
+    # quest: page 0, page too large, W > N, G > 8, short workspace
+    assert L.kve_quest_score(dummy, dummy, 0, 1, 1, 8, 2, 64, 8, 128, 0, dummy, dummy, big, null) == 1
+    assert L.kve_quest_score(dummy, dummy, 0, 1, 1, 8, 2, 64, 8, 128, 2000, dummy, dummy, big, null) == 1
+    assert L.kve_quest_score(dummy, dummy, 0, 1, 1, 8, 2, 64, 65, 128, 16, dummy, dummy, big, null) == 1
+    assert L.kve_quest_score(dummy, dummy, 0, 1, 1, 18, 2, 64, 8, 128, 16, dummy, dummy, big, null) == 2
+    assert L.kve_quest_score(dummy, dummy, 0, 1, 1, 8, 2, 64, 8, 128, 16, dummy, dummy, 8, null) == 3
+    # decode: G > 8, null count, short workspace, negative scale, k_cap 0, misaligned workspace
     assert L.kve_decode_attention(dummy, dummy, dummy, dummy, 0, 1, 1, 18, 2, 64, 128, 0.0, dummy, dummy, big, null) == 2
     assert L.kve_decode_attention(dummy, dummy, dummy, null, 0, 1, 1, 8, 2, 64, 128, 0.0, dummy, dummy, big, null) == 1
     assert L.kve_decode_attention(dummy, dummy, dummy, dummy, 0, 1, 1, 8, 2, 64, 128, 0.0, dummy, dummy, 8, null) == 3
@@ -179,3 +185,4 @@ def test_workspace_sizes_are_aligned_and_monotone(kve):
     w = kve.decode_workspace_size(32, 4, 32, 8, 1640, 128)
     assert w % 256 == 0 and w >= 1024 * 32 * (128 + 2) * 4 // 8
     assert kve.decode_workspace_size(1, 1, 32, 8, 0, 128) == 0
+    assert kve.quest_workspace_size(2, 1, 32, 8, 128) == 2 * 32 * 128 * 4

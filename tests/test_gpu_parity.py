@@ -223,6 +223,17 @@ def test_kv_compact_bit_exact(K, dtype, d):
                 assert not kob[s][m].any() and not vob[s][m].any()
 
 
+def check_quest_or_scores(gpu, ref, W, what):
+    """Scores of any scorer; the Quest window entries are +inf on both sides."""
+    N = len(ref)
+    if np.isinf(ref[N - W:]).all() and W > 0:
+        assert np.isinf(gpu[N - W:]).all() and (gpu[N - W:] > 0).all(), f"{what}: window not +inf"
+        if N - W > 0:
+            check_scores(gpu[:N - W], ref[:N - W], what)
+        return
+    check_scores(gpu, ref, what)
+
+
 def _pipeline_check(K, wl, inp, budget, policy, segs=None):
     """Run the whole step on the GPU and check scores, kept sets and compacted
     rows of the given segments against the oracle.  ``policy`` is a Policy or
@@ -253,10 +264,12 @@ def _pipeline_check(K, wl, inp, budget, policy, segs=None):
         kseg = f64(inp["k"][l, b, j])
         if wl.scorer == "h2o":
             s_ref = O.h2o_mass(f64(inp["q"][l, b, j * wl.G:(j + 1) * wl.G]), kseg, row_block=1024)
+        elif wl.scorer == "quest":
+            s_ref = O.quest_mass(f64(inp["q"][l, b, j * wl.G:(j + 1) * wl.G]), kseg, 16)
         else:
             s_ref = O.maxpool_prefix(O.snapkv_mass(f64(inp["q"][l, b, j * wl.G:(j + 1) * wl.G]), kseg),
                                      W, pool)
-        check_scores(f64(bufs.score[l, b, j]), s_ref, f"{wl.name} seg {(l, b, j)}")
+        check_quest_or_scores(f64(bufs.score[l, b, j]), s_ref, W, f"{wl.name} seg {(l, b, j)}")
         roles = ob[b]
         idx_ref = O.select_keep(s_ref, roles, qo[b], W)
         if policy.bucket_of is not None and policy.alpha == (1.0, 0.0) and sum(policy.bucket_of) == 1:
@@ -514,3 +527,70 @@ def test_decode_after_eviction_layer8k(K):
     wl = WL.get_workload("layer8k")
     inp = WL.make_inputs(wl, device="cuda")
     _decode_after_eviction(K, wl, inp, 0.1, list(np.ndindex(len(inp["layers"]), wl.B, wl.Hkv)))
+
+
+# ---------------------------------------------------------------------------
+# One-shot Quest analogue
+# ---------------------------------------------------------------------------
+
+QUEST_CASES = [
+    # name, L, B, Hq, Hkv, N, W, d, dtype, page
+    ("q16", 2, 2, 8, 2, 1000, 24, 128, "bf16", 16),
+    ("g1", 1, 1, 4, 4, 300, 8, 128, "bf16", 16),
+    ("g8", 1, 1, 16, 2, 513, 20, 128, "bf16", 16),
+    ("g3d64", 1, 2, 6, 2, 700, 16, 64, "bf16", 16),
+    ("page1", 1, 1, 8, 2, 200, 8, 128, "bf16", 1),
+    ("page37", 1, 1, 8, 2, 900, 8, 128, "bf16", 37),
+    ("wfull", 1, 1, 4, 1, 64, 64, 128, "bf16", 16),
+    ("f32", 1, 2, 8, 2, 333, 16, 128, "f32", 16),
+    ("f32d64", 1, 1, 8, 1, 500, 9, 64, "f32", 8),
+    ("long", 2, 1, 8, 2, 20000, 32, 128, "bf16", 16),
+]
+
+
+@pytest.mark.parametrize("case", QUEST_CASES, ids=lambda c: c[0])
+def test_quest_score_matches_oracle(K, case):
+    name, L, B, Hq, Hkv, N, W, d, dt, page = case
+    note(f"quest {name}")
+    wl = custom(name, L, B, Hq, Hkv, N, W, d, 1, dt, scorer="quest")
+    inp = WL.make_inputs(wl, device="cuda", with_v=False)
+    ws = torch.full((K.quest_workspace_size(L, B, Hq, Hkv, d),), 0xFF, dtype=torch.uint8, device="cuda")
+    sc = torch.full((L, B, Hkv, N), float("nan"), device="cuda")
+    K.quest_score(inp["q"], inp["k"], page, score=sc, workspace=ws)
+    torch.cuda.synchronize()
+    ref = O.quest_score(f64(inp["q"]), f64(inp["k"]), Hkv, page)
+    got = sc.cpu().numpy().astype(np.float64)
+    for idx in np.ndindex(L, B, Hkv):
+        check_quest_or_scores(got[idx], ref[idx], W, f"quest {name} seg {idx}")
+        # every token of a page carries the same bits
+        P = N - W
+        for p0 in range(0, P, page):
+            assert np.all(got[idx][p0:min(p0 + page, P)] == got[idx][p0])
+
+
+@pytest.mark.parametrize("budget,pol", [(0.1, "role"), (0.3, "role"), (0.1, "neutral")])
+def test_pipeline_quest(K, budget, pol):
+    wl = custom("quest_pipe", 2, 2, 8, 2, 3000, 32, 128, 1, "bf16", scorer="quest")
+    note(f"pipeline quest B={budget} {pol}")
+    inp = WL.make_inputs(wl, device="cuda")
+    if pol == "neutral":
+        from paper_2607_13205_amd.pipeline import Policy
+        roles1 = np.zeros_like(inp["roles"])
+        inp = dict(inp, roles=roles1, roles_t=torch.from_numpy(roles1).cuda())
+        policy = Policy(1, (1.0,))
+    else:
+        policy = WL.default_alpha(0.0)
+    _pipeline_check(K, wl, inp, budget, policy)
+
+
+def test_quest_full_size_one_layer(K):
+    """stack32k's shape (one layer of the 32): the launch configuration of a
+    whole-stack call at a quarter of the depth is the same per segment."""
+    wl = WL.get_workload("stack32k")
+    note("quest stack32k layer 5")
+    inp = WL.make_inputs(wl, device="cuda", layers=[5], with_v=False)
+    sc = K.quest_score(inp["q"], inp["k"], 16)
+    torch.cuda.synchronize()
+    for (b, j) in [(0, 0), (3, 7)]:
+        ref = O.quest_mass(f64(inp["q"][0, b, j * wl.G:(j + 1) * wl.G]), f64(inp["k"][0, b, j]), 16)
+        check_quest_or_scores(sc[0, b, j].cpu().numpy().astype(np.float64), ref, wl.W, f"quest stack32k {(b, j)}")

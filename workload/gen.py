@@ -67,7 +67,7 @@ class Workload:
     mix: tuple                      # target fractions (SINK, KEY, VALUE, OTHER)
     budgets: tuple
     pattern: str = "json"           # "json" or "table"
-    scorer: str = "snapkv"          # "snapkv" or "h2o"
+    scorer: str = "snapkv"          # "snapkv", "h2o" or "quest" (window queries, as snapkv)
     sink_c: float = 1.6             # sink-bias multiplier c
     burst_frac: float = 0.0
     q_mean: float = 3.0             # norm of the query offset shared by a KV group
