@@ -47,7 +47,13 @@ that uses it):
       window query, summed over the G heads of the group (as R2 sums their
       mass); every token carries its page's bound, window tokens +inf, and the
       same per-bucket top-k then keeps whole pages in bound order (the lower
-      index first on ties), the last one cut at the budget.
+      index first on ties), the last one cut at the budget;
+  R21 the linear role probe (§6 "Deployment: a linear role probe") scores
+      role r of token t as b[r] + sum over offsets o = -2..2 of
+      W[o + 2, id(t + o), r], skipping positions outside the sequence and ids
+      outside the vocabulary; the sum is taken in float32 in offset order
+      (b first), the precision the probe is stored in, and the label is the
+      argmax, the lowest role on ties.
 """
 
 from __future__ import annotations
@@ -81,6 +87,9 @@ __all__ = [
     "select_keep",
     "topk_select",
     "kv_compact",
+    "PROBE_OFFSETS",
+    "probe_logits",
+    "probe_roles",
     "decode_attention",
     "masked_decode_attention",
     "decode_attention_batch",
@@ -466,6 +475,45 @@ def kv_compact(kv: np.ndarray, idx: np.ndarray) -> np.ndarray:
     """Compacted rows kv[idx] of one (layer, batch, KV head): a pure copy,
     the dense cache a compacting implementation keeps (§6, systems cost)."""
     return np.asarray(kv)[np.asarray(idx)]
+
+
+# ---------------------------------------------------------------------------
+# Linear role probe (§6 "Deployment: a linear role probe"): role labels from a
+# multinomial logistic regression over the token ids at t-2 .. t+2
+# ---------------------------------------------------------------------------
+
+PROBE_OFFSETS = (-2, -1, 0, 1, 2)
+
+
+def probe_logits(ids: np.ndarray, weight: np.ndarray, bias: np.ndarray) -> np.ndarray:
+    """Float32 logits [n, R] of one sequence of token ids (R21): weight
+    [5, V, R] holds one table per offset of PROBE_OFFSETS, bias [R].  Each
+    logit is accumulated in float32, bias first, then the offsets in order."""
+    ids = np.asarray(ids, dtype=np.int64)
+    weight = np.asarray(weight, dtype=np.float32)
+    bias = np.asarray(bias, dtype=np.float32)
+    n = ids.shape[0]
+    V, R = weight.shape[1], weight.shape[2]
+    out = np.empty((n, R), dtype=np.float32)
+    for t in range(n):
+        acc = bias.copy()
+        for j, o in enumerate(PROBE_OFFSETS):
+            p = t + o
+            if 0 <= p < n and 0 <= ids[p] < V:
+                acc = (acc + weight[j, ids[p]]).astype(np.float32)
+        out[t] = acc
+    return out
+
+
+def probe_roles(ids: np.ndarray, weight: np.ndarray, bias: np.ndarray) -> np.ndarray:
+    """Role label of every token of ids [B, N] (or [N]): the argmax of its
+    float32 logits, the lowest role on ties.  int8, same shape as ids."""
+    ids = np.asarray(ids)
+    flat = ids.reshape(-1, ids.shape[-1])
+    out = np.empty(flat.shape, dtype=np.int8)
+    for b in range(flat.shape[0]):
+        out[b] = np.argmax(probe_logits(flat[b], weight, bias), axis=1)   # first maximum
+    return out.reshape(ids.shape)
 
 
 # ---------------------------------------------------------------------------
