@@ -17,7 +17,8 @@ same workload under fair eviction and the No-KEY counterfactual, which reuse
 every kernel with other quotas; ``decode`` times one decode query per head over
 the compacted cache of every layer against the same kernel over the full
 cache; ``quest`` times the one-shot Quest page-bound scorer on the same
-inputs, alone and as the score of the whole step.
+inputs, alone and as the score of the whole step; ``probe`` times the linear
+role probe labelling the batch's tokens (random weights of the paper's size).
 
 ``roofline.traffic`` is the measured HBM traffic of one score call, read from
 the counter summary in profiles/ (rocprofv3 FETCH_SIZE and WRITE_SIZE,
@@ -63,6 +64,7 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-h2o", action="store_true", help="skip the H2O scorer leg")
     ap.add_argument("--no-quest", action="store_true", help="skip the Quest scorer timings")
+    ap.add_argument("--no-probe", action="store_true", help="skip the role-probe timing")
     ap.add_argument("--no-decode", action="store_true",
                     help="skip the decode timings over the compacted and the full cache")
     ap.add_argument("--no-policies", action="store_true",
@@ -304,6 +306,22 @@ def quest_leg(K, pipeline, wl, inp, budget, alpha, steps):
             "tokens_per_s": round(B * N / (ms_step * 1e-3), 1)}
 
 
+def probe_leg(K, wl, steps):
+    """The linear role probe over the batch's B x N token ids: 5 tables of a
+    128256-id vocabulary x 6 roles (3.85 M float32 parameters, random)."""
+    import torch
+    V, R = 128256, 6
+    g = torch.Generator(device="cuda")
+    g.manual_seed(77)
+    weight = 0.1 * torch.randn((5, V, R), generator=g, device="cuda")
+    bias = 0.1 * torch.randn((R,), generator=g, device="cuda")
+    ids = torch.randint(0, V, (wl.B, wl.N), generator=g, device="cuda", dtype=torch.int32)
+    out = torch.empty((wl.B, wl.N), dtype=torch.int8, device="cuda")
+    ms = _time_calls(lambda: K.role_probe(ids, weight, bias, out=out), steps)
+    return {"kernel": "kve_role_probe", "tokens": wl.B * wl.N, "us": round(ms * 1000, 2),
+            "tokens_per_s": round(wl.B * wl.N / (ms * 1e-3), 1)}
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -400,6 +418,8 @@ def main():
     if not args.no_quest and scorer == "snapkv":
         print("[bench] Quest scorer", file=sys.stderr, flush=True)
         out["quest"] = quest_leg(K, pipeline, wl, inp, budget, alpha, max(3, args.steps // 2))
+    if not args.no_probe:
+        out["probe"] = probe_leg(K, wl, max(3, args.steps // 2))
     if not args.no_policies:
         print("[bench] fair-eviction and No-KEY steps", file=sys.stderr, flush=True)
         out["policies"] = policy_leg(WL, pipeline, wl, inp, budget, W, pool, max(3, args.steps // 2))

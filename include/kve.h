@@ -240,6 +240,30 @@ kve_status_t kve_role_allocate_fair(const int8_t* roles, int B, int N, int R,
 kve_status_t kve_role_map(const int8_t* roles, size_t n, const int8_t* map, int R_in,
                           int8_t* out);
 
+/*
+ * Linear role probe (§6 "Deployment: a linear role probe"): the role label of
+ * every token from a multinomial logistic regression over the token ids at
+ * t-2 .. t+2, in place of a structural parser.  For token t of sequence b the
+ * score of role r is
+ *   bias[r] + sum over o = 0..4 of weight[o, ids[b, t + o - 2], r],
+ * summed in float32 in that order (bias first), skipping positions outside
+ * [0, N) and ids outside [0, V); the label is the argmax, the lowest role on
+ * ties.  Labels are in the probe's own role order; kve_role_map turns them
+ * into the allocation's buckets.
+ *
+ *   ids       [B, N] int32 token ids (device)
+ *   weight    [5, V, R] float32 (device): one table per offset t-2 .. t+2
+ *   bias      [R] float32 (device)
+ *   R         roles, 1 .. 8
+ *   roles_out [B, N] int8 (device)
+ *
+ * Enqueued on `stream`.  Errors: KVE_ERR_INVALID_ARG (null pointers,
+ * non-positive sizes, R outside [1, 8]), KVE_ERR_UNSUPPORTED (too many
+ * tokens), KVE_ERR_HIP.
+ */
+kve_status_t kve_role_probe(const int32_t* ids, int B, int N, const float* weight,
+                            const float* bias, int V, int R, int8_t* roles_out, void* stream);
+
 /* ------------------------------------------------------------------------- */
 /* Per-role top-k selection (Algorithm 1, per-bucket top-k).                  */
 /* ------------------------------------------------------------------------- */

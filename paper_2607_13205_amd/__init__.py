@@ -8,6 +8,7 @@ The hot path runs in libkve.so (HIP); this package is its thin Python binding:
   role_allocate  per-bucket quotas with redistribution (host)
   role_allocate_fair  equal retention rate per bucket (host)
   role_map       relabel roles into buckets, e.g. the No-X counterfactual (host)
+  role_probe     role labels from the linear probe over token ids (device)
   topk_select    per-role top-k with the window kept, ascending indices
   kv_compact     dense K/V cache of the kept rows
   decode_attention  one decode query per head over the compacted cache
@@ -17,10 +18,10 @@ The hot path runs in libkve.so (HIP); this package is its thin Python binding:
 from .binding import (EXPORTED, KveError, decode_attention, decode_workspace_size,  # noqa: F401
                       h2o_score, h2o_workspace_size, kv_compact, last_error, quest_score,
                       quest_workspace_size, role_allocate,
-                      role_allocate_fair, role_map, snapkv_score, snapkv_workspace_size, topk_select)
+                      role_allocate_fair, role_map, role_probe, snapkv_score, snapkv_workspace_size, topk_select)
 from . import pipeline  # noqa: F401
 
 __all__ = ["snapkv_score", "h2o_score", "role_allocate", "role_allocate_fair", "role_map",
            "topk_select", "kv_compact", "snapkv_workspace_size", "h2o_workspace_size", "KveError",
            "last_error", "pipeline", "decode_attention", "decode_workspace_size", "quest_score",
-           "quest_workspace_size"]
+           "quest_workspace_size", "role_probe"]

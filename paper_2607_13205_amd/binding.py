@@ -31,7 +31,7 @@ EXPORTED = (
     "kve_version", "kve_last_error",
     "kve_snapkv_workspace_size", "kve_snapkv_score",
     "kve_h2o_workspace_size", "kve_h2o_score",
-    "kve_role_allocate", "kve_role_allocate_fair", "kve_role_map",
+    "kve_role_allocate", "kve_role_allocate_fair", "kve_role_map", "kve_role_probe",
     "kve_topk_workspace_size", "kve_topk_select",
     "kve_kv_compact",
     "kve_decode_workspace_size", "kve_decode_attention",
@@ -67,6 +67,7 @@ def _load():
         "kve_role_allocate_fair": (c_int, [c_void, c_int, c_int, c_int, c_double, c_int,
                                            c_void, c_void, c_void]),
         "kve_role_map": (c_int, [c_void, c_size, c_void, c_int, c_void]),
+        "kve_role_probe": (c_int, [c_void, c_int, c_int, c_void, c_void, c_int, c_int, c_void, c_void]),
         "kve_topk_workspace_size": (c_size, [c_int] * 5),
         "kve_topk_select": (c_int, [c_void, c_void, c_void] + [c_int] * 7 +
                             [c_void, c_void, c_void, c_size, c_void]),
@@ -327,4 +328,23 @@ def decode_attention(q, k_c, v_c, count, scale: float = 0.0, out=None, workspace
     _check(LIB.kve_decode_attention(_dev(q, "q"), _dev(k_c, "k_c"), _dev(v_c, "v_c"), _dev(count, "count"),
                                     _dtype_code(k_c), L, B, Hq, Hkv, k_cap, d, float(scale),
                                     _dev(out, "out"), _ptr(ws), wsb, _stream(stream)))
+    return out
+
+
+def role_probe(ids, weight, bias, out=None, stream=None):
+    """Probe role labels int8 [B, N] from token ids int32 [B, N], weight
+    float32 [5, V, R] and bias float32 [R] (all device tensors)."""
+    torch = _torch()
+    if ids.dim() != 2 or ids.dtype != torch.int32:
+        raise ValueError("ids must be int32 [B, N]")
+    if weight.dim() != 3 or weight.shape[0] != 5 or weight.dtype != torch.float32:
+        raise ValueError("weight must be float32 [5, V, R]")
+    B, N = ids.shape
+    V, R = weight.shape[1], weight.shape[2]
+    if tuple(bias.shape) != (R,) or bias.dtype != torch.float32:
+        raise ValueError("bias must be float32 [R]")
+    if out is None:
+        out = torch.empty((B, N), dtype=torch.int8, device=ids.device)
+    _check(LIB.kve_role_probe(_dev(ids, "ids"), B, N, _dev(weight, "weight"), _dev(bias, "bias"), V, R,
+                              _dev(out, "out"), _stream(stream)))
     return out

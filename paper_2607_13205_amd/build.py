@@ -22,7 +22,7 @@ BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libkve.so")
 ARCH = "gfx950"
 
-SOURCES = ["kve_api.cpp", "snapkv.hip", "h2o.hip", "topk.hip", "decode.hip", "quest.hip"]
+SOURCES = ["kve_api.cpp", "snapkv.hip", "h2o.hip", "topk.hip", "decode.hip", "quest.hip", "probe.hip"]
 
 COMMON = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}",
           "-I", os.path.join(ROOT, "include"), "-I", CSRC,

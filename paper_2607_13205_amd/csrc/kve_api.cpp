@@ -344,6 +344,18 @@ kve_status_t kve_decode_attention(const void* q, const void* k_c, const void* v_
                     fn);
 }
 
+kve_status_t kve_role_probe(const int32_t* ids, int B, int N, const float* weight, const float* bias, int V,
+                            int R, int8_t* roles_out, void* stream) {
+    const char* fn = "kve_role_probe";
+    if (ids == nullptr || weight == nullptr || bias == nullptr || roles_out == nullptr)
+        return fail(KVE_ERR_INVALID_ARG, "%s: null pointer", fn);
+    if (B <= 0 || N <= 0 || V <= 0) return fail(KVE_ERR_INVALID_ARG, "%s: B, N and V must be positive", fn);
+    if (R < 1 || R > 8) return fail(KVE_ERR_INVALID_ARG, "%s: R=%d outside [1, 8]", fn, R);
+    if ((long long)B * N > (long long)kMaxGrid * 256) return fail(KVE_ERR_UNSUPPORTED, "%s: shape too large", fn);
+    return from_hip(kve::launch_probe(ids, B, N, weight, bias, V, R, roles_out, static_cast<hipStream_t>(stream)),
+                    fn);
+}
+
 size_t kve_topk_workspace_size(int L, int B, int Hkv, int N, int R) {
     (void)L;
     (void)B;

@@ -110,6 +110,9 @@ hipError_t launch_decode(const void* q, const void* kc, const void* vc, const in
 hipError_t launch_quest(const void* q, const void* k, int dtype, int L, int B, int Hq, int Hkv, int N, int W,
                         int d, int page, float* score, void* ws, hipStream_t st);
 
+hipError_t launch_probe(const int32_t* ids, int B, int N, const float* weight, const float* bias, int V, int R,
+                        int8_t* out, hipStream_t st);
+
 hipError_t launch_compact(const void* k, const void* v, int elem_bytes, const int32_t* idx,
                           const int32_t* count, int L, int B, int Hkv, int N, int d, int k_cap,
                           void* k_out, void* v_out, hipStream_t st);

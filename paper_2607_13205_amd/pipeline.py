@@ -63,6 +63,21 @@ class Policy:
         return kb.role_allocate(buckets_host, self.R, self.alpha, budget, W)
 
 
+# The probe's roles (§6: KEY, VALUE, DELIM, HEADER, PROSE, WS) in the
+# allocation's four buckets (SINK 0, KEY 1, VALUE 2, OTHER 3): delimiters and
+# whitespace are the sink bucket, headers join the keys, prose is OTHER.
+PROBE_TO_BUCKET = (1, 2, 0, 1, 3, 0)
+
+
+def probe_buckets(ids, weight, bias, bucket_of=PROBE_TO_BUCKET):
+    """Bucket labels from the linear role probe on the device: returns (host
+    int8 [B, N], device int8 [B, N]).  The host copy feeds the allocation."""
+    labels = kb.role_probe(ids, weight, bias)
+    buckets = kb.role_map(labels.cpu().numpy(), bucket_of)
+    import torch
+    return buckets, torch.from_numpy(buckets).to(ids.device)
+
+
 def as_policy(policy) -> Policy:
     """A Policy, or a plain weight sequence read as the role-conditional policy."""
     return policy if isinstance(policy, Policy) else Policy.role(policy)

@@ -29,7 +29,7 @@ def _declared():
 
 def test_every_declared_symbol_is_exported(kve):
     names = _declared()
-    assert len(names) == 16
+    assert len(names) == 17
     assert sorted(kve.EXPORTED) == names
     lib = ctypes.CDLL(kve.binding._LIB_PATH)
     for n in names:
@@ -155,6 +155,10 @@ def test_device_entry_points_validate_before_launch(kve):
     assert L.kve_kv_compact(dummy, dummy, 0, dummy, dummy, 1, 1, 2, 64, 128, 10, dummy, null, null) == 1
     assert L.kve_kv_compact(dummy, null, 0, dummy, dummy, 1, 1, 2, 64, 80, 10, dummy, null, null) == 2
     big = 1 << 30
+    # probe: R out of range, null ids, empty batch
+    assert L.kve_role_probe(dummy, 1, 10, dummy, dummy, 100, 9, dummy, null) == 1
+    assert L.kve_role_probe(null, 1, 10, dummy, dummy, 100, 6, dummy, null) == 1
+    assert L.kve_role_probe(dummy, 0, 10, dummy, dummy, 100, 6, dummy, null) == 1
     # quest: page 0, page too large, W > N, G > 8, short workspace
     assert L.kve_quest_score(dummy, dummy, 0, 1, 1, 8, 2, 64, 8, 128, 0, dummy, dummy, big, null) == 1
     assert L.kve_quest_score(dummy, dummy, 0, 1, 1, 8, 2, 64, 8, 128, 2000, dummy, dummy, big, null) == 1

@@ -594,3 +594,60 @@ def test_quest_full_size_one_layer(K):
     for (b, j) in [(0, 0), (3, 7)]:
         ref = O.quest_mass(f64(inp["q"][0, b, j * wl.G:(j + 1) * wl.G]), f64(inp["k"][0, b, j]), 16)
         check_quest_or_scores(sc[0, b, j].cpu().numpy().astype(np.float64), ref, wl.W, f"quest stack32k {(b, j)}")
+
+
+# ---------------------------------------------------------------------------
+# Linear role probe
+# ---------------------------------------------------------------------------
+
+def _probe_tables(V, R, seed):
+    g = torch.Generator(device="cpu")
+    g.manual_seed(seed)
+    weight = (0.1 * torch.randn((5, V, R), generator=g)).float()
+    bias = (0.1 * torch.randn((R,), generator=g)).float()
+    return weight, bias
+
+
+@pytest.mark.parametrize("B,N,V,R", [(4, 3000, 128256, 6), (3, 1, 50, 6), (2, 2, 50, 3), (1, 5, 7, 8),
+                                     (2, 777, 1000, 1), (1, 4100, 32000, 5)])
+def test_role_probe_bit_exact(K, B, N, V, R):
+    """Labels are decided in float32 in the same order on both sides, so they
+    agree bit for bit; out-of-vocabulary ids add nothing."""
+    note(f"probe B={B} N={N} V={V} R={R}")
+    weight, bias = _probe_tables(V, R, 7 + N)
+    r = np.random.default_rng(N)
+    ids = r.integers(0, V, (B, N)).astype(np.int32)
+    ids[r.random((B, N)) < 0.02] = -5
+    ids[r.random((B, N)) < 0.02] = V + 3
+    out = K.role_probe(torch.from_numpy(ids).cuda(), weight.cuda(), bias.cuda())
+    torch.cuda.synchronize()
+    ref = O.probe_roles(ids, weight.numpy(), bias.numpy())
+    assert np.array_equal(out.cpu().numpy(), ref)
+
+
+def test_probe_drives_the_pipeline(K):
+    """Probe labels on the device, mapped to the four buckets, feed the
+    allocation and the selection like parser labels."""
+    from paper_2607_13205_amd import pipeline
+    wl = WL.get_workload("layer8k").with_(Hq=8, Hkv=2)
+    inp = WL.make_inputs(wl, device="cuda")
+    weight, bias = _probe_tables(32000, 6, 3)
+    ids = np.random.default_rng(5).integers(0, 32000, (wl.B, wl.N)).astype(np.int32)
+    buckets, buckets_t = pipeline.probe_buckets(torch.from_numpy(ids).cuda(), weight.cuda(), bias.cuda())
+    ref = O.role_map(O.probe_roles(ids, weight.numpy(), bias.numpy()), pipeline.PROBE_TO_BUCKET)
+    assert np.array_equal(buckets, ref)
+    inp = dict(inp, roles=buckets, roles_t=buckets_t)
+    _pipeline_check(K, wl, inp, 0.1, WL.default_alpha(0.02))
+
+
+def test_role_probe_full_size(K):
+    """stack32k's batch (4 x 32768 tokens) with a Llama-3-sized vocabulary;
+    the oracle recomputes the first and the last sequence."""
+    B, N, V, R = 4, 32768, 128256, 6
+    weight, bias = _probe_tables(V, R, 11)
+    ids = np.random.default_rng(9).integers(0, V, (B, N)).astype(np.int32)
+    out = K.role_probe(torch.from_numpy(ids).cuda(), weight.cuda(), bias.cuda())
+    torch.cuda.synchronize()
+    got = out.cpu().numpy()
+    for b in (0, B - 1):
+        assert np.array_equal(got[b], O.probe_roles(ids[b], weight.numpy(), bias.numpy()))
