@@ -65,6 +65,9 @@ def parse():
     ap.add_argument("--no-h2o", action="store_true", help="skip the H2O scorer leg")
     ap.add_argument("--no-quest", action="store_true", help="skip the Quest scorer timings")
     ap.add_argument("--no-probe", action="store_true", help="skip the role-probe timing")
+    ap.add_argument("--chunks", type=int, default=1,
+                    help="layer chunks of the step: each scored chunk's top-k and compaction run on a "
+                         "second stream while the next chunk is scored (1: no overlap)")
     ap.add_argument("--no-decode", action="store_true",
                     help="skip the decode timings over the compacted and the full cache")
     ap.add_argument("--no-policies", action="store_true",
@@ -353,9 +356,11 @@ def main():
     _, kept, k_cap = K.role_allocate(inp["roles"], 4, alpha, budget, W)
     bufs = pipeline.alloc_buffers(inp["k"], wl.Hq, W, 4, k_cap, scorer=scorer)
 
+    side = torch.cuda.Stream() if args.chunks > 1 else None
+
     def step():
         pipeline.evict(inp["q"], inp["k"], inp["v"], inp["roles"], inp["roles_t"], alpha, budget,
-                       W, pool, bufs, scorer=scorer)
+                       W, pool, bufs, scorer=scorer, chunks=args.chunks, side_stream=side)
 
     print(f"[bench] warmup {args.warmup}", file=sys.stderr, flush=True)
     for _ in range(args.warmup):
@@ -370,7 +375,8 @@ def main():
     t_all0.record()
     for i in range(args.steps):
         pipeline.evict(inp["q"], inp["k"], inp["v"], inp["roles"], inp["roles_t"], alpha, budget,
-                       W, pool, bufs, scorer=scorer, score_events=ev[i])
+                       W, pool, bufs, scorer=scorer, score_events=ev[i], chunks=args.chunks,
+                       side_stream=side)
     t_all1.record()
     torch.cuda.synchronize()
     ms_step = t_all0.elapsed_time(t_all1) / args.steps
@@ -399,7 +405,7 @@ def main():
                         f"alpha_KEY={args.alpha_key}, role mix {wl.mix}",
             "global_batch": wl.B, "seq_len": wl.N, "parallelism": "none (1 GPU)",
             "layer_tokens_per_s": round(value * wl.L, 1),
-            "k_cap": k_cap,
+            "k_cap": k_cap, "layer_chunks": args.chunks,
             "step_algorithmic_GBs": round(step_bytes / (ms_step * 1e-3) / 1e9, 1),
             "step_hbm_frac": round(step_bytes / (ms_step * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
         },

@@ -21,6 +21,8 @@
 // memory latency is paid once per group and not once per key; the loads are
 // unconditional (clamped to a valid position) so that none waits behind a
 // branch.
+#include <type_traits>
+
 #include "kve_device.h"
 #include "kve_internal.h"
 
@@ -105,29 +107,59 @@ __global__ __launch_bounds__(kThreads) void topk_kernel(const float* __restrict_
         if (!any) break;  // uniform: every thread reads the same LDS values
         for (int e = tid; e < R * kDigits; e += kThreads) (&sh.hist[0][0])[e] = 0u;
         __syncthreads();
-        for (int t00 = tid; t00 < P; t00 += kThreads * kBatch) {
-            int rv[kBatch];
-            float sv[kBatch];
+        // every bucket's state in registers; a key is counted when it matches
+        // its bucket's prefix, the bucket picked with selects (no branches)
+        bool act[R];
+        uint32_t pf[R];
+        int lov[R];
 #pragma unroll
-            for (int e = 0; e < kBatch; ++e) {  // unconditional loads (clamped index), then the bound
-                const int t = t00 + e * kThreads;
-                const int tc = min(t, P - 1);
-                const int r = ro[tc];
-                sv[e] = sc[tc];
-                rv[e] = t < P ? r : -1;
-            }
-#pragma unroll
-            for (int e = 0; e < kBatch; ++e) {
-                const int r = rv[e];
-                if (r < 0 || r >= R || sh.mode[r] != kModeSelect) continue;
-                const int lo = sh.lo[r];
-                if (lo == 0) continue;
-                const uint32_t key = score_key(sv[e]);
-                if (lo < 32 && (key >> lo) != sh.pref[r]) continue;
-                const int w = min(kDigitBits, lo);
-                atomicAdd(&sh.hist[r][(key >> (lo - w)) & ((1u << w) - 1u)], 1u);
-            }
+        for (int r = 0; r < R; ++r) {
+            act[r] = sh.mode[r] == kModeSelect && sh.lo[r] > 0;
+            pf[r] = sh.pref[r];
+            lov[r] = sh.lo[r];
         }
+        // the first pass counts every labelled candidate on its top digit (no
+        // prefix yet, every bucket still selecting); the later ones only the
+        // keys that match their bucket's prefix
+        auto count_keys = [&](auto first) {
+            for (int t00 = tid; t00 < P; t00 += kThreads * kBatch) {
+                int rv[kBatch];
+                float sv[kBatch];
+#pragma unroll
+                for (int e = 0; e < kBatch; ++e) {  // unconditional loads (clamped index), then the bound
+                    const int t = t00 + e * kThreads;
+                    const int tc = min(t, P - 1);
+                    const int r = ro[tc];
+                    sv[e] = sc[tc];
+                    rv[e] = t < P ? r : -1;
+                }
+#pragma unroll
+                for (int e = 0; e < kBatch; ++e) {
+                    const int r = rv[e];
+                    const uint32_t key = score_key(sv[e]);
+                    if constexpr (decltype(first)::value) {
+                        if ((unsigned)r < (unsigned)R) atomicAdd(&sh.hist[r][key >> (32 - kDigitBits)], 1u);
+                    } else {
+                        bool a = false;
+                        uint32_t p = 0u;
+                        int lo = 32;
+#pragma unroll
+                        for (int q = 0; q < R; ++q) {
+                            a = r == q ? act[q] : a;
+                            p = r == q ? pf[q] : p;
+                            lo = r == q ? lov[q] : lo;
+                        }
+                        a = a && (lo >= 32 || (key >> lo) == p);
+                        const int w = min(kDigitBits, lo);
+                        if (a) atomicAdd(&sh.hist[r][(key >> (lo - w)) & ((1u << w) - 1u)], 1u);
+                    }
+                }
+            }
+        };
+        if (pass == 0)
+            count_keys(std::true_type{});
+        else
+            count_keys(std::false_type{});
         __syncthreads();
         // Digit search, every thread at once: thread tid holds the kPerThread
         // bins from the top going down; a scan gives the count of keys in all
@@ -181,21 +213,21 @@ __global__ __launch_bounds__(kThreads) void topk_kernel(const float* __restrict_
     }
     const int run = (N + kWaves * kWave - 1) / (kWaves * kWave) * kWave;  // positions per wave, whole steps
     const int w0 = min(N, wave * run), w1 = min(N, w0 + run);
-    // class of position t: 1 kept, 2 + r equal to the threshold of bucket r, 0 dropped
+    // class of position t: 1 kept, 2 + r equal to the threshold of bucket r, 0
+    // dropped; the bucket's mode and threshold are picked with selects (a
+    // branch per bucket would cost every key a divergent branch)
     auto classify = [&](int t, int r, float x) {
-        if (t >= P) return 1;
-        int c = 0;
+        int m = kModeNone;
+        uint32_t thr = 0u;
 #pragma unroll
-        for (int q = 0; q < R; ++q)
-            if (r == q) {
-                if (mode[q] == kModeAll) {
-                    c = 1;
-                } else if (mode[q] == kModeSelect) {
-                    const uint32_t key = score_key(x);
-                    c = key > th[q] ? 1 : (key == th[q] ? 2 + q : 0);
-                }
-            }
-        return c;
+        for (int q = 0; q < R; ++q) {
+            m = r == q ? mode[q] : m;
+            thr = r == q ? th[q] : thr;
+        }
+        const uint32_t key = score_key(x);
+        const int sel = key > thr ? 1 : (key == thr ? 2 + r : 0);
+        const int c = m == kModeAll ? 1 : (m == kModeSelect ? sel : 0);
+        return t >= P ? 1 : c;
     };
     // visit(t, c) for every position of this wave's run, 64 consecutive per step
     auto sweep = [&](auto&& visit) {

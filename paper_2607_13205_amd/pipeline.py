@@ -121,30 +121,48 @@ def alloc_buffers(k, n_q_heads: int, W: int, R: int, k_cap: int, scorer: str = "
     )
 
 
+def _score(q, k, bufs, scorer, pool_k, scale, page, l0, l1, stream=None):
+    """Score layers [l0, l1) into bufs.score[l0:l1] on ``stream`` (None: current)."""
+    if scorer == "snapkv":
+        kb.snapkv_score(q[l0:l1], k[l0:l1], pool_k, scale, score=bufs.score[l0:l1],
+                        workspace=bufs.ws_score, stream=stream)
+    elif scorer == "quest":
+        kb.quest_score(q[l0:l1], k[l0:l1], page, score=bufs.score[l0:l1], workspace=bufs.ws_score,
+                       stream=stream)
+    else:
+        kb.h2o_score(q[l0:l1], k[l0:l1], scale, score=bufs.score[l0:l1], workspace=bufs.ws_score,
+                     stream=stream)
+
+
+def _select(k, v, roles_dev, bufs, W, R, l0, l1, stream=None):
+    """Top-k and compaction of layers [l0, l1) on ``stream`` (None: current)."""
+    kb.topk_select(bufs.score[l0:l1], roles_dev, bufs.quota_dev, W, R, bufs.k_cap,
+                   idx_out=bufs.idx[l0:l1], count_out=bufs.count[l0:l1], stream=stream)
+    kb.kv_compact(k[l0:l1], None if v is None else v[l0:l1], bufs.idx[l0:l1], bufs.count[l0:l1],
+                  k_out=bufs.k_out[l0:l1], v_out=None if bufs.v_out is None else bufs.v_out[l0:l1],
+                  stream=stream)
+
+
 def evict(q, k, v, roles_host: np.ndarray, roles_dev, policy, budget: float, W: int,
           pool_k: int, bufs: EvictBuffers, scorer: str = "snapkv", scale: float = 0.0,
-          score_events=None, page: int = 16):
+          score_events=None, page: int = 16, chunks: int = 1, side_stream=None):
     """One eviction step; returns (quota [B, R] host, kept [B] host).
 
     q is the window queries [L, B, Hq, W, d] (SnapKV; Quest, which scores
     pages of ``page`` tokens and ignores pool_k) or all queries [L, B, Hq, N, d]
-    (H2O, which uses W = 0 and no pool).  roles_host /
-    roles_dev are the bucket labels [B, N] of ``policy`` (a Policy, or the
-    weights of the role-conditional policy).  ``score_events``, a pair of
-    torch.cuda.Event, brackets the score call on the launch stream."""
+    (H2O, which uses W = 0 and no pool).  roles_host / roles_dev are the bucket
+    labels [B, N] of ``policy`` (a Policy, or the weights of the
+    role-conditional policy).  ``score_events``, a pair of torch.cuda.Event,
+    brackets the score calls on the launch stream.
+
+    The quotas depend on the labels only, so they are worked out first.  With
+    ``chunks`` > 1 and a ``side_stream``, the layers are scored in that many
+    chunks on the current stream while the top-k and compaction of each scored
+    chunk run on the side stream, overlapping the scoring of the next; the
+    current stream waits for the side stream before returning."""
     import torch
     policy = as_policy(policy)
     R = policy.R
-    if score_events is not None:
-        score_events[0].record()
-    if scorer == "snapkv":
-        kb.snapkv_score(q, k, pool_k, scale, score=bufs.score, workspace=bufs.ws_score)
-    elif scorer == "quest":
-        kb.quest_score(q, k, page, score=bufs.score, workspace=bufs.ws_score)
-    else:
-        kb.h2o_score(q, k, scale, score=bufs.score, workspace=bufs.ws_score)
-    if score_events is not None:
-        score_events[1].record()
     quota, kept, k_cap = policy.allocate(roles_host, budget, W)
     if k_cap > bufs.k_cap:
         raise ValueError(f"buffers hold {bufs.k_cap} rows, the allocation keeps {k_cap}")
@@ -154,7 +172,28 @@ def evict(q, k, v, roles_host: np.ndarray, roles_dev, policy, budget: float, W: 
     bufs.quota_host.numpy()[...] = quota
     bufs.quota_dev.copy_(bufs.quota_host, non_blocking=True)
     bufs.copy_done.record()
-    kb.topk_select(bufs.score, roles_dev, bufs.quota_dev, W, R, bufs.k_cap,
-                   idx_out=bufs.idx, count_out=bufs.count)
-    kb.kv_compact(k, v, bufs.idx, bufs.count, k_out=bufs.k_out, v_out=bufs.v_out)
+    L = k.shape[0]
+    if chunks <= 1 or side_stream is None:
+        if score_events is not None:
+            score_events[0].record()
+        _score(q, k, bufs, scorer, pool_k, scale, page, 0, L)
+        if score_events is not None:
+            score_events[1].record()
+        _select(k, v, roles_dev, bufs, W, R, 0, L)
+        return quota, kept
+    main = torch.cuda.current_stream()
+    side_stream.wait_stream(main)         # the quota upload and earlier work
+    per = (L + chunks - 1) // chunks
+    if score_events is not None:
+        score_events[0].record(main)
+    for l0 in range(0, L, per):
+        l1 = min(L, l0 + per)
+        _score(q, k, bufs, scorer, pool_k, scale, page, l0, l1)
+        done = torch.cuda.Event()
+        done.record(main)
+        side_stream.wait_event(done)
+        _select(k, v, roles_dev, bufs, W, R, l0, l1, stream=side_stream)
+    if score_events is not None:
+        score_events[1].record(main)
+    main.wait_stream(side_stream)
     return quota, kept

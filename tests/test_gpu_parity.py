@@ -234,7 +234,7 @@ def check_quest_or_scores(gpu, ref, W, what):
     check_scores(gpu, ref, what)
 
 
-def _pipeline_check(K, wl, inp, budget, policy, segs=None):
+def _pipeline_check(K, wl, inp, budget, policy, segs=None, chunks=1):
     """Run the whole step on the GPU and check scores, kept sets and compacted
     rows of the given segments against the oracle.  ``policy`` is a Policy or
     the weights of the role-conditional policy."""
@@ -247,8 +247,9 @@ def _pipeline_check(K, wl, inp, budget, policy, segs=None):
     buckets_t = inp["roles_t"] if policy.bucket_of is None else torch.from_numpy(buckets).cuda()
     _, _, k_cap = policy.allocate(buckets, budget, W)
     bufs = pipeline.alloc_buffers(inp["k"], wl.Hq, W, R, k_cap, scorer=wl.scorer)
+    side = torch.cuda.Stream() if chunks > 1 else None
     quota, kept = pipeline.evict(inp["q"], inp["k"], inp["v"], buckets, buckets_t, policy,
-                                 budget, W, pool, bufs, scorer=wl.scorer)
+                                 budget, W, pool, bufs, scorer=wl.scorer, chunks=chunks, side_stream=side)
     torch.cuda.synchronize()
     ob = inp["roles"] if policy.bucket_of is None else O.role_map(inp["roles"], policy.bucket_of)
     assert np.array_equal(buckets, ob)
@@ -355,6 +356,16 @@ def test_pipeline_snapkv_policies(K, pol, budget):
     _pipeline_check(K, wl, inp, budget, _policy(pol))
 
 
+@pytest.mark.parametrize("chunks", [2, 3])
+def test_pipeline_layer_chunks_on_two_streams(K, chunks):
+    """Scoring chunks of layers on one stream while the top-k and compaction of
+    the scored chunks run on a second stream gives the oracle's result."""
+    wl = WL.get_workload("layer8k").with_(L=5, Hq=8, Hkv=2, N=4000)
+    note(f"pipeline in {chunks} layer chunks")
+    inp = WL.make_inputs(wl, device="cuda")
+    _pipeline_check(K, wl, inp, 0.1, WL.default_alpha(0.0), chunks=chunks)
+
+
 def test_determinism(K):
     wl = WL.get_workload("layer8k")
     inp = WL.make_inputs(wl, device="cuda")
@@ -376,6 +387,7 @@ def test_determinism(K):
 @pytest.mark.parametrize("name,budget,segs,pol", [
     ("stack32k", 0.05, [(0, 0, 0), (17, 2, 5), (31, 3, 7)], "role"),
     ("stack32k", 0.05, [(9, 1, 4)], "fair"),
+    ("stack32k", 0.05, [(3, 0, 1), (30, 3, 6)], "role4chunks"),
     ("long128k", 0.05, [(0, 0, 0), (31, 0, 7)], "role"),
     ("long128k", 0.20, [(13, 0, 2)], "role"),
     ("h2o16k", 0.10, [(0, 0, 3)], "no_key"),
@@ -388,8 +400,8 @@ def test_pipeline_full_size_sampled(K, name, budget, segs, pol):
     inp = WL.make_inputs(wl, device="cuda")
     torch.cuda.synchronize()
     note("  running and checking sampled segments")
-    policy = WL.default_alpha(0.0) if pol == "role" else _policy(pol)
-    ties = _pipeline_check(K, wl, inp, budget, policy, segs=segs)
+    policy = WL.default_alpha(0.0) if pol.startswith("role") else _policy(pol)
+    ties = _pipeline_check(K, wl, inp, budget, policy, segs=segs, chunks=4 if pol == "role4chunks" else 1)
     note(f"  near-tie pairs: {ties}")
     if pol == "role" and wl.scorer == "snapkv":
         note("  decode over the compacted cache of the sampled segments")
