@@ -40,6 +40,7 @@ constexpr int kWaves = 4;
 constexpr int kThreads = kWaves * 64;
 constexpr int kKeys = kSnapChunkKeys;  // keys per chunk
 constexpr int kPoolTile = 4096;  // keys per pool workgroup
+constexpr int kPoolKeysPerThread = kPoolTile / kThreads;  // consecutive keys per thread
 constexpr int kMaxPoolHalf = 127;
 
 // LDS ring depth and workgroups per compute unit of each pass.  bf16: pass 1
@@ -284,7 +285,7 @@ __global__ __launch_bounds__(kThreads, Tune<T>::kOcc2) void snap_pass2(const T* 
 __global__ __launch_bounds__(kThreads) void snap_pool(const float* __restrict__ raw, int planes, int segs,
                                                       int N, int W, int pool_k, int tiles,
                                                       float* __restrict__ score) {
-    __shared__ float ss[kPoolTile + 2 * kMaxPoolHalf];
+    __shared__ __align__(16) float ss[kPoolTile + 2 * kMaxPoolHalf + 8];
     const int tile = blockIdx.x % tiles;
     const int seg = blockIdx.x / tiles;
     const int h = pool_k / 2;
@@ -310,7 +311,43 @@ __global__ __launch_bounds__(kThreads) void snap_pool(const float* __restrict__ 
         if (e < n) ss[e] = (u >= 0 && u < N) ? v[i] : -INFINITY;
     }
     __syncthreads();
-    for (int e = threadIdx.x; e < min(kPoolTile, N - t0); e += kThreads) {
+    // kernel 7 (the paper's), all 16 windows of this thread inside the prefix:
+    // thread i takes keys 16 i .. 16 i + 15 of the tile, its 22 staged values in
+    // registers, the window maxima built from pairwise and four-wide maxima, and
+    // writes them as 16-byte stores (rows of a multiple of 4 keys keep those aligned)
+    const int e0 = kPoolKeysPerThread * (int)threadIdx.x;
+    const bool fast = h == 3 && (N & 3) == 0 && t0 + e0 + kPoolKeysPerThread - 1 + h < P;
+    if (fast) {
+        float x[kPoolKeysPerThread + 8];  // staged keys t0 + e0 - 3 .. t0 + e0 + 18 (+ 2 unused)
+#pragma unroll
+        for (int a = 0; a < (kPoolKeysPerThread + 8) / 4; ++a) {
+            const float4 f = *reinterpret_cast<const float4*>(&ss[e0 + 4 * a]);
+            x[4 * a] = f.x;
+            x[4 * a + 1] = f.y;
+            x[4 * a + 2] = f.z;
+            x[4 * a + 3] = f.w;
+        }
+        float p2[kPoolKeysPerThread + 5], p4[kPoolKeysPerThread + 3];
+#pragma unroll
+        for (int j = 0; j < kPoolKeysPerThread + 5; ++j) p2[j] = fmaxf(x[j], x[j + 1]);
+#pragma unroll
+        for (int j = 0; j < kPoolKeysPerThread + 3; ++j) p4[j] = fmaxf(p2[j], p2[j + 2]);
+        float* dst = score + (size_t)seg * N + t0 + e0;
+#pragma unroll
+        for (int a = 0; a < kPoolKeysPerThread / 4; ++a) {
+            float m[4];
+#pragma unroll
+            for (int b = 0; b < 4; ++b) {
+                const int j = 4 * a + b;
+                m[b] = fmaxf(fmaxf(p4[j], p2[j + 4]), x[j + 6]);  // keys j .. j + 6 around key j + 3
+            }
+            *reinterpret_cast<float4*>(dst + 4 * a) = make_float4(m[0], m[1], m[2], m[3]);
+        }
+        return;
+    }
+    for (int j = 0; j < kPoolKeysPerThread; ++j) {
+        const int e = e0 + j;
+        if (e >= min(kPoolTile, N - t0)) break;
         const int t = t0 + e;
         float m;
         if (t < P) {
