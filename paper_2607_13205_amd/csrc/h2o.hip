@@ -72,6 +72,126 @@ struct RowChunks {
     }
 };
 
+// Products of one chunk's first 64 rows (the A operand, from LDS) with two
+// sets of 32 register rows: acc[s][b] is register set s against chunk block b
+// (element i belongs to chunk row 32 b + c_row(i, lane), the lane to register
+// row lane % 32 of set s).  Each fragment read from LDS feeds two products,
+// and the four accumulators are independent chains.  Start values: zero, or
+// init[chunk row] when given.
+template <typename T, int D>
+__device__ __forceinline__ void chunk_mma_x2(f32x16 (&acc)[2][2], const typename Geo<T, D>::Rd& rd,
+                                             const char* slot, const typename Geo<T, D>::Frags& r0,
+                                             const typename Geo<T, D>::Frags& r1, const float* init, int lane) {
+    using M = Mma<T>;
+    constexpr int NS = Geo<T, D>::C::NSTEP;
+    f32x16 c0[2];
+#pragma unroll
+    for (int b = 0; b < 2; ++b) {
+        if (init == nullptr) {
+            c0[b] = f32x16{};
+        } else {
+#pragma unroll
+            for (int a = 0; a < 4; ++a) {
+                const float4 v = *reinterpret_cast<const float4*>(init + 32 * b + c_row(4 * a, lane));
+                c0[b][4 * a] = v.x;
+                c0[b][4 * a + 1] = v.y;
+                c0[b][4 * a + 2] = v.z;
+                c0[b][4 * a + 3] = v.w;
+            }
+        }
+    }
+#pragma unroll
+    for (int st = 0; st < NS; ++st) {
+        const typename M::frag f[2] = {rd.get(slot, 0, st), rd.get(slot, 1, st)};
+#pragma unroll
+        for (int b = 0; b < 2; ++b) {
+            acc[0][b] = M::mma(f[b], r0[st], st == 0 ? c0[b] : acc[0][b]);
+            acc[1][b] = M::mma(f[b], r1[st], st == 0 ? c0[b] : acc[1][b]);
+        }
+    }
+    // keep the fragment reads two k-steps ahead of the products
+    __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
+#pragma unroll
+    for (int st = 0; st < NS; ++st) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
+        if (st + 2 < NS) __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+    }
+}
+
+// Pass 1 with two register row sets per wave (bf16): 256 rows per workgroup,
+// the G heads of a KV group at 256/G consecutive positions, position-major;
+// wave w holds rows 64 w .. 64 w + 63 as two sets of 32.
+template <typename T, int D>
+__global__ __launch_bounds__(kThreads, 2) void h2o_pass1_x2(const T* __restrict__ q, const T* __restrict__ k,
+                                                            int Hq, int Hkv, int N, int NP, int npos, int nblk,
+                                                            float sl2, float* __restrict__ linit) {
+    using G = Geo<T, D>;
+    __shared__ __align__(16) char ring[kRing * G::C::BYTES];
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int Gh = Hq / Hkv;
+    int bid = blockIdx.x;
+    const int pb = nblk - 1 - bid % nblk;  // longest causal rows first
+    bid /= nblk;
+    const int j = bid % Hkv;
+    const int lb = bid / Hkv;
+    const int p0 = pb * npos;
+    int pos[2], lim[2];
+    bool valid[2];
+    size_t head[2];
+    typename G::Frags qf[2];
+#pragma unroll
+    for (int rs = 0; rs < 2; ++rs) {
+        const int r = wave * 64 + rs * 32 + (lane & 31);
+        const int g = r % Gh;
+        pos[rs] = p0 + r / Gh;
+        valid[rs] = r < npos * Gh && pos[rs] < N;
+        head[rs] = (size_t)lb * Hq + (size_t)j * Gh + g;
+        load_row_frags<T, D>(qf[rs], q + (head[rs] * N + (valid[rs] ? pos[rs] : 0)) * D, valid[rs], lane);
+        lim[rs] = valid[rs] ? pos[rs] : -1;  // last key the row sees
+    }
+    const int t_end = min(N, p0 + npos);  // keys up to the block's last position
+    const int nch = (t_end + kKeys - 1) / kKeys;
+    typename G::Rd rd;
+    rd.init(lane, 0);
+    typename G::Ring ring_io;
+    ring_io.open(nch, wave, lane);
+    const RowChunks<T, D> src{reinterpret_cast<const char*>(k) + ((size_t)lb * Hkv + j) * N * G::C::ROW, 0, t_end};
+    ring_io.prologue(ring, src);
+
+    RowSum rsum[2];
+    for (int s0 = 0; s0 < nch; s0 += kRing) {
+#pragma unroll
+        for (int u = 0; u < kRing; ++u) {
+            const int s = s0 + u;
+            if (s >= nch) break;
+            ring_io.advance(ring, s, u, src);
+            f32x16 acc[2][2];
+            chunk_mma_x2<T, D>(acc, rd, ring + u * G::C::BYTES, qf[0], qf[1], nullptr, lane);
+            if ((s + 1) * kKeys > p0) {  // a key of the chunk lies after some row of the block
+#pragma unroll
+                for (int rs = 0; rs < 2; ++rs) {
+                    // key of element (kb, i) = base + 32 kb + 8 (i / 4) + i % 4
+                    const int last = lim[rs] - (s * kKeys + 4 * (lane >> 5));
+#pragma unroll
+                    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+                        for (int i = 0; i < 16; ++i)
+                            if (32 * kb + 8 * (i >> 2) + (i & 3) > last) acc[rs][kb][i] = -INFINITY;
+                }
+            }
+            rsum[0].add(acc[0], sl2);
+            rsum[1].add(acc[1], sl2);
+        }
+    }
+#pragma unroll
+    for (int rs = 0; rs < 2; ++rs) {
+        // the two lane halves hold the same row and different keys
+        lse2_merge(rsum[rs].m, rsum[rs].l, __shfl_xor(rsum[rs].m, 32), __shfl_xor(rsum[rs].l, 32));
+        if (lane < 32 && valid[rs]) linit[head[rs] * NP + pos[rs]] = -rsum[rs].lse2() / sl2;
+    }
+}
+
 template <typename T, int D>
 __global__ __launch_bounds__(kThreads, 2) void h2o_pass1(const T* __restrict__ q, const T* __restrict__ k,
                                                          int Hq, int Hkv, int N, int NP, int npos, int nblk,
@@ -204,6 +324,90 @@ __global__ __launch_bounds__(kThreads, 2) void h2o_pass2(const T* __restrict__ q
     if (lane < 32 && key < N) colsum[head * N + key] = col;
 }
 
+// Pass 2 with two register key sets per wave (bf16): 256 keys per workgroup,
+// wave w holding keys 64 w .. 64 w + 63 as two sets of 32; every chunk of
+// query rows read from LDS feeds both sets.
+template <typename T, int D>
+__global__ __launch_bounds__(kThreads, 2) void h2o_pass2_x2(const T* __restrict__ q, const T* __restrict__ k,
+                                                            const float* __restrict__ linit, int heads, int Hq,
+                                                            int Hkv, int N, int NP, float sl2,
+                                                            float* __restrict__ colsum) {
+    using G = Geo<T, D>;
+    constexpr int kBlock = 2 * kKeyBlock;
+    __shared__ __align__(16) char ring[kRing * G::C::BYTES];
+    __shared__ __align__(16) float sli[kRing][kKeys];  // -lse2/sl2 of each chunk row
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int Gh = Hq / Hkv;
+    const int kb = blockIdx.x / heads;  // key blocks near 0 (the most rows) first
+    const size_t head = (size_t)(blockIdx.x - kb * heads);  // over all layers and samples
+    const size_t lbj = head / Gh;                            // (layer, sample, KV head)
+    const int kb0 = kb * kBlock;
+    int key[2];
+    typename G::Frags kf[2];
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks) {
+        key[ks] = kb0 + wave * 64 + ks * 32 + (lane & 31);
+        load_row_frags<T, D>(kf[ks], k + (lbj * N + (key[ks] < N ? key[ks] : 0)) * D, key[ks] < N, lane);
+    }
+    // rows kb0 .. N - 1 of this head
+    const int nch = (N - kb0 + kKeys - 1) / kKeys;
+    typename G::Rd rd;
+    rd.init(lane, 0);
+    typename G::Wr wr;
+    wr.init(wave, lane);
+    // chunk c: rows from kb0 + 64 c, with their 64 start values (256 bytes:
+    // four 16-byte pieces per wave, lanes 0..3); as in h2o_pass2
+    auto issue = [&](int c, int slot) {
+        const int r0 = kb0 + c * kKeys;
+        const char* rows = reinterpret_cast<const char*>(q) + (head * N + r0) * G::C::ROW;
+        wr.issue(ring + slot * G::C::BYTES, rows, N - r0);
+        if (lane < 4)
+            lds_dma16(reinterpret_cast<const char*>(linit + head * NP + r0), (unsigned)(wave * 64 + lane * 16),
+                      reinterpret_cast<const char*>(&sli[slot][wave * 16]));
+    };
+    for (int c = 0; c < min(kRing - 1, nch); ++c) issue(c, c);
+
+    float col[2] = {0.0f, 0.0f};
+    for (int s0 = 0; s0 < nch; s0 += kRing) {
+#pragma unroll
+        for (int u = 0; u < kRing; ++u) {
+            const int s = s0 + u;
+            if (s >= nch) break;
+            wait_chunk<G::Wr::LPW + 1, kRing - 2>(min(kRing - 2, nch - 1 - s));
+            lds_barrier();
+            if (s + kRing - 1 < nch) issue(s + kRing - 1, (u + kRing - 1) % kRing);
+            f32x16 acc[2][2];
+            chunk_mma_x2<T, D>(acc, rd, ring + u * G::C::BYTES, kf[0], kf[1], &sli[u][0], lane);
+            const int r0 = kb0 + s * kKeys;
+            if (r0 < kb0 + kBlock || r0 + kKeys > N) {  // rows before some key, or past N
+#pragma unroll
+                for (int ks = 0; ks < 2; ++ks) {
+                    // row of element (b, i) = r0 + 32 b + 8 (i / 4) + 4 (lane / 32) + i % 4; it
+                    // counts iff key <= row < N
+                    const int lo = key[ks] - (r0 + 4 * (lane >> 5));
+                    const int hi = N - (r0 + 4 * (lane >> 5));
+#pragma unroll
+                    for (int b = 0; b < 2; ++b)
+#pragma unroll
+                        for (int i = 0; i < 16; ++i) {
+                            const int off = 32 * b + 8 * (i >> 2) + (i & 3);
+                            if (off < lo || off >= hi) acc[ks][b][i] = -INFINITY;
+                        }
+                }
+            }
+            col[0] += exp2_sum(acc[0], sl2);
+            col[1] += exp2_sum(acc[1], sl2);
+        }
+    }
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks) {
+        // the two lane halves hold the same key and different rows
+        const float c = col[ks] + __shfl_xor(col[ks], 32);
+        if (lane < 32 && key[ks] < N) colsum[head * N + key[ks]] = c;
+    }
+}
+
 // score of (layer, sample, KV head j) = sum of its G heads' column sums, in head order
 __global__ __launch_bounds__(kThreads) void h2o_heads(const float* __restrict__ colsum, int Gh, int N,
                                                       size_t total, float* __restrict__ score) {
@@ -225,15 +429,26 @@ hipError_t run_h2o(const void* q, const void* k, int L, int B, int Hq, int Hkv, 
     const T* qt = static_cast<const T*>(q);
     const T* kt = static_cast<const T*>(k);
     const int Gh = Hq / Hkv;
-    const int npos = kH2oRowsPerGroup / Gh;  // positions per pass-1 workgroup
-    const int nblk = (N + npos - 1) / npos;
-    const int nkb = (N + kKeyBlock - 1) / kKeyBlock;
     const int NP = h2o_pitch(N);
-    hipLaunchKernelGGL((h2o_pass1<T, D>), dim3((unsigned)((size_t)L * B * Hkv * nblk)), dim3(kThreads), 0, st, qt,
-                       kt, Hq, Hkv, N, NP, npos, nblk, sl2, linit);
     const int heads = L * B * Hq;
-    hipLaunchKernelGGL((h2o_pass2<T, D>), dim3((unsigned)((size_t)heads * nkb)), dim3(kThreads), 0, st, qt, kt,
-                       linit, heads, Hq, Hkv, N, NP, sl2, colsum);
+    // bf16: two register row sets per wave (fp32 fragments are twice the
+    // registers and keep one)
+    constexpr bool kX2 = sizeof(T) == 2;
+    const int npos = (kX2 ? 2 : 1) * kH2oRowsPerGroup / Gh;  // positions per pass-1 workgroup
+    const int nblk = (N + npos - 1) / npos;
+    const int kblock = (kX2 ? 2 : 1) * kKeyBlock;
+    const int nkb = (N + kblock - 1) / kblock;
+    if constexpr (kX2) {
+        hipLaunchKernelGGL((h2o_pass1_x2<T, D>), dim3((unsigned)((size_t)L * B * Hkv * nblk)), dim3(kThreads), 0,
+                           st, qt, kt, Hq, Hkv, N, NP, npos, nblk, sl2, linit);
+        hipLaunchKernelGGL((h2o_pass2_x2<T, D>), dim3((unsigned)((size_t)heads * nkb)), dim3(kThreads), 0, st, qt,
+                           kt, linit, heads, Hq, Hkv, N, NP, sl2, colsum);
+    } else {
+        hipLaunchKernelGGL((h2o_pass1<T, D>), dim3((unsigned)((size_t)L * B * Hkv * nblk)), dim3(kThreads), 0, st,
+                           qt, kt, Hq, Hkv, N, NP, npos, nblk, sl2, linit);
+        hipLaunchKernelGGL((h2o_pass2<T, D>), dim3((unsigned)((size_t)heads * nkb)), dim3(kThreads), 0, st, qt,
+                           kt, linit, heads, Hq, Hkv, N, NP, sl2, colsum);
+    }
     const size_t total = (size_t)L * B * Hkv * N;
     hipLaunchKernelGGL(h2o_heads, dim3((unsigned)std::min<size_t>((total + kThreads - 1) / kThreads, 4096)),
                        dim3(kThreads), 0, st, colsum, Gh, N, total, score);
