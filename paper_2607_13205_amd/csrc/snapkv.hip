@@ -43,10 +43,12 @@ constexpr int kPoolTile = 4096;  // keys per pool workgroup
 constexpr int kPoolKeysPerThread = kPoolTile / kThreads;  // consecutive keys per thread
 constexpr int kMaxPoolHalf = 127;
 
-// LDS ring depth and workgroups per compute unit of each pass.  bf16: pass 1
-// keeps two chunks in flight at three workgroups per CU, pass 2 one chunk at
-// four (its longer per-chunk work hides the shorter prefetch, and the extra
-// workgroup overlaps more of one wave's exponentials with another's products).
+// LDS ring depth and workgroups per compute unit of each pass.  bf16: both
+// passes keep one chunk in flight at four workgroups per CU (with non-temporal
+// chunk loads and conflict-free fragment reads, the fourth workgroup hides more
+// than a second chunk ahead: measured 1-2% faster than two chunks at three);
+// the extra workgroup also overlaps more of one wave's exponentials with
+// another's products.
 // fp32 fragments need twice the registers: two workgroups, three chunks ahead.
 template <typename T>
 struct Tune {
@@ -54,7 +56,7 @@ struct Tune {
 };
 template <>
 struct Tune<__bf16> {
-    static constexpr int kRing1 = 3, kOcc1 = 3, kRing2 = 2, kOcc2 = 4;
+    static constexpr int kRing1 = 2, kOcc1 = 4, kRing2 = 2, kOcc2 = 4;
 };
 
 // Each pass reads every key row once: non-temporal chunk loads (measured 3-4%
