@@ -68,6 +68,7 @@ __all__ = [
     "causal_logits",
     "causal_softmax",
     "snapkv_mass",
+    "window_lse",
     "h2o_mass",
     "maxpool_prefix",
     "snapkv_score",
@@ -158,6 +159,25 @@ def snapkv_mass(q_win: np.ndarray, k: np.ndarray, scale: float | None = None) ->
         p = causal_softmax(causal_logits(q_win[h], pos, k, scale))
         s += p.sum(axis=0)
     return s
+
+
+def window_lse(q_win: np.ndarray, k: np.ndarray, scale: float | None = None) -> np.ndarray:
+    """Natural-log log-sum-exp of every window row over its causal keys, the
+    statistic a prefill attention kernel returns per query row: [G, W] with
+    lse[h, i] = log sum_{t <= N-W+i} exp(scale <q_h[i], k_t>).  With it,
+    p_h[i, t] = exp(x - lse) (§2)."""
+    q_win = np.asarray(q_win, dtype=np.float64)
+    G, W, d = q_win.shape
+    N = k.shape[0]
+    if scale is None:
+        scale = 1.0 / math.sqrt(d)
+    pos = np.arange(N - W, N)
+    out = np.zeros((G, W), dtype=np.float64)
+    for h in range(G):
+        x = causal_logits(q_win[h], pos, k, scale)
+        m = np.max(x, axis=1, keepdims=True)
+        out[h] = (m + np.log(np.sum(np.exp(x - m), axis=1, keepdims=True)))[:, 0]
+    return out
 
 
 def h2o_mass(q: np.ndarray, k: np.ndarray, scale: float | None = None,

@@ -198,3 +198,21 @@ def test_pool_matches_scipy_on_prefix(kern, W):
 def test_pool_rejects_even_kernel():
     with pytest.raises(ValueError):
         O.maxpool_prefix(np.zeros(8), 2, 4)
+
+
+def test_window_lse_is_the_softmax_normaliser():
+    """The window rows' log-sum-exp matches scipy's logsumexp over the causal
+    keys, and exp(x - lse) rows sum to 1 and equal the oracle's softmax."""
+    from scipy.special import logsumexp
+    r = np.random.default_rng(700)
+    G, W, N, d = 3, 5, 40, 16
+    q, k = r.standard_normal((G, W, d)), r.standard_normal((N, d))
+    lse = O.window_lse(q, k)
+    pos = np.arange(N - W, N)
+    for h in range(G):
+        x = O.causal_logits(q[h], pos, k, 1.0 / np.sqrt(d))
+        for i in range(W):
+            assert np.isclose(lse[h, i], logsumexp(x[i, :pos[i] + 1]), rtol=1e-13, atol=1e-13)
+        p = np.exp(x - lse[h][:, None])
+        assert np.allclose(p.sum(axis=1), 1.0, atol=1e-12)
+        assert np.allclose(p, O.causal_softmax(x), atol=1e-13)
