@@ -18,7 +18,10 @@ every kernel with other quotas; ``decode`` times one decode query per head over
 the compacted cache of every layer against the same kernel over the full
 cache; ``quest`` times the one-shot Quest page-bound scorer on the same
 inputs, alone and as the score of the whole step; ``probe`` times the linear
-role probe labelling the batch's tokens (random weights of the paper's size).
+role probe labelling the batch's tokens (random weights of the paper's size);
+``prefill_lse`` times the score and the step when the window rows' log-sum-exp
+comes from the prefill attention (as such kernels return it per query row):
+K is then read once.  ``--lse`` makes that the main line (for profiling it).
 
 ``roofline.traffic`` is the measured HBM traffic of one score call, read from
 the counter summary in profiles/ (rocprofv3 FETCH_SIZE and WRITE_SIZE,
@@ -43,6 +46,8 @@ if ROOT not in sys.path:
 
 METRIC = "prefill tokens scored+compressed/s per GPU; % HBM peak (SnapKV), % MFMA (H2O)"
 TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "snapkv_score_stack32k_traffic.md")
+# the same for the score with the window statistics supplied (pass 2 + pool)
+TRAFFIC_SUMMARY_LSE = os.path.join(ROOT, "profiles", "snapkv_score_lse_stack32k_traffic.md")
 # sources of the kernels one score call launches
 SCORE_SOURCES = ("paper_2607_13205_amd/csrc/snapkv.hip", "paper_2607_13205_amd/csrc/kve_stream.h",
                  "paper_2607_13205_amd/csrc/kve_device.h", "paper_2607_13205_amd/csrc/kve_snap_plan.h")
@@ -64,6 +69,9 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-h2o", action="store_true", help="skip the H2O scorer leg")
     ap.add_argument("--no-quest", action="store_true", help="skip the Quest scorer timings")
+    ap.add_argument("--no-lse", action="store_true", help="skip the supplied-statistics timings")
+    ap.add_argument("--lse", action="store_true",
+                    help="main line with the window rows' log-sum-exp supplied (one read of K)")
     ap.add_argument("--no-probe", action="store_true", help="skip the role-probe timing")
     ap.add_argument("--chunks", type=int, default=1,
                     help="layer chunks of the step: each scored chunk's top-k and compaction run on a "
@@ -85,11 +93,11 @@ def score_sources_sha() -> str:
     return h.hexdigest()
 
 
-def measured_traffic(wl_name: str):
+def measured_traffic(wl_name: str, summary: str = TRAFFIC_SUMMARY):
     """HBM bytes per score call from the committed counter summary, or None when
     it is missing, covers another workload, or was taken on other sources."""
     try:
-        with open(TRAFFIC_SUMMARY) as f:
+        with open(summary) as f:
             text = f.read()
     except OSError:
         return None
@@ -325,6 +333,48 @@ def probe_leg(K, wl, steps):
             "tokens_per_s": round(wl.B * wl.N / (ms * 1e-3), 1)}
 
 
+def window_lse(q, k, wl):
+    """The window rows' natural-log log-sum-exp [L, B, Hq, W], float32, layer by
+    layer with torch: the statistic a prefill attention kernel returns per
+    query row (input preparation, outside every timed region)."""
+    import torch
+    L = k.shape[0]
+    out = torch.empty((L, wl.B, wl.Hq, wl.W), dtype=torch.float32, device=k.device)
+    pos = torch.arange(wl.N - wl.W, wl.N, device=k.device)
+    mask = torch.arange(wl.N, device=k.device)[None, :] <= pos[:, None]
+    scale = 1.0 / math.sqrt(wl.d)
+    for l in range(L):
+        qf = q[l].float().reshape(wl.B, wl.Hkv, wl.G * wl.W, wl.d)
+        kf = k[l].float().transpose(-1, -2).contiguous()
+        x = (torch.matmul(qf, kf) * scale).reshape(wl.B, wl.Hkv, wl.G, wl.W, wl.N)
+        out[l] = torch.logsumexp(x.masked_fill(~mask, float("-inf")), dim=-1).reshape(wl.B, wl.Hq, wl.W)
+        del qf, kf, x
+    torch.cuda.empty_cache()
+    return out
+
+
+def lse_leg(K, pipeline, wl, inp, lse, budget, alpha, steps):
+    """Score call and whole step with the window rows' statistics supplied."""
+    import torch
+    L, B, Hkv, N, d = inp["k"].shape
+    score = torch.empty((L, B, Hkv, N), dtype=torch.float32, device="cuda")
+    ws = torch.empty(K.snapkv_workspace_size(L, B, wl.Hq, Hkv, N, wl.W, d), dtype=torch.uint8, device="cuda")
+    ms = _time_calls(lambda: K.snapkv_score_lse(inp["q"], inp["k"], lse, wl.pool_k, score=score, workspace=ws),
+                     steps)
+    nbytes = snapkv_algorithmic_bytes(wl)
+    del score, ws
+    _, _, k_cap = K.role_allocate(inp["roles"], 4, alpha, budget, wl.W)
+    bufs = pipeline.alloc_buffers(inp["k"], wl.Hq, wl.W, 4, k_cap)
+    ms_step = _time_calls(lambda: pipeline.evict(inp["q"], inp["k"], inp["v"], inp["roles"], inp["roles_t"],
+                                                 alpha, budget, wl.W, wl.pool_k, bufs, lse_win=lse), steps)
+    del bufs
+    torch.cuda.empty_cache()
+    gbs = nbytes / (ms * 1e-3) / 1e9
+    return {"kernel": "kve_snapkv_score_lse (window statistics supplied; pass 2 + pool)", "ms": round(ms, 4),
+            "achieved_GBs": round(gbs, 1), "hbm_frac": round(gbs / HBM_PEAK_GBS, 4),
+            "ms_per_step": round(ms_step, 4), "tokens_per_s": round(wl.B * wl.N / (ms_step * 1e-3), 1)}
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -353,6 +403,11 @@ def main():
     scorer = wl.scorer
     W = 0 if scorer == "h2o" else wl.W
     pool = 1 if scorer == "h2o" else wl.pool_k
+    lse = None
+    if scorer == "snapkv" and (args.lse or not args.no_lse):
+        print("[bench] window-row statistics for the supplied-lse runs (untimed)", file=sys.stderr, flush=True)
+        lse = window_lse(inp["q"], inp["k"], wl)
+    main_lse = lse if args.lse else None
     _, kept, k_cap = K.role_allocate(inp["roles"], 4, alpha, budget, W)
     bufs = pipeline.alloc_buffers(inp["k"], wl.Hq, W, 4, k_cap, scorer=scorer)
 
@@ -360,7 +415,7 @@ def main():
 
     def step():
         pipeline.evict(inp["q"], inp["k"], inp["v"], inp["roles"], inp["roles_t"], alpha, budget,
-                       W, pool, bufs, scorer=scorer, chunks=args.chunks, side_stream=side)
+                       W, pool, bufs, scorer=scorer, chunks=args.chunks, side_stream=side, lse_win=main_lse)
 
     print(f"[bench] warmup {args.warmup}", file=sys.stderr, flush=True)
     for _ in range(args.warmup):
@@ -376,7 +431,7 @@ def main():
     for i in range(args.steps):
         pipeline.evict(inp["q"], inp["k"], inp["v"], inp["roles"], inp["roles_t"], alpha, budget,
                        W, pool, bufs, scorer=scorer, score_events=ev[i], chunks=args.chunks,
-                       side_stream=side)
+                       side_stream=side, lse_win=main_lse)
     t_all1.record()
     torch.cuda.synchronize()
     ms_step = t_all0.elapsed_time(t_all1) / args.steps
@@ -402,7 +457,8 @@ def main():
         "config": {
             "workload": f"{wl.name}: {wl.L} layers, batch {wl.B}, {wl.Hq}q/{wl.Hkv}kv heads, "
                         f"d={wl.d}, N={wl.N}, W={wl.W}, pool {wl.pool_k}, B={budget}, "
-                        f"alpha_KEY={args.alpha_key}, role mix {wl.mix}",
+                        f"alpha_KEY={args.alpha_key}, role mix {wl.mix}"
+                        + (", window-row log-sum-exp supplied (K read once)" if args.lse else ""),
             "global_batch": wl.B, "seq_len": wl.N, "parallelism": "none (1 GPU)",
             "layer_tokens_per_s": round(value * wl.L, 1),
             "k_cap": k_cap, "layer_chunks": args.chunks,
@@ -410,9 +466,11 @@ def main():
             "step_hbm_frac": round(step_bytes / (ms_step * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
         },
         "roofline": {
-            "kernel": "kve_snapkv_score (score passes + pool)",
+            "kernel": ("kve_snapkv_score_lse (pass 2 + pool)" if args.lse
+                       else "kve_snapkv_score (score passes + pool)"),
             "bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-            "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": measured_traffic(wl.name),
+            "frac": round(achieved / HBM_PEAK_GBS, 4),
+            "traffic": measured_traffic(wl.name, TRAFFIC_SUMMARY_LSE if args.lse else TRAFFIC_SUMMARY),
             "ms": round(ms_score, 4), "algorithmic_bytes": score_bytes,
         },
     }
@@ -421,6 +479,9 @@ def main():
         out["decode"] = decode_leg(K, wl, inp, bufs, max(3, args.steps // 2))
     del bufs
     torch.cuda.empty_cache()
+    if lse is not None and not args.lse and not args.no_lse:
+        print("[bench] supplied window statistics", file=sys.stderr, flush=True)
+        out["prefill_lse"] = lse_leg(K, pipeline, wl, inp, lse, budget, alpha, max(3, args.steps // 2))
     if not args.no_quest and scorer == "snapkv":
         print("[bench] Quest scorer", file=sys.stderr, flush=True)
         out["quest"] = quest_leg(K, pipeline, wl, inp, budget, alpha, max(3, args.steps // 2))

@@ -105,6 +105,27 @@ kve_status_t kve_snapkv_score(const void* q_win, const void* k, kve_dtype_t dtyp
                               float scale, int pool_k, float* score,
                               void* workspace, size_t workspace_bytes, void* stream);
 
+/*
+ * kve_snapkv_score with the window rows' statistics supplied by the caller:
+ * lse_win[l, b, h, i] is the natural-log log-sum-exp of window row i of
+ * query head h over its causal keys,
+ *   log sum over t <= N-W+i of exp(scale * <q_win[l, b, h, i], k[l, b, j, t]>),
+ * which is what a prefill attention kernel returns per query row (the
+ * softmax normaliser of §2).  The score then reads K once: the row
+ * statistics pass and its combine step are skipped, and the result is that of
+ * kve_snapkv_score up to the rounding of the supplied values.  The values
+ * must be finite and use the same scale.
+ *
+ *   lse_win   [L, B, Hq, W] float32 (device)
+ *   others    as for kve_snapkv_score (same workspace size)
+ *
+ * Errors: as for kve_snapkv_score, and KVE_ERR_INVALID_ARG for a null lse_win.
+ */
+kve_status_t kve_snapkv_score_lse(const void* q_win, const void* k, const float* lse_win,
+                                  kve_dtype_t dtype, int L, int B, int Hq, int Hkv, int N,
+                                  int W, int d, float scale, int pool_k, float* score,
+                                  void* workspace, size_t workspace_bytes, void* stream);
+
 /* ------------------------------------------------------------------------- */
 /* H2O accumulated score, the baseline scorer (paper §2, H2O family).         */
 /* ------------------------------------------------------------------------- */

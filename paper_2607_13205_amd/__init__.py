@@ -3,6 +3,7 @@
 The hot path runs in libkve.so (HIP); this package is its thin Python binding:
 
   snapkv_score   SnapKV windowed score + GQA sum + prefix max-pool
+  snapkv_score_lse  the same with the window rows' log-sum-exp supplied (one read of K)
   h2o_score      H2O accumulated score (baseline scorer)
   quest_score    one-shot Quest page-bound score (query-aware baseline scorer)
   role_allocate  per-bucket quotas with redistribution (host)
@@ -18,10 +19,10 @@ The hot path runs in libkve.so (HIP); this package is its thin Python binding:
 from .binding import (EXPORTED, KveError, decode_attention, decode_workspace_size,  # noqa: F401
                       h2o_score, h2o_workspace_size, kv_compact, last_error, quest_score,
                       quest_workspace_size, role_allocate,
-                      role_allocate_fair, role_map, role_probe, snapkv_score, snapkv_workspace_size, topk_select)
+                      role_allocate_fair, role_map, role_probe, snapkv_score, snapkv_score_lse, snapkv_workspace_size, topk_select)
 from . import pipeline  # noqa: F401
 
 __all__ = ["snapkv_score", "h2o_score", "role_allocate", "role_allocate_fair", "role_map",
            "topk_select", "kv_compact", "snapkv_workspace_size", "h2o_workspace_size", "KveError",
            "last_error", "pipeline", "decode_attention", "decode_workspace_size", "quest_score",
-           "quest_workspace_size", "role_probe"]
+           "quest_workspace_size", "role_probe", "snapkv_score_lse"]

@@ -29,7 +29,7 @@ DTYPE_F32 = 1
 #: every symbol include/kve.h declares
 EXPORTED = (
     "kve_version", "kve_last_error",
-    "kve_snapkv_workspace_size", "kve_snapkv_score",
+    "kve_snapkv_workspace_size", "kve_snapkv_score", "kve_snapkv_score_lse",
     "kve_h2o_workspace_size", "kve_h2o_score",
     "kve_role_allocate", "kve_role_allocate_fair", "kve_role_map", "kve_role_probe",
     "kve_topk_workspace_size", "kve_topk_select",
@@ -59,6 +59,8 @@ def _load():
         "kve_snapkv_workspace_size": (c_size, [c_int] * 7),
         "kve_snapkv_score": (c_int, [c_void, c_void, c_int] + [c_int] * 7 +
                              [c_float, c_int, c_void, c_void, c_size, c_void]),
+        "kve_snapkv_score_lse": (c_int, [c_void, c_void, c_void, c_int] + [c_int] * 7 +
+                                 [c_float, c_int, c_void, c_void, c_size, c_void]),
         "kve_h2o_workspace_size": (c_size, [c_int] * 6),
         "kve_h2o_score": (c_int, [c_void, c_void, c_int] + [c_int] * 6 +
                           [c_float, c_void, c_void, c_size, c_void]),
@@ -177,6 +179,27 @@ def snapkv_score(q_win, k, pool_k: int, scale: float = 0.0, score=None, workspac
     _check(LIB.kve_snapkv_score(_dev(q_win, "q_win"), _dev(k, "k"), _dtype_code(k),
                                 L, B, Hq, Hkv, N, W, d, float(scale), int(pool_k),
                                 _dev(score, "score"), _ptr(ws), wsb, _stream(stream)))
+    return score
+
+
+def snapkv_score_lse(q_win, k, lse_win, pool_k: int, scale: float = 0.0, score=None, workspace=None,
+                     stream=None):
+    """snapkv_score with the window rows' natural-log log-sum-exp supplied
+    (float32 [L, B, Hq, W], as a prefill attention kernel returns it): K is
+    read once."""
+    torch = _torch()
+    L, B, Hq, W, d = q_win.shape
+    Lk, Bk, Hkv, N, dk = k.shape
+    if (L, B, d) != (Lk, Bk, dk) or q_win.dtype != k.dtype:
+        raise ValueError("q_win and k disagree in L, B, d or dtype")
+    if tuple(lse_win.shape) != (L, B, Hq, W) or lse_win.dtype != torch.float32:
+        raise ValueError("lse_win must be float32 [L, B, Hq, W]")
+    if score is None:
+        score = torch.empty((L, B, Hkv, N), dtype=torch.float32, device=k.device)
+    ws, wsb = _workspace(snapkv_workspace_size(L, B, Hq, Hkv, N, W, d), k.device, workspace)
+    _check(LIB.kve_snapkv_score_lse(_dev(q_win, "q_win"), _dev(k, "k"), _dev(lse_win, "lse_win"), _dtype_code(k),
+                                    L, B, Hq, Hkv, N, W, d, float(scale), int(pool_k), _dev(score, "score"),
+                                    _ptr(ws), wsb, _stream(stream)))
     return score
 
 

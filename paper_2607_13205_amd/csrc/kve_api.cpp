@@ -136,24 +136,9 @@ int32_t allocate_sample(const long long* n, const double* alpha, int R, double b
     return (int32_t)sum;
 }
 
-}  // namespace
-
-extern "C" {
-
-int kve_version(void) { return KVE_ABI_VERSION; }
-
-const char* kve_last_error(void) { return g_error.c_str(); }
-
-size_t kve_snapkv_workspace_size(int L, int B, int Hq, int Hkv, int N, int W, int d) {
-    if (L <= 0 || B <= 0 || Hq <= 0 || Hkv <= 0 || N <= 0 || W <= 0 || Hq % Hkv != 0) return 0;
-    if (d != 64 && d != 128) return 0;
-    return kve::snap_plan(L, B, Hq, Hkv, N, W, d).total;
-}
-
-kve_status_t kve_snapkv_score(const void* q_win, const void* k, kve_dtype_t dtype, int L, int B,
-                              int Hq, int Hkv, int N, int W, int d, float scale, int pool_k,
-                              float* score, void* workspace, size_t workspace_bytes, void* stream) {
-    const char* fn = "kve_snapkv_score";
+kve_status_t snapkv_common(const char* fn, const void* q_win, const void* k, const float* lse_win,
+                           kve_dtype_t dtype, int L, int B, int Hq, int Hkv, int N, int W, int d, float scale,
+                           int pool_k, float* score, void* workspace, size_t workspace_bytes, void* stream) {
     kve_status_t st = check_common(fn, L, B, Hq, Hkv, N, d, (int)dtype);
     if (st != KVE_OK) return st;
     if (q_win == nullptr || k == nullptr || score == nullptr)
@@ -174,9 +159,38 @@ kve_status_t kve_snapkv_score(const void* q_win, const void* k, kve_dtype_t dtyp
                     p.total);
     if (!aligned(workspace)) return fail(KVE_ERR_INVALID_ARG, "%s: workspace not 256-byte aligned", fn);
     if (scale == 0.0f) scale = 1.0f / std::sqrt((float)d);
-    return from_hip(kve::launch_snapkv(q_win, k, (int)dtype, L, B, Hq, Hkv, N, W, d, scale, pool_k, score,
-                                       workspace, static_cast<hipStream_t>(stream)),
+    return from_hip(kve::launch_snapkv(q_win, k, lse_win, (int)dtype, L, B, Hq, Hkv, N, W, d, scale, pool_k,
+                                       score, workspace, static_cast<hipStream_t>(stream)),
                     fn);
+}
+
+}  // namespace
+
+extern "C" {
+
+int kve_version(void) { return KVE_ABI_VERSION; }
+
+const char* kve_last_error(void) { return g_error.c_str(); }
+
+size_t kve_snapkv_workspace_size(int L, int B, int Hq, int Hkv, int N, int W, int d) {
+    if (L <= 0 || B <= 0 || Hq <= 0 || Hkv <= 0 || N <= 0 || W <= 0 || Hq % Hkv != 0) return 0;
+    if (d != 64 && d != 128) return 0;
+    return kve::snap_plan(L, B, Hq, Hkv, N, W, d).total;
+}
+
+kve_status_t kve_snapkv_score(const void* q_win, const void* k, kve_dtype_t dtype, int L, int B,
+                              int Hq, int Hkv, int N, int W, int d, float scale, int pool_k,
+                              float* score, void* workspace, size_t workspace_bytes, void* stream) {
+    return snapkv_common("kve_snapkv_score", q_win, k, nullptr, dtype, L, B, Hq, Hkv, N, W, d, scale, pool_k,
+                         score, workspace, workspace_bytes, stream);
+}
+
+kve_status_t kve_snapkv_score_lse(const void* q_win, const void* k, const float* lse_win, kve_dtype_t dtype,
+                                  int L, int B, int Hq, int Hkv, int N, int W, int d, float scale, int pool_k,
+                                  float* score, void* workspace, size_t workspace_bytes, void* stream) {
+    if (lse_win == nullptr) return fail(KVE_ERR_INVALID_ARG, "kve_snapkv_score_lse: null lse_win");
+    return snapkv_common("kve_snapkv_score_lse", q_win, k, lse_win, dtype, L, B, Hq, Hkv, N, W, d, scale,
+                         pool_k, score, workspace, workspace_bytes, stream);
 }
 
 size_t kve_h2o_workspace_size(int L, int B, int Hq, int Hkv, int N, int d) {

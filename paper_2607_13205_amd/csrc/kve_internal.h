@@ -92,8 +92,10 @@ inline QuestPlan quest_plan(int L, int B, int Hq, int Hkv, int N, int W, int d, 
     return p;
 }
 
-hipError_t launch_snapkv(const void* q, const void* k, int dtype, int L, int B, int Hq, int Hkv,
-                         int N, int W, int d, float scale, int pool_k, float* score, void* ws,
+// lse_win: the window rows' natural-log log-sum-exp from the caller, or null
+// to compute it (pass 1 and the combine step)
+hipError_t launch_snapkv(const void* q, const void* k, const float* lse_win, int dtype, int L, int B, int Hq,
+                         int Hkv, int N, int W, int d, float scale, int pool_k, float* score, void* ws,
                          hipStream_t st);
 
 hipError_t launch_h2o(const void* q, const void* k, int dtype, int L, int B, int Hq, int Hkv,

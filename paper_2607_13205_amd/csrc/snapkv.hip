@@ -175,6 +175,18 @@ __global__ __launch_bounds__(kSnapRowsPerGroup) void snap_combine(const float* _
     lse[(size_t)vseg * kSnapRowsPerGroup + r] = (row < rows && b > 0.0f) ? a + log2f(b) : INFINITY;
 }
 
+// Row statistics supplied by the caller (the natural-log log-sum-exp of each
+// window row, [segments, G, W] as a prefill attention kernel returns it per
+// query row), turned into the combine step's output: log2 units, rows of the
+// vseg layout, +inf for padding rows.
+__global__ __launch_bounds__(kSnapRowsPerGroup) void snap_import_lse(const float* __restrict__ lse_win, int rows,
+                                                                     int rgroups, float* __restrict__ lse) {
+    const int vseg = blockIdx.x, r = threadIdx.x;
+    const int seg = vseg / rgroups;
+    const int row = (vseg - seg * rgroups) * kSnapRowsPerGroup + r;  // head-major: g * W + i
+    lse[(size_t)vseg * kSnapRowsPerGroup + r] = row < rows ? lse_win[(size_t)seg * rows + row] * kLog2e : INFINITY;
+}
+
 template <typename T, int D>
 __global__ __launch_bounds__(kThreads, Tune<T>::kOcc2) void snap_pass2(const T* __restrict__ q, const T* __restrict__ k,
                                                           int N, int W, int rows, int rgroups, int nranges,
@@ -364,8 +376,8 @@ __global__ __launch_bounds__(kThreads) void snap_pool(const float* __restrict__ 
 }
 
 template <typename T, int D>
-hipError_t run_snapkv(const void* q, const void* k, int L, int B, int Hq, int Hkv, int N, int W,
-                      float scale, int pool_k, float* score, void* ws, hipStream_t st) {
+hipError_t run_snapkv(const void* q, const void* k, const float* lse_win, int L, int B, int Hq, int Hkv, int N,
+                      int W, float scale, int pool_k, float* score, void* ws, hipStream_t st) {
     const SnapPlan p = snap_plan(L, B, Hq, Hkv, N, W, D);
     char* w = static_cast<char*>(ws);
     float* stats = reinterpret_cast<float*>(w + p.off_stats);
@@ -375,10 +387,15 @@ hipError_t run_snapkv(const void* q, const void* k, int L, int B, int Hq, int Hk
     const T* qt = static_cast<const T*>(q);
     const T* kt = static_cast<const T*>(k);
     const dim3 grid((unsigned)((size_t)p.n_vsegs * p.nranges));
-    hipLaunchKernelGGL((snap_pass1<T, D>), grid, dim3(kThreads), 0, st, qt, kt, N, W, p.rows, p.rgroups,
-                       p.nranges, p.range_keys, sl2, stats);
-    hipLaunchKernelGGL(snap_combine, dim3((unsigned)p.n_vsegs), dim3(kSnapRowsPerGroup), 0, st, stats,
-                       p.nranges, p.rows, p.rgroups, lse);
+    if (lse_win != nullptr) {  // row statistics from the caller: one read of K
+        hipLaunchKernelGGL(snap_import_lse, dim3((unsigned)p.n_vsegs), dim3(kSnapRowsPerGroup), 0, st, lse_win,
+                           p.rows, p.rgroups, lse);
+    } else {
+        hipLaunchKernelGGL((snap_pass1<T, D>), grid, dim3(kThreads), 0, st, qt, kt, N, W, p.rows, p.rgroups,
+                           p.nranges, p.range_keys, sl2, stats);
+        hipLaunchKernelGGL(snap_combine, dim3((unsigned)p.n_vsegs), dim3(kSnapRowsPerGroup), 0, st, stats,
+                           p.nranges, p.rows, p.rgroups, lse);
+    }
     hipLaunchKernelGGL((snap_pass2<T, D>), grid, dim3(kThreads), 0, st, qt, kt, N, W, p.rows, p.rgroups,
                        p.nranges, p.range_keys, sl2, lse, p.segs, raw);
     const int tiles = (N + kPoolTile - 1) / kPoolTile;
@@ -389,15 +406,16 @@ hipError_t run_snapkv(const void* q, const void* k, int L, int B, int Hq, int Hk
 
 }  // namespace
 
-hipError_t launch_snapkv(const void* q, const void* k, int dtype, int L, int B, int Hq, int Hkv,
-                         int N, int W, int d, float scale, int pool_k, float* score, void* ws,
+hipError_t launch_snapkv(const void* q, const void* k, const float* lse_win, int dtype, int L, int B, int Hq,
+                         int Hkv, int N, int W, int d, float scale, int pool_k, float* score, void* ws,
                          hipStream_t st) {
     if (dtype == 0) {
-        if (d == 128) return run_snapkv<__bf16, 128>(q, k, L, B, Hq, Hkv, N, W, scale, pool_k, score, ws, st);
-        return run_snapkv<__bf16, 64>(q, k, L, B, Hq, Hkv, N, W, scale, pool_k, score, ws, st);
+        if (d == 128)
+            return run_snapkv<__bf16, 128>(q, k, lse_win, L, B, Hq, Hkv, N, W, scale, pool_k, score, ws, st);
+        return run_snapkv<__bf16, 64>(q, k, lse_win, L, B, Hq, Hkv, N, W, scale, pool_k, score, ws, st);
     }
-    if (d == 128) return run_snapkv<float, 128>(q, k, L, B, Hq, Hkv, N, W, scale, pool_k, score, ws, st);
-    return run_snapkv<float, 64>(q, k, L, B, Hq, Hkv, N, W, scale, pool_k, score, ws, st);
+    if (d == 128) return run_snapkv<float, 128>(q, k, lse_win, L, B, Hq, Hkv, N, W, scale, pool_k, score, ws, st);
+    return run_snapkv<float, 64>(q, k, lse_win, L, B, Hq, Hkv, N, W, scale, pool_k, score, ws, st);
 }
 
 }  // namespace kve

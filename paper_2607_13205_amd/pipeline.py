@@ -121,9 +121,12 @@ def alloc_buffers(k, n_q_heads: int, W: int, R: int, k_cap: int, scorer: str = "
     )
 
 
-def _score(q, k, bufs, scorer, pool_k, scale, page, l0, l1, stream=None):
+def _score(q, k, bufs, scorer, pool_k, scale, page, l0, l1, stream=None, lse_win=None):
     """Score layers [l0, l1) into bufs.score[l0:l1] on ``stream`` (None: current)."""
-    if scorer == "snapkv":
+    if scorer == "snapkv" and lse_win is not None:
+        kb.snapkv_score_lse(q[l0:l1], k[l0:l1], lse_win[l0:l1], pool_k, scale, score=bufs.score[l0:l1],
+                            workspace=bufs.ws_score, stream=stream)
+    elif scorer == "snapkv":
         kb.snapkv_score(q[l0:l1], k[l0:l1], pool_k, scale, score=bufs.score[l0:l1],
                         workspace=bufs.ws_score, stream=stream)
     elif scorer == "quest":
@@ -145,7 +148,7 @@ def _select(k, v, roles_dev, bufs, W, R, l0, l1, stream=None):
 
 def evict(q, k, v, roles_host: np.ndarray, roles_dev, policy, budget: float, W: int,
           pool_k: int, bufs: EvictBuffers, scorer: str = "snapkv", scale: float = 0.0,
-          score_events=None, page: int = 16, chunks: int = 1, side_stream=None):
+          score_events=None, page: int = 16, chunks: int = 1, side_stream=None, lse_win=None):
     """One eviction step; returns (quota [B, R] host, kept [B] host).
 
     q is the window queries [L, B, Hq, W, d] (SnapKV; Quest, which scores
@@ -153,7 +156,9 @@ def evict(q, k, v, roles_host: np.ndarray, roles_dev, policy, budget: float, W: 
     (H2O, which uses W = 0 and no pool).  roles_host / roles_dev are the bucket
     labels [B, N] of ``policy`` (a Policy, or the weights of the
     role-conditional policy).  ``score_events``, a pair of torch.cuda.Event,
-    brackets the score calls on the launch stream.
+    brackets the score calls on the launch stream.  ``lse_win`` (SnapKV only),
+    the window rows' log-sum-exp [L, B, Hq, W] as the prefill attention
+    returned it, lets the score read K once.
 
     The quotas depend on the labels only, so they are worked out first.  With
     ``chunks`` > 1 and a ``side_stream``, the layers are scored in that many
@@ -176,7 +181,7 @@ def evict(q, k, v, roles_host: np.ndarray, roles_dev, policy, budget: float, W: 
     if chunks <= 1 or side_stream is None:
         if score_events is not None:
             score_events[0].record()
-        _score(q, k, bufs, scorer, pool_k, scale, page, 0, L)
+        _score(q, k, bufs, scorer, pool_k, scale, page, 0, L, lse_win=lse_win)
         if score_events is not None:
             score_events[1].record()
         _select(k, v, roles_dev, bufs, W, R, 0, L)
@@ -188,7 +193,7 @@ def evict(q, k, v, roles_host: np.ndarray, roles_dev, policy, budget: float, W: 
         score_events[0].record(main)
     for l0 in range(0, L, per):
         l1 = min(L, l0 + per)
-        _score(q, k, bufs, scorer, pool_k, scale, page, l0, l1)
+        _score(q, k, bufs, scorer, pool_k, scale, page, l0, l1, lse_win=lse_win)
         done = torch.cuda.Event()
         done.record(main)
         side_stream.wait_event(done)

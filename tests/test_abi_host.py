@@ -29,7 +29,7 @@ def _declared():
 
 def test_every_declared_symbol_is_exported(kve):
     names = _declared()
-    assert len(names) == 17
+    assert len(names) == 18
     assert sorted(kve.EXPORTED) == names
     lib = ctypes.CDLL(kve.binding._LIB_PATH)
     for n in names:
@@ -144,6 +144,10 @@ def test_device_entry_points_validate_before_launch(kve):
     assert L.kve_snapkv_score(dummy, dummy, 7, 1, 1, 4, 2, 64, 8, 128, 0.0, 7, dummy, dummy, 1 << 30, null) == 2
     assert L.kve_snapkv_score(dummy, dummy, 0, 1, 1, 64, 1, 64, 32, 128, 0.0, 7, dummy, dummy, 1 << 30, null) == 2
     assert "pool_k" in kve.last_error() or kve.last_error()
+    # snapkv with supplied row statistics: null lse_win, and the same checks as the plain score
+    assert L.kve_snapkv_score_lse(dummy, dummy, null, 0, 1, 1, 4, 2, 64, 8, 128, 0.0, 7, dummy, dummy, 1 << 30, null) == 1
+    assert L.kve_snapkv_score_lse(dummy, dummy, dummy, 0, 1, 1, 4, 2, 64, 8, 128, 0.0, 4, dummy, dummy, 1 << 30, null) == 1
+    assert L.kve_snapkv_score_lse(dummy, dummy, dummy, 0, 1, 1, 4, 2, 64, 8, 128, 0.0, 7, dummy, dummy, 16, null) == 3
     # h2o: short workspace, bad dtype
     assert L.kve_h2o_score(dummy, dummy, 0, 1, 1, 4, 2, 64, 128, 0.0, dummy, dummy, 8, null) == 3
     assert L.kve_h2o_score(dummy, dummy, 3, 1, 1, 4, 2, 64, 128, 0.0, dummy, dummy, 1 << 30, null) == 2

@@ -410,6 +410,78 @@ def test_pipeline_full_size_sampled(K, name, budget, segs, pol):
     torch.cuda.empty_cache()
 
 
+def _window_lse_oracle(inp, wl):
+    """The oracle's window-row log-sum-exp of every segment, float32 [L, B, Hq, W]."""
+    L = inp["k"].shape[0]
+    out = np.zeros((L, wl.B, wl.Hq, wl.W), dtype=np.float32)
+    for l, b, j in np.ndindex(L, wl.B, wl.Hkv):
+        out[l, b, j * wl.G:(j + 1) * wl.G] = O.window_lse(f64(inp["q"][l, b, j * wl.G:(j + 1) * wl.G]),
+                                                          f64(inp["k"][l, b, j]))
+    return out
+
+
+@pytest.mark.parametrize("wl", [WL.get_workload("tiny")] + [c for c in SNAP_CASES if c.name in
+                                ("ragged", "g8", "multirange", "f32d128", "wfull", "shorttail", "pool129")],
+                         ids=lambda w: w.name)
+def test_snapkv_score_lse_matches_oracle(K, wl):
+    """With the window rows' statistics supplied (one read of K), the score is
+    the oracle's."""
+    note(f"snapkv with supplied lse {wl.name}")
+    inp = WL.make_inputs(wl, device="cuda", with_v=False)
+    lse = torch.from_numpy(_window_lse_oracle(inp, wl)).cuda()
+    ws = torch.full((K.snapkv_workspace_size(wl.L, wl.B, wl.Hq, wl.Hkv, wl.N, wl.W, wl.d),), 0xFF,
+                    dtype=torch.uint8, device="cuda")
+    sc = K.snapkv_score_lse(inp["q"], inp["k"], lse, wl.pool_k, workspace=ws)
+    torch.cuda.synchronize()
+    ref = O.snapkv_score(f64(inp["q"]), f64(inp["k"]), wl.Hkv, wl.pool_k)
+    for idx in np.ndindex(wl.L, wl.B, wl.Hkv):
+        check_scores(f64(sc[idx]), ref[idx], f"{wl.name} lse seg {idx}")
+
+
+def test_pipeline_with_supplied_lse_full_size(K):
+    """stack32k's launch configuration with the statistics supplied (computed
+    here in float32 by torch, standing in for a prefill attention kernel); the
+    oracle recomputes sampled segments end to end."""
+    from paper_2607_13205_amd import pipeline
+    wl = WL.get_workload("stack32k")
+    note("pipeline stack32k with supplied lse")
+    inp = WL.make_inputs(wl, device="cuda")
+    lse = window_lse_torch(inp["q"], inp["k"], wl)
+    alpha = WL.default_alpha(0.0)
+    _, _, k_cap = K.role_allocate(inp["roles"], 4, alpha, 0.05, wl.W)
+    bufs = pipeline.alloc_buffers(inp["k"], wl.Hq, wl.W, 4, k_cap)
+    quota, kept = pipeline.evict(inp["q"], inp["k"], inp["v"], inp["roles"], inp["roles_t"], alpha, 0.05, wl.W,
+                                 wl.pool_k, bufs, lse_win=lse)
+    torch.cuda.synchronize()
+    for (l, b, j) in [(0, 0, 0), (20, 3, 6)]:
+        kseg = f64(inp["k"][l, b, j])
+        s_ref = O.maxpool_prefix(O.snapkv_mass(f64(inp["q"][l, b, j * wl.G:(j + 1) * wl.G]), kseg), wl.W, wl.pool_k)
+        check_scores(f64(bufs.score[l, b, j]), s_ref, f"stack32k lse seg {(l, b, j)}")
+        n = int(bufs.count[l, b, j])
+        idx_ref = O.select_keep(s_ref, inp["roles"][b], quota[b], wl.W)
+        check_kept_set(bufs.idx[l, b, j, :n].cpu().numpy(), idx_ref, s_ref, inp["roles"][b], wl.W, quota[b])
+    del inp
+    torch.cuda.empty_cache()
+
+
+def window_lse_torch(q, k, wl):
+    """Window-row log-sum-exp [L, B, Hq, W] in float32 on the device, layer by
+    layer (test input only, as a prefill attention kernel would return it)."""
+    L = k.shape[0]
+    out = torch.empty((L, wl.B, wl.Hq, wl.W), dtype=torch.float32, device=k.device)
+    pos = torch.arange(wl.N - wl.W, wl.N, device=k.device)
+    t = torch.arange(wl.N, device=k.device)
+    mask = t[None, :] <= pos[:, None]                                   # [W, N]
+    scale = 1.0 / math.sqrt(wl.d)
+    for l in range(L):
+        qf = q[l].float().reshape(wl.B, wl.Hkv, wl.G * wl.W, wl.d)
+        kf = k[l].float().transpose(-1, -2).contiguous()                 # [B, Hkv, d, N]
+        x = torch.matmul(qf, kf) * scale                                # [B, Hkv, G*W, N]
+        x = x.reshape(wl.B, wl.Hkv, wl.G, wl.W, wl.N).masked_fill(~mask, float("-inf"))
+        out[l] = torch.logsumexp(x, dim=-1).reshape(wl.B, wl.Hq, wl.W)
+    return out
+
+
 # ---------------------------------------------------------------------------
 # Decode through the keep-set over the compacted cache
 # ---------------------------------------------------------------------------
