@@ -151,7 +151,7 @@ kve_status_t snapkv_common(const char* fn, const void* q_win, const void* k, con
     const long long rows = (long long)(Hq / Hkv) * W;
     if (rows > kve::kSnapMaxRows)
         return fail(KVE_ERR_UNSUPPORTED, "%s: G*W=%lld exceeds %d", fn, rows, kve::kSnapMaxRows);
-    const kve::SnapPlan p = kve::snap_plan(L, B, Hq, Hkv, N, W, d);
+    const kve::SnapPlan p = kve::snap_plan(L, B, Hq, Hkv, N, W, d, dtype == KVE_DTYPE_BF16 ? 2 : 4);
     if ((long long)p.n_vsegs * p.nranges > kMaxGrid)
         return fail(KVE_ERR_UNSUPPORTED, "%s: shape too large", fn);
     if (workspace_bytes < p.total || (p.total > 0 && workspace == nullptr))
@@ -175,7 +175,10 @@ const char* kve_last_error(void) { return g_error.c_str(); }
 size_t kve_snapkv_workspace_size(int L, int B, int Hq, int Hkv, int N, int W, int d) {
     if (L <= 0 || B <= 0 || Hq <= 0 || Hkv <= 0 || N <= 0 || W <= 0 || Hq % Hkv != 0) return 0;
     if (d != 64 && d != 128) return 0;
-    return kve::snap_plan(L, B, Hq, Hkv, N, W, d).total;
+    // the layout differs by dtype: enough for either
+    const size_t a = kve::snap_plan(L, B, Hq, Hkv, N, W, d, 2).total;
+    const size_t b = kve::snap_plan(L, B, Hq, Hkv, N, W, d, 4).total;
+    return a > b ? a : b;
 }
 
 kve_status_t kve_snapkv_score(const void* q_win, const void* k, kve_dtype_t dtype, int L, int B,

@@ -10,7 +10,9 @@ inline size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
 // ---------------------------------------------------------------------------
 // SnapKV score: rows of one segment are the G*W window queries (head-major),
-// taken in row groups of 128 (a segment and a row group form a vseg).  Each
+// taken in row groups (a segment and a row group form a vseg) of 128 rows, or
+// of 256 for bf16 when the window has more than 128 rows: a wave then holds
+// two sets of 32 rows, so that K is read once per pass for up to 256 rows.  Each
 // vseg's keys are split into ranges of whole 64-key chunks, one workgroup each;
 // pass 1 writes one log-sum-exp per (vseg, range, row), a combine step reduces
 // them to one per row, pass 2 writes the column sums of each row group (a
@@ -23,16 +25,19 @@ constexpr int kSnapTargetGroups = 4096;  // workgroups per pass the range size a
 constexpr int kSnapMaxRangeChunks = 32;  // at most 2048 keys per range
 
 struct SnapPlan {
-    int segs, rows, rgroups, n_vsegs, range_keys, nranges, planes;
+    int segs, rows, sets, rpg, rgroups, n_vsegs, range_keys, nranges, planes;
     size_t off_stats, off_lse, off_raw, total;
 };
 
-inline SnapPlan snap_plan(int L, int B, int Hq, int Hkv, int N, int W, int d = 128) {
+// elem: bytes per element of the inputs (2 for bf16, 4 for fp32)
+inline SnapPlan snap_plan(int L, int B, int Hq, int Hkv, int N, int W, int d, int elem) {
     (void)d;
     SnapPlan p{};
     p.segs = L * B * Hkv;
     p.rows = (Hq / Hkv) * W;
-    p.rgroups = (p.rows + kSnapRowsPerGroup - 1) / kSnapRowsPerGroup;
+    p.sets = (elem == 2 && p.rows > kSnapRowsPerGroup) ? 2 : 1;  // 32-row sets per wave
+    p.rpg = p.sets * kSnapRowsPerGroup;                           // rows per row group
+    p.rgroups = (p.rows + p.rpg - 1) / p.rpg;
     p.n_vsegs = p.segs * p.rgroups;
     p.planes = p.rgroups;
     // whole chunks per range: about kSnapTargetGroups workgroups per pass (two
@@ -46,9 +51,9 @@ inline SnapPlan snap_plan(int L, int B, int Hq, int Hkv, int N, int W, int d = 1
     p.nranges = (int)((chunks + per - 1) / per);
     size_t off = 0;
     p.off_stats = off;
-    off = align_up(off + (size_t)p.n_vsegs * p.nranges * kSnapRowsPerGroup * sizeof(float));
+    off = align_up(off + (size_t)p.n_vsegs * p.nranges * p.rpg * sizeof(float));
     p.off_lse = off;
-    off = align_up(off + (size_t)p.n_vsegs * kSnapRowsPerGroup * sizeof(float));
+    off = align_up(off + (size_t)p.n_vsegs * p.rpg * sizeof(float));
     p.off_raw = off;
     off = align_up(off + (size_t)p.planes * p.segs * N * sizeof(float));
     p.total = off;

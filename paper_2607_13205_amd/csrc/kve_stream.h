@@ -282,6 +282,40 @@ __device__ __forceinline__ void chunk_mma(f32x16 (&acc)[2], const ChunkReader<T,
     }
 }
 
+// chunk_mma for RS sets of 32 register rows at once: acc[s][b] is register set
+// s against chunk block b, in the layout chunk_mma gives for one set.  Each
+// fragment read from LDS feeds RS products and the 2 RS accumulators are
+// independent chains.  c_init, when given, holds the start value of each set
+// (register rows, !LDS_A); otherwise the products start at zero.
+template <typename T, int D, int KEYS, bool LDS_A, int RS>
+__device__ __forceinline__ void chunk_mma_sets(f32x16 (&acc)[RS][2], const ChunkReader<T, D, KEYS>& rd,
+                                               const char* slot,
+                                               const typename Mma<T>::frag (&reg)[RS][KChunk<T, D, KEYS>::NSTEP],
+                                               const f32x16* c_init) {
+    using M = Mma<T>;
+    constexpr int NS = KChunk<T, D, KEYS>::NSTEP;
+#pragma unroll
+    for (int st = 0; st < NS; ++st) {
+        const typename M::frag f[2] = {rd.get(slot, 0, st), rd.get(slot, 1, st)};
+#pragma unroll
+        for (int rs = 0; rs < RS; ++rs)
+#pragma unroll
+            for (int b = 0; b < 2; ++b) {
+                const f32x16 c = st > 0 ? acc[rs][b] : (c_init != nullptr ? c_init[rs] : f32x16{});
+                acc[rs][b] = LDS_A ? M::mma(f[b], reg[rs][st], c) : M::mma(reg[rs][st], f[b], c);
+            }
+    }
+    if constexpr (ChunkReader<T, D, KEYS>::kTable) {
+        // keep the fragment reads two k-steps ahead of the products
+        __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);  // LDS reads of steps 0, 1
+#pragma unroll
+        for (int st = 0; st < NS; ++st) {
+            __builtin_amdgcn_sched_group_barrier(0x008, 2 * RS, 0);  // products of step st
+            if (st + 2 < NS) __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);  // reads of step st + 2
+        }
+    }
+}
+
 // Running softmax denominator of one row over chunks of 32 logits per lane
 // (x in acc units; sl2 turns them into log2 units).  The reference m is raised
 // only when a chunk's partial sum leaves [0, 2^64] (a logit more than 64 above

@@ -58,6 +58,14 @@ template <>
 struct Tune<__bf16> {
     static constexpr int kRing1 = 2, kOcc1 = 4, kRing2 = 2, kOcc2 = 4;
 };
+// two 32-row sets per wave (bf16, windows of more than 128 rows): twice the
+// query fragments and accumulators, two workgroups per CU, two chunks ahead
+template <typename T, int RS>
+struct TuneRS : Tune<T> {};
+template <typename T>
+struct TuneRS<T, 2> {
+    static constexpr int kRing1 = 3, kOcc1 = 2, kRing2 = 3, kOcc2 = 2;
+};
 
 // Each pass reads every key row once: non-temporal chunk loads (measured 3-4%
 // faster per pass than cached ones on the 32-layer, N = 32768 workload).
@@ -111,12 +119,12 @@ struct KeyChunks {
     }
 };
 
-template <typename T, int D>
-__global__ __launch_bounds__(kThreads, Tune<T>::kOcc1) void snap_pass1(const T* __restrict__ q, const T* __restrict__ k,
-                                                          int N, int W, int rows, int rgroups, int nranges,
-                                                          int range_keys, float sl2,
-                                                          float* __restrict__ stats) {
-    constexpr int kRing = Tune<T>::kRing1;
+template <typename T, int D, int RS>
+__global__ __launch_bounds__(kThreads, (TuneRS<T, RS>::kOcc1)) void snap_pass1(
+    const T* __restrict__ q, const T* __restrict__ k, int N, int W, int rows, int rgroups, int nranges,
+    int range_keys, float sl2, float* __restrict__ stats) {
+    constexpr int kRing = TuneRS<T, RS>::kRing1;
+    constexpr int kRpg = RS * kSnapRowsPerGroup;
     using G = Geo<T, D, kRing>;
     __shared__ __align__(16) char ring[kRing * G::C::BYTES];
     const int lane = threadIdx.x & 63;
@@ -124,10 +132,15 @@ __global__ __launch_bounds__(kThreads, Tune<T>::kOcc1) void snap_pass1(const T* 
     const Span sp = span_of(nranges, rgroups, range_keys, N);
     const int P_rows = N - W;
 
-    QRows<T, D> qf;
-    const int qr = sp.rg * kSnapRowsPerGroup + wave * 32 + (lane & 31);  // this lane's query row
-    load_q<T, D>(qf, q, sp.seg, rows, qr, lane);
-    const int lim = qr < rows ? P_rows + qr % W : -1;  // last key the row sees
+    // wave w holds rows 32 RS w .. 32 RS (w + 1) - 1 of the row group, in RS sets of 32
+    QRows<T, D> qf[RS];
+    int lim[RS];
+#pragma unroll
+    for (int rs = 0; rs < RS; ++rs) {
+        const int qr = sp.rg * kRpg + (wave * RS + rs) * 32 + (lane & 31);  // this lane's query row
+        load_q<T, D>(qf[rs], q, sp.seg, rows, qr, lane);
+        lim[rs] = qr < rows ? P_rows + qr % W : -1;  // last key the row sees
+    }
     typename G::Rd rd;
     rd.init(lane, 0);
     typename G::Ring ring_io;
@@ -136,69 +149,80 @@ __global__ __launch_bounds__(kThreads, Tune<T>::kOcc1) void snap_pass1(const T* 
                               sp.t_end};
     ring_io.prologue(ring, src);
 
-    RowSum rs;
+    RowSum rsum[RS];
     for (int s0 = 0; s0 < sp.nch; s0 += kRing) {
 #pragma unroll
         for (int u = 0; u < kRing; ++u) {
             const int s = s0 + u;
             if (s >= sp.nch) break;
             ring_io.advance(ring, s, u, src);
-            f32x16 acc[2];
-            chunk_mma<T, D, kKeys, true>(acc, rd, ring + u * G::C::BYTES, qf, nullptr, lane);
+            f32x16 acc[RS][2];
+            chunk_mma_sets<T, D, kKeys, true, RS>(acc, rd, ring + u * G::C::BYTES, qf, nullptr);
             if (sp.t_begin + (s + 1) * kKeys > P_rows) {  // keys past the range end or inside the causal window
-                // key of element (kb, i) = base + 32 kb + 8 (i / 4) + i % 4
-                const int last = min(lim, sp.t_end - 1) - (sp.t_begin + s * kKeys + 4 * (lane >> 5));
 #pragma unroll
-                for (int kb = 0; kb < 2; ++kb)
+                for (int rs = 0; rs < RS; ++rs) {
+                    // key of element (kb, i) = base + 32 kb + 8 (i / 4) + i % 4
+                    const int last = min(lim[rs], sp.t_end - 1) - (sp.t_begin + s * kKeys + 4 * (lane >> 5));
 #pragma unroll
-                    for (int i = 0; i < 16; ++i)
-                        if (32 * kb + 8 * (i >> 2) + (i & 3) > last) acc[kb][i] = -INFINITY;
+                    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+                        for (int i = 0; i < 16; ++i)
+                            if (32 * kb + 8 * (i >> 2) + (i & 3) > last) acc[rs][kb][i] = -INFINITY;
+                }
             }
-            rs.add(acc, sl2);
+#pragma unroll
+            for (int rs = 0; rs < RS; ++rs) rsum[rs].add(acc[rs], sl2);
         }
     }
-    // the two lane halves hold the same row and different keys
-    lse2_merge(rs.m, rs.l, __shfl_xor(rs.m, 32), __shfl_xor(rs.l, 32));
-    if (lane < 32) stats[((size_t)sp.vseg * nranges + sp.range) * kSnapRowsPerGroup + wave * 32 + lane] = rs.lse2();
+#pragma unroll
+    for (int rs = 0; rs < RS; ++rs) {
+        // the two lane halves hold the same row and different keys
+        lse2_merge(rsum[rs].m, rsum[rs].l, __shfl_xor(rsum[rs].m, 32), __shfl_xor(rsum[rs].l, 32));
+        if (lane < 32)
+            stats[((size_t)sp.vseg * nranges + sp.range) * kRpg + (wave * RS + rs) * 32 + lane] = rsum[rs].lse2();
+    }
 }
 
-__global__ __launch_bounds__(kSnapRowsPerGroup) void snap_combine(const float* __restrict__ stats, int nranges,
-                                                                  int rows, int rgroups, float* __restrict__ lse) {
-    const int vseg = blockIdx.x, r = threadIdx.x;
-    const int row = (vseg % rgroups) * kSnapRowsPerGroup + r;
+// one thread per row of a row group (rpg = blockDim.x rows)
+__global__ __launch_bounds__(2 * kSnapRowsPerGroup) void snap_combine(const float* __restrict__ stats, int nranges,
+                                                                      int rows, int rgroups,
+                                                                      float* __restrict__ lse) {
+    const int vseg = blockIdx.x, r = threadIdx.x, rpg = blockDim.x;
+    const int row = (vseg % rgroups) * rpg + r;
     float a = -INFINITY, b = 0.0f;
     for (int c = 0; c < nranges; ++c) {
-        const float v = stats[((size_t)vseg * nranges + c) * kSnapRowsPerGroup + r];
+        const float v = stats[((size_t)vseg * nranges + c) * rpg + r];
         lse2_merge(a, b, v, v == -INFINITY ? 0.0f : 1.0f);
     }
     // rows past the window rows contribute nothing to the column sums
-    lse[(size_t)vseg * kSnapRowsPerGroup + r] = (row < rows && b > 0.0f) ? a + log2f(b) : INFINITY;
+    lse[(size_t)vseg * rpg + r] = (row < rows && b > 0.0f) ? a + log2f(b) : INFINITY;
 }
 
 // Row statistics supplied by the caller (the natural-log log-sum-exp of each
 // window row, [segments, G, W] as a prefill attention kernel returns it per
 // query row), turned into the combine step's output: log2 units, rows of the
 // vseg layout, +inf for padding rows.
-__global__ __launch_bounds__(kSnapRowsPerGroup) void snap_import_lse(const float* __restrict__ lse_win, int rows,
-                                                                     int rgroups, float* __restrict__ lse) {
-    const int vseg = blockIdx.x, r = threadIdx.x;
+// one thread per row of a row group (rpg = blockDim.x rows)
+__global__ __launch_bounds__(2 * kSnapRowsPerGroup) void snap_import_lse(const float* __restrict__ lse_win,
+                                                                         int rows, int rgroups,
+                                                                         float* __restrict__ lse) {
+    const int vseg = blockIdx.x, r = threadIdx.x, rpg = blockDim.x;
     const int seg = vseg / rgroups;
-    const int row = (vseg - seg * rgroups) * kSnapRowsPerGroup + r;  // head-major: g * W + i
-    lse[(size_t)vseg * kSnapRowsPerGroup + r] = row < rows ? lse_win[(size_t)seg * rows + row] * kLog2e : INFINITY;
+    const int row = (vseg - seg * rgroups) * rpg + r;  // head-major: g * W + i
+    lse[(size_t)vseg * rpg + r] = row < rows ? lse_win[(size_t)seg * rows + row] * kLog2e : INFINITY;
 }
 
-template <typename T, int D>
-__global__ __launch_bounds__(kThreads, Tune<T>::kOcc2) void snap_pass2(const T* __restrict__ q, const T* __restrict__ k,
-                                                          int N, int W, int rows, int rgroups, int nranges,
-                                                          int range_keys, float sl2,
-                                                          const float* __restrict__ lse, int segs,
-                                                          float* __restrict__ raw) {
-    constexpr int kRing = Tune<T>::kRing2;
+template <typename T, int D, int RS>
+__global__ __launch_bounds__(kThreads, (TuneRS<T, RS>::kOcc2)) void snap_pass2(
+    const T* __restrict__ q, const T* __restrict__ k, int N, int W, int rows, int rgroups, int nranges,
+    int range_keys, float sl2, const float* __restrict__ lse, int segs, float* __restrict__ raw) {
+    constexpr int kRing = TuneRS<T, RS>::kRing2;
+    constexpr int kRpg = RS * kSnapRowsPerGroup;
     using G = Geo<T, D, kRing>;
     __shared__ __align__(16) char ring[kRing * G::C::BYTES];
-    __shared__ float scol[2][kWaves][kKeys];                   // column sums per row block, two chunks
-    __shared__ __align__(16) float sinit[kSnapRowsPerGroup];  // -lse / sl2 of each row
-    __shared__ __align__(16) int swin[kSnapRowsPerGroup];     // window index (row % W) of each row
+    __shared__ float scol[2][kWaves][kKeys];    // column sums per wave, two chunks
+    __shared__ __align__(16) float sinit[kRpg];  // -lse / sl2 of each row
+    __shared__ __align__(16) int swin[kRpg];     // window index (row % W) of each row
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const Span sp = span_of(nranges, rgroups, range_keys, N);
@@ -210,24 +234,30 @@ __global__ __launch_bounds__(kThreads, Tune<T>::kOcc2) void snap_pass2(const T* 
     // exactly 0.  The window index of each row stays in LDS for the masked
     // path: as registers the 32 loop-invariant bounds would stay live across
     // the whole loop.
-    if (threadIdx.x < kSnapRowsPerGroup) {
-        sinit[threadIdx.x] = -lse[(size_t)sp.vseg * kSnapRowsPerGroup + threadIdx.x] / sl2;
-        swin[threadIdx.x] = (sp.rg * kSnapRowsPerGroup + (int)threadIdx.x) % W;
+    for (int r = threadIdx.x; r < kRpg; r += kThreads) {
+        sinit[r] = -lse[(size_t)sp.vseg * kRpg + r] / sl2;
+        swin[r] = (sp.rg * kRpg + r) % W;
     }
-    QRows<T, D> qf;
-    load_q<T, D>(qf, q, sp.seg, rows, sp.rg * kSnapRowsPerGroup + wave * 32 + (lane & 31), lane);
-    __syncthreads();  // sinit, swin written (nothing streams yet)
-    // start values of this lane's 16 rows, the same for every chunk
-    f32x16 c_init;
+    // wave w holds rows 32 RS w .. 32 RS (w + 1) - 1 of the row group, in RS sets of 32
+    QRows<T, D> qf[RS];
 #pragma unroll
-    for (int a = 0; a < 4; ++a) {
-        const float4 v = *reinterpret_cast<const float4*>(&sinit[wave * 32 + c_row(4 * a, lane)]);
-        c_init[4 * a] = v.x;
-        c_init[4 * a + 1] = v.y;
-        c_init[4 * a + 2] = v.z;
-        c_init[4 * a + 3] = v.w;
+    for (int rs = 0; rs < RS; ++rs)
+        load_q<T, D>(qf[rs], q, sp.seg, rows, sp.rg * kRpg + (wave * RS + rs) * 32 + (lane & 31), lane);
+    __syncthreads();  // sinit, swin written (nothing streams yet)
+    // start values of this lane's 16 rows of each set, the same for every chunk
+    f32x16 c_init[RS];
+#pragma unroll
+    for (int rs = 0; rs < RS; ++rs) {
+#pragma unroll
+        for (int a = 0; a < 4; ++a) {
+            const float4 v = *reinterpret_cast<const float4*>(&sinit[(wave * RS + rs) * 32 + c_row(4 * a, lane)]);
+            c_init[rs][4 * a] = v.x;
+            c_init[rs][4 * a + 1] = v.y;
+            c_init[rs][4 * a + 2] = v.z;
+            c_init[rs][4 * a + 3] = v.w;
+        }
+        pin(c_init[rs]);
     }
-    pin(c_init);
     typename G::Rd rd;
     rd.init(lane, 0);
     typename G::Ring ring_io;
@@ -237,8 +267,8 @@ __global__ __launch_bounds__(kThreads, Tune<T>::kOcc2) void snap_pass2(const T* 
     ring_io.prologue(ring, src);
     float* out = raw + ((size_t)sp.rg * segs + sp.seg) * N;
 
-    // add the four row blocks of chunk s (every wave has written it); each wave
-    // adds 16 of the 64 keys and writes them out
+    // add the four waves' column sums of chunk s (every wave has written them);
+    // each wave adds 16 of the 64 keys and writes them out
     auto reduce = [&](int s) {
         if (lane < kKeys / kWaves) {
             const int key = wave * (kKeys / kWaves) + lane;
@@ -256,33 +286,38 @@ __global__ __launch_bounds__(kThreads, Tune<T>::kOcc2) void snap_pass2(const T* 
             // before their sum, and that sum before chunk s + 1 reuses the buffer
             ring_io.advance(ring, s, u, src);
             if (s >= 1) reduce(s - 1);
-            f32x16 acc[2];
-            chunk_mma<T, D, kKeys, false>(acc, rd, ring + u * G::C::BYTES, qf, nullptr, lane, &c_init);
+            f32x16 acc[RS][2];
+            chunk_mma_sets<T, D, kKeys, false, RS>(acc, rd, ring + u * G::C::BYTES, qf, c_init);
             if (sp.t_begin + (s + 1) * kKeys > P_rows) {  // keys past the range end or inside the causal window
                 // key t is visible to window query i (position P_rows + i) iff t - P_rows <= i
 #pragma unroll
-                for (int a = 0; a < 4; ++a) {
-                    const int4 w4 = *reinterpret_cast<const int4*>(&swin[wave * 32 + c_row(4 * a, lane)]);
-                    const int wv[4] = {w4.x, w4.y, w4.z, w4.w};
+                for (int rs = 0; rs < RS; ++rs)
 #pragma unroll
-                    for (int kb = 0; kb < 2; ++kb) {
-                        const int t = sp.t_begin + s * kKeys + 32 * kb + (lane & 31);
+                    for (int a = 0; a < 4; ++a) {
+                        const int4 w4 = *reinterpret_cast<const int4*>(&swin[(wave * RS + rs) * 32 + c_row(4 * a, lane)]);
+                        const int wv[4] = {w4.x, w4.y, w4.z, w4.w};
 #pragma unroll
-                        for (int e = 0; e < 4; ++e)
-                            if (!(t < sp.t_end && t - P_rows <= wv[e])) acc[kb][4 * a + e] = -INFINITY;
+                        for (int kb = 0; kb < 2; ++kb) {
+                            const int t = sp.t_begin + s * kKeys + 32 * kb + (lane & 31);
+#pragma unroll
+                            for (int e = 0; e < 4; ++e)
+                                if (!(t < sp.t_end && t - P_rows <= wv[e])) acc[rs][kb][4 * a + e] = -INFINITY;
+                        }
                     }
-                }
             }
-            // exponentials of each key block: a lane sum over its 16 rows and
-            // one shuffle for the other 16
+            // exponentials of each key block: a lane sum over its 16 rows per set
+            // and one shuffle for the other 16
 #pragma unroll
             for (int kb = 0; kb < 2; ++kb) {
+                float c = 0.0f;
 #pragma unroll
-                for (int i = 0; i < 16; ++i) acc[kb][i] = fast_exp2(acc[kb][i] * sl2);
-                const float c = ((acc[kb][0] + acc[kb][1]) + (acc[kb][2] + acc[kb][3]) +
-                                 ((acc[kb][4] + acc[kb][5]) + (acc[kb][6] + acc[kb][7]))) +
-                                (((acc[kb][8] + acc[kb][9]) + (acc[kb][10] + acc[kb][11])) +
-                                 ((acc[kb][12] + acc[kb][13]) + (acc[kb][14] + acc[kb][15])));
+                for (int rs = 0; rs < RS; ++rs) {
+                    f32x16& x = acc[rs][kb];
+#pragma unroll
+                    for (int i = 0; i < 16; ++i) x[i] = fast_exp2(x[i] * sl2);
+                    c += ((x[0] + x[1]) + (x[2] + x[3]) + ((x[4] + x[5]) + (x[6] + x[7]))) +
+                         (((x[8] + x[9]) + (x[10] + x[11])) + ((x[12] + x[13]) + (x[14] + x[15])));
+                }
                 const float v = c + __shfl_xor(c, 32);
                 if (lane < 32) scol[s & 1][wave][32 * kb + lane] = v;
             }
@@ -375,10 +410,27 @@ __global__ __launch_bounds__(kThreads) void snap_pool(const float* __restrict__ 
     }
 }
 
+template <typename T, int D, int RS>
+void launch_passes(const T* qt, const T* kt, const float* lse_win, const SnapPlan& p, int N, int W, float sl2,
+                   float* stats, float* lse, float* raw, hipStream_t st) {
+    const dim3 grid((unsigned)((size_t)p.n_vsegs * p.nranges));
+    if (lse_win != nullptr) {  // row statistics from the caller: one read of K
+        hipLaunchKernelGGL(snap_import_lse, dim3((unsigned)p.n_vsegs), dim3(p.rpg), 0, st, lse_win, p.rows,
+                           p.rgroups, lse);
+    } else {
+        hipLaunchKernelGGL((snap_pass1<T, D, RS>), grid, dim3(kThreads), 0, st, qt, kt, N, W, p.rows, p.rgroups,
+                           p.nranges, p.range_keys, sl2, stats);
+        hipLaunchKernelGGL(snap_combine, dim3((unsigned)p.n_vsegs), dim3(p.rpg), 0, st, stats, p.nranges, p.rows,
+                           p.rgroups, lse);
+    }
+    hipLaunchKernelGGL((snap_pass2<T, D, RS>), grid, dim3(kThreads), 0, st, qt, kt, N, W, p.rows, p.rgroups,
+                       p.nranges, p.range_keys, sl2, lse, p.segs, raw);
+}
+
 template <typename T, int D>
 hipError_t run_snapkv(const void* q, const void* k, const float* lse_win, int L, int B, int Hq, int Hkv, int N,
                       int W, float scale, int pool_k, float* score, void* ws, hipStream_t st) {
-    const SnapPlan p = snap_plan(L, B, Hq, Hkv, N, W, D);
+    const SnapPlan p = snap_plan(L, B, Hq, Hkv, N, W, D, (int)sizeof(T));
     char* w = static_cast<char*>(ws);
     float* stats = reinterpret_cast<float*>(w + p.off_stats);
     float* lse = reinterpret_cast<float*>(w + p.off_lse);
@@ -386,21 +438,17 @@ hipError_t run_snapkv(const void* q, const void* k, const float* lse_win, int L,
     const float sl2 = scale * kLog2e;
     const T* qt = static_cast<const T*>(q);
     const T* kt = static_cast<const T*>(k);
-    const dim3 grid((unsigned)((size_t)p.n_vsegs * p.nranges));
-    if (lse_win != nullptr) {  // row statistics from the caller: one read of K
-        hipLaunchKernelGGL(snap_import_lse, dim3((unsigned)p.n_vsegs), dim3(kSnapRowsPerGroup), 0, st, lse_win,
-                           p.rows, p.rgroups, lse);
+    if constexpr (sizeof(T) == 2) {
+        if (p.sets == 2)
+            launch_passes<T, D, 2>(qt, kt, lse_win, p, N, W, sl2, stats, lse, raw, st);
+        else
+            launch_passes<T, D, 1>(qt, kt, lse_win, p, N, W, sl2, stats, lse, raw, st);
     } else {
-        hipLaunchKernelGGL((snap_pass1<T, D>), grid, dim3(kThreads), 0, st, qt, kt, N, W, p.rows, p.rgroups,
-                           p.nranges, p.range_keys, sl2, stats);
-        hipLaunchKernelGGL(snap_combine, dim3((unsigned)p.n_vsegs), dim3(kSnapRowsPerGroup), 0, st, stats,
-                           p.nranges, p.rows, p.rgroups, lse);
+        launch_passes<T, D, 1>(qt, kt, lse_win, p, N, W, sl2, stats, lse, raw, st);
     }
-    hipLaunchKernelGGL((snap_pass2<T, D>), grid, dim3(kThreads), 0, st, qt, kt, N, W, p.rows, p.rgroups,
-                       p.nranges, p.range_keys, sl2, lse, p.segs, raw);
     const int tiles = (N + kPoolTile - 1) / kPoolTile;
-    hipLaunchKernelGGL(snap_pool, dim3((unsigned)(p.segs * tiles)), dim3(kThreads), 0, st, raw, p.planes,
-                       p.segs, N, W, pool_k, tiles, score);
+    hipLaunchKernelGGL(snap_pool, dim3((unsigned)(p.segs * tiles)), dim3(kThreads), 0, st, raw, p.planes, p.segs, N,
+                       W, pool_k, tiles, score);
     return hipGetLastError();
 }
 
