@@ -72,6 +72,8 @@ SNAP_CASES = [
     custom("pool131", 1, 2, 8, 4, 5000, 16, 128, 131, "bf16"),
     # a last range of 6 keys, shorter than the half-width 7
     custom("shorttail", 1, 1, 4, 2, 1030, 8, 64, 15, "bf16"),
+    # 300 window rows: two 256-row groups, the second with 44 rows and 212 padding rows
+    custom("rows300", 1, 2, 12, 2, 3000, 50, 128, 7, "bf16"),
 ]
 
 
@@ -421,7 +423,7 @@ def _window_lse_oracle(inp, wl):
 
 
 @pytest.mark.parametrize("wl", [WL.get_workload("tiny")] + [c for c in SNAP_CASES if c.name in
-                                ("ragged", "g8", "multirange", "f32d128", "wfull", "shorttail", "pool129")],
+                                ("ragged", "g8", "multirange", "f32d128", "wfull", "shorttail", "pool129", "rows300")],
                          ids=lambda w: w.name)
 def test_snapkv_score_lse_matches_oracle(K, wl):
     """With the window rows' statistics supplied (one read of K), the score is
