@@ -289,7 +289,9 @@ kve_status_t kve_role_probe(const int32_t* ids, int B, int N, const float* weigh
 /* Per-role top-k selection (Algorithm 1, per-bucket top-k).                  */
 /* ------------------------------------------------------------------------- */
 
-/* Workspace bytes kve_topk_select needs for these shapes. */
+/* Workspace bytes kve_topk_select needs for these shapes: 8 bytes per
+ * position of every segment, L*B*Hkv*N*8 rounded up to 256 (0 when a size is
+ * not positive). */
 size_t kve_topk_workspace_size(int L, int B, int Hkv, int N, int R);
 
 /*
@@ -309,6 +311,14 @@ size_t kve_topk_workspace_size(int L, int B, int Hkv, int N, int R);
  *             of each segment.  A value above k_cap means the output was
  *             truncated to its first k_cap indices (the caller's k_cap was too
  *             small for the quotas it passed).
+ *   workspace kve_topk_workspace_size bytes, 256-byte aligned, owned by the
+ *             caller: each segment's surely kept positions and threshold-bin
+ *             candidates, staged in order; contents on entry do not matter.
+ *
+ * Enqueued on `stream`.  Errors: KVE_ERR_INVALID_ARG (null pointers,
+ * non-positive sizes, W outside [0, N], R outside [1, 8], k_cap < 0,
+ * misaligned workspace), KVE_ERR_UNSUPPORTED (too many segments, N > 2^30),
+ * KVE_ERR_WORKSPACE (workspace missing or too small), KVE_ERR_HIP.
  */
 kve_status_t kve_topk_select(const float* score, const int8_t* roles, const int32_t* quota,
                              int L, int B, int Hkv, int N, int W, int R, int k_cap,

@@ -289,8 +289,12 @@ def role_map(roles, bucket_of):
     return out
 
 
+def topk_workspace_size(L, B, Hkv, N, R) -> int:
+    return int(LIB.kve_topk_workspace_size(L, B, Hkv, N, R))
+
+
 def topk_select(score, roles, quota, W: int, R: int, k_cap: int, idx_out=None, count_out=None,
-                stream=None):
+                workspace=None, stream=None):
     """Ascending kept indices [L, B, Hkv, k_cap] and per-segment counts [L, B, Hkv]."""
     torch = _torch()
     L, B, Hkv, N = score.shape
@@ -302,10 +306,11 @@ def topk_select(score, roles, quota, W: int, R: int, k_cap: int, idx_out=None, c
         idx_out = torch.full((L, B, Hkv, max(k_cap, 0)), -1, dtype=torch.int32, device=score.device)
     if count_out is None:
         count_out = torch.empty((L, B, Hkv), dtype=torch.int32, device=score.device)
+    ws, wsb = _workspace(topk_workspace_size(L, B, Hkv, N, R), score.device, workspace)
     _check(LIB.kve_topk_select(_dev(score, "score"), _dev(roles, "roles"), _dev(quota, "quota"),
                                L, B, Hkv, N, int(W), int(R), int(k_cap),
                                _dev(idx_out, "idx_out"), _dev(count_out, "count_out"),
-                               None, 0, _stream(stream)))
+                               _ptr(ws), wsb, _stream(stream)))
     return idx_out, count_out
 
 

@@ -374,20 +374,16 @@ kve_status_t kve_role_probe(const int32_t* ids, int B, int N, const float* weigh
 }
 
 size_t kve_topk_workspace_size(int L, int B, int Hkv, int N, int R) {
-    (void)L;
-    (void)B;
-    (void)Hkv;
-    (void)N;
     (void)R;
-    return 0;
+    if (L <= 0 || B <= 0 || Hkv <= 0 || N <= 0) return 0;
+    // one staged (position, tag) pair of 8 bytes per position of every segment
+    return kve::align_up((size_t)L * B * Hkv * N * 8);
 }
 
 kve_status_t kve_topk_select(const float* score, const int8_t* roles, const int32_t* quota, int L,
                              int B, int Hkv, int N, int W, int R, int k_cap, int32_t* idx_out,
                              int32_t* count_out, void* workspace, size_t workspace_bytes,
                              void* stream) {
-    (void)workspace;
-    (void)workspace_bytes;
     const char* fn = "kve_topk_select";
     if (score == nullptr || roles == nullptr || quota == nullptr)
         return fail(KVE_ERR_INVALID_ARG, "%s: null pointer", fn);
@@ -399,8 +395,12 @@ kve_status_t kve_topk_select(const float* score, const int8_t* roles, const int3
     if (k_cap > 0 && idx_out == nullptr) return fail(KVE_ERR_INVALID_ARG, "%s: null idx_out", fn);
     if ((long long)L * B * Hkv > kMaxGrid || N > (1 << 30))
         return fail(KVE_ERR_UNSUPPORTED, "%s: shape too large", fn);
+    const size_t need = kve_topk_workspace_size(L, B, Hkv, N, R);
+    if (workspace_bytes < need || workspace == nullptr)
+        return fail(KVE_ERR_WORKSPACE, "%s: workspace of %zu bytes < %zu needed", fn, workspace_bytes, need);
+    if (!aligned(workspace)) return fail(KVE_ERR_INVALID_ARG, "%s: workspace not 256-byte aligned", fn);
     return from_hip(kve::launch_topk(score, roles, quota, L, B, Hkv, N, W, R, k_cap, idx_out, count_out,
-                                     static_cast<hipStream_t>(stream)),
+                                     workspace, static_cast<hipStream_t>(stream)),
                     fn);
 }
 

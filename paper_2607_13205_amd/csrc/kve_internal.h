@@ -103,7 +103,7 @@ hipError_t launch_h2o(const void* q, const void* k, int dtype, int L, int B, int
 
 hipError_t launch_topk(const float* score, const int8_t* roles, const int32_t* quota, int L,
                        int B, int Hkv, int N, int W, int R, int k_cap, int32_t* idx_out,
-                       int32_t* count_out, hipStream_t st);
+                       int32_t* count_out, void* ws, hipStream_t st);
 
 hipError_t launch_decode(const void* q, const void* kc, const void* vc, const int32_t* count, int dtype, int L,
                          int B, int Hq, int Hkv, int k_cap, int d, float scale, float* out, void* ws,

@@ -3,25 +3,29 @@
 // dense cache of a compacting implementation).
 //
 // topk_select: one workgroup per (layer, sample, KV head) segment.  Scores are
-// mapped to order-preserving 32-bit keys (-0 -> +0, NaN lowest).
-//   1. Three most-significant-digit passes (11, 11 and 10 bits), all buckets
-//      at once with one LDS histogram per bucket, fix the key of the quota-th
-//      largest candidate (the threshold) and how many candidates equal to it
-//      stay.  The first digit holds the sign and all exponent bits, so float
-//      scores spread over its bins; the first histogram also gives each
-//      bucket's population, which decides whether the bucket is kept whole,
-//      skipped, or selected.  The digit is found by all threads at once (a
-//      scan over groups of bins).
-//   2. Each wave owns a contiguous quarter of the positions and walks it 64
-//      positions at a time: per-lane counts give what each wave run keeps
-//      (keys above the threshold, the window, whole buckets, and keys equal to
-//      the threshold lowest index first); ballots then rank the kept positions
-//      so that they come out in ascending order.
-// The sweeps read 16 positions per thread before they use any, so that the
-// memory latency is paid once per group and not once per key; the loads are
-// unconditional (clamped to a valid position) so that none waits behind a
-// branch.
-#include <type_traits>
+// mapped to order-preserving 32-bit keys (-0 -> +0, NaN lowest).  Two sweeps
+// read the segment's scores and labels:
+//   1. Histogram sweep: the top 11 bits of every labelled candidate's key (sign,
+//      exponent and two mantissa bits), one LDS histogram per bucket.  Per
+//      bucket this gives the population, which decides whether the bucket is
+//      kept whole, skipped or selected, and the top digit of the quota-th
+//      largest key: the threshold's bin.
+//   2. Staging sweep: each wave walks a contiguous quarter of the positions in
+//      order and sets aside, in order, every position that is surely kept (the
+//      window, whole buckets, keys above the threshold's bin) and every key
+//      inside the bin (with its bucket and the low 21 bits of its key), in its
+//      own part of the segment's workspace row (a position is staged at most
+//      once, so a wave's part never overflows).
+// Two more digit passes (11 and 10 bits) over the staged keys of the bins fix
+// each bucket's threshold key and how many keys equal to it stay; each wave
+// then walks its staged entries twice: it counts what it keeps (keys equal to
+// a threshold are kept lowest position first, so the earlier waves' counts
+// come first), then writes the kept positions in ascending order.
+// In the sweeps a lane takes 16 consecutive positions per step: four 16-byte
+// score loads and one 16-byte label load when the rows are 16-byte aligned,
+// one load per position otherwise.  Bucket state is looked up per key in small
+// LDS tables rather than picked from registers with a chain of selects.
+#include <stdint.h>
 
 #include "kve_device.h"
 #include "kve_internal.h"
@@ -34,7 +38,14 @@ constexpr int kWaves = kThreads / kWave;
 constexpr int kMaxR = 8;  // buckets supported (one kernel instantiation each)
 constexpr int kDigitBits = 11;
 constexpr int kDigits = 1 << kDigitBits;
-constexpr int kBatch = 16;
+constexpr int kLowBits = 32 - kDigitBits;  // key bits below the top digit
+constexpr uint32_t kLowMask = (1u << kLowBits) - 1u;
+constexpr int kSpan = 16;                     // consecutive positions per lane and step
+constexpr int kGroupStep = kThreads * kSpan;  // positions per workgroup step
+constexpr int kWaveStep = kWave * kSpan;      // positions per wave step
+constexpr int kBatch = 8;                     // staged entries per lane loaded before use
+constexpr uint32_t kNoKey = 0xffffffffu;      // above every key (+inf maps to 0xff800000)
+constexpr uint32_t kKept = 0xffffffffu;       // tag of a staged position that is surely kept
 
 enum : int { kModeNone = 0, kModeSelect = 1, kModeAll = 2 };
 
@@ -45,8 +56,11 @@ struct TopkShared {
     int lo[R];         // lowest fixed bit; 0 once the threshold is known
     int need[R];       // still to take among keys matching the prefix
     int mode[R];
-    int wave_eq[kWaves][R];  // equal-to-threshold candidates per wave run
-    int wave_keep[kWaves];       // kept positions per wave run
+    // staging: {lowest surely kept key, top digit of the threshold's bin} per
+    // bucket; entry R (labels outside [0, R)) is never kept and never staged
+    uint2 stage_cls[R + 1];
+    int wave_eq[kWaves][R];  // staged keys equal to a threshold, per wave
+    int wave_keep[kWaves];   // kept positions per wave
     int scan[kWaves];
 };
 
@@ -74,13 +88,113 @@ __device__ __forceinline__ int block_exclusive_scan(int v, int* tmp, int& total)
     return before + incl - v;
 }
 
+// Exclusive prefix sum over the lanes of a wave of v in [0, 31] (lane order),
+// and the wave's total: one ballot per bit.
+__device__ __forceinline__ int wave_exclusive_scan(int v, int& total) {
+    int excl = 0;
+    total = 0;
+#pragma unroll
+    for (int bit = 0; bit < 5; ++bit) {
+        const uint64_t m = __ballot((v >> bit) & 1);
+        excl += (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u))
+                << bit;
+        total += __popcll(m) << bit;
+    }
+    return excl;
+}
+
+// Digit search of one pass for bucket r, every thread at once: thread tid holds
+// kPerThread bins from the top going down; a scan gives the count of keys in
+// all higher bins, and the thread whose bins reach the wanted rank fixes the
+// digit.  In the first pass (quota >= 0) the population decides whether the
+// bucket is kept whole, skipped, or selected.  Every thread calls it.
 template <int R>
+__device__ __forceinline__ void find_digit(TopkShared<R>& sh, int r, int quota) {
+    constexpr int kPerThread = kDigits / kThreads;
+    const int tid = threadIdx.x;
+    // read before the scan's barriers: the thread that finds the digit rewrites them
+    int want = sh.need[r];
+    const int lo = sh.lo[r];
+    const int hi = kDigits - kPerThread * tid;  // bins [hi - kPerThread, hi)
+    int mine = 0;
+#pragma unroll
+    for (int e = 1; e <= kPerThread; ++e) mine += (int)sh.hist[r][hi - e];
+    int total;
+    const int above = block_exclusive_scan(mine, sh.scan, total);
+    if (quota >= 0) {
+        if (quota == 0 || quota >= total) {
+            if (tid == 0) sh.mode[r] = quota == 0 ? kModeNone : kModeAll;
+            __syncthreads();
+            return;
+        }
+        want = quota;
+    }
+    if (above < want && above + mine >= want) {  // exactly one thread
+        const int w = min(kDigitBits, lo);
+        int cum = above, dgt = hi - 1;
+        for (; dgt > hi - kPerThread; --dgt) {
+            const int h = (int)sh.hist[r][dgt];
+            if (cum + h >= want) break;
+            cum += h;
+        }
+        sh.pref[r] = (lo < 32 ? sh.pref[r] << w : 0u) | (uint32_t)dgt;
+        sh.need[r] = want - cum;
+        sh.lo[r] = lo - w;
+    }
+    __syncthreads();
+}
+
+// Scores and labels of positions t0 .. t0 + 15 (label of t0 + 4 j + i: byte i
+// of lab[j]).  VEC: t0 is a multiple of 16, the span lies inside the row and
+// rows are 16-byte aligned; otherwise one load per position, the position
+// clamped to [0, n).
+template <bool VEC>
+__device__ __forceinline__ void load_span(const float* sc, const int8_t* ro, int t0, int n, float (&s)[kSpan],
+                                          uint32_t (&lab)[4]) {
+    if constexpr (VEC) {
+        const u32x4* sp = reinterpret_cast<const u32x4*>(sc + t0);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const u32x4 v = sp[j];
+            s[4 * j] = __uint_as_float(v.x);
+            s[4 * j + 1] = __uint_as_float(v.y);
+            s[4 * j + 2] = __uint_as_float(v.z);
+            s[4 * j + 3] = __uint_as_float(v.w);
+        }
+        const u32x4 l = *reinterpret_cast<const u32x4*>(ro + t0);
+        lab[0] = l.x;
+        lab[1] = l.y;
+        lab[2] = l.z;
+        lab[3] = l.w;
+    } else {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            uint32_t w = 0u;
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int t = min(t0 + 4 * j + i, n - 1);
+                s[4 * j + i] = sc[t];
+                w |= (uint32_t)(uint8_t)ro[t] << (8 * i);
+            }
+            lab[j] = w;
+        }
+    }
+}
+
+// bucket of the label of position t0 + e; R for labels outside [0, R)
+template <int R>
+__device__ __forceinline__ uint32_t bucket_of(const uint32_t (&lab)[4], int e) {
+    return min((lab[e >> 2] >> (8 * (e & 3))) & 0xffu, (uint32_t)R);
+}
+
+template <int R, bool VEC>
 __global__ __launch_bounds__(kThreads) void topk_kernel(const float* __restrict__ score,
                                                         const int8_t* __restrict__ roles,
                                                         const int32_t* __restrict__ quota, int B,
                                                         int Hkv, int N, int W, int k_cap,
                                                         int32_t* __restrict__ idx_out,
-                                                        int32_t* __restrict__ count_out) {
+                                                        int32_t* __restrict__ count_out,
+                                                        uint2* __restrict__ stage) {
     __shared__ TopkShared<R> sh;
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -96,166 +210,130 @@ __global__ __launch_bounds__(kThreads) void topk_kernel(const float* __restrict_
         sh.lo[tid] = 32;
         sh.need[tid] = 0;
     }
+    for (int e = tid; e < R * kDigits; e += kThreads) (&sh.hist[0][0])[e] = 0u;
     __syncthreads();
 
-    // 1. radix passes over the keys, all buckets at once: digits of 11, 11 and
-    //    10 bits from the top; the first covers the sign and exponent bits
-    for (int pass = 0; pass < (32 + kDigitBits - 1) / kDigitBits; ++pass) {
+    // 1. histogram sweep: the top digit of every labelled candidate's key
+    for (int base = 0; base < P; base += kGroupStep) {
+        const int t0 = base + kSpan * tid;
+        if (t0 < P) {
+            float s[kSpan];
+            uint32_t lab[4];
+            load_span<VEC>(sc, ro, t0, N, s, lab);
+            const int nv = min(kSpan, P - t0);
+#pragma unroll
+            for (int e = 0; e < kSpan; ++e) {
+                const uint32_t r = bucket_of<R>(lab, e);
+                if (e < nv && r < (uint32_t)R) atomicAdd(&sh.hist[r][score_key(s[e]) >> kLowBits], 1u);
+            }
+        }
+    }
+    __syncthreads();
+    for (int r = 0; r < R; ++r) find_digit(sh, r, max(quota[(size_t)b * R + r], 0));
+    if (tid <= R) {
+        uint2 c = make_uint2(kNoKey, kNoKey);
+        if (tid < R && sh.mode[tid] == kModeAll) c.x = 0u;
+        if (tid < R && sh.mode[tid] == kModeSelect) {
+            // top digits are at most +inf's 0x7fc, so the shift does not overflow
+            c.x = (sh.pref[tid] + 1u) << kLowBits;
+            c.y = sh.pref[tid];
+        }
+        sh.stage_cls[tid] = c;
+    }
+    __syncthreads();
+
+    // 2. staging sweep over this wave's run [w0, w1), in order
+    const int run = (N + kWaves * kWaveStep - 1) / (kWaves * kWaveStep) * kWaveStep;
+    const int w0 = min(N, wave * run), w1 = min(N, w0 + run);
+    uint2* st = stage + (size_t)seg * N + w0;  // room for w1 - w0 entries
+    int n_st = 0;
+    for (int s0 = w0; s0 < w1; s0 += kWaveStep) {
+        const int t0 = s0 + kSpan * lane;
+        const int nv = max(0, min(kSpan, w1 - t0));
+        float s[kSpan];
+        uint32_t lab[4];
+        // lanes past the run load an in-bounds span and stage nothing
+        load_span<VEC>(sc, ro, VEC ? min(t0, N - kSpan) : t0, N, s, lab);
+        uint32_t smask = 0u, tag[kSpan];
+#pragma unroll
+        for (int e = 0; e < kSpan; ++e) {
+            const int t = t0 + e;
+            const uint32_t key = score_key(s[e]);
+            const uint32_t r = t < P ? bucket_of<R>(lab, e) : (uint32_t)R;
+            const uint2 c = sh.stage_cls[r];
+            const bool keep = t >= P || key >= c.x;
+            const bool cand = (key >> kLowBits) == c.y;
+            tag[e] = keep ? kKept : ((r << kLowBits) | (key & kLowMask));
+            smask |= (e < nv && (keep || cand)) ? (1u << e) : 0u;
+        }
+        int tot;
+        uint2* dst = st + n_st + wave_exclusive_scan(__popc(smask), tot);
+#pragma unroll
+        for (int e = 0; e < kSpan; ++e)
+            if ((smask >> e) & 1u) *dst++ = make_uint2((uint32_t)(t0 + e), tag[e]);
+        n_st += tot;
+    }
+    __syncthreads();
+
+    // the staged entries of this wave, kBatch per lane loaded before any is used;
+    // visit(position, tag) for every entry in order, (0, kKept) with valid =
+    // false past the end (every lane takes part in every step)
+    auto sweep_staged = [&](auto&& visit) {
+        for (int i0 = 0; i0 < n_st; i0 += kWave * kBatch) {
+            uint2 ent[kBatch];
+#pragma unroll
+            for (int j = 0; j < kBatch; ++j) ent[j] = st[min(i0 + j * kWave + lane, n_st - 1)];
+#pragma unroll
+            for (int j = 0; j < kBatch; ++j) visit(ent[j].x, ent[j].y, i0 + j * kWave + lane < n_st);
+        }
+    };
+    // full key of a staged key of a threshold bin
+    auto bin_key = [&](uint32_t tg, uint32_t& r) {
+        r = tg >> kLowBits;
+        return (sh.stage_cls[r].y << kLowBits) | (tg & kLowMask);
+    };
+
+    // 3. the remaining digits (11 and 10 bits) over the staged keys of the bins
+    for (int pass = 1; pass < 3; ++pass) {
         bool any = false;
 #pragma unroll
         for (int r = 0; r < R; ++r) any |= sh.mode[r] == kModeSelect && sh.lo[r] > 0;
         if (!any) break;  // uniform: every thread reads the same LDS values
         for (int e = tid; e < R * kDigits; e += kThreads) (&sh.hist[0][0])[e] = 0u;
         __syncthreads();
-        // every bucket's state in registers; a key is counted when it matches
-        // its bucket's prefix, the bucket picked with selects (no branches)
-        bool act[R];
-        uint32_t pf[R];
-        int lov[R];
-#pragma unroll
-        for (int r = 0; r < R; ++r) {
-            act[r] = sh.mode[r] == kModeSelect && sh.lo[r] > 0;
-            pf[r] = sh.pref[r];
-            lov[r] = sh.lo[r];
-        }
-        // the first pass counts every labelled candidate on its top digit (no
-        // prefix yet, every bucket still selecting); the later ones only the
-        // keys that match their bucket's prefix
-        auto count_keys = [&](auto first) {
-            for (int t00 = tid; t00 < P; t00 += kThreads * kBatch) {
-                int rv[kBatch];
-                float sv[kBatch];
-#pragma unroll
-                for (int e = 0; e < kBatch; ++e) {  // unconditional loads (clamped index), then the bound
-                    const int t = t00 + e * kThreads;
-                    const int tc = min(t, P - 1);
-                    const int r = ro[tc];
-                    sv[e] = sc[tc];
-                    rv[e] = t < P ? r : -1;
-                }
-#pragma unroll
-                for (int e = 0; e < kBatch; ++e) {
-                    const int r = rv[e];
-                    const uint32_t key = score_key(sv[e]);
-                    if constexpr (decltype(first)::value) {
-                        if ((unsigned)r < (unsigned)R) atomicAdd(&sh.hist[r][key >> (32 - kDigitBits)], 1u);
-                    } else {
-                        bool a = false;
-                        uint32_t p = 0u;
-                        int lo = 32;
-#pragma unroll
-                        for (int q = 0; q < R; ++q) {
-                            a = r == q ? act[q] : a;
-                            p = r == q ? pf[q] : p;
-                            lo = r == q ? lov[q] : lo;
-                        }
-                        a = a && (lo >= 32 || (key >> lo) == p);
-                        const int w = min(kDigitBits, lo);
-                        if (a) atomicAdd(&sh.hist[r][(key >> (lo - w)) & ((1u << w) - 1u)], 1u);
-                    }
-                }
+        const int lo = 32 - kDigitBits * pass;  // the same for every selecting bucket
+        const int w = min(kDigitBits, lo);
+        sweep_staged([&](uint32_t, uint32_t tg, bool valid) {
+            if (valid && tg != kKept) {
+                uint32_t r;
+                const uint32_t key = bin_key(tg, r);
+                if ((key >> lo) == sh.pref[r]) atomicAdd(&sh.hist[r][(key >> (lo - w)) & ((1u << w) - 1u)], 1u);
             }
-        };
-        if (pass == 0)
-            count_keys(std::true_type{});
-        else
-            count_keys(std::false_type{});
+        });
         __syncthreads();
-        // Digit search, every thread at once: thread tid holds the kPerThread
-        // bins from the top going down; a scan gives the count of keys in all
-        // higher bins, and the thread whose bins reach `want` finds the digit.
-        // After the first histogram (the bucket's whole population) the bucket
-        // is kept whole, skipped, or selected.
-#pragma unroll 1
-        for (int r = 0; r < R; ++r) {
-            if (!(sh.mode[r] == kModeSelect && sh.lo[r] > 0)) continue;  // uniform
-            constexpr int kPerThread = kDigits / kThreads;
-            const int hi = kDigits - kPerThread * tid;  // bins [hi - kPerThread, hi)
-            int mine = 0;
-#pragma unroll
-            for (int e = 1; e <= kPerThread; ++e) mine += (int)sh.hist[r][hi - e];
-            int total;
-            const int above = block_exclusive_scan(mine, sh.scan, total);
-            int want = sh.need[r];
-            if (pass == 0) {
-                const int q = max(quota[(size_t)b * R + r], 0);
-                if (q == 0 || q >= total) {
-                    if (tid == 0) sh.mode[r] = q == 0 ? kModeNone : kModeAll;
-                    __syncthreads();
-                    continue;
-                }
-                want = q;
-            }
-            if (above < want && above + mine >= want) {  // exactly one thread
-                const int lo = sh.lo[r], w = min(kDigitBits, lo);
-                int cum = above, dgt = hi - 1;
-                for (; dgt > hi - kPerThread; --dgt) {
-                    const int h = (int)sh.hist[r][dgt];
-                    if (cum + h >= want) break;
-                    cum += h;
-                }
-                sh.pref[r] = (lo < 32 ? sh.pref[r] << w : 0u) | (uint32_t)dgt;
-                sh.need[r] = want - cum;
-                sh.lo[r] = lo - w;
-            }
-            __syncthreads();
-        }
+        for (int r = 0; r < R; ++r)
+            if (sh.mode[r] == kModeSelect && sh.lo[r] > 0) find_digit(sh, r, -1);  // uniform
     }
 
-    // 2. ordered output over wave runs [w0, w1), 64 positions per step
-    int mode[R], need[R];
-    uint32_t th[R];  // threshold key of each selecting bucket
+    // 4. ordered output.  Class of a staged entry: 1 kept, 2 + r equal to bucket
+    //    r's threshold, 0 dropped.
+    int need[R];
 #pragma unroll
-    for (int r = 0; r < R; ++r) {
-        mode[r] = sh.mode[r];
-        th[r] = sh.pref[r];
-        need[r] = mode[r] == kModeSelect ? sh.need[r] : 0;
-    }
-    const int run = (N + kWaves * kWave - 1) / (kWaves * kWave) * kWave;  // positions per wave, whole steps
-    const int w0 = min(N, wave * run), w1 = min(N, w0 + run);
-    // class of position t: 1 kept, 2 + r equal to the threshold of bucket r, 0
-    // dropped; the bucket's mode and threshold are picked with selects (a
-    // branch per bucket would cost every key a divergent branch)
-    auto classify = [&](int t, int r, float x) {
-        int m = kModeNone;
-        uint32_t thr = 0u;
-#pragma unroll
-        for (int q = 0; q < R; ++q) {
-            m = r == q ? mode[q] : m;
-            thr = r == q ? th[q] : thr;
-        }
-        const uint32_t key = score_key(x);
-        const int sel = key > thr ? 1 : (key == thr ? 2 + r : 0);
-        const int c = m == kModeAll ? 1 : (m == kModeSelect ? sel : 0);
-        return t >= P ? 1 : c;
-    };
-    // visit(t, c) for every position of this wave's run, 64 consecutive per step
-    auto sweep = [&](auto&& visit) {
-        for (int s00 = w0; s00 < w1; s00 += kWave * kBatch) {
-            int rv[kBatch];
-            float sv[kBatch];
-#pragma unroll
-            for (int e = 0; e < kBatch; ++e) {  // unconditional loads (clamped index), then the bound
-                const int t = s00 + e * kWave + lane;
-                const int tc = max(0, min(t, min(w1, P) - 1));
-                const int r = ro[tc];
-                sv[e] = sc[tc];
-                rv[e] = t < min(w1, P) ? r : -1;
-            }
-#pragma unroll
-            for (int e = 0; e < kBatch; ++e) {
-                const int t = s00 + e * kWave + lane;
-                visit(t, t < w1 ? classify(t, rv[e], sv[e]) : 0);
-            }
-        }
+    for (int r = 0; r < R; ++r) need[r] = sh.mode[r] == kModeSelect ? sh.need[r] : 0;
+    auto classify = [&](uint32_t tg, bool valid) {
+        if (!valid) return 0;
+        if (tg == kKept) return 1;
+        uint32_t r;
+        const uint32_t key = bin_key(tg, r);
+        const uint32_t th = sh.pref[r];
+        return key > th ? 1 : (key == th ? 2 + (int)r : 0);
     };
     const uint64_t lt = (1ull << lane) - 1ull;
-    // count this run's kept positions and its equal keys per bucket, per lane,
-    // then over the wave
     int keep = 0, eq[R];
 #pragma unroll
     for (int r = 0; r < R; ++r) eq[r] = 0;
-    sweep([&](int, int c) {
+    sweep_staged([&](uint32_t, uint32_t tg, bool valid) {
+        const int c = classify(tg, valid);
         keep += c == 1;
 #pragma unroll
         for (int r = 0; r < R; ++r) eq[r] += c == 2 + r;
@@ -271,7 +349,7 @@ __global__ __launch_bounds__(kThreads) void topk_kernel(const float* __restrict_
         for (int r = 0; r < R; ++r) sh.wave_eq[wave][r] = eq[r];
     }
     __syncthreads();
-    // equal keys are kept lowest index first: the earlier runs' equal keys come first
+    // equal keys are kept lowest position first: the earlier waves' come first
     int eq_seen[R];
 #pragma unroll
     for (int r = 0; r < R; ++r) {
@@ -286,7 +364,8 @@ __global__ __launch_bounds__(kThreads) void topk_kernel(const float* __restrict_
         if (w < wave) pos += sh.wave_keep[w];
         total += sh.wave_keep[w];
     }
-    sweep([&](int t, int c) {
+    sweep_staged([&](uint32_t t, uint32_t tg, bool valid) {
+        const int c = classify(tg, valid);
         bool k = c == 1;
         if (__ballot(c >= 2) != 0ull) {  // rare: keys equal to a threshold in this step
 #pragma unroll
@@ -298,7 +377,7 @@ __global__ __launch_bounds__(kThreads) void topk_kernel(const float* __restrict_
         }
         const uint64_t km = __ballot(k);
         const int at = pos + __popcll(km & lt);
-        if (k && at < k_cap) idx_out[(size_t)seg * k_cap + at] = t;
+        if (k && at < k_cap) idx_out[(size_t)seg * k_cap + at] = (int32_t)t;
         pos += __popcll(km);
     });
     if (tid == 0 && count_out != nullptr) count_out[seg] = total;
@@ -337,14 +416,22 @@ __global__ __launch_bounds__(kThreads) void compact_kernel(const char* __restric
 
 hipError_t launch_topk(const float* score, const int8_t* roles, const int32_t* quota, int L, int B,
                        int Hkv, int N, int W, int R, int k_cap, int32_t* idx_out, int32_t* count_out,
-                       hipStream_t st) {
+                       void* ws, hipStream_t st) {
     const size_t segs = (size_t)L * B * Hkv;
     const dim3 grid((unsigned)segs), block(kThreads);
+    uint2* stage = static_cast<uint2*>(ws);
+    // 16-byte span loads: every score row and label row starts 16-byte aligned
+    const bool vec = N % kSpan == 0 && (reinterpret_cast<uintptr_t>(score) & 15u) == 0 &&
+                     (reinterpret_cast<uintptr_t>(roles) & 15u) == 0;
     switch (R) {
-#define KVE_TOPK_CASE(RR)                                                                                  \
-    case RR:                                                                                               \
-        hipLaunchKernelGGL(topk_kernel<RR>, grid, block, 0, st, score, roles, quota, B, Hkv, N, W, k_cap, \
-                           idx_out, count_out);                                                            \
+#define KVE_TOPK_CASE(RR)                                                                                      \
+    case RR:                                                                                                   \
+        if (vec)                                                                                               \
+            hipLaunchKernelGGL((topk_kernel<RR, true>), grid, block, 0, st, score, roles, quota, B, Hkv, N, W, \
+                               k_cap, idx_out, count_out, stage);                                              \
+        else                                                                                                   \
+            hipLaunchKernelGGL((topk_kernel<RR, false>), grid, block, 0, st, score, roles, quota, B, Hkv, N,   \
+                               W, k_cap, idx_out, count_out, stage);                                           \
         break;
         KVE_TOPK_CASE(1)
         KVE_TOPK_CASE(2)

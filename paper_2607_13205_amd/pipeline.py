@@ -87,6 +87,7 @@ def as_policy(policy) -> Policy:
 class EvictBuffers:
     score: object
     ws_score: object
+    ws_topk: object
     quota_host: object   # pinned int32 [B, R]
     quota_dev: object
     idx: object
@@ -111,6 +112,7 @@ def alloc_buffers(k, n_q_heads: int, W: int, R: int, k_cap: int, scorer: str = "
     return EvictBuffers(
         score=torch.empty((L, B, Hkv, N), dtype=torch.float32, device=dev),
         ws_score=torch.empty(max(wsb, 1), dtype=torch.uint8, device=dev),
+        ws_topk=torch.empty(kb.topk_workspace_size(L, B, Hkv, N, R), dtype=torch.uint8, device=dev),
         quota_host=torch.zeros((B, R), dtype=torch.int32).pin_memory(),
         quota_dev=torch.zeros((B, R), dtype=torch.int32, device=dev),
         idx=torch.full((L, B, Hkv, k_cap), -1, dtype=torch.int32, device=dev),
@@ -140,7 +142,8 @@ def _score(q, k, bufs, scorer, pool_k, scale, page, l0, l1, stream=None, lse_win
 def _select(k, v, roles_dev, bufs, W, R, l0, l1, stream=None):
     """Top-k and compaction of layers [l0, l1) on ``stream`` (None: current)."""
     kb.topk_select(bufs.score[l0:l1], roles_dev, bufs.quota_dev, W, R, bufs.k_cap,
-                   idx_out=bufs.idx[l0:l1], count_out=bufs.count[l0:l1], stream=stream)
+                   idx_out=bufs.idx[l0:l1], count_out=bufs.count[l0:l1], workspace=bufs.ws_topk,
+                   stream=stream)
     kb.kv_compact(k[l0:l1], None if v is None else v[l0:l1], bufs.idx[l0:l1], bufs.count[l0:l1],
                   k_out=bufs.k_out[l0:l1], v_out=None if bufs.v_out is None else bufs.v_out[l0:l1],
                   stream=stream)

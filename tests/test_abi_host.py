@@ -155,6 +155,11 @@ def test_device_entry_points_validate_before_launch(kve):
     assert L.kve_topk_select(dummy, dummy, dummy, 1, 1, 2, 64, 8, 9, 10, dummy, dummy, null, 0, null) == 1
     assert L.kve_topk_select(dummy, dummy, dummy, 1, 1, 2, 64, 65, 4, 10, dummy, dummy, null, 0, null) == 1
     assert L.kve_topk_select(dummy, dummy, dummy, 1, 1, 2, 64, 8, 4, -1, dummy, dummy, null, 0, null) == 1
+    # topk: no workspace, a short one, a misaligned one
+    assert L.kve_topk_select(dummy, dummy, dummy, 1, 1, 2, 64, 8, 4, 10, dummy, dummy, null, 0, null) == 3
+    assert L.kve_topk_select(dummy, dummy, dummy, 1, 1, 2, 64, 8, 4, 10, dummy, dummy, dummy, 1023, null) == 3
+    assert L.kve_topk_select(dummy, dummy, dummy, 1, 1, 2, 64, 8, 4, 10, dummy, dummy,
+                             ctypes.c_void_p(0x1008), 1 << 20, null) == 1
     # compact: v without v_out, bad head_dim
     assert L.kve_kv_compact(dummy, dummy, 0, dummy, dummy, 1, 1, 2, 64, 128, 10, dummy, null, null) == 1
     assert L.kve_kv_compact(dummy, null, 0, dummy, dummy, 1, 1, 2, 64, 80, 10, dummy, null, null) == 2
@@ -188,7 +193,10 @@ def test_workspace_sizes_are_aligned_and_monotone(kve):
     assert kve.h2o_workspace_size(1, 1, 32, 8, 16384, 128) == 2 * 32 * 16384 * 4
     h = kve.h2o_workspace_size(2, 1, 32, 8, 1000, 128)
     assert h % 256 == 0 and h >= 2 * 32 * 1024 * 4 + 2 * 32 * 1000 * 4
-    assert kve.binding.LIB.kve_topk_workspace_size(1, 1, 8, 8192, 4) == 0
+    # top-k: one staged 8-byte entry per position of every segment
+    assert kve.topk_workspace_size(1, 1, 8, 8192, 4) == 8 * 8192 * 8
+    assert kve.topk_workspace_size(2, 3, 1, 1001, 4) == (6 * 1001 * 8 + 255) // 256 * 256
+    assert kve.topk_workspace_size(1, 1, 8, 0, 4) == 0
     # decode: per (segment, split, head) a partial output row and a pair of floats
     w = kve.decode_workspace_size(32, 4, 32, 8, 1640, 128)
     assert w % 256 == 0 and w >= 1024 * 32 * (128 + 2) * 4 // 8

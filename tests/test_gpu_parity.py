@@ -153,11 +153,37 @@ def _random_selection_case(rng, N, R_labels, R):
     return s, roles
 
 
+def _topk_check(K, score, roles, quota, W, R, roles_dev=None, score_dev=None):
+    """Run the GPU top-k on host arrays and compare every segment with the oracle."""
+    L, B, Hkv, N = score.shape
+    kept = [W + sum(min(max(int(quota[b, r]), 0), int(np.sum(roles[b, :N - W] == r)))
+                    for r in range(R)) for b in range(B)]
+    k_cap = max(kept)
+    sd = torch.from_numpy(score).cuda() if score_dev is None else score_dev
+    rd = torch.from_numpy(roles).cuda() if roles_dev is None else roles_dev
+    idx, cnt = K.topk_select(sd, rd, torch.from_numpy(quota).cuda(), W, R, k_cap)
+    torch.cuda.synchronize()
+    idx, cnt = idx.cpu().numpy(), cnt.cpu().numpy()
+    for l in range(L):
+        for b in range(B):
+            for j in range(Hkv):
+                ref = O.select_keep(score[l, b, j], roles[b], quota[b], W)
+                assert cnt[l, b, j] == len(ref) == kept[b], (l, b, j)
+                assert idx[l, b, j, :len(ref)].tolist() == ref.tolist(), (l, b, j)
+
+
+# N per bucket count: ragged lengths take the one-load-per-position path, the
+# multiples of 16 the 16-byte span loads
+TOPK_N = {"ragged": [7, 300, 1000, 4097, 70001, 33, 2049, 65],
+          "aligned": [16, 304, 1024, 4096, 70000, 48, 2048, 64]}
+
+
+@pytest.mark.parametrize("layout", ["ragged", "aligned"])
 @pytest.mark.parametrize("R", range(1, 9))  # the kernel is instantiated per bucket count
-def test_topk_select_bit_exact_with_oracle(K, R):
-    rng = np.random.default_rng(R)
+def test_topk_select_bit_exact_with_oracle(K, R, layout):
+    rng = np.random.default_rng(R + (100 if layout == "aligned" else 0))
     L, B, Hkv = 2, 2, 3
-    N = [7, 300, 1000, 4097, 70000, 33, 2049, 65][R - 1]
+    N = TOPK_N[layout][R - 1]
     W = int(rng.integers(0, min(N, 40)))
     score = np.zeros((L, B, Hkv, N), dtype=np.float32)
     roles = np.zeros((B, N), dtype=np.int8)
@@ -168,19 +194,52 @@ def test_topk_select_bit_exact_with_oracle(K, R):
             for j in range(Hkv):
                 score[l, b, j], _ = _random_selection_case(rng, N, R, R)
     quota = rng.integers(-2, N // max(R, 1) + 3, (B, R)).astype(np.int32)
-    kept = [W + sum(min(max(int(quota[b, r]), 0), int(np.sum(roles[b, :N - W] == r)))
-                    for r in range(R)) for b in range(B)]
-    k_cap = max(kept)
-    idx, cnt = K.topk_select(torch.from_numpy(score).cuda(), torch.from_numpy(roles).cuda(),
-                             torch.from_numpy(quota).cuda(), W, R, k_cap)
-    torch.cuda.synchronize()
-    idx, cnt = idx.cpu().numpy(), cnt.cpu().numpy()
-    for l in range(L):
-        for b in range(B):
-            for j in range(Hkv):
-                ref = O.select_keep(score[l, b, j], roles[b], quota[b], W)
-                assert cnt[l, b, j] == len(ref) == kept[b]
-                assert idx[l, b, j, :len(ref)].tolist() == ref.tolist()
+    _topk_check(K, score, roles, quota, W, R)
+
+
+def test_topk_misaligned_rows_take_the_per_position_loads(K):
+    """N a multiple of 16 but the score and label rows not 16-byte aligned."""
+    rng = np.random.default_rng(41)
+    L, B, Hkv, N, R, W = 1, 2, 2, 4096, 4, 32
+    score = rng.random((L, B, Hkv, N)).astype(np.float32)
+    roles = rng.integers(0, R, (B, N)).astype(np.int8)
+    quota = rng.integers(0, N // R, (B, R)).astype(np.int32)
+    sbuf = torch.empty(L * B * Hkv * N + 1, dtype=torch.float32, device="cuda")
+    sbuf[1:] = torch.from_numpy(score.ravel()).cuda()
+    rbuf = torch.empty(B * N + 3, dtype=torch.int8, device="cuda")
+    rbuf[3:] = torch.from_numpy(roles.ravel()).cuda()
+    sd, rd = sbuf[1:].view(L, B, Hkv, N), rbuf[3:].view(B, N)
+    assert sd.data_ptr() % 16 and rd.data_ptr() % 16
+    _topk_check(K, score, roles, quota, W, R, roles_dev=rd, score_dev=sd)
+
+
+@pytest.mark.parametrize("case", ["all_equal", "all_nan", "two_values", "window_only", "no_window",
+                                  "one_bin", "inf"])
+def test_topk_degenerate_inputs(K, case):
+    """Every key in the threshold's bin, every key tied, no prefix, no window."""
+    rng = np.random.default_rng(50)
+    L, B, Hkv, N, R = 1, 2, 2, 2048, 3
+    W = 16
+    score = rng.random((L, B, Hkv, N)).astype(np.float32)
+    roles = rng.integers(0, R, (B, N)).astype(np.int8)
+    quota = np.array([[100, 0, 700], [1, 2000, 5]], dtype=np.int32)
+    if case == "all_equal":
+        score[:] = 0.25
+    elif case == "all_nan":
+        score[:] = np.nan
+    elif case == "two_values":
+        score[:] = np.where(rng.random(score.shape) < 0.5, 1.0, -0.0).astype(np.float32)
+    elif case == "window_only":
+        W = N
+    elif case == "no_window":
+        W = 0
+    elif case == "one_bin":
+        # distinct keys that all share the top 11 bits (one quarter binade)
+        score[:] = (1.0 + rng.random(score.shape) * 0.24).astype(np.float32)
+    elif case == "inf":
+        score[rng.random(score.shape) < 0.3] = np.inf
+        score[rng.random(score.shape) < 0.3] = -np.inf
+    _topk_check(K, score, roles, quota, W, R)
 
 
 def test_topk_reports_truncation(K):
