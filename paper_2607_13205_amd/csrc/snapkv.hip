@@ -190,9 +190,14 @@ __global__ __launch_bounds__(2 * kSnapRowsPerGroup) void snap_combine(const floa
     const int vseg = blockIdx.x, r = threadIdx.x, rpg = blockDim.x;
     const int row = (vseg % rgroups) * rpg + r;
     float a = -INFINITY, b = 0.0f;
-    for (int c = 0; c < nranges; ++c) {
-        const float v = stats[((size_t)vseg * nranges + c) * rpg + r];
-        lse2_merge(a, b, v, v == -INFINITY ? 0.0f : 1.0f);
+    // eight ranges' values loaded before any is merged (merged in range order)
+    for (int c0 = 0; c0 < nranges; c0 += 8) {
+        float v[8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) v[j] = stats[((size_t)vseg * nranges + min(c0 + j, nranges - 1)) * rpg + r];
+#pragma unroll
+        for (int j = 0; j < 8; ++j)
+            if (c0 + j < nranges) lse2_merge(a, b, v[j], v[j] == -INFINITY ? 0.0f : 1.0f);
     }
     // rows past the window rows contribute nothing to the column sums
     lse[(size_t)vseg * rpg + r] = (row < rows && b > 0.0f) ? a + log2f(b) : INFINITY;

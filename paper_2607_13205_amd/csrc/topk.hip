@@ -2,15 +2,16 @@
 // always kept, and the coalesced K/V compaction of the kept rows (§6: the
 // dense cache of a compacting implementation).
 //
-// topk_select: one workgroup per (layer, sample, KV head) segment.  Scores are
-// mapped to order-preserving 32-bit keys (-0 -> +0, NaN lowest).  Two sweeps
-// read the segment's scores and labels:
+// topk_select: one workgroup per (layer, sample, KV head) segment, of 4 waves,
+// or of 16 when there are too few segments to fill the chip with 4-wave ones.
+// Scores are mapped to order-preserving 32-bit keys (-0 -> +0, NaN lowest).
+// Two sweeps read the segment's scores and labels:
 //   1. Histogram sweep: the top 11 bits of every labelled candidate's key (sign,
 //      exponent and two mantissa bits), one LDS histogram per bucket.  Per
 //      bucket this gives the population, which decides whether the bucket is
 //      kept whole, skipped or selected, and the top digit of the quota-th
 //      largest key: the threshold's bin.
-//   2. Staging sweep: each wave walks a contiguous quarter of the positions in
+//   2. Staging sweep: each wave walks a contiguous share of the positions in
 //      order and sets aside, in order, every position that is surely kept (the
 //      window, whole buckets, keys above the threshold's bin) and every key
 //      inside the bin (with its bucket and the low 21 bits of its key), in its
@@ -33,23 +34,23 @@
 namespace kve {
 namespace {
 
-constexpr int kThreads = 256;
-constexpr int kWaves = kThreads / kWave;
+constexpr int kThreads = 256;      // top-k workgroup when segments fill the chip (and compaction)
+constexpr int kWideThreads = 1024; // top-k workgroup when there are few segments
+constexpr int kWideBelow = 512;    // segments below which the wide workgroup is used
 constexpr int kMaxR = 8;  // buckets supported (one kernel instantiation each)
 constexpr int kDigitBits = 11;
 constexpr int kDigits = 1 << kDigitBits;
 constexpr int kLowBits = 32 - kDigitBits;  // key bits below the top digit
 constexpr uint32_t kLowMask = (1u << kLowBits) - 1u;
 constexpr int kSpan = 16;                     // consecutive positions per lane and step
-constexpr int kGroupStep = kThreads * kSpan;  // positions per workgroup step
-constexpr int kWaveStep = kWave * kSpan;      // positions per wave step
+constexpr int kWaveStep = kWave * kSpan;  // positions per wave step
 constexpr int kBatch = 8;                     // staged entries per lane loaded before use
 constexpr uint32_t kNoKey = 0xffffffffu;      // above every key (+inf maps to 0xff800000)
 constexpr uint32_t kKept = 0xffffffffu;       // tag of a staged position that is surely kept
 
 enum : int { kModeNone = 0, kModeSelect = 1, kModeAll = 2 };
 
-template <int R>
+template <int R, int NW>
 struct TopkShared {
     uint32_t hist[R][kDigits];
     uint32_t pref[R];  // key bits fixed so far (bits lo .. 31)
@@ -59,13 +60,14 @@ struct TopkShared {
     // staging: {lowest surely kept key, top digit of the threshold's bin} per
     // bucket; entry R (labels outside [0, R)) is never kept and never staged
     uint2 stage_cls[R + 1];
-    int wave_eq[kWaves][R];  // staged keys equal to a threshold, per wave
-    int wave_keep[kWaves];   // kept positions per wave
-    int scan[kWaves];
+    int wave_eq[NW][R];  // staged keys equal to a threshold, per wave
+    int wave_keep[NW];   // kept positions per wave
+    int scan[NW];
 };
 
-// Exclusive prefix sum over the workgroup of one value per thread (in thread
-// order); every thread also gets the total.  `tmp` holds kWaves ints.
+// Exclusive prefix sum over a workgroup of NW waves of one value per thread (in
+// thread order); every thread also gets the total.  `tmp` holds NW ints.
+template <int NW>
 __device__ __forceinline__ int block_exclusive_scan(int v, int* tmp, int& total) {
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     int incl = v;
@@ -79,7 +81,7 @@ __device__ __forceinline__ int block_exclusive_scan(int v, int* tmp, int& total)
     int before = 0;
     total = 0;
 #pragma unroll
-    for (int w = 0; w < kWaves; ++w) {
+    for (int w = 0; w < NW; ++w) {
         const int t = tmp[w];
         if (w < wave) before += t;
         total += t;
@@ -108,9 +110,9 @@ __device__ __forceinline__ int wave_exclusive_scan(int v, int& total) {
 // all higher bins, and the thread whose bins reach the wanted rank fixes the
 // digit.  In the first pass (quota >= 0) the population decides whether the
 // bucket is kept whole, skipped, or selected.  Every thread calls it.
-template <int R>
-__device__ __forceinline__ void find_digit(TopkShared<R>& sh, int r, int quota) {
-    constexpr int kPerThread = kDigits / kThreads;
+template <int R, int NW>
+__device__ __forceinline__ void find_digit(TopkShared<R, NW>& sh, int r, int quota) {
+    constexpr int kPerThread = kDigits / (NW * kWave);
     const int tid = threadIdx.x;
     // read before the scan's barriers: the thread that finds the digit rewrites them
     int want = sh.need[r];
@@ -120,7 +122,7 @@ __device__ __forceinline__ void find_digit(TopkShared<R>& sh, int r, int quota) 
 #pragma unroll
     for (int e = 1; e <= kPerThread; ++e) mine += (int)sh.hist[r][hi - e];
     int total;
-    const int above = block_exclusive_scan(mine, sh.scan, total);
+    const int above = block_exclusive_scan<NW>(mine, sh.scan, total);
     if (quota >= 0) {
         if (quota == 0 || quota >= total) {
             if (tid == 0) sh.mode[r] = quota == 0 ? kModeNone : kModeAll;
@@ -187,15 +189,17 @@ __device__ __forceinline__ uint32_t bucket_of(const uint32_t (&lab)[4], int e) {
     return min((lab[e >> 2] >> (8 * (e & 3))) & 0xffu, (uint32_t)R);
 }
 
-template <int R, bool VEC>
-__global__ __launch_bounds__(kThreads) void topk_kernel(const float* __restrict__ score,
+template <int R, bool VEC, int NT>
+__global__ __launch_bounds__(NT) void topk_kernel(const float* __restrict__ score,
                                                         const int8_t* __restrict__ roles,
                                                         const int32_t* __restrict__ quota, int B,
                                                         int Hkv, int N, int W, int k_cap,
                                                         int32_t* __restrict__ idx_out,
                                                         int32_t* __restrict__ count_out,
                                                         uint2* __restrict__ stage) {
-    __shared__ TopkShared<R> sh;
+    constexpr int NW = NT / kWave;
+    constexpr int kGroupStep = NT * kSpan;  // positions per workgroup step
+    __shared__ TopkShared<R, NW> sh;
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int seg = blockIdx.x;
@@ -210,7 +214,7 @@ __global__ __launch_bounds__(kThreads) void topk_kernel(const float* __restrict_
         sh.lo[tid] = 32;
         sh.need[tid] = 0;
     }
-    for (int e = tid; e < R * kDigits; e += kThreads) (&sh.hist[0][0])[e] = 0u;
+    for (int e = tid; e < R * kDigits; e += NT) (&sh.hist[0][0])[e] = 0u;
     __syncthreads();
 
     // 1. histogram sweep: the top digit of every labelled candidate's key
@@ -243,7 +247,7 @@ __global__ __launch_bounds__(kThreads) void topk_kernel(const float* __restrict_
     __syncthreads();
 
     // 2. staging sweep over this wave's run [w0, w1), in order
-    const int run = (N + kWaves * kWaveStep - 1) / (kWaves * kWaveStep) * kWaveStep;
+    const int run = (N + NW * kWaveStep - 1) / (NW * kWaveStep) * kWaveStep;
     const int w0 = min(N, wave * run), w1 = min(N, w0 + run);
     uint2* st = stage + (size_t)seg * N + w0;  // room for w1 - w0 entries
     int n_st = 0;
@@ -299,7 +303,7 @@ __global__ __launch_bounds__(kThreads) void topk_kernel(const float* __restrict_
 #pragma unroll
         for (int r = 0; r < R; ++r) any |= sh.mode[r] == kModeSelect && sh.lo[r] > 0;
         if (!any) break;  // uniform: every thread reads the same LDS values
-        for (int e = tid; e < R * kDigits; e += kThreads) (&sh.hist[0][0])[e] = 0u;
+        for (int e = tid; e < R * kDigits; e += NT) (&sh.hist[0][0])[e] = 0u;
         __syncthreads();
         const int lo = 32 - kDigitBits * pass;  // the same for every selecting bucket
         const int w = min(kDigitBits, lo);
@@ -360,7 +364,7 @@ __global__ __launch_bounds__(kThreads) void topk_kernel(const float* __restrict_
     if (lane == 0) sh.wave_keep[wave] = keep;
     __syncthreads();
     int pos = 0, total = 0;
-    for (int w = 0; w < kWaves; ++w) {
+    for (int w = 0; w < NW; ++w) {
         if (w < wave) pos += sh.wave_keep[w];
         total += sh.wave_keep[w];
     }
@@ -385,30 +389,50 @@ __global__ __launch_bounds__(kThreads) void topk_kernel(const float* __restrict_
 
 constexpr int kCompactRows = 64;
 
+// One workgroup per (segment, 64 kept rows); a row is PARTS pieces of 16 bytes
+// (8, 16 or 32), piece e of the block being part e % PARTS of row e / PARTS.
+// Every thread takes 64 PARTS / 256 pieces and issues all its index loads, then
+// all its row loads, then all its stores, so that a block waits for memory
+// about twice instead of once per piece.
+template <int PARTS>
 __global__ __launch_bounds__(kThreads) void compact_kernel(const char* __restrict__ k,
-                                                           const char* __restrict__ v, int row_bytes,
+                                                           const char* __restrict__ v,
                                                            const int32_t* __restrict__ idx,
                                                            const int32_t* __restrict__ count, int N,
                                                            int k_cap, int nblk, char* __restrict__ k_out,
                                                            char* __restrict__ v_out) {
+    constexpr int kRowBytes = PARTS * 16;
+    constexpr int kItems = kCompactRows * PARTS / kThreads;
+    static_assert(kItems * kThreads == kCompactRows * PARTS, "whole pieces per thread");
     const int blk = blockIdx.x % nblk;
     const int seg = blockIdx.x / nblk;
     const int cnt = min(count[seg], k_cap);
     const int m0 = blk * kCompactRows;
     if (m0 >= cnt) return;
-    const int parts = row_bytes / 16;
-    const int total = kCompactRows * parts;
-    for (int e = threadIdx.x; e < total; e += kThreads) {
-        const int mm = e / parts;
-        const int part = e - mm * parts;
-        const int m = m0 + mm;
-        if (m >= cnt) break;
-        const int t = idx[(size_t)seg * k_cap + m];
-        if (t < 0 || t >= N) continue;
-        const size_t src = ((size_t)seg * N + t) * row_bytes + (size_t)part * 16;
-        const size_t dst = ((size_t)seg * k_cap + m) * row_bytes + (size_t)part * 16;
-        st16(k_out + dst, ld16(k + src));
-        if (v != nullptr) st16(v_out + dst, ld16(v + src));
+    const int total = min(kCompactRows, cnt - m0) * PARTS;
+    int t[kItems];
+#pragma unroll
+    for (int i = 0; i < kItems; ++i) {
+        const int e = min(i * kThreads + (int)threadIdx.x, total - 1);
+        t[i] = idx[(size_t)seg * k_cap + m0 + e / PARTS];
+    }
+    u32x4 kv[kItems], vv[kItems];
+#pragma unroll
+    for (int i = 0; i < kItems; ++i) {
+        const int e = min(i * kThreads + (int)threadIdx.x, total - 1);
+        const int tt = min(max(t[i], 0), N - 1);  // out-of-range indices are skipped below
+        const size_t src = ((size_t)seg * N + tt) * kRowBytes + (size_t)(e % PARTS) * 16;
+        kv[i] = ld16(k + src);
+        if (v != nullptr) vv[i] = ld16(v + src);
+    }
+#pragma unroll
+    for (int i = 0; i < kItems; ++i) {
+        const int e = i * kThreads + (int)threadIdx.x;
+        if (e < total && t[i] >= 0 && t[i] < N) {
+            const size_t dst = ((size_t)seg * k_cap + m0 + e / PARTS) * kRowBytes + (size_t)(e % PARTS) * 16;
+            st16(k_out + dst, kv[i]);
+            if (v != nullptr) st16(v_out + dst, vv[i]);
+        }
     }
 }
 
@@ -418,20 +442,30 @@ hipError_t launch_topk(const float* score, const int8_t* roles, const int32_t* q
                        int Hkv, int N, int W, int R, int k_cap, int32_t* idx_out, int32_t* count_out,
                        void* ws, hipStream_t st) {
     const size_t segs = (size_t)L * B * Hkv;
-    const dim3 grid((unsigned)segs), block(kThreads);
     uint2* stage = static_cast<uint2*>(ws);
     // 16-byte span loads: every score row and label row starts 16-byte aligned
     const bool vec = N % kSpan == 0 && (reinterpret_cast<uintptr_t>(score) & 15u) == 0 &&
                      (reinterpret_cast<uintptr_t>(roles) & 15u) == 0;
+    // few segments: sixteen waves per segment instead of four
+    const bool wide = segs < (size_t)kWideBelow;
+    const dim3 grid((unsigned)segs);
     switch (R) {
+#define KVE_TOPK_LAUNCH(RR, V, NT)                                                                             \
+    hipLaunchKernelGGL((topk_kernel<RR, V, NT>), grid, dim3(NT), 0, st, score, roles, quota, B, Hkv, N, W,   \
+                       k_cap, idx_out, count_out, stage)
 #define KVE_TOPK_CASE(RR)                                                                                      \
     case RR:                                                                                                   \
-        if (vec)                                                                                               \
-            hipLaunchKernelGGL((topk_kernel<RR, true>), grid, block, 0, st, score, roles, quota, B, Hkv, N, W, \
-                               k_cap, idx_out, count_out, stage);                                              \
-        else                                                                                                   \
-            hipLaunchKernelGGL((topk_kernel<RR, false>), grid, block, 0, st, score, roles, quota, B, Hkv, N,   \
-                               W, k_cap, idx_out, count_out, stage);                                           \
+        if (wide) {                                                                                            \
+            if (vec)                                                                                           \
+                KVE_TOPK_LAUNCH(RR, true, kWideThreads);                                                       \
+            else                                                                                               \
+                KVE_TOPK_LAUNCH(RR, false, kWideThreads);                                                      \
+        } else {                                                                                               \
+            if (vec)                                                                                           \
+                KVE_TOPK_LAUNCH(RR, true, kThreads);                                                           \
+            else                                                                                               \
+                KVE_TOPK_LAUNCH(RR, false, kThreads);                                                          \
+        }                                                                                                      \
         break;
         KVE_TOPK_CASE(1)
         KVE_TOPK_CASE(2)
@@ -442,6 +476,7 @@ hipError_t launch_topk(const float* score, const int8_t* roles, const int32_t* q
         KVE_TOPK_CASE(7)
         KVE_TOPK_CASE(8)
 #undef KVE_TOPK_CASE
+#undef KVE_TOPK_LAUNCH
         default:
             return hipErrorInvalidValue;
     }
@@ -454,9 +489,27 @@ hipError_t launch_compact(const void* k, const void* v, int elem_bytes, const in
     const size_t segs = (size_t)L * B * Hkv;
     const int nblk = (k_cap + kCompactRows - 1) / kCompactRows;
     if (nblk == 0 || segs == 0) return hipSuccess;
-    hipLaunchKernelGGL(compact_kernel, dim3((unsigned)(segs * nblk)), dim3(kThreads), 0, st,
-                       static_cast<const char*>(k), static_cast<const char*>(v), d * elem_bytes, idx,
-                       count, N, k_cap, nblk, static_cast<char*>(k_out), static_cast<char*>(v_out));
+    const dim3 grid((unsigned)(segs * nblk));
+    const char* kc = static_cast<const char*>(k);
+    const char* vc = static_cast<const char*>(v);
+    char* ko = static_cast<char*>(k_out);
+    char* vo = static_cast<char*>(v_out);
+    switch (d * elem_bytes / 16) {  // 16-byte pieces per row
+        case 8:
+            hipLaunchKernelGGL(compact_kernel<8>, grid, dim3(kThreads), 0, st, kc, vc, idx, count, N, k_cap, nblk,
+                               ko, vo);
+            break;
+        case 16:
+            hipLaunchKernelGGL(compact_kernel<16>, grid, dim3(kThreads), 0, st, kc, vc, idx, count, N, k_cap, nblk,
+                               ko, vo);
+            break;
+        case 32:
+            hipLaunchKernelGGL(compact_kernel<32>, grid, dim3(kThreads), 0, st, kc, vc, idx, count, N, k_cap, nblk,
+                               ko, vo);
+            break;
+        default:
+            return hipErrorInvalidValue;
+    }
     return hipGetLastError();
 }
 

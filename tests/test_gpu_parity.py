@@ -199,6 +199,24 @@ def test_topk_select_bit_exact_with_oracle(K, R, layout):
     _topk_check(K, score, roles, quota, W, R)
 
 
+@pytest.mark.parametrize("R,N", [(4, 301), (4, 304), (8, 1000), (1, 4096)])
+def test_topk_many_segments_take_the_four_wave_workgroups(K, R, N):
+    """512 segments and more use four-wave workgroups (fewer use sixteen waves)."""
+    rng = np.random.default_rng(60 + R + N)
+    L, B, Hkv = 4, 4, 32
+    W = 20
+    score = np.zeros((L, B, Hkv, N), dtype=np.float32)
+    roles = np.zeros((B, N), dtype=np.int8)
+    for b in range(B):
+        _, roles[b] = _random_selection_case(rng, N, R + 1, R)
+    for l in range(L):
+        for b in range(B):
+            for j in range(Hkv):
+                score[l, b, j], _ = _random_selection_case(rng, N, R, R)
+    quota = rng.integers(-1, N // R + 2, (B, R)).astype(np.int32)
+    _topk_check(K, score, roles, quota, W, R)
+
+
 def test_topk_misaligned_rows_take_the_per_position_loads(K):
     """N a multiple of 16 but the score and label rows not 16-byte aligned."""
     rng = np.random.default_rng(41)
