@@ -80,6 +80,8 @@ def parse():
                     help="skip the decode timings over the compacted and the full cache")
     ap.add_argument("--no-policies", action="store_true",
                     help="skip the fair-eviction and No-KEY step timings")
+    ap.add_argument("--no-graph", action="store_true",
+                    help="skip the step timing through a captured HIP graph")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a plain device copy of 1 GiB (5 times), for counter calibration")
     return ap.parse_args()
@@ -242,6 +244,22 @@ def policy_leg(WL, pipeline, wl, inp, budget, W, pool, steps):
         del bufs
         torch.cuda.empty_cache()
     return out
+
+
+def graph_leg(pipeline, inp, alpha, budget, W, pool, bufs, scorer, steps, lse_win=None):
+    """Step time with the device part captured once as a HIP graph and replayed
+    (the host allocation still runs every step), and whether the replays give
+    the eager step's kept indices and counts."""
+    import torch
+    idx0, cnt0 = bufs.idx.clone(), bufs.count.clone()
+    g = pipeline.StepGraph(inp["q"], inp["k"], inp["v"], inp["roles_t"], alpha, W, pool, bufs, scorer=scorer,
+                           lse_win=lse_win)
+    ms = _time_calls(lambda: g.replay(inp["roles"], budget), steps)
+    torch.cuda.synchronize()
+    same = bool(torch.equal(bufs.idx, idx0) and torch.equal(bufs.count, cnt0))
+    return {"ms_per_step": round(ms, 4), "matches_eager": same,
+            "launch": "one HIP graph replay per step (quota copy, score, top-k, compaction); "
+                      "allocation on the host"}
 
 
 def _time_calls(fn, steps):
@@ -474,6 +492,10 @@ def main():
             "ms": round(ms_score, 4), "algorithmic_bytes": score_bytes,
         },
     }
+    if not args.no_graph and args.chunks <= 1:
+        print("[bench] step through a HIP graph", file=sys.stderr, flush=True)
+        out["graph"] = graph_leg(pipeline, inp, alpha, budget, W, pool, bufs, scorer, max(3, args.steps // 2),
+                                 lse_win=main_lse)
     if not args.no_decode and scorer == "snapkv":
         print("[bench] decode over the compacted and the full cache", file=sys.stderr, flush=True)
         out["decode"] = decode_leg(K, wl, inp, bufs, max(3, args.steps // 2))

@@ -205,3 +205,64 @@ def evict(q, k, v, roles_host: np.ndarray, roles_dev, policy, budget: float, W: 
         score_events[1].record(main)
     main.wait_stream(side_stream)
     return quota, kept
+
+
+class StepGraph:
+    """The device part of an eviction step (quota upload, score, top-k,
+    compaction) captured as a HIP graph and replayed, for callers that run the
+    step inside captured work (serving loops, launch-bound small shapes).
+
+    Two graphs are captured, each copying the quotas from its own pinned host
+    buffer, and replays alternate between them: a replay writes the quotas the
+    host allocation has just produced into its buffer once the replay before
+    last (the previous user of that buffer) has finished, so the host work of
+    one step overlaps the device work of the previous one.  The inputs, labels
+    and buffers are the tensors given here (refill them in place between
+    replays).  The library launches no memset and allocates nothing, so each
+    graph holds only kernel nodes and the one copy."""
+
+    def __init__(self, q, k, v, roles_dev, policy, W: int, pool_k: int, bufs: EvictBuffers,
+                 scorer: str = "snapkv", scale: float = 0.0, page: int = 16, lse_win=None):
+        import torch
+        self.policy = as_policy(policy)
+        self.W = W
+        self.bufs = bufs
+        L = k.shape[0]
+        R = self.policy.R
+        self.quota_host = [bufs.quota_host, torch.zeros_like(bufs.quota_host).pin_memory()]
+
+        def step(src):
+            bufs.quota_dev.copy_(src, non_blocking=True)
+            _score(q, k, bufs, scorer, pool_k, scale, page, 0, L, lse_win=lse_win)
+            _select(k, v, roles_dev, bufs, W, R, 0, L)
+
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            step(self.quota_host[0])    # one eager run on the capture stream first
+        torch.cuda.current_stream().wait_stream(side)
+        torch.cuda.synchronize()
+        self.graphs = []
+        for src in self.quota_host:
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g, stream=side):
+                step(src)
+            self.graphs.append(g)
+        self.done = [torch.cuda.Event(), torch.cuda.Event()]
+        for e in self.done:
+            e.record()
+        self.turn = 0
+
+    def replay(self, roles_host: np.ndarray, budget: float):
+        """Allocate on the host for these bucket labels and budget, then replay
+        the captured step on the current stream; returns (quota, kept)."""
+        quota, kept, k_cap = self.policy.allocate(roles_host, budget, self.W)
+        if k_cap > self.bufs.k_cap:
+            raise ValueError(f"buffers hold {self.bufs.k_cap} rows, the allocation keeps {k_cap}")
+        i = self.turn
+        self.done[i].synchronize()      # the replay before last has read this buffer
+        self.quota_host[i].numpy()[...] = quota
+        self.graphs[i].replay()
+        self.done[i].record()
+        self.turn = 1 - i
+        return quota, kept

@@ -304,6 +304,40 @@ def test_kv_compact_bit_exact(K, dtype, d):
                 assert not kob[s][m].any() and not vob[s][m].any()
 
 
+def test_step_graph_replays_match_eager_steps(K):
+    """The step captured as a HIP graph, replayed at several budgets with eager
+    steps and synchronisations in between, gives the eager step's quotas,
+    scores, kept indices, counts and compacted rows bit for bit."""
+    from paper_2607_13205_amd import pipeline
+    wl = WL.get_workload("layer8k")
+    note("step graph layer8k")
+    inp = WL.make_inputs(wl, device="cuda")
+    alpha = WL.default_alpha(0.0)
+    budgets = [0.05, 0.20, 0.10, 0.05, 0.50]
+    cap = max(K.role_allocate(inp["roles"], 4, alpha, b, wl.W)[2] for b in budgets)
+    bufs_g = pipeline.alloc_buffers(inp["k"], wl.Hq, wl.W, 4, cap)
+    bufs_e = pipeline.alloc_buffers(inp["k"], wl.Hq, wl.W, 4, cap)
+    g = pipeline.StepGraph(inp["q"], inp["k"], inp["v"], inp["roles_t"], alpha, wl.W, wl.pool_k, bufs_g)
+    for b in budgets:
+        qg, kg = g.replay(inp["roles"], b)
+        torch.cuda.synchronize()
+        qe, ke = pipeline.evict(inp["q"], inp["k"], inp["v"], inp["roles"], inp["roles_t"], alpha, b,
+                                wl.W, wl.pool_k, bufs_e)
+        torch.cuda.synchronize()
+        assert np.array_equal(qg, qe) and np.array_equal(kg, ke)
+        for name in ("score", "idx", "count", "k_out", "v_out"):
+            assert torch.equal(getattr(bufs_g, name), getattr(bufs_e, name)), (b, name)
+    # and the last replay against the oracle's kept sets for two segments
+    ref_q, _, _ = O.role_allocate_batch(inp["roles"], 4, alpha, budgets[-1], wl.W)
+    assert np.array_equal(ref_q, qg)
+    s_all = O.snapkv_score(f64(inp["q"]), f64(inp["k"]), wl.Hkv, wl.pool_k)
+    for (l, b, j) in [(0, 0, 0), (0, 0, 7)]:
+        s_ref = s_all[l, b, j]
+        ref = O.select_keep(s_ref, inp["roles"][b], qg[b], wl.W)
+        got = bufs_g.idx[l, b, j, :int(bufs_g.count[l, b, j])].cpu().numpy()
+        check_kept_set(got, ref, s_ref, inp["roles"][b], wl.W, qg[b])
+
+
 def check_quest_or_scores(gpu, ref, W, what):
     """Scores of any scorer; the Quest window entries are +inf on both sides."""
     N = len(ref)
