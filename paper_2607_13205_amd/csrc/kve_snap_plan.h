@@ -41,10 +41,15 @@ inline SnapPlan snap_plan(int L, int B, int Hq, int Hkv, int N, int W, int d, in
     p.n_vsegs = p.segs * p.rgroups;
     p.planes = p.rgroups;
     // whole chunks per range: about kSnapTargetGroups workgroups per pass (two
-    // per compute unit at a time), 4 .. 32 chunks each (fewer when N is short)
+    // per compute unit at a time), at most 32 chunks each, and at least as many
+    // keys as the group has query rows (a workgroup loads its rows' queries
+    // once, so its keys should outweigh them); short problems thus get short
+    // ranges rather than a few workgroups walking many chunks in turn
     const long long chunks = (N + kSnapChunkKeys - 1) / kSnapChunkKeys;
     long long per = (chunks * p.n_vsegs + kSnapTargetGroups - 1) / kSnapTargetGroups;
-    if (per < 4) per = 4;
+    const int group_rows = p.rows < p.rpg ? p.rows : p.rpg;
+    const long long min_per = (group_rows + kSnapChunkKeys - 1) / kSnapChunkKeys;
+    if (per < min_per) per = min_per;
     if (per > kSnapMaxRangeChunks) per = kSnapMaxRangeChunks;
     if (per > chunks) per = chunks;
     p.range_keys = (int)(per * kSnapChunkKeys);

@@ -183,24 +183,33 @@ __global__ __launch_bounds__(kThreads, (TuneRS<T, RS>::kOcc1)) void snap_pass1(
     }
 }
 
-// one thread per row of a row group (rpg = blockDim.x rows)
-__global__ __launch_bounds__(2 * kSnapRowsPerGroup) void snap_combine(const float* __restrict__ stats, int nranges,
-                                                                      int rows, int rgroups,
-                                                                      float* __restrict__ lse) {
-    const int vseg = blockIdx.x, r = threadIdx.x, rpg = blockDim.x;
+// Four threads per row of a row group (thread 4 r + s, rpg = blockDim.x / 4
+// rows): thread s merges every fourth range from range s, 32 ranges' values
+// loaded before any is merged, then the four partial sums of a row merge by
+// shuffles.
+constexpr int kCombineSplit = 4;
+__global__ __launch_bounds__(2 * kSnapRowsPerGroup * kCombineSplit) void snap_combine(
+    const float* __restrict__ stats, int nranges, int rows, int rgroups, float* __restrict__ lse) {
+    const int vseg = blockIdx.x, rpg = blockDim.x / kCombineSplit;
+    const int r = threadIdx.x / kCombineSplit, sub = threadIdx.x % kCombineSplit;
     const int row = (vseg % rgroups) * rpg + r;
     float a = -INFINITY, b = 0.0f;
-    // eight ranges' values loaded before any is merged (merged in range order)
-    for (int c0 = 0; c0 < nranges; c0 += 8) {
-        float v[8];
+    for (int c0 = sub; c0 < nranges; c0 += 32 * kCombineSplit) {
+        float v[32];
 #pragma unroll
-        for (int j = 0; j < 8; ++j) v[j] = stats[((size_t)vseg * nranges + min(c0 + j, nranges - 1)) * rpg + r];
+        for (int j = 0; j < 32; ++j)
+            v[j] = stats[((size_t)vseg * nranges + min(c0 + j * kCombineSplit, nranges - 1)) * rpg + r];
 #pragma unroll
-        for (int j = 0; j < 8; ++j)
-            if (c0 + j < nranges) lse2_merge(a, b, v[j], v[j] == -INFINITY ? 0.0f : 1.0f);
+        for (int j = 0; j < 32; ++j)
+            if (c0 + j * kCombineSplit < nranges) lse2_merge(a, b, v[j], v[j] == -INFINITY ? 0.0f : 1.0f);
+    }
+#pragma unroll
+    for (int m = 1; m < kCombineSplit; m <<= 1) {
+        const float ao = __shfl_xor(a, m), bo = __shfl_xor(b, m);
+        lse2_merge(a, b, ao, bo);
     }
     // rows past the window rows contribute nothing to the column sums
-    lse[(size_t)vseg * rpg + r] = (row < rows && b > 0.0f) ? a + log2f(b) : INFINITY;
+    if (sub == 0) lse[(size_t)vseg * rpg + r] = (row < rows && b > 0.0f) ? a + log2f(b) : INFINITY;
 }
 
 // Row statistics supplied by the caller (the natural-log log-sum-exp of each
@@ -425,7 +434,8 @@ void launch_passes(const T* qt, const T* kt, const float* lse_win, const SnapPla
     } else {
         hipLaunchKernelGGL((snap_pass1<T, D, RS>), grid, dim3(kThreads), 0, st, qt, kt, N, W, p.rows, p.rgroups,
                            p.nranges, p.range_keys, sl2, stats);
-        hipLaunchKernelGGL(snap_combine, dim3((unsigned)p.n_vsegs), dim3(p.rpg), 0, st, stats, p.nranges, p.rows,
+        hipLaunchKernelGGL(snap_combine, dim3((unsigned)p.n_vsegs), dim3(p.rpg * kCombineSplit), 0, st, stats,
+                           p.nranges, p.rows,
                            p.rgroups, lse);
     }
     hipLaunchKernelGGL((snap_pass2<T, D, RS>), grid, dim3(kThreads), 0, st, qt, kt, N, W, p.rows, p.rgroups,

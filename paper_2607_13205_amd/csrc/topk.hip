@@ -62,32 +62,45 @@ struct TopkShared {
     uint2 stage_cls[R + 1];
     int wave_eq[NW][R];  // staged keys equal to a threshold, per wave
     int wave_keep[NW];   // kept positions per wave
-    int scan[NW];
+    int scan[NW][R < 4 ? R : 4];
 };
 
-// Exclusive prefix sum over a workgroup of NW waves of one value per thread (in
-// thread order); every thread also gets the total.  `tmp` holds NW ints.
-template <int NW>
-__device__ __forceinline__ int block_exclusive_scan(int v, int* tmp, int& total) {
+// Exclusive prefix sums over a workgroup of NW waves of R values per thread (in
+// thread order, each value on its own); every thread also gets the totals.
+// `tmp` holds NW x R ints.
+template <int R, int NW>
+__device__ __forceinline__ void block_exclusive_scan(const int (&v)[R], int (&excl)[R], int (&total)[R],
+                                                     int (*tmp)[R]) {
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    int incl = v;
+    int incl[R];
+#pragma unroll
+    for (int r = 0; r < R; ++r) incl[r] = v[r];
 #pragma unroll
     for (int off = 1; off < kWave; off <<= 1) {
-        const int o = __shfl_up(incl, off);
-        if (lane >= off) incl += o;
-    }
-    if (lane == kWave - 1) tmp[wave] = incl;
-    __syncthreads();
-    int before = 0;
-    total = 0;
 #pragma unroll
-    for (int w = 0; w < NW; ++w) {
-        const int t = tmp[w];
-        if (w < wave) before += t;
-        total += t;
+        for (int r = 0; r < R; ++r) {
+            const int o = __shfl_up(incl[r], off);
+            if (lane >= off) incl[r] += o;
+        }
+    }
+    if (lane == kWave - 1) {
+#pragma unroll
+        for (int r = 0; r < R; ++r) tmp[wave][r] = incl[r];
     }
     __syncthreads();
-    return before + incl - v;
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+        int before = 0, all = 0;
+#pragma unroll
+        for (int w = 0; w < NW; ++w) {
+            const int t = tmp[w][r];
+            if (w < wave) before += t;
+            all += t;
+        }
+        excl[r] = before + incl[r] - v[r];
+        total[r] = all;
+    }
+    __syncthreads();
 }
 
 // Exclusive prefix sum over the lanes of a wave of v in [0, 31] (lane order),
@@ -105,43 +118,64 @@ __device__ __forceinline__ int wave_exclusive_scan(int v, int& total) {
     return excl;
 }
 
-// Digit search of one pass for bucket r, every thread at once: thread tid holds
-// kPerThread bins from the top going down; a scan gives the count of keys in
-// all higher bins, and the thread whose bins reach the wanted rank fixes the
-// digit.  In the first pass (quota >= 0) the population decides whether the
-// bucket is kept whole, skipped, or selected.  Every thread calls it.
+// Digit search of one pass for every bucket still selecting, in groups of up
+// to four buckets (one scan per group, which bounds the registers the scan
+// holds): thread tid holds kPerThread bins from the top going down per bucket;
+// the scan gives the count of keys in all higher bins, and the thread whose
+// bins reach a bucket's wanted rank fixes its digit.  In the first pass (quota
+// given) the population decides whether a bucket is kept whole, skipped, or
+// selected.  Every thread calls it.
+constexpr int kScanGroup = 4;
 template <int R, int NW>
-__device__ __forceinline__ void find_digit(TopkShared<R, NW>& sh, int r, int quota) {
+__device__ __forceinline__ void find_digits(TopkShared<R, NW>& sh, const int32_t* quota) {
     constexpr int kPerThread = kDigits / (NW * kWave);
+    constexpr int G = R < kScanGroup ? R : kScanGroup;
     const int tid = threadIdx.x;
-    // read before the scan's barriers: the thread that finds the digit rewrites them
-    int want = sh.need[r];
-    const int lo = sh.lo[r];
     const int hi = kDigits - kPerThread * tid;  // bins [hi - kPerThread, hi)
-    int mine = 0;
+#pragma unroll 1
+    for (int r0 = 0; r0 < R; r0 += G) {
+        // read before the scan's barriers: the threads that find the digits rewrite them
+        bool act[G];
+        int want[G], lo[G], mine[G];
 #pragma unroll
-    for (int e = 1; e <= kPerThread; ++e) mine += (int)sh.hist[r][hi - e];
-    int total;
-    const int above = block_exclusive_scan<NW>(mine, sh.scan, total);
-    if (quota >= 0) {
-        if (quota == 0 || quota >= total) {
-            if (tid == 0) sh.mode[r] = quota == 0 ? kModeNone : kModeAll;
-            __syncthreads();
-            return;
+        for (int g = 0; g < G; ++g) {
+            const int r = r0 + g;
+            act[g] = r < R && sh.mode[r] == kModeSelect && sh.lo[r] > 0;
+            want[g] = act[g] ? sh.need[r] : 0;
+            lo[g] = act[g] ? sh.lo[r] : 0;
+            mine[g] = 0;
+            if (act[g]) {
+#pragma unroll
+                for (int e = 1; e <= kPerThread; ++e) mine[g] += (int)sh.hist[r][hi - e];
+            }
         }
-        want = quota;
-    }
-    if (above < want && above + mine >= want) {  // exactly one thread
-        const int w = min(kDigitBits, lo);
-        int cum = above, dgt = hi - 1;
-        for (; dgt > hi - kPerThread; --dgt) {
-            const int h = (int)sh.hist[r][dgt];
-            if (cum + h >= want) break;
-            cum += h;
+        int above[G], total[G];
+        block_exclusive_scan<G, NW>(mine, above, total, sh.scan);
+#pragma unroll
+        for (int g = 0; g < G; ++g) {
+            const int r = r0 + g;
+            if (!act[g]) continue;
+            if (quota != nullptr) {
+                const int q = max(quota[r], 0);
+                if (q == 0 || q >= total[g]) {
+                    if (tid == 0) sh.mode[r] = q == 0 ? kModeNone : kModeAll;
+                    continue;
+                }
+                want[g] = q;
+            }
+            if (above[g] < want[g] && above[g] + mine[g] >= want[g]) {  // exactly one thread
+                const int w = min(kDigitBits, lo[g]);
+                int cum = above[g], dgt = hi - 1;
+                for (; dgt > hi - kPerThread; --dgt) {
+                    const int h = (int)sh.hist[r][dgt];
+                    if (cum + h >= want[g]) break;
+                    cum += h;
+                }
+                sh.pref[r] = (lo[g] < 32 ? sh.pref[r] << w : 0u) | (uint32_t)dgt;
+                sh.need[r] = want[g] - cum;
+                sh.lo[r] = lo[g] - w;
+            }
         }
-        sh.pref[r] = (lo < 32 ? sh.pref[r] << w : 0u) | (uint32_t)dgt;
-        sh.need[r] = want - cum;
-        sh.lo[r] = lo - w;
     }
     __syncthreads();
 }
@@ -233,7 +267,7 @@ __global__ __launch_bounds__(NT) void topk_kernel(const float* __restrict__ scor
         }
     }
     __syncthreads();
-    for (int r = 0; r < R; ++r) find_digit(sh, r, max(quota[(size_t)b * R + r], 0));
+    find_digits(sh, quota + (size_t)b * R);
     if (tid <= R) {
         uint2 c = make_uint2(kNoKey, kNoKey);
         if (tid < R && sh.mode[tid] == kModeAll) c.x = 0u;
@@ -315,8 +349,7 @@ __global__ __launch_bounds__(NT) void topk_kernel(const float* __restrict__ scor
             }
         });
         __syncthreads();
-        for (int r = 0; r < R; ++r)
-            if (sh.mode[r] == kModeSelect && sh.lo[r] > 0) find_digit(sh, r, -1);  // uniform
+        find_digits(sh, static_cast<const int32_t*>(nullptr));
     }
 
     // 4. ordered output.  Class of a staged entry: 1 kept, 2 + r equal to bucket
@@ -391,9 +424,9 @@ constexpr int kCompactRows = 64;
 
 // One workgroup per (segment, 64 kept rows); a row is PARTS pieces of 16 bytes
 // (8, 16 or 32), piece e of the block being part e % PARTS of row e / PARTS.
-// Every thread takes 64 PARTS / 256 pieces and issues all its index loads, then
-// all its row loads, then all its stores, so that a block waits for memory
-// about twice instead of once per piece.
+// Every thread takes 64 PARTS / 256 pieces, in rounds of at most four: it
+// issues the round's index loads, then its row loads, then its stores, so that
+// a block waits for memory about twice per round instead of once per piece.
 template <int PARTS>
 __global__ __launch_bounds__(kThreads) void compact_kernel(const char* __restrict__ k,
                                                            const char* __restrict__ v,
@@ -403,35 +436,39 @@ __global__ __launch_bounds__(kThreads) void compact_kernel(const char* __restric
                                                            char* __restrict__ v_out) {
     constexpr int kRowBytes = PARTS * 16;
     constexpr int kItems = kCompactRows * PARTS / kThreads;
-    static_assert(kItems * kThreads == kCompactRows * PARTS, "whole pieces per thread");
+    constexpr int kRound = kItems < 4 ? kItems : 4;
+    static_assert(kItems * kThreads == kCompactRows * PARTS && kItems % kRound == 0, "whole pieces per thread");
     const int blk = blockIdx.x % nblk;
     const int seg = blockIdx.x / nblk;
     const int cnt = min(count[seg], k_cap);
     const int m0 = blk * kCompactRows;
     if (m0 >= cnt) return;
     const int total = min(kCompactRows, cnt - m0) * PARTS;
-    int t[kItems];
+    for (int i0 = 0; i0 < kItems; i0 += kRound) {
+        if (i0 * kThreads >= total) break;  // uniform
+        int t[kRound];
 #pragma unroll
-    for (int i = 0; i < kItems; ++i) {
-        const int e = min(i * kThreads + (int)threadIdx.x, total - 1);
-        t[i] = idx[(size_t)seg * k_cap + m0 + e / PARTS];
-    }
-    u32x4 kv[kItems], vv[kItems];
+        for (int i = 0; i < kRound; ++i) {
+            const int e = min((i0 + i) * kThreads + (int)threadIdx.x, total - 1);
+            t[i] = idx[(size_t)seg * k_cap + m0 + e / PARTS];
+        }
+        u32x4 kv[kRound], vv[kRound];
 #pragma unroll
-    for (int i = 0; i < kItems; ++i) {
-        const int e = min(i * kThreads + (int)threadIdx.x, total - 1);
-        const int tt = min(max(t[i], 0), N - 1);  // out-of-range indices are skipped below
-        const size_t src = ((size_t)seg * N + tt) * kRowBytes + (size_t)(e % PARTS) * 16;
-        kv[i] = ld16(k + src);
-        if (v != nullptr) vv[i] = ld16(v + src);
-    }
+        for (int i = 0; i < kRound; ++i) {
+            const int e = min((i0 + i) * kThreads + (int)threadIdx.x, total - 1);
+            const int tt = min(max(t[i], 0), N - 1);  // out-of-range indices are skipped below
+            const size_t src = ((size_t)seg * N + tt) * kRowBytes + (size_t)(e % PARTS) * 16;
+            kv[i] = ld16(k + src);
+            if (v != nullptr) vv[i] = ld16(v + src);
+        }
 #pragma unroll
-    for (int i = 0; i < kItems; ++i) {
-        const int e = i * kThreads + (int)threadIdx.x;
-        if (e < total && t[i] >= 0 && t[i] < N) {
-            const size_t dst = ((size_t)seg * k_cap + m0 + e / PARTS) * kRowBytes + (size_t)(e % PARTS) * 16;
-            st16(k_out + dst, kv[i]);
-            if (v != nullptr) st16(v_out + dst, vv[i]);
+        for (int i = 0; i < kRound; ++i) {
+            const int e = (i0 + i) * kThreads + (int)threadIdx.x;
+            if (e < total && t[i] >= 0 && t[i] < N) {
+                const size_t dst = ((size_t)seg * k_cap + m0 + e / PARTS) * kRowBytes + (size_t)(e % PARTS) * 16;
+                st16(k_out + dst, kv[i]);
+                if (v != nullptr) st16(v_out + dst, vv[i]);
+            }
         }
     }
 }

@@ -64,10 +64,10 @@ SNAP_CASES = [
     custom("g8", 1, 1, 16, 2, 513, 20, 128, 7, "bf16"),
     custom("rounds", 8, 2, 8, 4, 2000, 16, 128, 7, "bf16"),
     custom("wide", 1, 1, 8, 1, 3000, 64, 128, 7, "bf16"),
-    # 32 vsegs x 71 chunks: ranges of three 128-key chunks, the last one ragged
+    # 32 vsegs x 141 chunks: 71 ranges of two 64-key chunks, the last a single ragged chunk of 40 keys
     custom("multirange", 2, 2, 8, 8, 9000, 16, 128, 7, "bf16"),
     custom("f32multirange", 2, 2, 8, 4, 9000, 8, 64, 5, "f32"),
-    # wide pools across many ranges of 256 keys (half-widths 64 and 65)
+    # wide pools across many one-chunk ranges of 64 keys (half-widths 64 and 65)
     custom("pool129", 1, 2, 8, 4, 5000, 16, 128, 129, "bf16"),
     custom("pool131", 1, 2, 8, 4, 5000, 16, 128, 131, "bf16"),
     # a last range of 6 keys, shorter than the half-width 7
