@@ -143,12 +143,16 @@ def _stream(stream=None):
     return ctypes.c_void_p(s.cuda_stream)
 
 
-def _workspace(nbytes, device, workspace=None):
+def _workspace(size, device, workspace=None):
+    """(tensor, bytes) of the caller's workspace, or of one allocated here of
+    size() bytes (the size is only computed when allocating: the library checks
+    a caller's workspace itself)."""
     torch = _torch()
-    if nbytes == 0:
-        return None, 0
     if workspace is not None:
         return workspace, workspace.numel() * workspace.element_size()
+    nbytes = size()
+    if nbytes == 0:
+        return None, 0
     return torch.empty(int(nbytes), dtype=torch.uint8, device=device), int(nbytes)
 
 
@@ -175,7 +179,7 @@ def snapkv_score(q_win, k, pool_k: int, scale: float = 0.0, score=None, workspac
         raise ValueError("q_win and k disagree in L, B, d or dtype")
     if score is None:
         score = torch.empty((L, B, Hkv, N), dtype=torch.float32, device=k.device)
-    ws, wsb = _workspace(snapkv_workspace_size(L, B, Hq, Hkv, N, W, d), k.device, workspace)
+    ws, wsb = _workspace(lambda: snapkv_workspace_size(L, B, Hq, Hkv, N, W, d), k.device, workspace)
     _check(LIB.kve_snapkv_score(_dev(q_win, "q_win"), _dev(k, "k"), _dtype_code(k),
                                 L, B, Hq, Hkv, N, W, d, float(scale), int(pool_k),
                                 _dev(score, "score"), _ptr(ws), wsb, _stream(stream)))
@@ -196,7 +200,7 @@ def snapkv_score_lse(q_win, k, lse_win, pool_k: int, scale: float = 0.0, score=N
         raise ValueError("lse_win must be float32 [L, B, Hq, W]")
     if score is None:
         score = torch.empty((L, B, Hkv, N), dtype=torch.float32, device=k.device)
-    ws, wsb = _workspace(snapkv_workspace_size(L, B, Hq, Hkv, N, W, d), k.device, workspace)
+    ws, wsb = _workspace(lambda: snapkv_workspace_size(L, B, Hq, Hkv, N, W, d), k.device, workspace)
     _check(LIB.kve_snapkv_score_lse(_dev(q_win, "q_win"), _dev(k, "k"), _dev(lse_win, "lse_win"), _dtype_code(k),
                                     L, B, Hq, Hkv, N, W, d, float(scale), int(pool_k), _dev(score, "score"),
                                     _ptr(ws), wsb, _stream(stream)))
@@ -216,7 +220,7 @@ def h2o_score(q, k, scale: float = 0.0, score=None, workspace=None, stream=None)
         raise ValueError("q and k disagree in L, B, N, d or dtype")
     if score is None:
         score = torch.empty((L, B, Hkv, N), dtype=torch.float32, device=k.device)
-    ws, wsb = _workspace(h2o_workspace_size(L, B, Hq, Hkv, N, d), k.device, workspace)
+    ws, wsb = _workspace(lambda: h2o_workspace_size(L, B, Hq, Hkv, N, d), k.device, workspace)
     _check(LIB.kve_h2o_score(_dev(q, "q"), _dev(k, "k"), _dtype_code(k), L, B, Hq, Hkv, N, d,
                              float(scale), _dev(score, "score"), _ptr(ws), wsb, _stream(stream)))
     return score
@@ -235,7 +239,7 @@ def quest_score(q_win, k, page: int = 16, score=None, workspace=None, stream=Non
         raise ValueError("q_win and k disagree in L, B, d or dtype")
     if score is None:
         score = torch.empty((L, B, Hkv, N), dtype=torch.float32, device=k.device)
-    ws, wsb = _workspace(quest_workspace_size(L, B, Hq, Hkv, d), k.device, workspace)
+    ws, wsb = _workspace(lambda: quest_workspace_size(L, B, Hq, Hkv, d), k.device, workspace)
     _check(LIB.kve_quest_score(_dev(q_win, "q_win"), _dev(k, "k"), _dtype_code(k), L, B, Hq, Hkv, N, W, d,
                                int(page), _dev(score, "score"), _ptr(ws), wsb, _stream(stream)))
     return score
@@ -306,7 +310,7 @@ def topk_select(score, roles, quota, W: int, R: int, k_cap: int, idx_out=None, c
         idx_out = torch.full((L, B, Hkv, max(k_cap, 0)), -1, dtype=torch.int32, device=score.device)
     if count_out is None:
         count_out = torch.empty((L, B, Hkv), dtype=torch.int32, device=score.device)
-    ws, wsb = _workspace(topk_workspace_size(L, B, Hkv, N, R), score.device, workspace)
+    ws, wsb = _workspace(lambda: topk_workspace_size(L, B, Hkv, N, R), score.device, workspace)
     _check(LIB.kve_topk_select(_dev(score, "score"), _dev(roles, "roles"), _dev(quota, "quota"),
                                L, B, Hkv, N, int(W), int(R), int(k_cap),
                                _dev(idx_out, "idx_out"), _dev(count_out, "count_out"),
@@ -352,7 +356,7 @@ def decode_attention(q, k_c, v_c, count, scale: float = 0.0, out=None, workspace
         raise ValueError("count must be int32 [L, B, Hkv]")
     if out is None:
         out = torch.empty((L, B, Hq, d), dtype=torch.float32, device=k_c.device)
-    ws, wsb = _workspace(decode_workspace_size(L, B, Hq, Hkv, k_cap, d), k_c.device, workspace)
+    ws, wsb = _workspace(lambda: decode_workspace_size(L, B, Hq, Hkv, k_cap, d), k_c.device, workspace)
     _check(LIB.kve_decode_attention(_dev(q, "q"), _dev(k_c, "k_c"), _dev(v_c, "v_c"), _dev(count, "count"),
                                     _dtype_code(k_c), L, B, Hq, Hkv, k_cap, d, float(scale),
                                     _dev(out, "out"), _ptr(ws), wsb, _stream(stream)))

@@ -181,22 +181,22 @@ def evict(q, k, v, roles_host: np.ndarray, roles_dev, policy, budget: float, W: 
     bufs.quota_dev.copy_(bufs.quota_host, non_blocking=True)
     bufs.copy_done.record()
     L = k.shape[0]
+    main = torch.cuda.current_stream()
     if chunks <= 1 or side_stream is None:
         if score_events is not None:
-            score_events[0].record()
-        _score(q, k, bufs, scorer, pool_k, scale, page, 0, L, lse_win=lse_win)
+            score_events[0].record(main)
+        _score(q, k, bufs, scorer, pool_k, scale, page, 0, L, stream=main, lse_win=lse_win)
         if score_events is not None:
-            score_events[1].record()
-        _select(k, v, roles_dev, bufs, W, R, 0, L)
+            score_events[1].record(main)
+        _select(k, v, roles_dev, bufs, W, R, 0, L, stream=main)
         return quota, kept
-    main = torch.cuda.current_stream()
     side_stream.wait_stream(main)         # the quota upload and earlier work
     per = (L + chunks - 1) // chunks
     if score_events is not None:
         score_events[0].record(main)
     for l0 in range(0, L, per):
         l1 = min(L, l0 + per)
-        _score(q, k, bufs, scorer, pool_k, scale, page, l0, l1, lse_win=lse_win)
+        _score(q, k, bufs, scorer, pool_k, scale, page, l0, l1, stream=main, lse_win=lse_win)
         done = torch.cuda.Event()
         done.record(main)
         side_stream.wait_event(done)
