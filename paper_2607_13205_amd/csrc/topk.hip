@@ -251,19 +251,29 @@ __global__ __launch_bounds__(NT) void topk_kernel(const float* __restrict__ scor
     for (int e = tid; e < R * kDigits; e += NT) (&sh.hist[0][0])[e] = 0u;
     __syncthreads();
 
-    // 1. histogram sweep: the top digit of every labelled candidate's key
-    for (int base = 0; base < P; base += kGroupStep) {
-        const int t0 = base + kSpan * tid;
-        if (t0 < P) {
-            float s[kSpan];
-            uint32_t lab[4];
-            load_span<VEC>(sc, ro, t0, N, s, lab);
-            const int nv = min(kSpan, P - t0);
+    // 1. histogram sweep: the top digit of every labelled candidate's key; each
+    //    step's span is in flight while the previous one is counted
+    {
+        float s[kSpan] = {}, sn[kSpan] = {};
+        uint32_t lab[4] = {}, labn[4] = {};
+        int t0 = kSpan * tid;
+        if (t0 < P) load_span<VEC>(sc, ro, t0, N, s, lab);
+        for (int base = 0; base < P; base += kGroupStep) {
+            const int tn = t0 + kGroupStep;
+            if (tn < P) load_span<VEC>(sc, ro, tn, N, sn, labn);
+            if (t0 < P) {
+                const int nv = min(kSpan, P - t0);
 #pragma unroll
-            for (int e = 0; e < kSpan; ++e) {
-                const uint32_t r = bucket_of<R>(lab, e);
-                if (e < nv && r < (uint32_t)R) atomicAdd(&sh.hist[r][score_key(s[e]) >> kLowBits], 1u);
+                for (int e = 0; e < kSpan; ++e) {
+                    const uint32_t r = bucket_of<R>(lab, e);
+                    if (e < nv && r < (uint32_t)R) atomicAdd(&sh.hist[r][score_key(s[e]) >> kLowBits], 1u);
+                }
             }
+#pragma unroll
+            for (int e = 0; e < kSpan; ++e) s[e] = sn[e];
+#pragma unroll
+            for (int j = 0; j < 4; ++j) lab[j] = labn[j];
+            t0 = tn;
         }
     }
     __syncthreads();
@@ -285,31 +295,41 @@ __global__ __launch_bounds__(NT) void topk_kernel(const float* __restrict__ scor
     const int w0 = min(N, wave * run), w1 = min(N, w0 + run);
     uint2* st = stage + (size_t)seg * N + w0;  // room for w1 - w0 entries
     int n_st = 0;
-    for (int s0 = w0; s0 < w1; s0 += kWaveStep) {
-        const int t0 = s0 + kSpan * lane;
-        const int nv = max(0, min(kSpan, w1 - t0));
-        float s[kSpan];
-        uint32_t lab[4];
-        // lanes past the run load an in-bounds span and stage nothing
-        load_span<VEC>(sc, ro, VEC ? min(t0, N - kSpan) : t0, N, s, lab);
-        uint32_t smask = 0u, tag[kSpan];
+    {
+        // each step's span is in flight while the previous one is staged; lanes
+        // past the run load an in-bounds span and stage nothing
+        float s[kSpan] = {}, sn[kSpan] = {};
+        uint32_t lab[4] = {}, labn[4] = {};
+        int t0 = w0 + kSpan * lane;
+        if (w0 < w1) load_span<VEC>(sc, ro, VEC ? min(t0, N - kSpan) : t0, N, s, lab);
+        for (int s0 = w0; s0 < w1; s0 += kWaveStep) {
+            const int tn = t0 + kWaveStep;
+            if (s0 + kWaveStep < w1) load_span<VEC>(sc, ro, VEC ? min(tn, N - kSpan) : tn, N, sn, labn);
+            const int nv = max(0, min(kSpan, w1 - t0));
+            uint32_t smask = 0u, tag[kSpan];
 #pragma unroll
-        for (int e = 0; e < kSpan; ++e) {
-            const int t = t0 + e;
-            const uint32_t key = score_key(s[e]);
-            const uint32_t r = t < P ? bucket_of<R>(lab, e) : (uint32_t)R;
-            const uint2 c = sh.stage_cls[r];
-            const bool keep = t >= P || key >= c.x;
-            const bool cand = (key >> kLowBits) == c.y;
-            tag[e] = keep ? kKept : ((r << kLowBits) | (key & kLowMask));
-            smask |= (e < nv && (keep || cand)) ? (1u << e) : 0u;
+            for (int e = 0; e < kSpan; ++e) {
+                const int t = t0 + e;
+                const uint32_t key = score_key(s[e]);
+                const uint32_t r = t < P ? bucket_of<R>(lab, e) : (uint32_t)R;
+                const uint2 c = sh.stage_cls[r];
+                const bool keep = t >= P || key >= c.x;
+                const bool cand = (key >> kLowBits) == c.y;
+                tag[e] = keep ? kKept : ((r << kLowBits) | (key & kLowMask));
+                smask |= (e < nv && (keep || cand)) ? (1u << e) : 0u;
+            }
+            int tot;
+            uint2* dst = st + n_st + wave_exclusive_scan(__popc(smask), tot);
+#pragma unroll
+            for (int e = 0; e < kSpan; ++e)
+                if ((smask >> e) & 1u) *dst++ = make_uint2((uint32_t)(t0 + e), tag[e]);
+            n_st += tot;
+#pragma unroll
+            for (int e = 0; e < kSpan; ++e) s[e] = sn[e];
+#pragma unroll
+            for (int j = 0; j < 4; ++j) lab[j] = labn[j];
+            t0 = tn;
         }
-        int tot;
-        uint2* dst = st + n_st + wave_exclusive_scan(__popc(smask), tot);
-#pragma unroll
-        for (int e = 0; e < kSpan; ++e)
-            if ((smask >> e) & 1u) *dst++ = make_uint2((uint32_t)(t0 + e), tag[e]);
-        n_st += tot;
     }
     __syncthreads();
 
