@@ -262,6 +262,16 @@ def graph_leg(pipeline, inp, alpha, budget, W, pool, bufs, scorer, steps, lse_wi
                       "allocation on the host"}
 
 
+def _optional_leg(name, fn):
+    """Run an optional leg of the bench; a failure becomes an error entry in the
+    output line instead of ending the run (the main step is already timed)."""
+    try:
+        return fn()
+    except Exception as e:  # noqa: BLE001 - reported, not hidden
+        print(f"[bench] {name} leg failed: {e!r}", file=sys.stderr, flush=True)
+        return {"error": f"{type(e).__name__}: {e}"}
+
+
 def _time_calls(fn, steps):
     import torch
     for _ in range(2):
@@ -494,30 +504,34 @@ def main():
     }
     if not args.no_graph and args.chunks <= 1:
         print("[bench] step through a HIP graph", file=sys.stderr, flush=True)
-        out["graph"] = graph_leg(pipeline, inp, alpha, budget, W, pool, bufs, scorer, max(3, args.steps // 2),
-                                 lse_win=main_lse)
+        out["graph"] = _optional_leg("graph", lambda: graph_leg(
+            pipeline, inp, alpha, budget, W, pool, bufs, scorer, max(3, args.steps // 2), lse_win=main_lse))
     if not args.no_decode and scorer == "snapkv":
         print("[bench] decode over the compacted and the full cache", file=sys.stderr, flush=True)
-        out["decode"] = decode_leg(K, wl, inp, bufs, max(3, args.steps // 2))
+        out["decode"] = _optional_leg("decode", lambda: decode_leg(K, wl, inp, bufs, max(3, args.steps // 2)))
     del bufs
     torch.cuda.empty_cache()
     if lse is not None and not args.lse and not args.no_lse:
         print("[bench] supplied window statistics", file=sys.stderr, flush=True)
-        out["prefill_lse"] = lse_leg(K, pipeline, wl, inp, lse, budget, alpha, max(3, args.steps // 2))
+        out["prefill_lse"] = _optional_leg("prefill_lse", lambda: lse_leg(
+            K, pipeline, wl, inp, lse, budget, alpha, max(3, args.steps // 2)))
     if not args.no_quest and scorer == "snapkv":
         print("[bench] Quest scorer", file=sys.stderr, flush=True)
-        out["quest"] = quest_leg(K, pipeline, wl, inp, budget, alpha, max(3, args.steps // 2))
+        out["quest"] = _optional_leg("quest", lambda: quest_leg(
+            K, pipeline, wl, inp, budget, alpha, max(3, args.steps // 2)))
     if not args.no_probe:
-        out["probe"] = probe_leg(K, wl, max(3, args.steps // 2))
+        out["probe"] = _optional_leg("probe", lambda: probe_leg(K, wl, max(3, args.steps // 2)))
     if not args.no_policies:
         print("[bench] fair-eviction and No-KEY steps", file=sys.stderr, flush=True)
-        out["policies"] = policy_leg(WL, pipeline, wl, inp, budget, W, pool, max(3, args.steps // 2))
+        out["policies"] = _optional_leg("policies", lambda: policy_leg(
+            WL, pipeline, wl, inp, budget, W, pool, max(3, args.steps // 2)))
     if not args.no_h2o and wl.name != "h2o16k":
         print("[bench] H2O leg", file=sys.stderr, flush=True)
-        out["h2o"] = h2o_leg(K, WL, max(3, args.steps // 2))
+        out["h2o"] = _optional_leg("h2o", lambda: h2o_leg(K, WL, max(3, args.steps // 2)))
     if not args.no_cpu_baseline:
         print("[bench] CPU oracle baseline", file=sys.stderr, flush=True)
-        out["cpu_baseline"] = cpu_baseline(wl, inp, budget, alpha, args.cpu_seconds)
+        out["cpu_baseline"] = _optional_leg("cpu_baseline", lambda: cpu_baseline(
+            wl, inp, budget, alpha, args.cpu_seconds))
     print(json.dumps(out), flush=True)
 
 
