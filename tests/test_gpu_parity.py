@@ -217,6 +217,29 @@ def test_topk_many_segments_take_the_four_wave_workgroups(K, R, N):
     _topk_check(K, score, roles, quota, W, R)
 
 
+@pytest.mark.parametrize("N,W", [(1, 0), (1, 1), (2, 0), (2, 1), (3, 3), (17, 0), (17, 5), (16, 16)])
+def test_topk_very_short_rows(K, N, W):
+    """Rows shorter than one 16-position span, a row that is all window, and a
+    call that keeps nothing (k_cap 0, empty index output)."""
+    rng = np.random.default_rng(70 + 31 * N + W)
+    L, B, Hkv, R = 1, 2, 3, 3
+    score = np.zeros((L, B, Hkv, N), dtype=np.float32)
+    roles = np.zeros((B, N), dtype=np.int8)
+    for b in range(B):
+        _, roles[b] = _random_selection_case(rng, N, R + 1, R)
+        for j in range(Hkv):
+            score[0, b, j], _ = _random_selection_case(rng, N, R, R)
+    quota = rng.integers(0, 3, (B, R)).astype(np.int32)
+    _topk_check(K, score, roles, quota, W, R)
+    if W == 0:
+        # nothing kept at all: zero quotas, k_cap 0
+        zero = np.zeros((B, R), dtype=np.int32)
+        idx, cnt = K.topk_select(torch.from_numpy(score).cuda(), torch.from_numpy(roles).cuda(),
+                                 torch.from_numpy(zero).cuda(), W, R, 0)
+        torch.cuda.synchronize()
+        assert idx.shape[-1] == 0 and not cnt.cpu().numpy().any()
+
+
 def test_topk_misaligned_rows_take_the_per_position_loads(K):
     """N a multiple of 16 but the score and label rows not 16-byte aligned."""
     rng = np.random.default_rng(41)
