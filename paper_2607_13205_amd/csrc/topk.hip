@@ -34,19 +34,18 @@
 namespace kve {
 namespace {
 
-constexpr int kThreads = 256;      // top-k workgroup when segments fill the chip (and compaction)
-constexpr int kWideThreads = 1024; // top-k workgroup when there are few segments
-constexpr int kWideBelow = 512;    // segments below which the wide workgroup is used
-constexpr int kMaxR = 8;  // buckets supported (one kernel instantiation each)
+constexpr int kThreads = 256;        // top-k workgroup when segments fill the chip (and compaction)
+constexpr int kWideThreads = 1024;   // top-k workgroup when there are few segments
+constexpr int kWideBelow = 512;      // segments below which the wide workgroup is used
 constexpr int kDigitBits = 11;
 constexpr int kDigits = 1 << kDigitBits;
 constexpr int kLowBits = 32 - kDigitBits;  // key bits below the top digit
 constexpr uint32_t kLowMask = (1u << kLowBits) - 1u;
-constexpr int kSpan = 16;                     // consecutive positions per lane and step
-constexpr int kWaveStep = kWave * kSpan;  // positions per wave step
-constexpr int kBatch = 8;                     // staged entries per lane loaded before use
-constexpr uint32_t kNoKey = 0xffffffffu;      // above every key (+inf maps to 0xff800000)
-constexpr uint32_t kKept = 0xffffffffu;       // tag of a staged position that is surely kept
+constexpr int kSpan = 16;                  // consecutive positions per lane and step
+constexpr int kWaveStep = kWave * kSpan;   // positions per wave step
+constexpr int kBatch = 8;                  // staged entries per lane loaded before use
+constexpr uint32_t kNoKey = 0xffffffffu;   // above every key (+inf maps to 0xff800000)
+constexpr uint32_t kKept = 0xffffffffu;    // tag of a staged position that is surely kept
 
 enum : int { kModeNone = 0, kModeSelect = 1, kModeAll = 2 };
 
@@ -224,13 +223,10 @@ __device__ __forceinline__ uint32_t bucket_of(const uint32_t (&lab)[4], int e) {
 }
 
 template <int R, bool VEC, int NT>
-__global__ __launch_bounds__(NT) void topk_kernel(const float* __restrict__ score,
-                                                        const int8_t* __restrict__ roles,
-                                                        const int32_t* __restrict__ quota, int B,
-                                                        int Hkv, int N, int W, int k_cap,
-                                                        int32_t* __restrict__ idx_out,
-                                                        int32_t* __restrict__ count_out,
-                                                        uint2* __restrict__ stage) {
+__global__ __launch_bounds__(NT) void topk_kernel(const float* __restrict__ score, const int8_t* __restrict__ roles,
+                                                  const int32_t* __restrict__ quota, int B, int Hkv, int N, int W,
+                                                  int k_cap, int32_t* __restrict__ idx_out,
+                                                  int32_t* __restrict__ count_out, uint2* __restrict__ stage) {
     constexpr int NW = NT / kWave;
     constexpr int kGroupStep = NT * kSpan;  // positions per workgroup step
     __shared__ TopkShared<R, NW> sh;
