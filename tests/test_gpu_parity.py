@@ -832,6 +832,20 @@ def test_quest_full_size_one_layer(K):
         check_quest_or_scores(sc[0, b, j].cpu().numpy().astype(np.float64), ref, wl.W, f"quest stack32k {(b, j)}")
 
 
+def test_quest_full_size_all_layers(K):
+    """The Quest leg's launch configuration: all 32 layers of stack32k in one
+    call; sampled segments against the oracle."""
+    wl = WL.get_workload("stack32k")
+    note("quest stack32k, all layers in one call (sampled segments)")
+    inp = WL.make_inputs(wl, device="cuda", with_v=False)
+    sc = K.quest_score(inp["q"], inp["k"], 16)
+    torch.cuda.synchronize()
+    for (l, b, j) in [(0, 0, 0), (13, 1, 4), (31, 3, 7)]:
+        ref = O.quest_mass(f64(inp["q"][l, b, j * wl.G:(j + 1) * wl.G]), f64(inp["k"][l, b, j]), 16)
+        check_quest_or_scores(sc[l, b, j].cpu().numpy().astype(np.float64), ref, wl.W,
+                              f"quest stack32k {(l, b, j)}")
+
+
 # ---------------------------------------------------------------------------
 # Linear role probe
 # ---------------------------------------------------------------------------
