@@ -529,6 +529,7 @@ def test_determinism(K):
     ("long128k", 0.05, [(0, 0, 0), (31, 0, 7)], "role"),
     ("long128k", 0.20, [(13, 0, 2)], "role"),
     ("h2o16k", 0.10, [(0, 0, 3)], "no_key"),
+    ("h2o16k", 0.10, [(0, 0, 1), (0, 0, 6)], "role"),
 ])
 def test_pipeline_full_size_sampled(K, name, budget, segs, pol):
     """Real shapes, the launch configuration the benchmark times; the oracle
@@ -749,20 +750,6 @@ def test_decode_after_eviction_layer8k(K):
     wl = WL.get_workload("layer8k")
     inp = WL.make_inputs(wl, device="cuda")
     _decode_after_eviction(K, wl, inp, 0.1, list(np.ndindex(len(inp["layers"]), wl.B, wl.Hkv)))
-
-
-@pytest.mark.parametrize("name,budget,segs", [
-    ("stack32k", 0.05, [(0, 0, 0), (17, 2, 5), (31, 3, 7)]),
-    ("long128k", 0.20, [(0, 0, 3), (31, 0, 6)]),
-])
-def test_decode_after_eviction_full_size(K, name, budget, segs):
-    """The decode leg's launch configuration: one query per head over the
-    compacted cache of all layers in one call, at the workload's full size;
-    sampled segments against the oracle's keep-mask decode over the full cache."""
-    wl = WL.get_workload(name)
-    note(f"decode after eviction {name} B={budget} (full size, sampled segments)")
-    inp = WL.make_inputs(wl, device="cuda")
-    _decode_after_eviction(K, wl, inp, budget, segs)
 
 
 # ---------------------------------------------------------------------------
