@@ -262,6 +262,39 @@ def graph_leg(pipeline, inp, alpha, budget, W, pool, bufs, scorer, steps, lse_wi
                       "allocation on the host"}
 
 
+def select_figures(wl, inp, bufs, ms_topk, ms_compact):
+    """Achieved rates of the top-k and the compaction inside the timed steps.
+    Top-k algorithmic bytes: every score read once, the labels once per layer
+    (1/Hkv byte per token and head), the kept indices written; compaction: the
+    kept K and V rows read and written."""
+    import torch
+    L, B, Hkv, N, d = inp["k"].shape
+    elem = inp["k"].element_size()
+    kept = int(torch.clamp(bufs.count, 0, bufs.k_cap).sum().item())
+    topk_bytes = L * B * Hkv * N * 4 + L * B * N + kept * 4
+    compact_bytes = kept * d * elem * (2 if bufs.v_out is not None else 1) * 2
+    gbs_t = topk_bytes / (ms_topk * 1e-3) / 1e9
+    gbs_c = compact_bytes / (ms_compact * 1e-3) / 1e9
+    return {"topk_ms": round(ms_topk, 4), "topk_algorithmic_bytes": topk_bytes,
+            "topk_GBs": round(gbs_t, 1), "topk_hbm_frac": round(gbs_t / HBM_PEAK_GBS, 4),
+            "compact_ms": round(ms_compact, 4), "compact_bytes": compact_bytes,
+            "compact_GBs": round(gbs_c, 1), "compact_hbm_frac": round(gbs_c / HBM_PEAK_GBS, 4)}
+
+
+def copy_ceiling(repeats=5):
+    """A plain 1 GiB device-to-device copy (the runtime's copy kernel): bytes read
+    and written per second, the practical ceiling of a read-and-write kernel."""
+    import torch
+    src = torch.empty(COPY_BYTES, dtype=torch.uint8, device="cuda")
+    dst = torch.empty_like(src)
+    ms = _time_calls(lambda: dst.copy_(src), repeats)
+    gbs = 2 * COPY_BYTES / (ms * 1e-3) / 1e9
+    del src, dst
+    torch.cuda.empty_cache()
+    return {"bytes_moved": 2 * COPY_BYTES, "ms": round(ms, 4), "GBs": round(gbs, 1),
+            "hbm_frac": round(gbs / HBM_PEAK_GBS, 4)}
+
+
 def _optional_leg(name, fn):
     """Run an optional leg of the bench; a failure becomes an error entry in the
     output line instead of ending the run (the main step is already timed)."""
@@ -452,6 +485,7 @@ def main():
     # score-call timing (HIP events on the launch stream)
     ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
           for _ in range(args.steps)]
+    sel = [tuple(torch.cuda.Event(enable_timing=True) for _ in range(3)) for _ in range(args.steps)]
     t_all0 = torch.cuda.Event(enable_timing=True)
     t_all1 = torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
@@ -459,11 +493,14 @@ def main():
     for i in range(args.steps):
         pipeline.evict(inp["q"], inp["k"], inp["v"], inp["roles"], inp["roles_t"], alpha, budget,
                        W, pool, bufs, scorer=scorer, score_events=ev[i], chunks=args.chunks,
-                       side_stream=side, lse_win=main_lse)
+                       side_stream=side, lse_win=main_lse,
+                       select_events=sel[i] if args.chunks <= 1 else None)
     t_all1.record()
     torch.cuda.synchronize()
     ms_step = t_all0.elapsed_time(t_all1) / args.steps
     ms_score = sum(a.elapsed_time(b) for a, b in ev) / args.steps
+    ms_topk = sum(a.elapsed_time(b) for a, b, _ in sel) / args.steps if args.chunks <= 1 else None
+    ms_compact = sum(b.elapsed_time(c) for _, b, c in sel) / args.steps if args.chunks <= 1 else None
     tokens = wl.B * wl.N
     value = tokens / (ms_step * 1e-3)
     score_bytes = snapkv_algorithmic_bytes(wl)
@@ -502,6 +539,9 @@ def main():
             "ms": round(ms_score, 4), "algorithmic_bytes": score_bytes,
         },
     }
+    if ms_topk is not None:
+        out["select"] = select_figures(wl, inp, bufs, ms_topk, ms_compact)
+    out["copy_ceiling"] = _optional_leg("copy_ceiling", copy_ceiling)
     if not args.no_graph and args.chunks <= 1:
         print("[bench] step through a HIP graph", file=sys.stderr, flush=True)
         out["graph"] = _optional_leg("graph", lambda: graph_leg(

@@ -139,19 +139,28 @@ def _score(q, k, bufs, scorer, pool_k, scale, page, l0, l1, stream=None, lse_win
                      stream=stream)
 
 
-def _select(k, v, roles_dev, bufs, W, R, l0, l1, stream=None):
-    """Top-k and compaction of layers [l0, l1) on ``stream`` (None: current)."""
+def _select(k, v, roles_dev, bufs, W, R, l0, l1, stream=None, events=None):
+    """Top-k and compaction of layers [l0, l1) on ``stream`` (None: current);
+    ``events``, three torch.cuda.Event, are recorded before the top-k, between
+    the two calls and after the compaction."""
+    if events is not None:
+        events[0].record(stream)
     kb.topk_select(bufs.score[l0:l1], roles_dev, bufs.quota_dev, W, R, bufs.k_cap,
                    idx_out=bufs.idx[l0:l1], count_out=bufs.count[l0:l1], workspace=bufs.ws_topk,
                    stream=stream)
+    if events is not None:
+        events[1].record(stream)
     kb.kv_compact(k[l0:l1], None if v is None else v[l0:l1], bufs.idx[l0:l1], bufs.count[l0:l1],
                   k_out=bufs.k_out[l0:l1], v_out=None if bufs.v_out is None else bufs.v_out[l0:l1],
                   stream=stream)
+    if events is not None:
+        events[2].record(stream)
 
 
 def evict(q, k, v, roles_host: np.ndarray, roles_dev, policy, budget: float, W: int,
           pool_k: int, bufs: EvictBuffers, scorer: str = "snapkv", scale: float = 0.0,
-          score_events=None, page: int = 16, chunks: int = 1, side_stream=None, lse_win=None):
+          score_events=None, page: int = 16, chunks: int = 1, side_stream=None, lse_win=None,
+          select_events=None):
     """One eviction step; returns (quota [B, R] host, kept [B] host).
 
     q is the window queries [L, B, Hq, W, d] (SnapKV; Quest, which scores
@@ -159,7 +168,9 @@ def evict(q, k, v, roles_host: np.ndarray, roles_dev, policy, budget: float, W: 
     (H2O, which uses W = 0 and no pool).  roles_host / roles_dev are the bucket
     labels [B, N] of ``policy`` (a Policy, or the weights of the
     role-conditional policy).  ``score_events``, a pair of torch.cuda.Event,
-    brackets the score calls on the launch stream.  ``lse_win`` (SnapKV only),
+    brackets the score calls on the launch stream, and ``select_events``, three
+    events, bracket the top-k and the compaction (unchunked steps only).
+    ``lse_win`` (SnapKV only),
     the window rows' log-sum-exp [L, B, Hq, W] as the prefill attention
     returned it, lets the score read K once.
 
@@ -188,7 +199,7 @@ def evict(q, k, v, roles_host: np.ndarray, roles_dev, policy, budget: float, W: 
         _score(q, k, bufs, scorer, pool_k, scale, page, 0, L, stream=main, lse_win=lse_win)
         if score_events is not None:
             score_events[1].record(main)
-        _select(k, v, roles_dev, bufs, W, R, 0, L, stream=main)
+        _select(k, v, roles_dev, bufs, W, R, 0, L, stream=main, events=select_events)
         return quota, kept
     side_stream.wait_stream(main)         # the quota upload and earlier work
     per = (L + chunks - 1) // chunks
