@@ -281,6 +281,30 @@ def select_figures(wl, inp, bufs, ms_topk, ms_compact):
             "compact_GBs": round(gbs_c, 1), "compact_hbm_frac": round(gbs_c / HBM_PEAK_GBS, 4)}
 
 
+def flushed_leg(step, steps):
+    """Per-step times (HIP events around the step alone) with 512 MiB written to a
+    scratch buffer before every step, so that neither the L2s nor the 256 MB
+    last-level cache hold anything of the previous step; the median is reported."""
+    import statistics
+    import torch
+    scratch = torch.empty(512 << 20, dtype=torch.uint8, device="cuda")
+    times = []
+    for i in range(steps + 1):
+        scratch.fill_(i & 0xff)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        step()
+        e1.record()
+        torch.cuda.synchronize()
+        if i:  # the first is a warmup
+            times.append(e0.elapsed_time(e1))
+    del scratch
+    torch.cuda.empty_cache()
+    return {"median_ms_per_step": round(statistics.median(times), 4),
+            "min_ms": round(min(times), 4), "max_ms": round(max(times), 4), "steps": steps,
+            "flush": "512 MiB written before every step, outside the timed events"}
+
+
 def copy_ceiling(repeats=5):
     """A plain 1 GiB device-to-device copy (the runtime's copy kernel): bytes read
     and written per second, the practical ceiling of a read-and-write kernel."""
@@ -542,6 +566,7 @@ def main():
     if ms_topk is not None:
         out["select"] = select_figures(wl, inp, bufs, ms_topk, ms_compact)
     out["copy_ceiling"] = _optional_leg("copy_ceiling", copy_ceiling)
+    out["flushed"] = _optional_leg("flushed", lambda: flushed_leg(step, max(5, args.steps)))
     if not args.no_graph and args.chunks <= 1:
         print("[bench] step through a HIP graph", file=sys.stderr, flush=True)
         out["graph"] = _optional_leg("graph", lambda: graph_leg(
