@@ -183,7 +183,20 @@ def cpu_baseline(wl, inp, budget, alpha, target_s):
     tokens_per_s = units * wl.N / wl.L / el
     return {"value": tokens_per_s, "unit": "tokens/s", "cores": int(threads), "kind": "oracle",
             "sample": f"{units} (layer, sample) units of {wl.name} ({wl.Hkv} KV heads, N={wl.N}) "
-                      f"in {el:.1f} s: float64 score, pool, selection and compaction"}
+                      f"in {el:.1f} s: float64 score, pool, selection and compaction",
+            "host_cpus": os.cpu_count(), "cpu_model": _cpu_model()}
+
+
+def _cpu_model():
+    """The host CPU's model name as /proc/cpuinfo gives it (None elsewhere)."""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
 
 
 def h2o_leg(K, WL, steps):
