@@ -158,7 +158,7 @@ kve_status_t kve_h2o_score(const void* q, const void* k, kve_dtype_t dtype,
                            void* stream);
 
 /* ------------------------------------------------------------------------- */
-/* One-shot Quest analogue (paper §5 "Query-aware baseline"): page key bounds  */
+/* One-shot Quest analogue (paper §4.1 "Query-aware baseline"): page key bounds  */
 /* against the mean window query, a second scorer for the same selection.     */
 /* ------------------------------------------------------------------------- */
 
@@ -230,7 +230,7 @@ kve_status_t kve_role_allocate(const int8_t* roles, int B, int N, int R,
                                int32_t* k_cap_out);
 
 /*
- * Fair-eviction quotas (§5 "Fair-eviction baseline": the same retention rate
+ * Fair-eviction quotas (§4.1 "Fair-eviction baseline": the same retention rate
  * for every bucket).  kve_role_allocate with each sample's own bucket
  * populations as the weights, alpha_r = n_r: with P = N - W candidates and
  * K_p as above, bucket r keeps ceil(n_r * K_p / P) of its n_r candidates (no
@@ -246,7 +246,7 @@ kve_status_t kve_role_allocate_fair(const int8_t* roles, int B, int N, int R,
 /*
  * Bucket relabelling: out[i] = map[roles[i]] for i < n.  With it the same
  * allocator and top-k express policies over a coarser partition than the
- * labels, e.g. the No-X counterfactual of §3 ("Counterfactual", Table 2):
+ * labels, e.g. the No-X counterfactual of §4 ("Counterfactual", Table 2):
  * map role X to bucket 1 and every other role to bucket 0, then allocate with
  * alpha = (1, 0), so that the K_p prefix slots go to the best-scoring tokens
  * of any role but X.

@@ -19,9 +19,12 @@ Every function names the passage of the paper it follows (section, equation,
 algorithm or table).  The readings taken where the paper is silent are listed
 in the module docstring of ``reference``.
 
-Parity status: every function here is pinned by ``tests/test_oracle_*.py``
-against closed forms, invariants, library routines, brute force or numbers the
-paper prints; none is "parity unpinned".
+Parity status: every exported function is pinned by ``tests/test_oracle_*.py``
+(directly, or through the function that calls it: ``quest_page_bounds``
+through ``quest_mass``, ``rank_key`` through ``select_keep``) against closed
+forms, invariants, library routines, brute force or numbers the paper prints.
+The whole-tensor wrappers ``snapkv_score``, ``h2o_score`` and ``quest_score``,
+which group query heads into KV heads, have their own grouping pins.
 """
 
 from .reference import *  # noqa: F401,F403

@@ -64,13 +64,17 @@ def pool_loops(s, W, kernel):
     return out
 
 
+def _rank(score, idx):
+    """Sort key of a candidate, best first: every number before every NaN
+    (NaN ranks below -inf), then the larger score, then the lower index."""
+    if math.isnan(score):
+        return (1, 0.0, idx)
+    return (0, -score, idx)
+
+
 def _better(a_score, a_idx, b_score, b_idx):
-    """True when candidate a outranks b: larger score, then lower index."""
-    ka = -math.inf if math.isnan(a_score) else a_score
-    kb = -math.inf if math.isnan(b_score) else b_score
-    if ka != kb:
-        return ka > kb
-    return a_idx < b_idx
+    """True when candidate a outranks b (see _rank)."""
+    return _rank(a_score, a_idx) < _rank(b_score, b_idx)
 
 
 def select_exhaustive(score, roles, quota, W):
@@ -87,7 +91,7 @@ def select_exhaustive(score, roles, quota, W):
         q = min(q, len(cand))
         best = None
         for sub in itertools.combinations(cand, q):
-            ordered = sorted(sub, key=lambda t: (-(-math.inf if math.isnan(score[t]) else score[t]), t))
+            ordered = sorted(sub, key=lambda t: _rank(score[t], t))
             if best is None or _lex_better(ordered, best, score):
                 best = ordered
         keep.update(best)
@@ -124,7 +128,7 @@ def decode_loops(q_heads, k, v, keep, scale=None):
 
 
 def quest_loops(q_win, k, page):
-    """Page bounds of the one-shot Quest analogue with loops (§5 "Query-aware
+    """Page bounds of the one-shot Quest analogue with loops (§4.1 "Query-aware
     baseline"): q_win[h][i] window rows of head h, k the key rows; returns the
     score of every position (window positions: +inf)."""
     G, W, d = len(q_win), len(q_win[0]), len(k[0])

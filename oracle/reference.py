@@ -34,14 +34,14 @@ that uses it):
       budget B >= 1 is the full-cache baseline and keeps all N tokens;
   R12 equal scores: the lower token index wins;
   R13 -0.0 ranks equal to +0.0 and NaN ranks below every number;
-  R17 the No-X counterfactual (§3 "Counterfactual", Table 2) keeps the same
+  R17 the No-X counterfactual (§4 "Counterfactual", Table 2) keeps the same
       K_p prefix slots as the other policies, filled by score from the prefix
       tokens whose role is not X; when fewer such tokens exist the slots left
       stay empty;
-  R18 fair eviction (§5 "Fair-eviction baseline") retains every bucket at the
+  R18 fair eviction (§4.1 "Fair-eviction baseline") retains every bucket at the
       same rate: bucket r keeps ceil(n_r * K_p / P) of its n_r candidates, the
       ceiling of R7 as for the role policy;
-  R20 the one-shot Quest analogue (§5 "Query-aware baseline") scores pages of
+  R20 the one-shot Quest analogue (§4.1 "Query-aware baseline") scores pages of
       16 consecutive prefix tokens (the last one ragged; the window belongs to
       no page) by Quest's per-channel key bound against each head's mean
       window query, summed over the G heads of the group (as R2 sums their
@@ -86,7 +86,6 @@ __all__ = [
     "fair_allocate_batch",
     "rank_key",
     "select_keep",
-    "topk_select",
     "kv_compact",
     "PROBE_OFFSETS",
     "probe_logits",
@@ -257,7 +256,7 @@ def h2o_score(q: np.ndarray, k: np.ndarray, n_kv_heads: int,
 
 
 def quest_page_bounds(q_mean: np.ndarray, k: np.ndarray, page: int) -> np.ndarray:
-    """Quest's page bound (§5 "Query-aware baseline"; R20) for the pages of
+    """Quest's page bound (§4.1 "Query-aware baseline"; R20) for the pages of
     the key rows k [P, d]: page j covers rows [j*page, min((j+1)*page, P)).
     For each head h, sum_c max(qbar_h[c] * kmin_j[c], qbar_h[c] * kmax_j[c])
     with kmin/kmax the per-channel minimum and maximum of the page's keys,
@@ -375,7 +374,7 @@ def role_allocate_batch(roles: np.ndarray, R: int, alpha, budget: float, W: int)
 
 # ---------------------------------------------------------------------------
 # Other policies over the same partition-and-allocate container: the No-X
-# counterfactual (§3 "Counterfactual", Table 2) and fair eviction (§5)
+# counterfactual (§4 "Counterfactual", Table 2) and fair eviction (§4.1)
 # ---------------------------------------------------------------------------
 
 def role_map(roles: np.ndarray, bucket_of) -> np.ndarray:
@@ -403,7 +402,7 @@ def no_role_keep(score: np.ndarray, roles: np.ndarray, x: int, budget: float,
                  W: int) -> np.ndarray:
     """Kept indices of one segment under No-X, from the definition (R17): the
     window, plus the K_p best-scoring prefix tokens whose role is not x (score
-    descending, index ascending; NaN last), ascending."""
+    descending, index ascending; NaN below every number), ascending."""
     score = np.asarray(score, dtype=np.float64)
     roles = np.asarray(roles)
     N = score.shape[0]
@@ -411,9 +410,9 @@ def no_role_keep(score: np.ndarray, roles: np.ndarray, x: int, budget: float,
         return np.arange(N, dtype=np.int64)
     K = min(N, ceil_guarded(budget * N))
     K_p = max(0, K - W)
-    key = np.where(np.isnan(score), -np.inf, score)
+    nan = np.isnan(score)
     allowed = [t for t in range(N - W) if roles[t] != x]
-    allowed.sort(key=lambda t: (-key[t], t))
+    allowed.sort(key=lambda t: (1, 0.0, t) if nan[t] else (0, -score[t], t))
     kept = allowed[:K_p] + list(range(N - W, N))
     return np.array(sorted(kept), dtype=np.int64)
 
@@ -452,11 +451,15 @@ def fair_allocate_batch(roles: np.ndarray, R: int, budget: float, W: int):
 # Selection and compaction
 # ---------------------------------------------------------------------------
 
-def rank_key(score: np.ndarray) -> np.ndarray:
-    """Value used for ranking: NaN becomes -inf (R13).  -0.0 already compares
-    equal to +0.0 in IEEE arithmetic, so equal keys fall back to the index."""
+def rank_key(score: np.ndarray):
+    """Ranking keys (R13): (is_nan, value) with NaN values replaced by 0.
+    Candidates are ordered by is_nan ascending (every number, -inf included,
+    before every NaN), then by value descending, then by index ascending.
+    -0.0 already compares equal to +0.0 in IEEE arithmetic, so equal values
+    fall back to the index."""
     s = np.asarray(score, dtype=np.float64)
-    return np.where(np.isnan(s), -np.inf, s)
+    nan = np.isnan(s)
+    return nan, np.where(nan, 0.0, s)
 
 
 def select_keep(score: np.ndarray, roles: np.ndarray, quota, W: int) -> np.ndarray:
@@ -470,25 +473,16 @@ def select_keep(score: np.ndarray, roles: np.ndarray, quota, W: int) -> np.ndarr
     score = np.asarray(score)
     roles = np.asarray(roles)
     N = score.shape[0]
-    key = rank_key(score)
+    nan, key = rank_key(score)
     keep = [np.arange(N - W, N)]
     t_all = np.arange(N - W)
     for r, q in enumerate(quota):
         cand = t_all[roles[:N - W] == r]
         if q <= 0 or cand.size == 0:
             continue
-        order = np.lexsort((cand, -key[cand]))      # last key is primary
+        order = np.lexsort((cand, -key[cand], nan[cand]))      # last key is primary
         keep.append(cand[order[:int(q)]])
     return np.sort(np.concatenate(keep)).astype(np.int64)
-
-
-def topk_select(score: np.ndarray, roles: np.ndarray, quota: np.ndarray,
-                W: int) -> list:
-    """select_keep over score [L, B, Hkv, N] with roles [B, N], quota [B, R].
-    Returns a nested list idx[l][b][j] of ascending int64 arrays."""
-    L, Bt, H, N = score.shape
-    return [[[select_keep(score[l, b, j], roles[b], quota[b], W)
-              for j in range(H)] for b in range(Bt)] for l in range(L)]
 
 
 def kv_compact(kv: np.ndarray, idx: np.ndarray) -> np.ndarray:

@@ -1,4 +1,4 @@
-// One-shot Quest analogue (§5 "Query-aware baseline"): the candidate prefix
+// One-shot Quest analogue (§4.1 "Query-aware baseline"): the candidate prefix
 // of every segment (layer, sample, KV head) is cut into pages of `page`
 // consecutive tokens (the last one ragged; the window belongs to no page).
 // A page's score is Quest's key bound: per head h of the group, the sum over

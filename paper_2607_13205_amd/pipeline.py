@@ -6,8 +6,8 @@ per-role top-k  ->  K/V compaction.  Buffers are allocated once by
 ``EvictBuffers`` so that repeated steps allocate nothing.
 
 ``Policy`` names how the budget is split over buckets: the role-conditional
-weights of §4.1, fair eviction (§5, the same rate for every bucket) or the
-No-X counterfactual of §3 (one role banned from the prefix).
+weights of §4.1, fair eviction (§4.1, the same rate for every bucket) or the
+No-X counterfactual of §4 (one role banned from the prefix).
 """
 
 from __future__ import annotations

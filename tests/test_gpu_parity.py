@@ -257,7 +257,7 @@ def test_topk_misaligned_rows_take_the_per_position_loads(K):
 
 
 @pytest.mark.parametrize("case", ["all_equal", "all_nan", "two_values", "window_only", "no_window",
-                                  "one_bin", "inf"])
+                                  "one_bin", "inf", "nan_below_neginf"])
 def test_topk_degenerate_inputs(K, case):
     """Every key in the threshold's bin, every key tied, no prefix, no window."""
     rng = np.random.default_rng(50)
@@ -282,6 +282,13 @@ def test_topk_degenerate_inputs(K, case):
     elif case == "inf":
         score[rng.random(score.shape) < 0.3] = np.inf
         score[rng.random(score.shape) < 0.3] = -np.inf
+    elif case == "nan_below_neginf":
+        # about 10% finite, 45% -inf, 45% NaN: the quotas put bucket boundaries
+        # inside the -inf run and inside the NaN run (NaN ranks below -inf)
+        u = rng.random(score.shape)
+        score[u < 0.45] = -np.inf
+        score[u > 0.55] = np.nan
+        quota = np.array([[400, 0, 350], [1, 2000, 380]], dtype=np.int32)
     _topk_check(K, score, roles, quota, W, R)
 
 
@@ -478,7 +485,7 @@ def _policy(name):
 @pytest.mark.parametrize("pol,budget", [("no_key", 0.1), ("no_key", 0.5), ("no_sink", 0.3),
                                         ("no_value", 0.75), ("fair", 0.1)])
 def test_pipeline_h2o_policies(K, pol, budget):
-    """The counterfactual No-X conditions over the H2O score (§3), and fair
+    """The counterfactual No-X conditions over the H2O score (§4), and fair
     eviction, through the same allocator, top-k and compaction."""
     wl = custom("h2o_pol", 1, 2, 8, 2, 1500, 0, 128, 1, "bf16", scorer="h2o")
     note(f"pipeline h2o {pol} B={budget}")

@@ -136,6 +136,7 @@ def test_allocation_rejects_bad_arguments():
 def _tie_scores(r, N):
     s = r.integers(0, 4, N).astype(np.float64) / 4.0      # many exact ties
     s[r.random(N) < 0.1] = -0.0
+    s[r.random(N) < 0.1] = -np.inf
     s[r.random(N) < 0.1] = np.nan
     return s
 
@@ -164,6 +165,26 @@ def test_selection_tie_rule_lower_index_and_nan_last():
     assert O.select_keep(s, roles, [3], 2).tolist() == [0, 1, 3, 6, 7]
     assert O.select_keep(s, roles, [5], 2).tolist() == [0, 1, 3, 4, 5, 6, 7]
     assert O.select_keep(s, roles, [6], 2).tolist() == [0, 1, 2, 3, 4, 5, 6, 7]
+
+
+def test_selection_ranks_nan_below_minus_infinity():
+    """NaN ranks strictly below -inf (not equal to it): with the boundary
+    inside a run of -inf and NaN scores, every -inf is taken before any NaN,
+    whatever their positions; NaNs among themselves go lowest index first."""
+    s = np.array([np.nan, -np.inf, np.nan, -np.inf, 1.0, np.nan])
+    roles = np.zeros(6, dtype=np.int8)
+    assert O.select_keep(s, roles, [1], 0).tolist() == [4]
+    assert O.select_keep(s, roles, [2], 0).tolist() == [1, 4]
+    assert O.select_keep(s, roles, [3], 0).tolist() == [1, 3, 4]
+    assert O.select_keep(s, roles, [4], 0).tolist() == [0, 1, 3, 4]
+    assert O.select_keep(s, roles, [5], 0).tolist() == [0, 1, 2, 3, 4]
+    for q in range(7):
+        assert O.select_keep(s, roles, [q], 0).tolist() == brute.select_exhaustive(s.tolist(), [0] * 6, [q], 0)
+    # two buckets with the boundary of each between -inf and NaN
+    roles2 = np.array([0, 1, 1, 0, 0, 1], dtype=np.int8)
+    assert O.select_keep(s, roles2, [2, 1], 0).tolist() == [1, 3, 4]
+    # the No-X definition ranks the same way
+    assert O.no_role_keep(s, np.zeros(6, dtype=np.int8), 1, 0.5, 0).tolist() == [1, 3, 4]
 
 
 def test_neutral_single_bucket_is_plain_snapkv():

@@ -1,6 +1,6 @@
 """Pins of the oracle's other policies over the partition-and-allocate
-container: fair eviction (§5 "Fair-eviction baseline") and the No-X
-counterfactual (§3 "Counterfactual", Table 2).
+container: fair eviction (§4.1 "Fair-eviction baseline") and the No-X
+counterfactual (§4 "Counterfactual", Table 2).
 
 Fair eviction is pinned by its closed form in exact rational arithmetic (the
 same retention rate K_p / P for every bucket, rounded up per bucket); No-X by

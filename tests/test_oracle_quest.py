@@ -1,4 +1,4 @@
-"""Pins of the oracle's one-shot Quest analogue (§5 "Query-aware baseline").
+"""Pins of the oracle's one-shot Quest analogue (§4.1 "Query-aware baseline").
 
 The page bound is pinned by pure-Python loops, by its defining property (no
 key of a page scores above the page's bound, and the bound is reached when a
@@ -100,3 +100,29 @@ def test_selection_keeps_whole_pages_in_bound_order(seed):
                 take.append(t)
     ref = sorted(take + list(range(P, N)))
     assert got.tolist() == ref and len(got) == kept
+
+
+def test_quest_wrapper_groups_heads_contiguously_and_sums_them():
+    """oracle.quest_score: query heads 0,1 read KV head 0 and heads 2,3 KV
+    head 1, and the bounds of a group's heads are summed.  Heads 0,1 have mean
+    window query 2*e0, heads 2,3 mean 2*e1; pages of 2 tokens, N = 10, W = 2
+    (four pages).  KV head 0: keys zero except t = 2 (3 along e0, page 1) and
+    t = 5 (5 along e1, page 2); KV head 1: t = 1 (4 along e0, page 0) and t = 6
+    (2 along e1, page 3).  With contiguous groups only the channel a group
+    looks along counts: KV head 0 scores page 1 at 2 heads * 2 * 3 = 12, KV
+    head 1 page 3 at 2 * 2 * 2 = 8, every other page 0 and the window +inf.
+    A strided grouping (heads 0,2 | 1,3) would score page 2 of KV head 0 at
+    10 and page 1 at 6."""
+    N, W, d, page = 10, 2, 4, 2
+    q = np.zeros((1, 1, 4, W, d))
+    q[0, 0, 0:2, :, 0] = 2.0
+    q[0, 0, 2:4, :, 1] = 2.0
+    k = np.zeros((1, 1, 2, N, d))
+    k[0, 0, 0, 2, 0] = 3.0
+    k[0, 0, 0, 5, 1] = 5.0
+    k[0, 0, 1, 1, 0] = 4.0
+    k[0, 0, 1, 6, 1] = 2.0
+    s = O.quest_score(q, k, n_kv_heads=2, page=page)
+    inf = np.inf
+    assert s[0, 0, 0].tolist() == [0, 0, 12, 12, 0, 0, 0, 0, inf, inf]
+    assert s[0, 0, 1].tolist() == [0, 0, 0, 0, 0, 0, 8, 8, inf, inf]

@@ -163,6 +163,33 @@ def test_gqa_groups_are_contiguous_and_summed():
     assert s[0, 0, 0, 3] > 0.99 * 2 * W
 
 
+def test_h2o_wrapper_groups_heads_contiguously_and_sums_them():
+    """oracle.h2o_score: query heads 0,1 read KV head 0 and heads 2,3 KV head 1
+    (contiguous groups), and the mass of a group's heads is summed.  Heads 0,1
+    look along e0, heads 2,3 along e1; KV head 0 has one key large along e0
+    (t = 3), KV head 1 one key large along e1 (t = 5).  With contiguous groups
+    each head of a group puts nearly all its mass on that key from the first
+    query that sees it, so s(3) and s(5) approach G * (N - t); a strided
+    grouping (heads 0,2 | 1,3) halves them, a swapped one moves the argmax."""
+    N, d, G = 10, 4, 2
+    q = np.zeros((1, 1, 4, N, d))
+    q[0, 0, 0:2, :, 0] = 6.0
+    q[0, 0, 2:4, :, 1] = 6.0
+    k = np.zeros((1, 1, 2, N, d))
+    k[0, 0, 0, 3, 0] = 3.0
+    k[0, 0, 1, 5, 1] = 3.0
+    s = O.h2o_score(q, k, n_kv_heads=2, scale=1.0)
+    assert s.shape == (1, 1, 2, N)
+    assert np.argmax(s[0, 0, 0]) == 3 and np.argmax(s[0, 0, 1]) == 5
+    assert s[0, 0, 0, 3] > 0.999 * G * (N - 3)
+    assert s[0, 0, 1, 5] > 0.999 * G * (N - 5)
+    # every query row's probabilities sum to 1: total mass G * N per KV head
+    np.testing.assert_allclose(s[0, 0].sum(axis=1), [G * N, G * N], rtol=1e-12)
+    # keys before the spike share each query's mass uniformly: key 0 of KV
+    # head 0 gets 1, 1/2, 1/3 from queries 0..2 of each of the two heads
+    np.testing.assert_allclose(s[0, 0, 0, 0], G * (1 + 1 / 2 + 1 / 3), rtol=1e-6)
+
+
 @pytest.mark.parametrize("seed", range(4))
 def test_brute_force_agreement(seed):
     r = _rng(100 + seed)
