@@ -61,6 +61,11 @@ typedef enum kve_dtype {
 /* ABI version (KVE_ABI_VERSION of the built library). */
 int kve_version(void);
 
+/* SHA-256 (64 hex digits) of the sources and build flags the library was
+ * compiled from, as computed by the package's build script; "unknown" for a
+ * build that did not supply it.  Static storage, never freed. */
+const char* kve_source_hash(void);
+
 /* Message describing the last error returned on the calling thread ("" if none).
  * The pointer stays valid until the next kve_* call on the same thread. */
 const char* kve_last_error(void);

@@ -28,7 +28,7 @@ DTYPE_F32 = 1
 
 #: every symbol include/kve.h declares
 EXPORTED = (
-    "kve_version", "kve_last_error",
+    "kve_version", "kve_last_error", "kve_source_hash",
     "kve_snapkv_workspace_size", "kve_snapkv_score", "kve_snapkv_score_lse",
     "kve_h2o_workspace_size", "kve_h2o_score",
     "kve_role_allocate", "kve_role_allocate_fair", "kve_role_map", "kve_role_probe",
@@ -56,6 +56,7 @@ def _load():
     sig = {
         "kve_version": (c_int, []),
         "kve_last_error": (ctypes.c_char_p, []),
+        "kve_source_hash": (ctypes.c_char_p, []),
         "kve_snapkv_workspace_size": (c_size, [c_int] * 7),
         "kve_snapkv_score": (c_int, [c_void, c_void, c_int] + [c_int] * 7 +
                              [c_float, c_int, c_void, c_void, c_size, c_void]),
@@ -104,6 +105,11 @@ LIB = _Lib()
 
 def last_error() -> str:
     return LIB.kve_last_error().decode()
+
+
+def source_hash() -> str:
+    """SHA-256 of the sources the loaded library was built from."""
+    return LIB.kve_source_hash().decode()
 
 
 def _check(status: int):

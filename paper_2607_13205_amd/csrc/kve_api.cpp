@@ -170,6 +170,11 @@ extern "C" {
 
 int kve_version(void) { return KVE_ABI_VERSION; }
 
+#ifndef KVE_SOURCE_HASH
+#define KVE_SOURCE_HASH "unknown"
+#endif
+const char* kve_source_hash(void) { return KVE_SOURCE_HASH; }
+
 const char* kve_last_error(void) { return g_error.c_str(); }
 
 size_t kve_snapkv_workspace_size(int L, int B, int Hq, int Hkv, int N, int W, int d) {

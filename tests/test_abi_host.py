@@ -29,12 +29,21 @@ def _declared():
 
 def test_every_declared_symbol_is_exported(kve):
     names = _declared()
-    assert len(names) == 18
+    assert len(names) == 19
     assert sorted(kve.EXPORTED) == names
     lib = ctypes.CDLL(kve.binding._LIB_PATH)
     for n in names:
         assert hasattr(lib, n), n
     assert kve.binding.LIB.kve_version() == 1
+
+
+def test_library_reports_the_hash_of_its_sources(kve):
+    """The loaded library was built from the present csrc/ and include/ (the
+    build embeds the hash; ensure_built rebuilds when the sources change)."""
+    from paper_2607_13205_amd.build import built_hash, source_hash
+    h = kve.source_hash()
+    assert re.fullmatch(r"[0-9a-f]{64}", h), h
+    assert h == source_hash() == built_hash()
 
 
 @pytest.mark.parametrize("ex_seed", range(3))
