@@ -131,6 +131,34 @@ kve_status_t kve_snapkv_score_lse(const void* q_win, const void* k, const float*
                                   int W, int d, float scale, int pool_k, float* score,
                                   void* workspace, size_t workspace_bytes, void* stream);
 
+/*
+ * kve_snapkv_score for callers that cannot allocate device memory (code under
+ * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc):
+ * the same kernels and the same result, bit for bit, with the workspace taken
+ * from a static device array of kve_snapkv_scratch_bytes() bytes (64 MiB)
+ * instead of a caller's buffer.  The call allocates nothing.  Each GPU the
+ * library runs on holds its own copy of the array from the library's first
+ * use on it until the process ends; its address is taken on the first call
+ * on each device (the current device, to which `stream` must belong).
+ *
+ * Every call on a GPU shares that GPU's array: calls that overlap in time on
+ * one GPU (different streams, or host threads enqueueing concurrently) race on
+ * it and must be serialised by the caller.  The array's contents on entry do
+ * not matter (nothing in it needs to start at zero).
+ *
+ * Arguments as for kve_snapkv_score, without the workspace.  Errors: as for
+ * kve_snapkv_score; KVE_ERR_WORKSPACE when kve_snapkv_workspace_size() of
+ * these shapes exceeds kve_snapkv_scratch_bytes() (about 15 layers of a
+ * batch-4, 8-KV-head, N = 32768 stack fit; split larger problems by layer);
+ * KVE_ERR_HIP when the array's address cannot be obtained.
+ */
+kve_status_t kve_snapkv_score_noalloc(const void* q_win, const void* k, kve_dtype_t dtype,
+                                      int L, int B, int Hq, int Hkv, int N, int W, int d,
+                                      float scale, int pool_k, float* score, void* stream);
+
+/* Size in bytes of the static scratch array of kve_snapkv_score_noalloc. */
+size_t kve_snapkv_scratch_bytes(void);
+
 /* ------------------------------------------------------------------------- */
 /* H2O accumulated score, the baseline scorer (paper §2, H2O family).         */
 /* ------------------------------------------------------------------------- */

@@ -16,7 +16,7 @@ The hot path runs in libkve.so (HIP); this package is its thin Python binding:
   pipeline.evict the whole step over resident tensors
 """
 
-from .binding import (EXPORTED, KveError, decode_attention, decode_workspace_size,  # noqa: F401
+from .binding import (EXPORTED, KveError, decode_attention, decode_workspace_size, snapkv_score_noalloc,  # noqa: F401
                       h2o_score, h2o_workspace_size, kv_compact, last_error, quest_score, source_hash,
                       quest_workspace_size, role_allocate,
                       role_allocate_fair, role_map, role_probe, snapkv_score, snapkv_score_lse, snapkv_workspace_size,
@@ -26,4 +26,5 @@ from . import pipeline  # noqa: F401
 __all__ = ["snapkv_score", "h2o_score", "role_allocate", "role_allocate_fair", "role_map",
            "topk_select", "kv_compact", "snapkv_workspace_size", "h2o_workspace_size", "KveError",
            "last_error", "pipeline", "decode_attention", "decode_workspace_size", "quest_score",
-           "quest_workspace_size", "role_probe", "snapkv_score_lse", "topk_workspace_size", "source_hash"]
+           "quest_workspace_size", "role_probe", "snapkv_score_lse", "topk_workspace_size", "source_hash",
+           "snapkv_score_noalloc"]

@@ -30,6 +30,7 @@ DTYPE_F32 = 1
 EXPORTED = (
     "kve_version", "kve_last_error", "kve_source_hash",
     "kve_snapkv_workspace_size", "kve_snapkv_score", "kve_snapkv_score_lse",
+    "kve_snapkv_score_noalloc", "kve_snapkv_scratch_bytes",
     "kve_h2o_workspace_size", "kve_h2o_score",
     "kve_role_allocate", "kve_role_allocate_fair", "kve_role_map", "kve_role_probe",
     "kve_topk_workspace_size", "kve_topk_select",
@@ -62,6 +63,9 @@ def _load():
                              [c_float, c_int, c_void, c_void, c_size, c_void]),
         "kve_snapkv_score_lse": (c_int, [c_void, c_void, c_void, c_int] + [c_int] * 7 +
                                  [c_float, c_int, c_void, c_void, c_size, c_void]),
+        "kve_snapkv_score_noalloc": (c_int, [c_void, c_void, c_int] + [c_int] * 7 +
+                                     [c_float, c_int, c_void, c_void]),
+        "kve_snapkv_scratch_bytes": (c_size, []),
         "kve_h2o_workspace_size": (c_size, [c_int] * 6),
         "kve_h2o_score": (c_int, [c_void, c_void, c_int] + [c_int] * 6 +
                           [c_float, c_void, c_void, c_size, c_void]),
@@ -210,6 +214,22 @@ def snapkv_score_lse(q_win, k, lse_win, pool_k: int, scale: float = 0.0, score=N
     _check(LIB.kve_snapkv_score_lse(_dev(q_win, "q_win"), _dev(k, "k"), _dev(lse_win, "lse_win"), _dtype_code(k),
                                     L, B, Hq, Hkv, N, W, d, float(scale), int(pool_k), _dev(score, "score"),
                                     _ptr(ws), wsb, _stream(stream)))
+    return score
+
+
+def snapkv_score_noalloc(q_win, k, pool_k: int, scale: float = 0.0, score=None, stream=None):
+    """snapkv_score with the workspace taken from the library's static device
+    scratch array (kve_snapkv_score_noalloc): the library allocates nothing."""
+    torch = _torch()
+    L, B, Hq, W, d = q_win.shape
+    Lk, Bk, Hkv, N, dk = k.shape
+    if (L, B, d) != (Lk, Bk, dk) or q_win.dtype != k.dtype:
+        raise ValueError("q_win and k disagree in L, B, d or dtype")
+    if score is None:
+        score = torch.empty((L, B, Hkv, N), dtype=torch.float32, device=k.device)
+    _check(LIB.kve_snapkv_score_noalloc(_dev(q_win, "q_win"), _dev(k, "k"), _dtype_code(k),
+                                        L, B, Hq, Hkv, N, W, d, float(scale), int(pool_k),
+                                        _dev(score, "score"), _stream(stream)))
     return score
 
 

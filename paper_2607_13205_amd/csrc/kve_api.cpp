@@ -136,9 +136,12 @@ int32_t allocate_sample(const long long* n, const double* alpha, int R, double b
     return (int32_t)sum;
 }
 
+// use_scratch: the workspace is this GPU's static scratch array (workspace
+// and workspace_bytes are ignored); the plan must fit in it
 kve_status_t snapkv_common(const char* fn, const void* q_win, const void* k, const float* lse_win,
                            kve_dtype_t dtype, int L, int B, int Hq, int Hkv, int N, int W, int d, float scale,
-                           int pool_k, float* score, void* workspace, size_t workspace_bytes, void* stream) {
+                           int pool_k, float* score, void* workspace, size_t workspace_bytes, void* stream,
+                           bool use_scratch = false) {
     kve_status_t st = check_common(fn, L, B, Hq, Hkv, N, d, (int)dtype);
     if (st != KVE_OK) return st;
     if (q_win == nullptr || k == nullptr || score == nullptr)
@@ -154,10 +157,20 @@ kve_status_t snapkv_common(const char* fn, const void* q_win, const void* k, con
     const kve::SnapPlan p = kve::snap_plan(L, B, Hq, Hkv, N, W, d, dtype == KVE_DTYPE_BF16 ? 2 : 4);
     if ((long long)p.n_vsegs * p.nranges > kMaxGrid)
         return fail(KVE_ERR_UNSUPPORTED, "%s: shape too large", fn);
-    if (workspace_bytes < p.total || (p.total > 0 && workspace == nullptr))
-        return fail(KVE_ERR_WORKSPACE, "%s: workspace of %zu bytes < %zu needed", fn, workspace_bytes,
-                    p.total);
-    if (!aligned(workspace)) return fail(KVE_ERR_INVALID_ARG, "%s: workspace not 256-byte aligned", fn);
+    if (use_scratch) {
+        if (p.total > kve::kSnapScratchBytes)
+            return fail(KVE_ERR_WORKSPACE,
+                        "%s: these shapes need %zu bytes of workspace, above the %zu-byte static scratch "
+                        "(call kve_snapkv_score with a workspace, or fewer layers per call)",
+                        fn, p.total, kve::kSnapScratchBytes);
+        const hipError_t e = kve::snapkv_scratch(&workspace);
+        if (e != hipSuccess) return from_hip(e, fn);
+    } else {
+        if (workspace_bytes < p.total || (p.total > 0 && workspace == nullptr))
+            return fail(KVE_ERR_WORKSPACE, "%s: workspace of %zu bytes < %zu needed", fn, workspace_bytes,
+                        p.total);
+        if (!aligned(workspace)) return fail(KVE_ERR_INVALID_ARG, "%s: workspace not 256-byte aligned", fn);
+    }
     if (scale == 0.0f) scale = 1.0f / std::sqrt((float)d);
     return from_hip(kve::launch_snapkv(q_win, k, lse_win, (int)dtype, L, B, Hq, Hkv, N, W, d, scale, pool_k,
                                        score, workspace, static_cast<hipStream_t>(stream)),
@@ -200,6 +213,15 @@ kve_status_t kve_snapkv_score_lse(const void* q_win, const void* k, const float*
     return snapkv_common("kve_snapkv_score_lse", q_win, k, lse_win, dtype, L, B, Hq, Hkv, N, W, d, scale,
                          pool_k, score, workspace, workspace_bytes, stream);
 }
+
+kve_status_t kve_snapkv_score_noalloc(const void* q_win, const void* k, kve_dtype_t dtype, int L, int B, int Hq,
+                                      int Hkv, int N, int W, int d, float scale, int pool_k, float* score,
+                                      void* stream) {
+    return snapkv_common("kve_snapkv_score_noalloc", q_win, k, nullptr, dtype, L, B, Hq, Hkv, N, W, d, scale,
+                         pool_k, score, nullptr, 0, stream, true);
+}
+
+size_t kve_snapkv_scratch_bytes(void) { return kve::kSnapScratchBytes; }
 
 size_t kve_h2o_workspace_size(int L, int B, int Hq, int Hkv, int N, int d) {
     (void)Hkv;

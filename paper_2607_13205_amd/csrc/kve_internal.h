@@ -98,6 +98,10 @@ hipError_t launch_snapkv(const void* q, const void* k, const float* lse_win, int
                          int Hkv, int N, int W, int d, float scale, int pool_k, float* score, void* ws,
                          hipStream_t st);
 
+// Device address of this GPU's static SnapKV scratch array (kSnapScratchBytes
+// bytes), taken once per device with that device current.
+hipError_t snapkv_scratch(void** out);
+
 hipError_t launch_h2o(const void* q, const void* k, int dtype, int L, int B, int Hq, int Hkv,
                       int N, int d, float scale, float* score, void* ws, hipStream_t st);
 

@@ -24,6 +24,10 @@ constexpr int kSnapChunkKeys = 64;
 constexpr int kSnapTargetGroups = 4096;  // workgroups per pass the range size aims at
 constexpr int kSnapMaxRangeChunks = 32;  // at most 2048 keys per range
 
+// Bytes of the static device scratch array the allocation-free SnapKV entry
+// point uses as its workspace (one copy per GPU, held until the process ends).
+constexpr size_t kSnapScratchBytes = (size_t)64 << 20;
+
 struct SnapPlan {
     int segs, rows, sets, rpg, rgroups, n_vsegs, range_keys, nranges, planes;
     size_t off_stats, off_lse, off_raw, total;

@@ -29,9 +29,17 @@
 //
 // Logits are kept in log2 units (x = scale * log2(e) * <q, k>) so that every
 // exponential is a single v_exp_f32.
+#include <mutex>
+
 #include "kve_device.h"
+#include "kve_internal.h"
 #include "kve_snap_plan.h"
 #include "kve_stream.h"
+
+// Workspace of the allocation-free entry point: a static device array, one
+// copy per GPU the library runs on.  In host code its name is not a device
+// address; kernels only ever receive the address snapkv_scratch() returns.
+static __device__ __align__(256) char scratch[kve::kSnapScratchBytes];
 
 namespace kve {
 namespace {
@@ -468,6 +476,29 @@ hipError_t run_snapkv(const void* q, const void* k, const float* lse_win, int L,
 }
 
 }  // namespace
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch[kMaxDevices];  // device address of `scratch`, per device
+}  // namespace
+
+hipError_t snapkv_scratch(void** out) {
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (g_scratch[dev] == nullptr) {
+        void* p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return e;
+        if (p == nullptr) return hipErrorInvalidSymbol;
+        g_scratch[dev] = p;
+    }
+    *out = g_scratch[dev];
+    return hipSuccess;
+}
 
 hipError_t launch_snapkv(const void* q, const void* k, const float* lse_win, int dtype, int L, int B, int Hq,
                          int Hkv, int N, int W, int d, float scale, int pool_k, float* score, void* ws,
