@@ -9,9 +9,16 @@ workload is the 32-layer Llama-3-8B-shaped stack (32 query / 8 KV heads,
 d=128, N=32768, W=32, pool 7, batch 4, B=0.05) on synthetic inputs.
 
 Prints one JSON line.  ``value`` is prefill tokens scored and compressed per
-second (a token counts once it has passed through all layers and KV heads);
-``roofline`` refers to the SnapKV score call, timed with HIP events on the
-stream it is launched on; ``cpu_baseline`` times the float64 CPU oracle on a
+second (a token counts once it has passed through all layers and KV heads) at
+``ms_per_step``, the median of the K timed steps, each run after 512 MiB have
+been written to a scratch buffer so that no cache holds the previous step's
+data (``loop`` gives the mean of K back-to-back steps as well); ``roofline``
+refers to the SnapKV score call, timed with HIP events on the stream it is
+launched on (mean over the timed steps); ``long128k`` times the 131072-token
+32-layer stack at B = 0.05 and 0.20 the same way; ``read_ceilings`` gives the
+streaming HBM read rate and the last-level-cache re-read rate of a plain read
+kernel; ``near_ties`` counts, on the last timed step's scores, the selection
+boundaries a relative score change of 1e-3 could move; ``cpu_baseline`` times the float64 CPU oracle on a
 bounded sample of the same workload; ``policies`` gives the step time of the
 same workload under fair eviction and the No-KEY counterfactual, which reuse
 every kernel with other quotas; ``decode`` times one decode query per head over
@@ -82,6 +89,8 @@ def parse():
                     help="skip the fair-eviction and No-KEY step timings")
     ap.add_argument("--no-graph", action="store_true",
                     help="skip the step timing through a captured HIP graph")
+    ap.add_argument("--no-long", action="store_true", help="skip the long128k legs")
+    ap.add_argument("--no-ceilings", action="store_true", help="skip the read-ceiling probes")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a plain device copy of 1 GiB (5 times), for counter calibration")
     return ap.parse_args()
@@ -243,16 +252,7 @@ def policy_leg(WL, pipeline, wl, inp, budget, W, pool, steps):
             pipeline.evict(inp["q"], inp["k"], inp["v"], buckets, buckets_t, pol, budget, W, pool,
                            bufs, scorer=wl.scorer)
 
-        for _ in range(2):
-            step()
-        torch.cuda.synchronize()
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record()
-        for _ in range(steps):
-            step()
-        e1.record()
-        torch.cuda.synchronize()
-        out[name] = {"ms_per_step": round(e0.elapsed_time(e1) / steps, 4), "k_cap": k_cap,
+        out[name] = {"ms_per_step": round(_median_calls(step, steps), 4), "k_cap": k_cap,
                      "kept_mean": round(float(kept.mean()), 1)}
         del bufs
         torch.cuda.empty_cache()
@@ -267,7 +267,7 @@ def graph_leg(pipeline, inp, alpha, budget, W, pool, bufs, scorer, steps, lse_wi
     idx0, cnt0 = bufs.idx.clone(), bufs.count.clone()
     g = pipeline.StepGraph(inp["q"], inp["k"], inp["v"], inp["roles_t"], alpha, W, pool, bufs, scorer=scorer,
                            lse_win=lse_win)
-    ms = _time_calls(lambda: g.replay(inp["roles"], budget), steps)
+    ms = _median_calls(lambda: g.replay(inp["roles"], budget), steps)
     torch.cuda.synchronize()
     same = bool(torch.equal(bufs.idx, idx0) and torch.equal(bufs.count, cnt0))
     return {"ms_per_step": round(ms, 4), "matches_eager": same,
@@ -294,28 +294,84 @@ def select_figures(wl, inp, bufs, ms_topk, ms_compact):
             "compact_GBs": round(gbs_c, 1), "compact_hbm_frac": round(gbs_c / HBM_PEAK_GBS, 4)}
 
 
-def flushed_leg(step, steps):
-    """Per-step times (HIP events around the step alone) with 512 MiB written to a
-    scratch buffer before every step, so that neither the L2s nor the 256 MB
-    last-level cache hold anything of the previous step; the median is reported."""
+def flushed_steps(run, steps, with_select=True):
+    """Time `steps` eviction steps one by one, 512 MiB written to a scratch
+    buffer before each (outside its events) so that neither the L2s nor the
+    256 MB last-level cache hold anything of the previous step.  run(score_ev,
+    select_ev) runs one step recording the given events.  Returns the median,
+    minimum and maximum step time and the mean score, top-k and compaction
+    times (ms)."""
     import statistics
     import torch
     scratch = torch.empty(512 << 20, dtype=torch.uint8, device="cuda")
-    times = []
-    for i in range(steps + 1):
+    mk = lambda n: tuple(torch.cuda.Event(enable_timing=True) for _ in range(n))  # noqa: E731
+    step_ev = [mk(2) for _ in range(steps)]
+    score_ev = [mk(2) for _ in range(steps)]
+    sel_ev = [mk(3) for _ in range(steps)]
+    torch.cuda.synchronize()
+    for i in range(steps):
         scratch.fill_(i & 0xff)
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record()
-        step()
-        e1.record()
+        step_ev[i][0].record()
+        run(score_ev[i], sel_ev[i] if with_select else None)
+        step_ev[i][1].record()
         torch.cuda.synchronize()
-        if i:  # the first is a warmup
-            times.append(e0.elapsed_time(e1))
     del scratch
+    times = [a.elapsed_time(b) for a, b in step_ev]
+    out = {"median_ms": statistics.median(times), "min_ms": min(times), "max_ms": max(times),
+           "score_ms": sum(a.elapsed_time(b) for a, b in score_ev) / steps}
+    if with_select:
+        out["topk_ms"] = sum(a.elapsed_time(b) for a, b, _ in sel_ev) / steps
+        out["compact_ms"] = sum(b.elapsed_time(c) for _, b, c in sel_ev) / steps
+    return out
+
+
+def loop_leg(step, steps, tokens):
+    """The same step back to back with nothing in between (the caches keep what
+    the previous step left): the mean over `steps` steps."""
+    ms = _time_calls(step, steps)
+    return {"ms_per_step": round(ms, 4), "tokens_per_s": round(tokens / (ms * 1e-3), 1),
+            "protocol": "mean of back-to-back steps, no cache flush"}
+
+
+def long_leg(K, WL, pipeline, alpha, steps):
+    """long128k (32 layers, batch 1, N = 131072, W = 64, 256 window rows per KV
+    head) at B = 0.05 and 0.20: the flushed median step and the mean score
+    call, with the score's HBM fraction on algorithmic bytes and its
+    matrix-core fraction on the two passes' products (2 x 2.2 TFLOP)."""
+    import torch
+    wl = WL.get_workload("long128k")
+    inp = WL.make_inputs(wl, device="cuda")
+    torch.cuda.synchronize()
+    res = {"workload": f"long128k: {wl.L} layers, batch {wl.B}, {wl.Hq}q/{wl.Hkv}kv heads, d={wl.d}, "
+                       f"N={wl.N}, W={wl.W}, pool {wl.pool_k}, role mix {wl.mix}, table pattern"}
+    segs = wl.L * wl.B * wl.Hkv
+    flops_2pass = 2 * segs * (wl.G * wl.W) * wl.N * wl.d * 2
+    for budget in wl.budgets:
+        _, kept, k_cap = K.role_allocate(inp["roles"], 4, alpha, budget, wl.W)
+        bufs = pipeline.alloc_buffers(inp["k"], wl.Hq, wl.W, 4, k_cap)
+
+        def run(e=None, s_=None):
+            pipeline.evict(inp["q"], inp["k"], inp["v"], inp["roles"], inp["roles_t"], alpha, budget, wl.W,
+                           wl.pool_k, bufs, score_events=e, select_events=s_)
+
+        for _ in range(2):
+            run()
+        t = flushed_steps(run, steps)
+        sb = snapkv_algorithmic_bytes(wl)
+        stb = step_algorithmic_bytes(wl, kept)
+        gbs = sb / (t["score_ms"] * 1e-3) / 1e9
+        tf = flops_2pass / (t["score_ms"] * 1e-3) / 1e12
+        res[f"B={budget}"] = {
+            "ms_per_step": round(t["median_ms"], 4), "tokens_per_s": round(wl.B * wl.N / (t["median_ms"] * 1e-3), 1),
+            "step_hbm_frac": round(stb / (t["median_ms"] * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+            "score_ms": round(t["score_ms"], 4), "score_hbm_frac": round(gbs / HBM_PEAK_GBS, 4),
+            "score_tflops_2pass": round(tf, 1), "score_mfma_frac_2pass": round(tf / BF16_MFMA_PEAK_TFLOPS, 4),
+            "topk_ms": round(t["topk_ms"], 4), "compact_ms": round(t["compact_ms"], 4), "k_cap": k_cap}
+        del bufs
+        torch.cuda.empty_cache()
+    del inp
     torch.cuda.empty_cache()
-    return {"median_ms_per_step": round(statistics.median(times), 4),
-            "min_ms": round(min(times), 4), "max_ms": round(max(times), 4), "steps": steps,
-            "flush": "512 MiB written before every step, outside the timed events"}
+    return res
 
 
 def copy_ceiling(repeats=5):
@@ -332,6 +388,79 @@ def copy_ceiling(repeats=5):
             "hbm_frac": round(gbs / HBM_PEAK_GBS, 4)}
 
 
+def read_ceilings(K, repeats=10):
+    """Read rates of the probe kernel (kve_read_probe): a 4 GiB buffer streamed
+    once with non-temporal loads (the HBM streaming-read ceiling the score
+    passes are held to), and a 128 MiB buffer read again and again with cached
+    loads (it fits in the 256 MB last-level cache but not in the 32 MB of L2:
+    the rate at which that cache serves a second read of the same data)."""
+    import torch
+    blocks = 32768   # the fastest of 1024 .. 32768 workgroups in a sweep
+    out = {"kernel": f"kve_read_probe (16-byte loads, 8 in flight per thread, {blocks} workgroups of 256)"}
+    big = torch.empty(4 << 30, dtype=torch.uint8, device="cuda")
+    big.fill_(1)
+    sink = torch.empty(blocks, dtype=torch.float32, device="cuda")
+    ms = _time_calls(lambda: K.binding.read_probe(big, True, blocks, sink), repeats)
+    gbs = big.numel() / (ms * 1e-3) / 1e9
+    out["stream_read"] = {"bytes": big.numel(), "ms": round(ms, 4), "GBs": round(gbs, 1),
+                          "hbm_frac": round(gbs / HBM_PEAK_GBS, 4)}
+    del big
+    torch.cuda.empty_cache()
+    small = torch.empty(128 << 20, dtype=torch.uint8, device="cuda")
+    small.fill_(1)
+    ms = _time_calls(lambda: K.binding.read_probe(small, False, blocks, sink), 4 * repeats)
+    gbs = small.numel() / (ms * 1e-3) / 1e9
+    out["llc_reread"] = {"bytes": small.numel(), "ms": round(ms, 4), "GBs": round(gbs, 1),
+                         "note": "128 MiB read repeatedly: served by the last-level cache"}
+    del small, sink
+    torch.cuda.empty_cache()
+    return out
+
+
+def near_ties(score, roles, quota, W, rtol=1e-3):
+    """Selection boundaries that a relative score change of rtol could move,
+    from the step's own float32 scores (untimed): per (segment, bucket) with a
+    proper cut (0 < quota < population), the dropped candidates whose score is
+    within rtol of the bucket's boundary (quota-th best) score.  These are the
+    places where a kept set computed from scores within the parity tolerance
+    (the float64 oracle's) may legitimately differ."""
+    import numpy as np
+    L, B, H, N = score.shape
+    P = N - W
+    n_cuts = n_cut_ties = n_seg_ties = n_cand = n_equal = 0
+    for b in range(B):
+        rb = roles[b, :P]
+        masks = [rb == r for r in range(quota.shape[1])]
+        for l in range(L):
+            for j in range(H):
+                s = score[l, b, j, :P]
+                seg_has = False
+                for r, m in enumerate(masks):
+                    q = int(quota[b, r])
+                    cand = s[m]
+                    if q <= 0 or q >= cand.size:
+                        continue
+                    n_cuts += 1
+                    part = np.partition(cand, cand.size - q)
+                    bnd = float(part[cand.size - q])          # q-th largest
+                    dropped = part[:cand.size - q]
+                    # dropped candidates equal to the boundary score are exact ties,
+                    # decided by the index rule alike on every side; the others within
+                    # rtol are the near-ties
+                    n_equal += int(np.count_nonzero(dropped == bnd))
+                    close = int(np.count_nonzero((dropped >= bnd - rtol * abs(bnd)) & (dropped != bnd)))
+                    if close:
+                        n_cand += close
+                        n_cut_ties += 1
+                        seg_has = True
+                if seg_has:
+                    n_seg_ties += 1
+    return {"rtol": rtol, "bucket_cuts": n_cuts, "cuts_with_near_ties": n_cut_ties,
+            "segments_with_near_ties": n_seg_ties, "segments": L * B * H,
+            "dropped_candidates_within_rtol_of_boundary": n_cand,
+            "dropped_candidates_equal_to_boundary": n_equal}
+
+
 def _optional_leg(name, fn):
     """Run an optional leg of the bench; a failure becomes an error entry in the
     output line instead of ending the run (the main step is already timed)."""
@@ -340,6 +469,26 @@ def _optional_leg(name, fn):
     except Exception as e:  # noqa: BLE001 - reported, not hidden
         print(f"[bench] {name} leg failed: {e!r}", file=sys.stderr, flush=True)
         return {"error": f"{type(e).__name__}: {e}"}
+
+
+def _median_calls(fn, steps):
+    """Median time (ms) of `steps` single calls of fn, each bracketed by HIP
+    events and followed by a synchronisation (after two untimed calls): one
+    host-side stall moves a mean of back-to-back calls, not this median."""
+    import statistics
+    import torch
+    for _ in range(2):
+        fn()
+    torch.cuda.synchronize()
+    times = []
+    for _ in range(steps):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        fn()
+        e1.record()
+        torch.cuda.synchronize()
+        times.append(e0.elapsed_time(e1))
+    return statistics.median(times)
 
 
 def _time_calls(fn, steps):
@@ -405,8 +554,8 @@ def quest_leg(K, pipeline, wl, inp, budget, alpha, steps):
     del score, ws
     _, _, k_cap = K.role_allocate(inp["roles"], 4, alpha, budget, wl.W)
     bufs = pipeline.alloc_buffers(inp["k"], wl.Hq, wl.W, 4, k_cap, scorer="quest")
-    ms_step = _time_calls(lambda: pipeline.evict(inp["q"], inp["k"], inp["v"], inp["roles"], inp["roles_t"],
-                                                 alpha, budget, wl.W, 1, bufs, scorer="quest"), steps)
+    ms_step = _median_calls(lambda: pipeline.evict(inp["q"], inp["k"], inp["v"], inp["roles"], inp["roles_t"],
+                                                   alpha, budget, wl.W, 1, bufs, scorer="quest"), steps)
     del bufs
     torch.cuda.empty_cache()
     return {"kernel": "kve_quest_score (mean query + page bounds), page 16", "ms": round(ms, 4),
@@ -463,8 +612,8 @@ def lse_leg(K, pipeline, wl, inp, lse, budget, alpha, steps):
     del score, ws
     _, _, k_cap = K.role_allocate(inp["roles"], 4, alpha, budget, wl.W)
     bufs = pipeline.alloc_buffers(inp["k"], wl.Hq, wl.W, 4, k_cap)
-    ms_step = _time_calls(lambda: pipeline.evict(inp["q"], inp["k"], inp["v"], inp["roles"], inp["roles_t"],
-                                                 alpha, budget, wl.W, wl.pool_k, bufs, lse_win=lse), steps)
+    ms_step = _median_calls(lambda: pipeline.evict(inp["q"], inp["k"], inp["v"], inp["roles"], inp["roles_t"],
+                                                   alpha, budget, wl.W, wl.pool_k, bufs, lse_win=lse), steps)
     del bufs
     torch.cuda.empty_cache()
     gbs = nbytes / (ms * 1e-3) / 1e9
@@ -519,25 +668,17 @@ def main():
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
-    # score-call timing (HIP events on the launch stream)
-    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-          for _ in range(args.steps)]
-    sel = [tuple(torch.cuda.Event(enable_timing=True) for _ in range(3)) for _ in range(args.steps)]
-    t_all0 = torch.cuda.Event(enable_timing=True)
-    t_all1 = torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    t_all0.record()
-    for i in range(args.steps):
-        pipeline.evict(inp["q"], inp["k"], inp["v"], inp["roles"], inp["roles_t"], alpha, budget,
-                       W, pool, bufs, scorer=scorer, score_events=ev[i], chunks=args.chunks,
-                       side_stream=side, lse_win=main_lse,
-                       select_events=sel[i] if args.chunks <= 1 else None)
-    t_all1.record()
-    torch.cuda.synchronize()
-    ms_step = t_all0.elapsed_time(t_all1) / args.steps
-    ms_score = sum(a.elapsed_time(b) for a, b in ev) / args.steps
-    ms_topk = sum(a.elapsed_time(b) for a, b, _ in sel) / args.steps if args.chunks <= 1 else None
-    ms_compact = sum(b.elapsed_time(c) for _, b, c in sel) / args.steps if args.chunks <= 1 else None
+    # timed region: K steps, each after 512 MiB written to a scratch buffer
+    # (outside its events) so that no cache holds the previous step's data;
+    # HIP events on the launch stream around each step, the score call, the
+    # top-k and the compaction
+    timed = flushed_steps(lambda e, s_: pipeline.evict(
+        inp["q"], inp["k"], inp["v"], inp["roles"], inp["roles_t"], alpha, budget, W, pool, bufs,
+        scorer=scorer, score_events=e, chunks=args.chunks, side_stream=side, lse_win=main_lse,
+        select_events=s_ if args.chunks <= 1 else None), args.steps, with_select=args.chunks <= 1)
+    ms_step = timed["median_ms"]
+    ms_score = timed["score_ms"]
+    ms_topk, ms_compact = timed.get("topk_ms"), timed.get("compact_ms")
     tokens = wl.B * wl.N
     value = tokens / (ms_step * 1e-3)
     score_bytes = snapkv_algorithmic_bytes(wl)
@@ -564,6 +705,8 @@ def main():
             "global_batch": wl.B, "seq_len": wl.N, "parallelism": "none (1 GPU)",
             "layer_tokens_per_s": round(value * wl.L, 1),
             "k_cap": k_cap, "layer_chunks": args.chunks,
+            "ms_per_step_is": "median of the timed steps, 512 MiB written before each one (outside its events)",
+            "step_ms_min_max": [round(timed["min_ms"], 4), round(timed["max_ms"], 4)],
             "step_algorithmic_GBs": round(step_bytes / (ms_step * 1e-3) / 1e9, 1),
             "step_hbm_frac": round(step_bytes / (ms_step * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
         },
@@ -573,13 +716,21 @@ def main():
             "bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
             "frac": round(achieved / HBM_PEAK_GBS, 4),
             "traffic": measured_traffic(wl.name, TRAFFIC_SUMMARY_LSE if args.lse else TRAFFIC_SUMMARY),
-            "ms": round(ms_score, 4), "algorithmic_bytes": score_bytes,
+            "ms": round(ms_score, 4), "ms_is": "mean of the score call over the timed steps",
+            "algorithmic_bytes": score_bytes,
         },
     }
     if ms_topk is not None:
         out["select"] = select_figures(wl, inp, bufs, ms_topk, ms_compact)
+    if scorer != "h2o":
+        print("[bench] near-ties of the last timed step (untimed)", file=sys.stderr, flush=True)
+        out["near_ties"] = _optional_leg("near_ties", lambda: near_ties(
+            bufs.score.cpu().numpy(), inp["roles"], bufs.quota_host.numpy().copy(), W))
+    out["loop"] = _optional_leg("loop", lambda: loop_leg(step, args.steps, tokens))
     out["copy_ceiling"] = _optional_leg("copy_ceiling", copy_ceiling)
-    out["flushed"] = _optional_leg("flushed", lambda: flushed_leg(step, max(5, args.steps)))
+    if not args.no_ceilings:
+        print("[bench] read ceilings", file=sys.stderr, flush=True)
+        out["read_ceilings"] = _optional_leg("read_ceilings", lambda: read_ceilings(K))
     if not args.no_graph and args.chunks <= 1:
         print("[bench] step through a HIP graph", file=sys.stderr, flush=True)
         out["graph"] = _optional_leg("graph", lambda: graph_leg(
@@ -603,6 +754,10 @@ def main():
         print("[bench] fair-eviction and No-KEY steps", file=sys.stderr, flush=True)
         out["policies"] = _optional_leg("policies", lambda: policy_leg(
             WL, pipeline, wl, inp, budget, W, pool, max(3, args.steps // 2)))
+    if not args.no_long and wl.name == "stack32k" and not args.lse:
+        print("[bench] long128k legs", file=sys.stderr, flush=True)
+        out["long128k"] = _optional_leg("long128k", lambda: long_leg(
+            K, WL, pipeline, alpha, max(5, args.steps // 2)))
     if not args.no_h2o and wl.name != "h2o16k":
         print("[bench] H2O leg", file=sys.stderr, flush=True)
         out["h2o"] = _optional_leg("h2o", lambda: h2o_leg(K, WL, max(3, args.steps // 2)))

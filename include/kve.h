@@ -415,6 +415,28 @@ kve_status_t kve_decode_attention(const void* q, const void* k_c, const void* v_
                                   int Hq, int Hkv, int k_cap, int d, float scale, float* out,
                                   void* workspace, size_t workspace_bytes, void* stream);
 
+/* ------------------------------------------------------------------------- */
+/* Measurement helper (not part of the eviction path).                        */
+/* ------------------------------------------------------------------------- */
+
+/*
+ * Reads `bytes` bytes of device memory at `buf` once, with 16-byte loads
+ * (non-temporal when `nontemporal` is non-zero) from `blocks` workgroups of
+ * 256 threads striding over the buffer, and writes one float per workgroup,
+ * derived from the bytes read, to sink[0 .. blocks).  Timed around a buffer
+ * far larger than the last-level cache it gives the streaming HBM read rate
+ * the eviction kernels are compared with; repeated over a buffer that fits in
+ * the last-level cache, that cache's re-read rate.
+ *
+ *   buf      device, 16-byte aligned; bytes a positive multiple of 16
+ *   sink     device, at least `blocks` floats
+ *   blocks   1 .. 65536
+ *
+ * Enqueued on `stream`.  Errors: KVE_ERR_INVALID_ARG, KVE_ERR_HIP.
+ */
+kve_status_t kve_read_probe(const void* buf, size_t bytes, int nontemporal, float* sink, int blocks,
+                            void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -37,6 +37,7 @@ EXPORTED = (
     "kve_kv_compact",
     "kve_decode_workspace_size", "kve_decode_attention",
     "kve_quest_workspace_size", "kve_quest_score",
+    "kve_read_probe",
 )
 
 
@@ -83,6 +84,7 @@ def _load():
         "kve_decode_workspace_size": (c_size, [c_int] * 6),
         "kve_quest_workspace_size": (c_size, [c_int] * 5),
         "kve_quest_score": (c_int, [c_void, c_void, c_int] + [c_int] * 8 + [c_void, c_void, c_size, c_void]),
+        "kve_read_probe": (c_int, [c_void, c_size, c_int, c_void, c_int, c_void]),
         "kve_decode_attention": (c_int, [c_void, c_void, c_void, c_void, c_int] + [c_int] * 6 +
                                  [c_float, c_void, c_void, c_size, c_void]),
     }
@@ -406,3 +408,15 @@ def role_probe(ids, weight, bias, out=None, stream=None):
     _check(LIB.kve_role_probe(_dev(ids, "ids"), B, N, _dev(weight, "weight"), _dev(bias, "bias"), V, R,
                               _dev(out, "out"), _stream(stream)))
     return out
+
+
+def read_probe(buf, nontemporal: bool = True, blocks: int = 4096, sink=None, stream=None):
+    """Stream every byte of the device tensor `buf` once (kve_read_probe);
+    returns the sink tensor (one float per workgroup)."""
+    torch = _torch()
+    nbytes = buf.numel() * buf.element_size()
+    if sink is None:
+        sink = torch.empty(blocks, dtype=torch.float32, device=buf.device)
+    _check(LIB.kve_read_probe(_dev(buf, "buf"), nbytes, int(bool(nontemporal)), _dev(sink, "sink"), int(blocks),
+                              _stream(stream)))
+    return sink

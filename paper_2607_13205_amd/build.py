@@ -24,7 +24,8 @@ LIB = os.path.join(PKG, "libkve.so")
 HASH_FILE = LIB + ".sha256"  # hash of the sources the library was built from
 ARCH = "gfx950"
 
-SOURCES = ["kve_api.cpp", "snapkv.hip", "h2o.hip", "topk.hip", "decode.hip", "quest.hip", "probe.hip"]
+SOURCES = ["kve_api.cpp", "snapkv.hip", "h2o.hip", "topk.hip", "decode.hip", "quest.hip", "probe.hip",
+           "ceiling.hip"]
 
 COMMON = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}",
           "-I", os.path.join(ROOT, "include"), "-I", CSRC,

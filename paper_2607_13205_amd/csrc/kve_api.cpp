@@ -452,4 +452,17 @@ kve_status_t kve_kv_compact(const void* k, const void* v, kve_dtype_t dtype, con
                     fn);
 }
 
+kve_status_t kve_read_probe(const void* buf, size_t bytes, int nontemporal, float* sink, int blocks,
+                            void* stream) {
+    const char* fn = "kve_read_probe";
+    if (buf == nullptr || sink == nullptr) return fail(KVE_ERR_INVALID_ARG, "%s: null pointer", fn);
+    if (bytes == 0 || bytes % 16 != 0)
+        return fail(KVE_ERR_INVALID_ARG, "%s: bytes must be a positive multiple of 16", fn);
+    if ((reinterpret_cast<uintptr_t>(buf) & 15u) != 0)
+        return fail(KVE_ERR_INVALID_ARG, "%s: buffer not 16-byte aligned", fn);
+    if (blocks < 1 || blocks > 65536) return fail(KVE_ERR_INVALID_ARG, "%s: blocks outside [1, 65536]", fn);
+    return from_hip(kve::launch_read_probe(buf, bytes, nontemporal, sink, blocks, static_cast<hipStream_t>(stream)),
+                    fn);
+}
+
 }  // extern "C"

@@ -119,6 +119,11 @@ hipError_t launch_quest(const void* q, const void* k, int dtype, int L, int B, i
 hipError_t launch_probe(const int32_t* ids, int B, int N, const float* weight, const float* bias, int V, int R,
                         int8_t* out, hipStream_t st);
 
+// read-bandwidth probe (measurement helper): `blocks` workgroups stream
+// `bytes` (a multiple of 16) once, one value per workgroup written to sink
+hipError_t launch_read_probe(const void* buf, size_t bytes, int nontemporal, float* sink, int blocks,
+                             hipStream_t st);
+
 hipError_t launch_compact(const void* k, const void* v, int elem_bytes, const int32_t* idx,
                           const int32_t* count, int L, int B, int Hkv, int N, int d, int k_cap,
                           void* k_out, void* v_out, hipStream_t st);
