@@ -16,6 +16,19 @@ import numpy as np
 RTOL = 1e-3
 FLOOR_FRAC = 1e-6
 
+# Figures the GPU tests record (near-tie counts, worst error ratios); the
+# conftest prints them in pytest's terminal summary so that they reach the
+# records of a passing run too.
+REPORT: dict = {}
+
+
+def report(key: str, value) -> None:
+    """Record one figure under `key` (numbers under one key are summed)."""
+    if isinstance(value, (int, float)) and isinstance(REPORT.get(key), (int, float)):
+        REPORT[key] += value
+    else:
+        REPORT[key] = value
+
 
 def check_scores(gpu: np.ndarray, orc: np.ndarray, what: str = "score"):
     gpu = np.asarray(gpu, dtype=np.float64)
