@@ -766,6 +766,11 @@ def main():
         out["cpu_baseline"] = _optional_leg("cpu_baseline", lambda: cpu_baseline(
             wl, inp, budget, alpha, args.cpu_seconds))
     print(json.dumps(out), flush=True)
+    # nothing left in flight, device and pinned host memory handed back before
+    # the interpreter and the runtime shut down
+    del inp, lse
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
 
 
 if __name__ == "__main__":

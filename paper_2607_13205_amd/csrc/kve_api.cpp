@@ -9,27 +9,26 @@
 #include <cstdio>
 #include <cstdlib>
 #include <cstring>
-#include <string>
 #include <vector>
 
 #include "kve_internal.h"
 
 namespace {
 
-thread_local std::string g_error;
+// The calling thread's last error message.  A plain character array, so that
+// the library registers no thread-exit or process-exit destructor.
+thread_local char g_error[512];
 
 kve_status_t fail(kve_status_t st, const char* fmt, ...) {
-    char buf[512];
     va_list ap;
     va_start(ap, fmt);
-    vsnprintf(buf, sizeof(buf), fmt, ap);
+    vsnprintf(g_error, sizeof(g_error), fmt, ap);
     va_end(ap);
-    g_error = buf;
     return st;
 }
 
 kve_status_t ok() {
-    g_error.clear();
+    g_error[0] = '\0';
     return KVE_OK;
 }
 
@@ -188,7 +187,7 @@ int kve_version(void) { return KVE_ABI_VERSION; }
 #endif
 const char* kve_source_hash(void) { return KVE_SOURCE_HASH; }
 
-const char* kve_last_error(void) { return g_error.c_str(); }
+const char* kve_last_error(void) { return g_error; }
 
 size_t kve_snapkv_workspace_size(int L, int B, int Hq, int Hkv, int N, int W, int d) {
     if (L <= 0 || B <= 0 || Hq <= 0 || Hkv <= 0 || N <= 0 || W <= 0 || Hq % Hkv != 0) return 0;

@@ -92,6 +92,14 @@ struct VPiece<float> {
     }
 };
 
+// x[l] + x[l ^ 32] in every lane l: the two halves of the wave swapped with
+// v_permlane32_swap (a vector-unit instruction of gfx950) and added; the sum of
+// the swap's two results is the same whichever half each result holds.
+__device__ __forceinline__ float half_wave_sum(float x) {
+    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
 // Row of output register i held by lane l in a 32x32 block (see Mma).
 __device__ __forceinline__ int c_row(int i, int lane) {
     return 8 * (i >> 2) + 4 * (lane >> 5) + (i & 3);

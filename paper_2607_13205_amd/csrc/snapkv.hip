@@ -242,7 +242,7 @@ __global__ __launch_bounds__(kThreads, (TuneRS<T, RS>::kOcc2)) void snap_pass2(
     constexpr int kRpg = RS * kSnapRowsPerGroup;
     using G = Geo<T, D, kRing>;
     __shared__ __align__(16) char ring[kRing * G::C::BYTES];
-    __shared__ float scol[2][kWaves][kKeys];    // column sums per wave, two chunks
+    __shared__ __align__(16) float scol[2][kKeys][kWaves];  // column sums per key and wave, two chunks
     __shared__ __align__(16) float sinit[kRpg];  // -lse / sl2 of each row
     __shared__ __align__(16) int swin[kRpg];     // window index (row % W) of each row
     const int lane = threadIdx.x & 63;
@@ -289,14 +289,14 @@ __global__ __launch_bounds__(kThreads, (TuneRS<T, RS>::kOcc2)) void snap_pass2(
     ring_io.prologue(ring, src);
     float* out = raw + ((size_t)sp.rg * segs + sp.seg) * N;
 
-    // add the four waves' column sums of chunk s (every wave has written them);
-    // each wave adds 16 of the 64 keys and writes them out
+    // add the four waves' column sums of chunk s (every wave has written them):
+    // the waves take the chunks in turn, lane l adding the four sums of key l
+    // (one 16-byte LDS read) and the wave writing all 64 as one 256-byte store
     auto reduce = [&](int s) {
-        if (lane < kKeys / kWaves) {
-            const int key = wave * (kKeys / kWaves) + lane;
-            const int t = sp.t_begin + s * kKeys + key;
-            const float* c = &scol[s & 1][0][key];
-            if (t < sp.t_end) out[t] = (c[0] + c[kKeys]) + (c[2 * kKeys] + c[3 * kKeys]);
+        if (wave == (s & (kWaves - 1))) {
+            const int t = sp.t_begin + s * kKeys + lane;
+            const float4 c = *reinterpret_cast<const float4*>(&scol[s & 1][lane][0]);
+            if (t < sp.t_end) out[t] = (c.x + c.y) + (c.z + c.w);
         }
     };
     for (int s0 = 0; s0 < sp.nch; s0 += kRing) {
@@ -328,7 +328,10 @@ __global__ __launch_bounds__(kThreads, (TuneRS<T, RS>::kOcc2)) void snap_pass2(
                     }
             }
             // exponentials of each key block: a lane sum over its 16 rows per set
-            // and one shuffle for the other 16
+            // and the other 16 rows from the other half of the wave (a lane
+            // swap on the vector unit, not an LDS permute); lane l then writes
+            // the sum of key l (block 0 in the lower half, block 1 in the upper)
+            float v[2];
 #pragma unroll
             for (int kb = 0; kb < 2; ++kb) {
                 float c = 0.0f;
@@ -340,9 +343,9 @@ __global__ __launch_bounds__(kThreads, (TuneRS<T, RS>::kOcc2)) void snap_pass2(
                     c += ((x[0] + x[1]) + (x[2] + x[3]) + ((x[4] + x[5]) + (x[6] + x[7]))) +
                          (((x[8] + x[9]) + (x[10] + x[11])) + ((x[12] + x[13]) + (x[14] + x[15])));
                 }
-                const float v = c + __shfl_xor(c, 32);
-                if (lane < 32) scol[s & 1][wave][32 * kb + lane] = v;
+                v[kb] = half_wave_sum(c);
             }
+            scol[s & 1][lane][wave] = lane < 32 ? v[0] : v[1];
         }
     }
     __syncthreads();
