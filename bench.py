@@ -259,6 +259,24 @@ def policy_leg(WL, pipeline, wl, inp, budget, W, pool, steps):
     return out
 
 
+def fused_leg(pipeline, wl, inp, alpha, budget, W, pool, k_cap, steps):
+    """The same step with the fused role epilogue (the score's pool step counts
+    the top-k's first digit per bucket): flushed median step, mean score and
+    top-k times, as for the main line."""
+    import torch
+    bufs = pipeline.alloc_buffers(inp["k"], wl.Hq, W, 4, k_cap, fused=True)
+    run = lambda e, s_: pipeline.evict(inp["q"], inp["k"], inp["v"], inp["roles"], inp["roles_t"], alpha,  # noqa: E731
+                                       budget, W, pool, bufs, score_events=e, select_events=s_)
+    for _ in range(2):
+        run(None, None)
+    t = flushed_steps(run, steps)
+    del bufs
+    torch.cuda.empty_cache()
+    return {"calls": "kve_snapkv_score_hist + kve_topk_select_hist", "ms_per_step": round(t["median_ms"], 4),
+            "score_ms": round(t["score_ms"], 4), "topk_ms": round(t["topk_ms"], 4),
+            "compact_ms": round(t["compact_ms"], 4)}
+
+
 def graph_leg(pipeline, inp, alpha, budget, W, pool, bufs, scorer, steps, lse_win=None):
     """Step time with the device part captured once as a HIP graph and replayed
     (the host allocation still runs every step), and whether the replays give
@@ -731,6 +749,10 @@ def main():
     if not args.no_ceilings:
         print("[bench] read ceilings", file=sys.stderr, flush=True)
         out["read_ceilings"] = _optional_leg("read_ceilings", lambda: read_ceilings(K))
+    if scorer == "snapkv" and not args.lse and args.chunks <= 1:
+        print("[bench] fused role epilogue", file=sys.stderr, flush=True)
+        out["fused_epilogue"] = _optional_leg("fused_epilogue", lambda: fused_leg(
+            pipeline, wl, inp, alpha, budget, W, pool, k_cap, max(5, args.steps // 2)))
     if not args.no_graph and args.chunks <= 1:
         print("[bench] step through a HIP graph", file=sys.stderr, flush=True)
         out["graph"] = _optional_leg("graph", lambda: graph_leg(

@@ -359,6 +359,61 @@ kve_status_t kve_topk_select(const float* score, const int8_t* roles, const int3
                              void* workspace, size_t workspace_bytes, void* stream);
 
 /* ------------------------------------------------------------------------- */
+/* Fused role epilogue (§4.1: top-k within each role bucket; Algorithm 1,     */
+/* per-bucket top-k): the score's pool step counts what the per-bucket top-k  */
+/* would otherwise count in a first sweep over the scores.                    */
+/* ------------------------------------------------------------------------- */
+
+/* Bytes of the role histograms of L*B*Hkv segments of N positions and R
+ * buckets (0 if invalid). */
+size_t kve_role_hist_size(int L, int B, int Hkv, int N, int R);
+
+/*
+ * kve_snapkv_score that also counts, for every segment (l, b, j) and bucket r,
+ * the candidate positions t < N-W labelled r by the top 11 bits of their
+ * pooled score's order-preserving key (sign, exponent and two mantissa bits,
+ * -0 counted as +0, NaN below -inf): the first radix digit of the per-bucket
+ * top-k, counted in the pool step's epilogue while the pooled scores are in
+ * registers.  The counts are kept per tile of 4096 positions, each tile as a
+ * record of four header words {lowest bin counted (0xffffffff: none), 1 if the
+ * tile's bins spanned more than its 512-bin window, 0, 0} followed by R x 256
+ * words holding the 16-bit counts of bins lowest .. lowest + 511 in pairs (low
+ * half first); records are ordered [l, b, j, tile].  kve_topk_select_hist adds
+ * a segment's records instead of sweeping its scores and labels (and sweeps
+ * when a tile overflowed); the kept sets are those of kve_topk_select, bit for
+ * bit.
+ *
+ *   roles  [B, N] int8 bucket labels (device); labels outside [0, R) are not
+ *          counted (and never kept by the top-k)
+ *   R      buckets, 1 .. 8
+ *   hist   kve_role_hist_size bytes (device, 16-byte aligned): written by the
+ *          call (its contents on entry do not matter); the rest as for
+ *          kve_snapkv_score (same workspace size).
+ *
+ * Errors: as for kve_snapkv_score; KVE_ERR_INVALID_ARG for null roles or hist,
+ * R outside [1, 8] or a misaligned hist.
+ */
+kve_status_t kve_snapkv_score_hist(const void* q_win, const void* k, kve_dtype_t dtype,
+                                   int L, int B, int Hq, int Hkv, int N, int W, int d,
+                                   float scale, int pool_k, const int8_t* roles, int R,
+                                   float* score, uint32_t* hist,
+                                   void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * kve_topk_select with the first digit's counts supplied: hist is what
+ * kve_snapkv_score_hist wrote for these scores, labels, N and R.  The kept
+ * indices and counts are those of kve_topk_select on the same scores, bit for
+ * bit; counts that do not belong to the scores give an unspecified kept set
+ * (never an access outside the buffers).  Arguments and errors as for
+ * kve_topk_select, plus hist (kve_role_hist_size bytes, device, 16-byte
+ * aligned; KVE_ERR_INVALID_ARG when null or misaligned).
+ */
+kve_status_t kve_topk_select_hist(const float* score, const int8_t* roles, const int32_t* quota,
+                                  const uint32_t* hist, int L, int B, int Hkv, int N, int W, int R,
+                                  int k_cap, int32_t* idx_out, int32_t* count_out,
+                                  void* workspace, size_t workspace_bytes, void* stream);
+
+/* ------------------------------------------------------------------------- */
 /* K/V compaction: the dense cache of a compacting implementation (§6).      */
 /* ------------------------------------------------------------------------- */
 

@@ -34,6 +34,7 @@ EXPORTED = (
     "kve_h2o_workspace_size", "kve_h2o_score",
     "kve_role_allocate", "kve_role_allocate_fair", "kve_role_map", "kve_role_probe",
     "kve_topk_workspace_size", "kve_topk_select",
+    "kve_role_hist_size", "kve_snapkv_score_hist", "kve_topk_select_hist",
     "kve_kv_compact",
     "kve_decode_workspace_size", "kve_decode_attention",
     "kve_quest_workspace_size", "kve_quest_score",
@@ -79,6 +80,11 @@ def _load():
         "kve_topk_workspace_size": (c_size, [c_int] * 5),
         "kve_topk_select": (c_int, [c_void, c_void, c_void] + [c_int] * 7 +
                             [c_void, c_void, c_void, c_size, c_void]),
+        "kve_role_hist_size": (c_size, [c_int] * 5),
+        "kve_snapkv_score_hist": (c_int, [c_void, c_void, c_int] + [c_int] * 7 +
+                                  [c_float, c_int, c_void, c_int, c_void, c_void, c_void, c_size, c_void]),
+        "kve_topk_select_hist": (c_int, [c_void, c_void, c_void, c_void] + [c_int] * 7 +
+                                 [c_void, c_void, c_void, c_size, c_void]),
         "kve_kv_compact": (c_int, [c_void, c_void, c_int, c_void, c_void] + [c_int] * 6 +
                            [c_void, c_void, c_void]),
         "kve_decode_workspace_size": (c_size, [c_int] * 6),
@@ -343,6 +349,56 @@ def topk_select(score, roles, quota, W: int, R: int, k_cap: int, idx_out=None, c
                                L, B, Hkv, N, int(W), int(R), int(k_cap),
                                _dev(idx_out, "idx_out"), _dev(count_out, "count_out"),
                                _ptr(ws), wsb, _stream(stream)))
+    return idx_out, count_out
+
+
+def role_hist_size(L, B, Hkv, N, R) -> int:
+    return int(LIB.kve_role_hist_size(L, B, Hkv, N, R))
+
+
+def snapkv_score_hist(q_win, k, roles, R: int, pool_k: int, scale: float = 0.0, score=None, hist=None,
+                      workspace=None, stream=None):
+    """snapkv_score with the fused role epilogue: also the per-tile role
+    histograms of the pooled scores (kve_snapkv_score_hist; an int32 tensor of
+    role_hist_size / 4 words).  Returns (score, hist)."""
+    torch = _torch()
+    L, B, Hq, W, d = q_win.shape
+    Lk, Bk, Hkv, N, dk = k.shape
+    if (L, B, d) != (Lk, Bk, dk) or q_win.dtype != k.dtype:
+        raise ValueError("q_win and k disagree in L, B, d or dtype")
+    if tuple(roles.shape) != (B, N) or roles.dtype != torch.int8:
+        raise ValueError("roles must be int8 [B, N]")
+    if score is None:
+        score = torch.empty((L, B, Hkv, N), dtype=torch.float32, device=k.device)
+    if hist is None:
+        hist = torch.empty((role_hist_size(L, B, Hkv, N, R) // 4,), dtype=torch.int32, device=k.device)
+    ws, wsb = _workspace(lambda: snapkv_workspace_size(L, B, Hq, Hkv, N, W, d), k.device, workspace)
+    _check(LIB.kve_snapkv_score_hist(_dev(q_win, "q_win"), _dev(k, "k"), _dtype_code(k),
+                                     L, B, Hq, Hkv, N, W, d, float(scale), int(pool_k), _dev(roles, "roles"), int(R),
+                                     _dev(score, "score"), _dev(hist, "hist"), _ptr(ws), wsb, _stream(stream)))
+    return score, hist
+
+
+def topk_select_hist(score, roles, quota, hist, W: int, R: int, k_cap: int, idx_out=None, count_out=None,
+                     workspace=None, stream=None):
+    """topk_select with the first digit's counts from snapkv_score_hist."""
+    torch = _torch()
+    L, B, Hkv, N = score.shape
+    if tuple(roles.shape) != (B, N) or roles.dtype != torch.int8:
+        raise ValueError("roles must be int8 [B, N]")
+    if tuple(quota.shape) != (B, R) or quota.dtype != torch.int32:
+        raise ValueError("quota must be int32 [B, R]")
+    if hist.numel() * 4 < role_hist_size(L, B, Hkv, N, R) or hist.dtype != torch.int32:
+        raise ValueError("hist must be int32 with role_hist_size / 4 words")
+    if idx_out is None:
+        idx_out = torch.full((L, B, Hkv, max(k_cap, 0)), -1, dtype=torch.int32, device=score.device)
+    if count_out is None:
+        count_out = torch.empty((L, B, Hkv), dtype=torch.int32, device=score.device)
+    ws, wsb = _workspace(lambda: topk_workspace_size(L, B, Hkv, N, R), score.device, workspace)
+    _check(LIB.kve_topk_select_hist(_dev(score, "score"), _dev(roles, "roles"), _dev(quota, "quota"),
+                                    _dev(hist, "hist"), L, B, Hkv, N, int(W), int(R), int(k_cap),
+                                    _dev(idx_out, "idx_out"), _dev(count_out, "count_out"),
+                                    _ptr(ws), wsb, _stream(stream)))
     return idx_out, count_out
 
 

@@ -137,10 +137,12 @@ int32_t allocate_sample(const long long* n, const double* alpha, int R, double b
 
 // use_scratch: the workspace is this GPU's static scratch array (workspace
 // and workspace_bytes are ignored); the plan must fit in it
+// roles/R/hist: the fused role epilogue (roles == nullptr: none)
 kve_status_t snapkv_common(const char* fn, const void* q_win, const void* k, const float* lse_win,
                            kve_dtype_t dtype, int L, int B, int Hq, int Hkv, int N, int W, int d, float scale,
                            int pool_k, float* score, void* workspace, size_t workspace_bytes, void* stream,
-                           bool use_scratch = false) {
+                           bool use_scratch = false, const int8_t* roles = nullptr, int R = 0,
+                           uint32_t* hist = nullptr) {
     kve_status_t st = check_common(fn, L, B, Hq, Hkv, N, d, (int)dtype);
     if (st != KVE_OK) return st;
     if (q_win == nullptr || k == nullptr || score == nullptr)
@@ -150,6 +152,13 @@ kve_status_t snapkv_common(const char* fn, const void* q_win, const void* k, con
         return fail(KVE_ERR_INVALID_ARG, "%s: pool_k must be odd in [1, 255] (got %d)", fn, pool_k);
     if (!(std::isfinite(scale) && scale >= 0.0f))
         return fail(KVE_ERR_INVALID_ARG, "%s: scale must be finite and >= 0", fn);
+    if (roles != nullptr) {
+        if (hist == nullptr) return fail(KVE_ERR_INVALID_ARG, "%s: null hist", fn);
+        if (R < 1 || R > kve::kRoleHistMaxR)
+            return fail(KVE_ERR_INVALID_ARG, "%s: R=%d outside [1, %d]", fn, R, kve::kRoleHistMaxR);
+        if ((reinterpret_cast<uintptr_t>(hist) & 15u) != 0)
+            return fail(KVE_ERR_INVALID_ARG, "%s: hist not 16-byte aligned", fn);
+    }
     const long long rows = (long long)(Hq / Hkv) * W;
     if (rows > kve::kSnapMaxRows)
         return fail(KVE_ERR_UNSUPPORTED, "%s: G*W=%lld exceeds %d", fn, rows, kve::kSnapMaxRows);
@@ -172,7 +181,34 @@ kve_status_t snapkv_common(const char* fn, const void* q_win, const void* k, con
     }
     if (scale == 0.0f) scale = 1.0f / std::sqrt((float)d);
     return from_hip(kve::launch_snapkv(q_win, k, lse_win, (int)dtype, L, B, Hq, Hkv, N, W, d, scale, pool_k,
-                                       score, workspace, static_cast<hipStream_t>(stream)),
+                                       score, roles, R, hist, workspace, static_cast<hipStream_t>(stream)),
+                    fn);
+}
+
+// Checks of kve_topk_select and its fused-histogram variant.
+kve_status_t topk_common(const char* fn, const float* score, const int8_t* roles, const int32_t* quota,
+                         const uint32_t* hist, bool want_hist, int L, int B, int Hkv, int N, int W, int R,
+                         int k_cap, int32_t* idx_out, int32_t* count_out, void* workspace, size_t workspace_bytes,
+                         void* stream) {
+    if (score == nullptr || roles == nullptr || quota == nullptr)
+        return fail(KVE_ERR_INVALID_ARG, "%s: null pointer", fn);
+    if (want_hist && hist == nullptr) return fail(KVE_ERR_INVALID_ARG, "%s: null hist", fn);
+    if (want_hist && (reinterpret_cast<uintptr_t>(hist) & 15u) != 0)
+        return fail(KVE_ERR_INVALID_ARG, "%s: hist not 16-byte aligned", fn);
+    if (L <= 0 || B <= 0 || Hkv <= 0 || N <= 0)
+        return fail(KVE_ERR_INVALID_ARG, "%s: sizes must be positive", fn);
+    if (W < 0 || W > N) return fail(KVE_ERR_INVALID_ARG, "%s: need 0 <= W <= N", fn);
+    if (R < 1 || R > 8) return fail(KVE_ERR_INVALID_ARG, "%s: R=%d outside [1, 8]", fn, R);
+    if (k_cap < 0) return fail(KVE_ERR_INVALID_ARG, "%s: k_cap < 0", fn);
+    if (k_cap > 0 && idx_out == nullptr) return fail(KVE_ERR_INVALID_ARG, "%s: null idx_out", fn);
+    if ((long long)L * B * Hkv > kMaxGrid || N > (1 << 30))
+        return fail(KVE_ERR_UNSUPPORTED, "%s: shape too large", fn);
+    const size_t need = kve::align_up((size_t)L * B * Hkv * N * 8);
+    if (workspace_bytes < need || workspace == nullptr)
+        return fail(KVE_ERR_WORKSPACE, "%s: workspace of %zu bytes < %zu needed", fn, workspace_bytes, need);
+    if (!aligned(workspace)) return fail(KVE_ERR_INVALID_ARG, "%s: workspace not 256-byte aligned", fn);
+    return from_hip(kve::launch_topk(score, roles, quota, want_hist ? hist : nullptr, L, B, Hkv, N, W, R, k_cap,
+                                     idx_out, count_out, workspace, static_cast<hipStream_t>(stream)),
                     fn);
 }
 
@@ -410,24 +446,30 @@ kve_status_t kve_topk_select(const float* score, const int8_t* roles, const int3
                              int B, int Hkv, int N, int W, int R, int k_cap, int32_t* idx_out,
                              int32_t* count_out, void* workspace, size_t workspace_bytes,
                              void* stream) {
-    const char* fn = "kve_topk_select";
-    if (score == nullptr || roles == nullptr || quota == nullptr)
-        return fail(KVE_ERR_INVALID_ARG, "%s: null pointer", fn);
-    if (L <= 0 || B <= 0 || Hkv <= 0 || N <= 0)
-        return fail(KVE_ERR_INVALID_ARG, "%s: sizes must be positive", fn);
-    if (W < 0 || W > N) return fail(KVE_ERR_INVALID_ARG, "%s: need 0 <= W <= N", fn);
-    if (R < 1 || R > 8) return fail(KVE_ERR_INVALID_ARG, "%s: R=%d outside [1, 8]", fn, R);
-    if (k_cap < 0) return fail(KVE_ERR_INVALID_ARG, "%s: k_cap < 0", fn);
-    if (k_cap > 0 && idx_out == nullptr) return fail(KVE_ERR_INVALID_ARG, "%s: null idx_out", fn);
-    if ((long long)L * B * Hkv > kMaxGrid || N > (1 << 30))
-        return fail(KVE_ERR_UNSUPPORTED, "%s: shape too large", fn);
-    const size_t need = kve_topk_workspace_size(L, B, Hkv, N, R);
-    if (workspace_bytes < need || workspace == nullptr)
-        return fail(KVE_ERR_WORKSPACE, "%s: workspace of %zu bytes < %zu needed", fn, workspace_bytes, need);
-    if (!aligned(workspace)) return fail(KVE_ERR_INVALID_ARG, "%s: workspace not 256-byte aligned", fn);
-    return from_hip(kve::launch_topk(score, roles, quota, L, B, Hkv, N, W, R, k_cap, idx_out, count_out,
-                                     workspace, static_cast<hipStream_t>(stream)),
-                    fn);
+    return topk_common("kve_topk_select", score, roles, quota, nullptr, false, L, B, Hkv, N, W, R, k_cap, idx_out,
+                       count_out, workspace, workspace_bytes, stream);
+}
+
+kve_status_t kve_topk_select_hist(const float* score, const int8_t* roles, const int32_t* quota,
+                                  const uint32_t* hist, int L, int B, int Hkv, int N, int W, int R, int k_cap,
+                                  int32_t* idx_out, int32_t* count_out, void* workspace, size_t workspace_bytes,
+                                  void* stream) {
+    return topk_common("kve_topk_select_hist", score, roles, quota, hist, true, L, B, Hkv, N, W, R, k_cap, idx_out,
+                       count_out, workspace, workspace_bytes, stream);
+}
+
+size_t kve_role_hist_size(int L, int B, int Hkv, int N, int R) {
+    if (L <= 0 || B <= 0 || Hkv <= 0 || N <= 0 || R < 1 || R > kve::kRoleHistMaxR) return 0;
+    return (size_t)L * B * Hkv * kve::role_hist_tiles(N) * kve::role_hist_tile_words(R) * sizeof(uint32_t);
+}
+
+kve_status_t kve_snapkv_score_hist(const void* q_win, const void* k, kve_dtype_t dtype, int L, int B, int Hq,
+                                   int Hkv, int N, int W, int d, float scale, int pool_k, const int8_t* roles, int R,
+                                   float* score, uint32_t* hist, void* workspace, size_t workspace_bytes,
+                                   void* stream) {
+    if (roles == nullptr) return fail(KVE_ERR_INVALID_ARG, "kve_snapkv_score_hist: null roles");
+    return snapkv_common("kve_snapkv_score_hist", q_win, k, nullptr, dtype, L, B, Hq, Hkv, N, W, d, scale, pool_k,
+                         score, workspace, workspace_bytes, stream, false, roles, R, hist);
 }
 
 kve_status_t kve_kv_compact(const void* k, const void* v, kve_dtype_t dtype, const int32_t* idx,

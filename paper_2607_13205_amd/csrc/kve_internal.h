@@ -93,10 +93,12 @@ inline QuestPlan quest_plan(int L, int B, int Hq, int Hkv, int N, int W, int d, 
 }
 
 // lse_win: the window rows' natural-log log-sum-exp from the caller, or null
-// to compute it (pass 1 and the combine step)
+// to compute it (pass 1 and the combine step).  roles: bucket labels [B, N] of
+// the fused role epilogue, or null; with them the call also writes the role
+// histograms hist [L*B*Hkv, R, kRoleHistBins] (zeroed and filled in the call).
 hipError_t launch_snapkv(const void* q, const void* k, const float* lse_win, int dtype, int L, int B, int Hq,
-                         int Hkv, int N, int W, int d, float scale, int pool_k, float* score, void* ws,
-                         hipStream_t st);
+                         int Hkv, int N, int W, int d, float scale, int pool_k, float* score, const int8_t* roles,
+                         int R, uint32_t* hist, void* ws, hipStream_t st);
 
 // Device address of this GPU's static SnapKV scratch array (kSnapScratchBytes
 // bytes), taken once per device with that device current.
@@ -105,7 +107,9 @@ hipError_t snapkv_scratch(void** out);
 hipError_t launch_h2o(const void* q, const void* k, int dtype, int L, int B, int Hq, int Hkv,
                       int N, int d, float scale, float* score, void* ws, hipStream_t st);
 
-hipError_t launch_topk(const float* score, const int8_t* roles, const int32_t* quota, int L,
+// hist: the role histograms of the scores (as the fused SnapKV epilogue writes
+// them), or null to count them in a first sweep over the scores
+hipError_t launch_topk(const float* score, const int8_t* roles, const int32_t* quota, const uint32_t* hist, int L,
                        int B, int Hkv, int N, int W, int R, int k_cap, int32_t* idx_out,
                        int32_t* count_out, void* ws, hipStream_t st);
 

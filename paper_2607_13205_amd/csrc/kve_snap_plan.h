@@ -24,6 +24,25 @@ constexpr int kSnapChunkKeys = 64;
 constexpr int kSnapTargetGroups = 4096;  // workgroups per pass the range size aims at
 constexpr int kSnapMaxRangeChunks = 32;  // at most 2048 keys per range
 
+// Fused role epilogue: per (segment, bucket), the number of candidate
+// positions by the top kRoleHistBits bits of their order-preserving score key
+// (the top-k's first radix digit), counted by the pool step.  The pool counts
+// each tile of kRoleHistTile positions in a window of kRoleHistWindow bins from
+// the tile's lowest bin, as 16-bit counts (a tile has fewer than 2^16
+// positions); a tile record is a header of four words {lowest bin (all ones:
+// no candidate), window overflowed (0/1), 0, 0} and R x kRoleHistWindow / 2
+// words of count pairs.  The top-k adds the records of a segment's tiles, or
+// counts the segment itself when a tile's bins did not fit its window.
+constexpr int kRoleHistBits = 11;
+constexpr int kRoleHistBins = 1 << kRoleHistBits;
+constexpr int kRoleHistMaxR = 8;
+constexpr int kRoleHistTile = 4096;
+constexpr int kRoleHistWindow = 512;
+constexpr int kRoleHistHeader = 4;
+
+inline size_t role_hist_tile_words(int R) { return (size_t)kRoleHistHeader + (size_t)R * kRoleHistWindow / 2; }
+inline int role_hist_tiles(int N) { return (N + kRoleHistTile - 1) / kRoleHistTile; }
+
 // Bytes of the static device scratch array the allocation-free SnapKV entry
 // point uses as its workspace (one copy per GPU, held until the process ends).
 constexpr size_t kSnapScratchBytes = (size_t)64 << 20;

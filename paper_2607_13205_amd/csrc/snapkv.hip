@@ -29,6 +29,7 @@
 //
 // Logits are kept in log2 units (x = scale * log2(e) * <q, k>) so that every
 // exponential is a single v_exp_f32.
+#include <cstring>
 #include <mutex>
 
 #include "kve_device.h"
@@ -47,7 +48,7 @@ namespace {
 constexpr int kWaves = 4;
 constexpr int kThreads = kWaves * 64;
 constexpr int kKeys = kSnapChunkKeys;  // keys per chunk
-constexpr int kPoolTile = 4096;  // keys per pool workgroup
+constexpr int kPoolTile = kRoleHistTile;  // keys per pool workgroup (and per role-histogram tile)
 constexpr int kPoolKeysPerThread = kPoolTile / kThreads;  // consecutive keys per thread
 constexpr int kMaxPoolHalf = 127;
 
@@ -86,6 +87,16 @@ struct Geo {
 
 struct Span {
     int vseg, seg, rg, range, t_begin, t_end, nch;
+};
+
+// Fused role epilogue of the pool step: one tile record per (segment, pool
+// tile) of the role histograms (layout in kve_snap_plan.h).  roles == nullptr:
+// no histogram.
+struct RoleHist {
+    const int8_t* roles;  // [B, N] bucket labels; labels outside [0, R) are not counted
+    uint32_t* hist;       // [segs, tiles, role_hist_tile_words(R)]
+    int R, B, Hkv;
+    uint32_t lo;          // first bin of every tile's window
 };
 
 __device__ __forceinline__ Span span_of(int nranges, int rgroups, int range_keys, int N) {
@@ -356,17 +367,53 @@ __global__ __launch_bounds__(kThreads, (TuneRS<T, RS>::kOcc2)) void snap_pass2(
 // halo of h keys on each side are summed over the planes into LDS (16 keys per
 // thread, loads first), then each key takes the max over its window, which
 // stops at the end of the candidate prefix; window keys keep their raw score.
+// With a role histogram (rh.roles set) the workgroup also counts its candidate
+// keys per bucket and top key digit in LDS and adds the non-zero counts to the
+// segment's histogram.
+// Counting: a tile's candidate keys span few bins (scores of one segment lie
+// within a few binades), so the workgroup first finds its lowest bin, counts in
+// an LDS window of kRoleHistWindow bins per bucket from there (16-bit halves of
+// LDS words) and writes the window as its tile record with plain stores: no
+// global atomics, no zero fill, and the latency-bound pool keeps about the LDS,
+// and so the residency, it has without counting.  A tile whose bins do not fit
+// the window marks its record; the top-k then counts that segment itself.
+constexpr int kPoolHistWindow = kRoleHistWindow;
+constexpr uint32_t kNoBin = 0xffffffffu;
+
+__device__ __forceinline__ uint32_t role_bin(float m) { return score_key(m) >> (32 - kRoleHistBits); }
+
 __global__ __launch_bounds__(kThreads) void snap_pool(const float* __restrict__ raw, int planes, int segs,
                                                       int N, int W, int pool_k, int tiles,
-                                                      float* __restrict__ score) {
+                                                      float* __restrict__ score, RoleHist rh, int lab4) {
     __shared__ __align__(16) float ss[kPoolTile + 2 * kMaxPoolHalf + 8];
+    extern __shared__ __align__(16) uint32_t lh[];  // [R][kPoolHistWindow / 2] pairs of 16-bit counts when counting
     const int tile = blockIdx.x % tiles;
     const int seg = blockIdx.x / tiles;
     const int h = pool_k / 2;
     const int P = N - W;
     const int t0 = tile * kPoolTile;
     const int n = min(kPoolTile, N - t0) + 2 * h;  // staged keys t0 - h .. t0 + n - h - 1
+    const bool counting = rh.roles != nullptr;
+    const int8_t* ro = counting ? rh.roles + (size_t)((seg / rh.Hkv) % rh.B) * N : nullptr;
+    if (counting)
+        for (int e = threadIdx.x; e < rh.R * kPoolHistWindow / 2; e += kThreads) lh[e] = 0u;
     constexpr int kPer = (kPoolTile + 2 * kMaxPoolHalf + kThreads - 1) / kThreads;
+    const int e0 = kPoolKeysPerThread * (int)threadIdx.x;
+    // labels of this thread's keys, loaded with the sums (their latency hidden
+    // behind the pooling): four per word, four-byte loads when rows allow
+    uint32_t lab[kPoolKeysPerThread / 4] = {};
+    if (counting) {
+#pragma unroll
+        for (int a = 0; a < kPoolKeysPerThread / 4; ++a) {
+            const int t = min(t0 + e0 + 4 * a, N - 4 > 0 ? N - 4 : 0);
+            if (lab4) {
+                lab[a] = *reinterpret_cast<const uint32_t*>(ro + t);
+            } else {
+#pragma unroll
+                for (int b = 0; b < 4; ++b) lab[a] |= (uint32_t)(uint8_t)ro[min(t0 + e0 + 4 * a + b, N - 1)] << (8 * b);
+            }
+        }
+    }
     float v[kPer];
 #pragma unroll
     for (int i = 0; i < kPer; ++i) v[i] = 0.0f;
@@ -385,11 +432,14 @@ __global__ __launch_bounds__(kThreads) void snap_pool(const float* __restrict__ 
         if (e < n) ss[e] = (u >= 0 && u < N) ? v[i] : -INFINITY;
     }
     __syncthreads();
+    // this thread's keys t0 + e0 .. t0 + e0 + 15: pooled values in mv, and the
+    // bucket of each candidate (R: not counted) in rv
+    float mv[kPoolKeysPerThread];
+    uint32_t rv[kPoolKeysPerThread];
     // kernel 7 (the paper's), all 16 windows of this thread inside the prefix:
-    // thread i takes keys 16 i .. 16 i + 15 of the tile, its 22 staged values in
-    // registers, the window maxima built from pairwise and four-wide maxima, and
-    // writes them as 16-byte stores (rows of a multiple of 4 keys keep those aligned)
-    const int e0 = kPoolKeysPerThread * (int)threadIdx.x;
+    // the 22 staged values in registers, the window maxima built from pairwise
+    // and four-wide maxima, written as 16-byte stores (rows of a multiple of 4
+    // keys keep those aligned)
     const bool fast = h == 3 && (N & 3) == 0 && t0 + e0 + kPoolKeysPerThread - 1 + h < P;
     if (fast) {
         float x[kPoolKeysPerThread + 8];  // staged keys t0 + e0 - 3 .. t0 + e0 + 18 (+ 2 unused)
@@ -409,30 +459,83 @@ __global__ __launch_bounds__(kThreads) void snap_pool(const float* __restrict__ 
         float* dst = score + (size_t)seg * N + t0 + e0;
 #pragma unroll
         for (int a = 0; a < kPoolKeysPerThread / 4; ++a) {
-            float m[4];
 #pragma unroll
             for (int b = 0; b < 4; ++b) {
                 const int j = 4 * a + b;
-                m[b] = fmaxf(fmaxf(p4[j], p2[j + 4]), x[j + 6]);  // keys j .. j + 6 around key j + 3
+                mv[j] = fmaxf(fmaxf(p4[j], p2[j + 4]), x[j + 6]);  // keys j .. j + 6 around key j + 3
             }
-            *reinterpret_cast<float4*>(dst + 4 * a) = make_float4(m[0], m[1], m[2], m[3]);
+            *reinterpret_cast<float4*>(dst + 4 * a) = make_float4(mv[4 * a], mv[4 * a + 1], mv[4 * a + 2],
+                                                                  mv[4 * a + 3]);
         }
-        return;
+        if (counting) {
+#pragma unroll
+            for (int a = 0; a < kPoolKeysPerThread / 4; ++a)
+#pragma unroll
+                for (int b = 0; b < 4; ++b) rv[4 * a + b] = min((lab[a] >> (8 * b)) & 0xffu, (uint32_t)rh.R);
+        }
+    } else {
+        const int valid = min(kPoolTile, N - t0) - e0;  // keys of this thread inside the row
+#pragma unroll
+        for (int j = 0; j < kPoolKeysPerThread; ++j) {
+            const int t = t0 + e0 + j;
+            float m = 0.0f;
+            uint32_t r = (uint32_t)rh.R;
+            if (j < valid) {
+                if (t < P) {
+                    const int lo = max(0, t - h), hi = min(P - 1, t + h);
+                    m = -INFINITY;
+                    for (int u = lo; u <= hi; ++u) m = fmaxf(m, ss[u - t0 + h]);
+                    if (counting) r = min((lab[j >> 2] >> (8 * (j & 3))) & 0xffu, (uint32_t)rh.R);
+                } else {
+                    m = ss[e0 + j + h];
+                }
+                score[(size_t)seg * N + t] = m;
+            }
+            mv[j] = m;
+            rv[j] = r;
+        }
     }
+    if (!counting) return;  // uniform
+    // the window: the kPoolHistWindow bins up to that of the largest score a
+    // segment can have (the G*W window rows' probabilities summed, rh.top); a
+    // candidate below it (a score under 2^-117 of that, an exact 0, a NaN)
+    // marks the tile, whose segment the top-k then counts itself
+    const uint32_t lo = rh.lo;
+    bool out_of_window = false;
+    uint32_t cur = 0xffffffffu, cnt = 0u;
+#pragma unroll
     for (int j = 0; j < kPoolKeysPerThread; ++j) {
-        const int e = e0 + j;
-        if (e >= min(kPoolTile, N - t0)) break;
-        const int t = t0 + e;
-        float m;
-        if (t < P) {
-            const int lo = max(0, t - h), hi = min(P - 1, t + h);
-            m = -INFINITY;
-            for (int u = lo; u <= hi; ++u) m = fmaxf(m, ss[u - t0 + h]);
-        } else {
-            m = ss[e + h];
+        // runs of equal (bucket, bin) along the thread's consecutive keys (the
+        // max-pool's plateaus) go in with one atomic: fewer lanes contend for
+        // the same LDS word in each atomic instruction
+        uint32_t e = 0xffffffffu;
+        if (rv[j] < (uint32_t)rh.R) {
+            const uint32_t off = role_bin(mv[j]) - lo;
+            if (off < (uint32_t)kPoolHistWindow)
+                e = rv[j] * kPoolHistWindow + off;
+            else
+                out_of_window = true;
         }
-        score[(size_t)seg * N + t] = m;
+        if (e != cur) {
+            if (cnt != 0u) atomicAdd(&lh[cur >> 1], cnt << (16 * (cur & 1u)));
+            cur = e;
+            cnt = 0u;
+        }
+        cnt += e != 0xffffffffu ? 1u : 0u;
     }
+    if (cnt != 0u) atomicAdd(&lh[cur >> 1], cnt << (16 * (cur & 1u)));
+    const bool fits = !__syncthreads_or(out_of_window);
+    // the tile record: header, then the window's count pairs (16-byte stores)
+    uint32_t* rec = rh.hist + ((size_t)seg * tiles + tile) * (size_t)(kRoleHistHeader + rh.R * kPoolHistWindow / 2);
+    if (threadIdx.x == 0) {
+        u32x4 hd = zero16();
+        hd.x = lo;
+        hd.y = fits ? 0u : 1u;
+        st16(rec, hd);
+    }
+    u32x4* body = reinterpret_cast<u32x4*>(rec + kRoleHistHeader);
+    for (int e = threadIdx.x; e < rh.R * kPoolHistWindow / 8; e += kThreads)
+        body[e] = fits ? *reinterpret_cast<const u32x4*>(&lh[4 * e]) : zero16();
 }
 
 template <typename T, int D, int RS>
@@ -455,7 +558,7 @@ void launch_passes(const T* qt, const T* kt, const float* lse_win, const SnapPla
 
 template <typename T, int D>
 hipError_t run_snapkv(const void* q, const void* k, const float* lse_win, int L, int B, int Hq, int Hkv, int N,
-                      int W, float scale, int pool_k, float* score, void* ws, hipStream_t st) {
+                      int W, float scale, int pool_k, float* score, const RoleHist& rh, void* ws, hipStream_t st) {
     const SnapPlan p = snap_plan(L, B, Hq, Hkv, N, W, D, (int)sizeof(T));
     char* w = static_cast<char*>(ws);
     float* stats = reinterpret_cast<float*>(w + p.off_stats);
@@ -473,8 +576,11 @@ hipError_t run_snapkv(const void* q, const void* k, const float* lse_win, int L,
         launch_passes<T, D, 1>(qt, kt, lse_win, p, N, W, sl2, stats, lse, raw, st);
     }
     const int tiles = (N + kPoolTile - 1) / kPoolTile;
-    hipLaunchKernelGGL(snap_pool, dim3((unsigned)(p.segs * tiles)), dim3(kThreads), 0, st, raw, p.planes, p.segs, N,
-                       W, pool_k, tiles, score);
+    // label rows 4-byte aligned: the pool reads four labels at a time
+    const int lab4 = rh.roles != nullptr && N % 4 == 0 && (reinterpret_cast<uintptr_t>(rh.roles) & 3u) == 0;
+    const unsigned lds = rh.roles != nullptr ? (unsigned)(rh.R * kPoolHistWindow / 2 * sizeof(uint32_t)) : 0u;
+    hipLaunchKernelGGL(snap_pool, dim3((unsigned)(p.segs * tiles)), dim3(kThreads), lds, st, raw, p.planes, p.segs,
+                       N, W, pool_k, tiles, score, rh, lab4);
     return hipGetLastError();
 }
 
@@ -504,15 +610,23 @@ hipError_t snapkv_scratch(void** out) {
 }
 
 hipError_t launch_snapkv(const void* q, const void* k, const float* lse_win, int dtype, int L, int B, int Hq,
-                         int Hkv, int N, int W, int d, float scale, int pool_k, float* score, void* ws,
-                         hipStream_t st) {
+                         int Hkv, int N, int W, int d, float scale, int pool_k, float* score, const int8_t* roles,
+                         int R, uint32_t* hist, void* ws, hipStream_t st) {
+    // the largest pooled score is the sum over the G*W window rows of one
+    // probability each: the window ends at its bin (+1 for rounding)
+    const float top = (float)((Hq / Hkv) * W);
+    uint32_t bits;
+    std::memcpy(&bits, &top, sizeof(bits));
+    const uint32_t top_bin = ((bits | 0x80000000u) >> (32 - kRoleHistBits)) + 1u;
+    const RoleHist rh{roles, hist, R, B, Hkv, top_bin >= kRoleHistWindow - 1 ? top_bin + 1u - kRoleHistWindow : 0u};
     if (dtype == 0) {
         if (d == 128)
-            return run_snapkv<__bf16, 128>(q, k, lse_win, L, B, Hq, Hkv, N, W, scale, pool_k, score, ws, st);
-        return run_snapkv<__bf16, 64>(q, k, lse_win, L, B, Hq, Hkv, N, W, scale, pool_k, score, ws, st);
+            return run_snapkv<__bf16, 128>(q, k, lse_win, L, B, Hq, Hkv, N, W, scale, pool_k, score, rh, ws, st);
+        return run_snapkv<__bf16, 64>(q, k, lse_win, L, B, Hq, Hkv, N, W, scale, pool_k, score, rh, ws, st);
     }
-    if (d == 128) return run_snapkv<float, 128>(q, k, lse_win, L, B, Hq, Hkv, N, W, scale, pool_k, score, ws, st);
-    return run_snapkv<float, 64>(q, k, lse_win, L, B, Hq, Hkv, N, W, scale, pool_k, score, ws, st);
+    if (d == 128)
+        return run_snapkv<float, 128>(q, k, lse_win, L, B, Hq, Hkv, N, W, scale, pool_k, score, rh, ws, st);
+    return run_snapkv<float, 64>(q, k, lse_win, L, B, Hq, Hkv, N, W, scale, pool_k, score, rh, ws, st);
 }
 
 }  // namespace kve

@@ -37,7 +37,7 @@ namespace {
 constexpr int kThreads = 256;        // top-k workgroup when segments fill the chip (and compaction)
 constexpr int kWideThreads = 1024;   // top-k workgroup when there are few segments
 constexpr int kWideBelow = 512;      // segments below which the wide workgroup is used
-constexpr int kDigitBits = 11;
+constexpr int kDigitBits = kRoleHistBits;  // the first digit is the fused score epilogue's histogram bin
 constexpr int kDigits = 1 << kDigitBits;
 constexpr int kLowBits = 32 - kDigitBits;  // key bits below the top digit
 constexpr uint32_t kLowMask = (1u << kLowBits) - 1u;
@@ -59,6 +59,7 @@ struct TopkShared {
     // staging: {lowest surely kept key, top digit of the threshold's bin} per
     // bucket; entry R (labels outside [0, R)) is never kept and never staged
     uint2 stage_cls[R + 1];
+    int over;            // a fused-histogram tile of this segment overflowed its window
     int wave_eq[NW][R];  // staged keys equal to a threshold, per wave
     int wave_keep[NW];   // kept positions per wave
     int scan[NW][R < 4 ? R : 4];
@@ -224,8 +225,9 @@ __device__ __forceinline__ uint32_t bucket_of(const uint32_t (&lab)[4], int e) {
 
 template <int R, bool VEC, int NT>
 __global__ __launch_bounds__(NT) void topk_kernel(const float* __restrict__ score, const int8_t* __restrict__ roles,
-                                                  const int32_t* __restrict__ quota, int B, int Hkv, int N, int W,
-                                                  int k_cap, int32_t* __restrict__ idx_out,
+                                                  const int32_t* __restrict__ quota,
+                                                  const uint32_t* __restrict__ hist_in, int B, int Hkv, int N,
+                                                  int W, int k_cap, int32_t* __restrict__ idx_out,
                                                   int32_t* __restrict__ count_out, uint2* __restrict__ stage) {
     constexpr int NW = NT / kWave;
     constexpr int kGroupStep = NT * kSpan;  // positions per workgroup step
@@ -245,7 +247,39 @@ __global__ __launch_bounds__(NT) void topk_kernel(const float* __restrict__ scor
         sh.need[tid] = 0;
     }
     for (int e = tid; e < R * kDigits; e += NT) (&sh.hist[0][0])[e] = 0u;
+    // 1. the first digit's counts: added up from the fused score epilogue's tile
+    //    records when every tile fitted its window, otherwise counted in a sweep
+    bool sweep = true;
+    if (hist_in != nullptr) {
+        const int tiles = (N + kRoleHistTile - 1) / kRoleHistTile;
+        constexpr int kTw = kRoleHistHeader + R * kRoleHistWindow / 2;  // words per tile record
+        const uint32_t* rec = hist_in + (size_t)seg * tiles * kTw;
+        if (tid == 0) sh.over = 0;
+        __syncthreads();
+        for (int t = tid; t < tiles; t += NT)
+            if (rec[(size_t)t * kTw + 1] != 0u) sh.over = 1;
+        __syncthreads();  // also orders the zero fill before the adds
+        sweep = sh.over != 0;  // uniform
+        if (!sweep) {
+            constexpr int kQ = R * kRoleHistWindow / 8;  // 16-byte words of count pairs per record
+            for (int e = tid; e < tiles * kQ; e += NT) {
+                const int t = e / kQ, q = e - t * kQ;
+                const uint32_t* r0 = rec + (size_t)t * kTw;
+                const uint32_t lo = r0[0];
+                const u32x4 c = reinterpret_cast<const u32x4*>(r0 + kRoleHistHeader)[q];
+                const int r = (4 * q) / (kRoleHistWindow / 2);
+                const uint32_t bin0 = lo + 2u * (uint32_t)(4 * q - r * (kRoleHistWindow / 2));
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const uint32_t w = c[i], b = bin0 + 2u * i;
+                    if ((w & 0xffffu) != 0u && b < (uint32_t)kDigits) atomicAdd(&sh.hist[r][b], w & 0xffffu);
+                    if ((w >> 16) != 0u && b + 1u < (uint32_t)kDigits) atomicAdd(&sh.hist[r][b + 1], w >> 16);
+                }
+            }
+        }
+    }
     __syncthreads();
+    if (sweep) {
 
     // 1. histogram sweep: the top digit of every labelled candidate's key; each
     //    step's span is in flight while the previous one is counted
@@ -273,6 +307,7 @@ __global__ __launch_bounds__(NT) void topk_kernel(const float* __restrict__ scor
         }
     }
     __syncthreads();
+    }
     find_digits(sh, quota + (size_t)b * R);
     if (tid <= R) {
         uint2 c = make_uint2(kNoKey, kNoKey);
@@ -491,8 +526,8 @@ __global__ __launch_bounds__(kThreads) void compact_kernel(const char* __restric
 
 }  // namespace
 
-hipError_t launch_topk(const float* score, const int8_t* roles, const int32_t* quota, int L, int B,
-                       int Hkv, int N, int W, int R, int k_cap, int32_t* idx_out, int32_t* count_out,
+hipError_t launch_topk(const float* score, const int8_t* roles, const int32_t* quota, const uint32_t* hist,
+                       int L, int B, int Hkv, int N, int W, int R, int k_cap, int32_t* idx_out, int32_t* count_out,
                        void* ws, hipStream_t st) {
     const size_t segs = (size_t)L * B * Hkv;
     uint2* stage = static_cast<uint2*>(ws);
@@ -504,8 +539,8 @@ hipError_t launch_topk(const float* score, const int8_t* roles, const int32_t* q
     const dim3 grid((unsigned)segs);
     switch (R) {
 #define KVE_TOPK_LAUNCH(RR, V, NT)                                                                             \
-    hipLaunchKernelGGL((topk_kernel<RR, V, NT>), grid, dim3(NT), 0, st, score, roles, quota, B, Hkv, N, W,   \
-                       k_cap, idx_out, count_out, stage)
+    hipLaunchKernelGGL((topk_kernel<RR, V, NT>), grid, dim3(NT), 0, st, score, roles, quota, hist, B, Hkv, N, \
+                       W, k_cap, idx_out, count_out, stage)
 #define KVE_TOPK_CASE(RR)                                                                                      \
     case RR:                                                                                                   \
         if (wide) {                                                                                            \

@@ -96,10 +96,16 @@ class EvictBuffers:
     v_out: object
     k_cap: int
     copy_done: object = None   # event after the last quota upload from quota_host
+    hist: object = None        # per-tile role histograms of the fused SnapKV epilogue, [L, words per layer]
 
 
 def alloc_buffers(k, n_q_heads: int, W: int, R: int, k_cap: int, scorer: str = "snapkv",
-                  with_v: bool = True) -> EvictBuffers:
+                  with_v: bool = True, fused: bool = False) -> EvictBuffers:
+    """Buffers of repeated eviction steps.  fused (SnapKV only): the score's
+    pool epilogue counts the top-k's first digit per role bucket
+    (snapkv_score_hist / topk_select_hist) and the histograms live here.  Off
+    by default: on the 32-layer N = 32768 step the counting adds more to the
+    pool (about 60 us) than it takes off the top-k (about 25 us)."""
     import torch
     L, B, Hkv, N, d = k.shape
     dev = k.device
@@ -120,12 +126,22 @@ def alloc_buffers(k, n_q_heads: int, W: int, R: int, k_cap: int, scorer: str = "
         k_out=torch.zeros((L, B, Hkv, k_cap, d), dtype=k.dtype, device=dev),
         v_out=torch.zeros((L, B, Hkv, k_cap, d), dtype=k.dtype, device=dev) if with_v else None,
         k_cap=k_cap,
+        hist=(torch.empty((L, kb.role_hist_size(1, B, Hkv, N, R) // 4), dtype=torch.int32, device=dev)
+              if fused and scorer == "snapkv" else None),
     )
 
 
-def _score(q, k, bufs, scorer, pool_k, scale, page, l0, l1, stream=None, lse_win=None):
-    """Score layers [l0, l1) into bufs.score[l0:l1] on ``stream`` (None: current)."""
-    if scorer == "snapkv" and lse_win is not None:
+def _fused(bufs, scorer, lse_win):
+    return bufs.hist is not None and scorer == "snapkv" and lse_win is None
+
+
+def _score(q, k, bufs, scorer, pool_k, scale, page, l0, l1, stream=None, lse_win=None, roles_dev=None, R=0):
+    """Score layers [l0, l1) into bufs.score[l0:l1] on ``stream`` (None: current);
+    with the fused role epilogue also their role histograms."""
+    if _fused(bufs, scorer, lse_win):
+        kb.snapkv_score_hist(q[l0:l1], k[l0:l1], roles_dev, R, pool_k, scale, score=bufs.score[l0:l1],
+                             hist=bufs.hist[l0:l1], workspace=bufs.ws_score, stream=stream)
+    elif scorer == "snapkv" and lse_win is not None:
         kb.snapkv_score_lse(q[l0:l1], k[l0:l1], lse_win[l0:l1], pool_k, scale, score=bufs.score[l0:l1],
                             workspace=bufs.ws_score, stream=stream)
     elif scorer == "snapkv":
@@ -139,15 +155,21 @@ def _score(q, k, bufs, scorer, pool_k, scale, page, l0, l1, stream=None, lse_win
                      stream=stream)
 
 
-def _select(k, v, roles_dev, bufs, W, R, l0, l1, stream=None, events=None):
+def _select(k, v, roles_dev, bufs, W, R, l0, l1, stream=None, events=None, fused=False):
     """Top-k and compaction of layers [l0, l1) on ``stream`` (None: current);
     ``events``, three torch.cuda.Event, are recorded before the top-k, between
-    the two calls and after the compaction."""
+    the two calls and after the compaction.  fused: the score call counted the
+    first digit (bufs.hist)."""
     if events is not None:
         events[0].record(stream)
-    kb.topk_select(bufs.score[l0:l1], roles_dev, bufs.quota_dev, W, R, bufs.k_cap,
-                   idx_out=bufs.idx[l0:l1], count_out=bufs.count[l0:l1], workspace=bufs.ws_topk,
-                   stream=stream)
+    if fused:
+        kb.topk_select_hist(bufs.score[l0:l1], roles_dev, bufs.quota_dev, bufs.hist[l0:l1], W, R, bufs.k_cap,
+                            idx_out=bufs.idx[l0:l1], count_out=bufs.count[l0:l1], workspace=bufs.ws_topk,
+                            stream=stream)
+    else:
+        kb.topk_select(bufs.score[l0:l1], roles_dev, bufs.quota_dev, W, R, bufs.k_cap,
+                       idx_out=bufs.idx[l0:l1], count_out=bufs.count[l0:l1], workspace=bufs.ws_topk,
+                       stream=stream)
     if events is not None:
         events[1].record(stream)
     kb.kv_compact(k[l0:l1], None if v is None else v[l0:l1], bufs.idx[l0:l1], bufs.count[l0:l1],
@@ -193,13 +215,15 @@ def evict(q, k, v, roles_host: np.ndarray, roles_dev, policy, budget: float, W: 
     bufs.copy_done.record()
     L = k.shape[0]
     main = torch.cuda.current_stream()
+    fused = _fused(bufs, scorer, lse_win)
     if chunks <= 1 or side_stream is None:
         if score_events is not None:
             score_events[0].record(main)
-        _score(q, k, bufs, scorer, pool_k, scale, page, 0, L, stream=main, lse_win=lse_win)
+        _score(q, k, bufs, scorer, pool_k, scale, page, 0, L, stream=main, lse_win=lse_win, roles_dev=roles_dev,
+               R=R)
         if score_events is not None:
             score_events[1].record(main)
-        _select(k, v, roles_dev, bufs, W, R, 0, L, stream=main, events=select_events)
+        _select(k, v, roles_dev, bufs, W, R, 0, L, stream=main, events=select_events, fused=fused)
         return quota, kept
     side_stream.wait_stream(main)         # the quota upload and earlier work
     per = (L + chunks - 1) // chunks
@@ -207,11 +231,12 @@ def evict(q, k, v, roles_host: np.ndarray, roles_dev, policy, budget: float, W: 
         score_events[0].record(main)
     for l0 in range(0, L, per):
         l1 = min(L, l0 + per)
-        _score(q, k, bufs, scorer, pool_k, scale, page, l0, l1, stream=main, lse_win=lse_win)
+        _score(q, k, bufs, scorer, pool_k, scale, page, l0, l1, stream=main, lse_win=lse_win, roles_dev=roles_dev,
+               R=R)
         done = torch.cuda.Event()
         done.record(main)
         side_stream.wait_event(done)
-        _select(k, v, roles_dev, bufs, W, R, l0, l1, stream=side_stream)
+        _select(k, v, roles_dev, bufs, W, R, l0, l1, stream=side_stream, fused=fused)
     if score_events is not None:
         score_events[1].record(main)
     main.wait_stream(side_stream)
@@ -242,10 +267,12 @@ class StepGraph:
         R = self.policy.R
         self.quota_host = [bufs.quota_host, torch.zeros_like(bufs.quota_host).pin_memory()]
 
+        fused = _fused(bufs, scorer, lse_win)
+
         def step(src):
             bufs.quota_dev.copy_(src, non_blocking=True)
-            _score(q, k, bufs, scorer, pool_k, scale, page, 0, L, lse_win=lse_win)
-            _select(k, v, roles_dev, bufs, W, R, 0, L)
+            _score(q, k, bufs, scorer, pool_k, scale, page, 0, L, lse_win=lse_win, roles_dev=roles_dev, R=R)
+            _select(k, v, roles_dev, bufs, W, R, 0, L, fused=fused)
 
         side = torch.cuda.Stream()
         side.wait_stream(torch.cuda.current_stream())

@@ -983,3 +983,138 @@ def test_role_probe_full_size(K):
     got = out.cpu().numpy()
     for b in (0, B - 1):
         assert np.array_equal(got[b], O.probe_roles(ids[b], weight.numpy(), bias.numpy()))
+
+
+# ---------------------------------------------------------------------------
+# Fused role epilogue: the score's pool step counts the top-k's first digit
+# ---------------------------------------------------------------------------
+
+def _host_role_hist(score, roles, W, R):
+    """Histogram [L, B, Hkv, R, 2048] of the candidates' top 11 key bits,
+    counted on the host from the scores (order-preserving key: -0 as +0, every
+    NaN below -inf)."""
+    L, B, H, N = score.shape
+    bits = np.ascontiguousarray(score, dtype=np.float32).view(np.uint32).copy()
+    bits[bits == 0x80000000] = 0
+    key = np.where(bits & 0x80000000, ~bits, bits | 0x80000000).astype(np.uint32)
+    key[np.isnan(score)] = 0
+    digit = (key >> 21).astype(np.int64)
+    out = np.zeros((L, B, H, R, 2048), dtype=np.int64)
+    P = N - W
+    for l, b, j in np.ndindex(L, B, H):
+        lab = roles[b, :P].astype(np.int64)
+        ok = (lab >= 0) & (lab < R)
+        np.add.at(out[l, b, j], (lab[ok], digit[l, b, j, :P][ok]), 1)
+    return out
+
+
+def _decode_tile_records(words, L, B, H, N, R):
+    """The per-segment histograms [L, B, H, R, 2048] the tile records add up to
+    (the record layout of include/kve.h), and which segments had a tile whose
+    bins overflowed its window."""
+    tiles = (N + 4095) // 4096
+    tw = 4 + R * 256
+    rec = words.view(np.uint32).reshape(L, B, H, tiles, tw)
+    out = np.zeros((L, B, H, R, 2048), dtype=np.int64)
+    over = np.zeros((L, B, H), dtype=bool)
+    for l, b, j, t in np.ndindex(L, B, H, tiles):
+        lo, ov = int(rec[l, b, j, t, 0]), int(rec[l, b, j, t, 1])
+        if ov:
+            over[l, b, j] = True
+            continue
+        if lo == 0xFFFFFFFF:
+            continue
+        body = rec[l, b, j, t, 4:].reshape(R, 256)
+        cnt = np.stack([body & 0xFFFF, body >> 16], axis=-1).reshape(R, 512).astype(np.int64)
+        hi = min(2048, lo + 512)
+        out[l, b, j, :, lo:hi] += cnt[:, :hi - lo]
+    return out, over
+
+
+FUSED_CASES = [
+    # name, L, B, Hq, Hkv, N, W, d, pool, dtype, R, budget
+    ("tiny_f32", 1, 1, 2, 1, 512, 16, 64, 5, "f32", 4, 0.10),
+    ("layer8k", 1, 1, 32, 8, 8192, 32, 128, 7, "bf16", 4, 0.05),
+    ("ragged_pool1", 2, 2, 8, 2, 3001, 24, 128, 1, "bf16", 4, 0.20),
+    ("ragged_pool7", 2, 2, 8, 2, 5003, 32, 128, 7, "bf16", 3, 0.10),
+    ("r1", 2, 1, 8, 2, 4096, 32, 128, 7, "bf16", 1, 0.10),
+    ("r8_labels_out_of_range", 1, 2, 8, 2, 6000, 16, 128, 7, "bf16", 8, 0.30),
+    ("overflow", 1, 1, 4, 1, 4096, 16, 128, 7, "bf16", 4, 0.10),
+]
+
+
+@pytest.mark.parametrize("case", FUSED_CASES, ids=lambda c: c[0])
+def test_fused_role_epilogue_matches_unfused(K, case):
+    """kve_snapkv_score_hist + kve_topk_select_hist against kve_snapkv_score +
+    kve_topk_select: scores, kept indices and counts bit for bit, and the
+    histograms equal to the host's count over the GPU's scores."""
+    name, L, B, Hq, Hkv, N, W, d, pool, dt, R, budget = case
+    note(f"fused role epilogue {name}")
+    wl = custom(name, L, B, Hq, Hkv, N, W, d, pool, dt)
+    inp = WL.make_inputs(wl, device="cuda", with_v=False)
+    if name == "overflow":
+        # every window query along one direction, one key far along it: that key
+        # takes all the mass (pooled score near G*W = 64, about bin 1560) while
+        # the keys beyond its pool window score exactly 0 (bin 1024) in the same
+        # tile: the bins span more than the 512-bin window
+        u = torch.zeros(d, device="cuda")
+        u[0] = 1.0
+        inp["q"][:] = (4.0 * u).to(inp["q"].dtype)
+        inp["k"][:] = (0.01 * torch.randn_like(inp["k"], dtype=torch.float32)).to(inp["k"].dtype)
+        inp["k"][0, 0, 0, 1000] = (400.0 * u).to(inp["k"].dtype)
+    rng = np.random.default_rng(11)
+    roles = rng.integers(0, R, (B, N)).astype(np.int8)
+    if name.startswith("r8"):
+        roles[rng.random((B, N)) < 0.1] = -3      # labels outside [0, R): never counted, never kept
+        roles[rng.random((B, N)) < 0.05] = 9
+    rd = torch.from_numpy(roles).cuda()
+    alpha = [1.0 / R] * R
+    clean = np.where((roles >= 0) & (roles < R), roles, 0).astype(np.int8)
+    quota, kept, k_cap = K.role_allocate(clean, R, alpha, budget, W)
+    qd = torch.from_numpy(quota).cuda()
+    ws = torch.full((K.snapkv_workspace_size(L, B, Hq, Hkv, N, W, d),), 0xFF, dtype=torch.uint8, device="cuda")
+    hist = torch.full((K.role_hist_size(L, B, Hkv, N, R) // 4,), 12345, dtype=torch.int32, device="cuda")  # stale
+    s_f, h_f = K.snapkv_score_hist(inp["q"], inp["k"], rd, R, pool, hist=hist, workspace=ws)
+    i_f, c_f = K.topk_select_hist(s_f, rd, qd, h_f, W, R, k_cap)
+    s_u = K.snapkv_score(inp["q"], inp["k"], pool)
+    i_u, c_u = K.topk_select(s_u, rd, qd, W, R, k_cap)
+    torch.cuda.synchronize()
+    assert torch.equal(s_f.view(torch.int32), s_u.view(torch.int32)), "fused scores differ"
+    assert torch.equal(c_f, c_u), "fused counts differ"
+    cnt = c_u.cpu().numpy()
+    fi, ui = i_f.cpu().numpy(), i_u.cpu().numpy()
+    for idx in np.ndindex(L, B, Hkv):
+        n = int(cnt[idx])
+        assert np.array_equal(fi[idx][:n], ui[idx][:n]), idx
+    ref = _host_role_hist(s_u.cpu().numpy(), roles, W, R)
+    got, over = _decode_tile_records(h_f.cpu().numpy(), L, B, Hkv, N, R)
+    assert np.array_equal(got[~over], ref[~over]), "histogram differs from the host count"
+    report(f"fused epilogue {name}: segments counted in the top-k's own sweep (a tile overflowed)",
+           int(over.sum()))
+    if name == "overflow":
+        assert over.any()
+
+
+def test_fused_pipeline_matches_unfused_stack32k(K):
+    """The step with the fused epilogue against the same step with the
+    separate calls (the default): every index, count and compacted row."""
+    from paper_2607_13205_amd import pipeline
+    wl = WL.get_workload("stack32k")
+    note("fused vs unfused pipeline stack32k")
+    inp = WL.make_inputs(wl, device="cuda")
+    alpha = WL.default_alpha(0.0)
+    _, _, k_cap = K.role_allocate(inp["roles"], 4, alpha, 0.05, wl.W)
+    res = []
+    for fused in (True, False):
+        bufs = pipeline.alloc_buffers(inp["k"], wl.Hq, wl.W, 4, k_cap, fused=fused)
+        assert (bufs.hist is not None) == fused
+        pipeline.evict(inp["q"], inp["k"], inp["v"], inp["roles"], inp["roles_t"], alpha, 0.05, wl.W, wl.pool_k, bufs)
+        torch.cuda.synchronize()
+        res.append(bufs)
+    a, b = res
+    assert torch.equal(a.score.view(torch.int32), b.score.view(torch.int32))
+    assert torch.equal(a.count, b.count) and torch.equal(a.idx, b.idx)
+    assert torch.equal(a.k_out.view(torch.int16), b.k_out.view(torch.int16))
+    assert torch.equal(a.v_out.view(torch.int16), b.v_out.view(torch.int16))
+    del inp, res, a, b
+    torch.cuda.empty_cache()
