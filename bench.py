@@ -55,6 +55,8 @@ METRIC = "prefill tokens scored+compressed/s per GPU; % HBM peak (SnapKV), % MFM
 TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "snapkv_score_stack32k_traffic.md")
 # the same for the score with the window statistics supplied (pass 2 + pool)
 TRAFFIC_SUMMARY_LSE = os.path.join(ROOT, "profiles", "snapkv_score_lse_stack32k_traffic.md")
+# the score on the 128K-token workload (kernel times, matrix-core counters, traffic)
+TRAFFIC_SUMMARY_LONG = os.path.join(ROOT, "profiles", "long128k_score_profile.md")
 # sources of the kernels one score call launches
 SCORE_SOURCES = ("paper_2607_13205_amd/csrc/snapkv.hip", "paper_2607_13205_amd/csrc/kve_stream.h",
                  "paper_2607_13205_amd/csrc/kve_device.h", "paper_2607_13205_amd/csrc/kve_snap_plan.h")
@@ -90,6 +92,7 @@ def parse():
     ap.add_argument("--no-graph", action="store_true",
                     help="skip the step timing through a captured HIP graph")
     ap.add_argument("--no-long", action="store_true", help="skip the long128k legs")
+    ap.add_argument("--no-fused", action="store_true", help="skip the fused role-epilogue step")
     ap.add_argument("--no-ceilings", action="store_true", help="skip the read-ceiling probes")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a plain device copy of 1 GiB (5 times), for counter calibration")
@@ -379,11 +382,14 @@ def long_leg(K, WL, pipeline, alpha, steps):
         stb = step_algorithmic_bytes(wl, kept)
         gbs = sb / (t["score_ms"] * 1e-3) / 1e9
         tf = flops_2pass / (t["score_ms"] * 1e-3) / 1e12
+        traffic = measured_traffic(wl.name, TRAFFIC_SUMMARY_LONG)
         res[f"B={budget}"] = {
             "ms_per_step": round(t["median_ms"], 4), "tokens_per_s": round(wl.B * wl.N / (t["median_ms"] * 1e-3), 1),
             "step_hbm_frac": round(stb / (t["median_ms"] * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
             "score_ms": round(t["score_ms"], 4), "score_hbm_frac": round(gbs / HBM_PEAK_GBS, 4),
             "score_tflops_2pass": round(tf, 1), "score_mfma_frac_2pass": round(tf / BF16_MFMA_PEAK_TFLOPS, 4),
+            "score_traffic": traffic,
+            "score_traffic_GBs": None if traffic is None else round(traffic / (t["score_ms"] * 1e-3) / 1e9, 1),
             "topk_ms": round(t["topk_ms"], 4), "compact_ms": round(t["compact_ms"], 4), "k_cap": k_cap}
         del bufs
         torch.cuda.empty_cache()
@@ -733,7 +739,8 @@ def main():
                        else "kve_snapkv_score (score passes + pool)"),
             "bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
             "frac": round(achieved / HBM_PEAK_GBS, 4),
-            "traffic": measured_traffic(wl.name, TRAFFIC_SUMMARY_LSE if args.lse else TRAFFIC_SUMMARY),
+            "traffic": measured_traffic(wl.name, TRAFFIC_SUMMARY_LSE if args.lse else
+                                        TRAFFIC_SUMMARY_LONG if wl.name == "long128k" else TRAFFIC_SUMMARY),
             "ms": round(ms_score, 4), "ms_is": "mean of the score call over the timed steps",
             "algorithmic_bytes": score_bytes,
         },
@@ -749,7 +756,7 @@ def main():
     if not args.no_ceilings:
         print("[bench] read ceilings", file=sys.stderr, flush=True)
         out["read_ceilings"] = _optional_leg("read_ceilings", lambda: read_ceilings(K))
-    if scorer == "snapkv" and not args.lse and args.chunks <= 1:
+    if scorer == "snapkv" and not args.lse and args.chunks <= 1 and not args.no_fused:
         print("[bench] fused role epilogue", file=sys.stderr, flush=True)
         out["fused_epilogue"] = _optional_leg("fused_epilogue", lambda: fused_leg(
             pipeline, wl, inp, alpha, budget, W, pool, k_cap, max(5, args.steps // 2)))
