@@ -180,8 +180,7 @@ __global__ __launch_bounds__(kThreads, 2) void h2o_pass1_x2(const T* __restrict_
                             if (32 * kb + 8 * (i >> 2) + (i & 3) > last) acc[rs][kb][i] = -INFINITY;
                 }
             }
-            rsum[0].add(acc[0], sl2);
-            rsum[1].add(acc[1], sl2);
+            row_sums_add<2>(rsum, acc, sl2);
         }
     }
 #pragma unroll

@@ -324,22 +324,23 @@ __device__ __forceinline__ void chunk_mma_sets(f32x16 (&acc)[RS][2], const Chunk
 struct RowSum {
     float m = -INFINITY, l = 0.0f;
 
-    __device__ __forceinline__ void add(const f32x16 (&x)[2], float sl2) {
+    // partial sum of exp2(sl2 x - m) over the 32 values (tree order)
+    __device__ __forceinline__ float part(const f32x16 (&x)[2], float sl2) const {
         f32x16 ex[2];  // the logits stay in x for a possible new reference
 #pragma unroll
         for (int b = 0; b < 2; ++b)
 #pragma unroll
             for (int i = 0; i < 16; ++i) ex[b][i] = fast_exp2(fmaf(x[b][i], sl2, -m));
-        float part[4];
+        float p[4];
 #pragma unroll
         for (int e = 0; e < 4; ++e)
-            part[e] = (ex[0][e] + ex[0][e + 4]) + (ex[0][e + 8] + ex[0][e + 12]) +
-                      ((ex[1][e] + ex[1][e + 4]) + (ex[1][e + 8] + ex[1][e + 12]));
-        const float ln = l + ((part[0] + part[1]) + (part[2] + part[3]));
-        if (ln <= 0x1p64f) {  // false for inf and NaN
-            l = ln;
-            return;
-        }
+            p[e] = (ex[0][e] + ex[0][e + 4]) + (ex[0][e + 8] + ex[0][e + 12]) +
+                   ((ex[1][e] + ex[1][e + 4]) + (ex[1][e + 8] + ex[1][e + 12]));
+        return (p[0] + p[1]) + (p[2] + p[3]);
+    }
+    // the chunk's sum left [0, 2^64] (or there is no reference yet): raise
+    // the reference to the largest logit seen so far and add the chunk again
+    __device__ __forceinline__ void reset(const f32x16 (&x)[2], float sl2) {
         float mx = -INFINITY;
 #pragma unroll
         for (int b = 0; b < 2; ++b)
@@ -355,9 +356,42 @@ struct RowSum {
         l = a;
         m = mn;
     }
+    __device__ __forceinline__ void add(const f32x16 (&x)[2], float sl2) {
+        const float ln = l + part(x, sl2);
+        if (ln <= 0x1p64f) {  // false for inf and NaN
+            l = ln;
+            return;
+        }
+        reset(x, sl2);
+    }
     // log2 of the sum, -inf when empty
     __device__ __forceinline__ float lse2() const { return (m != -INFINITY && l > 0.0f) ? m + log2f(l) : -INFINITY; }
 };
+
+// RowSum::add for RS sets at once: the exponentials and sums of every set in
+// one block (one wave's vector work per chunk), then one test of all sums.
+template <int RS>
+__device__ __forceinline__ void row_sums_add(RowSum (&r)[RS], const f32x16 (&x)[RS][2], float sl2) {
+    float ln[RS];
+    bool ok = true;
+#pragma unroll
+    for (int rs = 0; rs < RS; ++rs) {
+        ln[rs] = r[rs].l + r[rs].part(x[rs], sl2);
+        ok = ok && ln[rs] <= 0x1p64f;  // false for inf and NaN
+    }
+    if (__builtin_expect(ok, 1)) {
+#pragma unroll
+        for (int rs = 0; rs < RS; ++rs) r[rs].l = ln[rs];
+        return;
+    }
+#pragma unroll
+    for (int rs = 0; rs < RS; ++rs) {
+        if (ln[rs] <= 0x1p64f)
+            r[rs].l = ln[rs];
+        else
+            r[rs].reset(x[rs], sl2);
+    }
+}
 
 // Sum of exp2(sl2 * x) over the 32 values a lane holds in x (in place: the
 // logits are not needed again), as a tree.

@@ -189,8 +189,7 @@ __global__ __launch_bounds__(kThreads, (TuneRS<T, RS>::kOcc1)) void snap_pass1(
                             if (32 * kb + 8 * (i >> 2) + (i & 3) > last) acc[rs][kb][i] = -INFINITY;
                 }
             }
-#pragma unroll
-            for (int rs = 0; rs < RS; ++rs) rsum[rs].add(acc[rs], sl2);
+            row_sums_add<RS>(rsum, acc, sl2);
         }
     }
 #pragma unroll

@@ -74,6 +74,9 @@ SNAP_CASES = [
     custom("shorttail", 1, 1, 4, 2, 1030, 8, 64, 15, "bf16"),
     # 300 window rows: two 256-row groups, the second with 44 rows and 212 padding rows
     custom("rows300", 1, 2, 12, 2, 3000, 50, 128, 7, "bf16"),
+    # 160 window rows (one 256-row group): ranges of three chunks and a last range of one
+    # chunk of 10 keys, so that the second wave group of the 256-row kernels has nothing to do
+    custom("rows160tail", 1, 1, 4, 1, 394, 40, 128, 7, "bf16"),
     # kernel 7 on rows too short for the register path: every key taken one by one
     custom("short7", 1, 2, 4, 2, 20, 4, 128, 7, "bf16"),
 ]
