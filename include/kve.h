@@ -58,6 +58,22 @@ typedef enum kve_dtype {
     KVE_DTYPE_F32 = 1
 } kve_dtype_t;
 
+/*
+ * Element strides of a 4-D view [layer, batch, head, token] of rows of d
+ * contiguous elements.  A dense [L, B, H, T, d] tensor has strides
+ * (B*H*T*d, H*T*d, T*d, d); a token-major cache [L, B, T, H, d] seen as
+ * [L, B, H, T, d] has (B*T*H*d, T*H*d, d, H*d); a slice of rows keeps its
+ * parent's strides.  The strided entry points take a pointer to this struct
+ * per input (NULL: dense).  Every stride must be >= 0 with stride times the
+ * element size a multiple of 16 bytes, the base pointer 16-byte aligned, and
+ * the token stride at most 2^25 bytes; views may overlap (inputs are only
+ * read).  The library cannot check that a view stays inside its allocation:
+ * that is the caller's part.
+ */
+typedef struct kve_strides {
+    int64_t layer, batch, head, token;
+} kve_strides_t;
+
 /* ABI version (KVE_ABI_VERSION of the built library). */
 int kve_version(void);
 
@@ -109,6 +125,21 @@ kve_status_t kve_snapkv_score(const void* q_win, const void* k, kve_dtype_t dtyp
                               int L, int B, int Hq, int Hkv, int N, int W, int d,
                               float scale, int pool_k, float* score,
                               void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * kve_snapkv_score on strided views of its inputs (kve_strides_t; NULL means
+ * dense): q_win as [L, B, Hq, W, d] (for instance the last W rows of the
+ * prefill queries [L, B, Hq, N, d], whose strides it keeps) and k as
+ * [L, B, Hkv, N, d] (for instance a token-major cache).  Same arithmetic in
+ * the same order: the scores are bit-identical to kve_snapkv_score on dense
+ * copies of the views.  Errors: as for kve_snapkv_score, and
+ * KVE_ERR_INVALID_ARG for strides the view rules above exclude.
+ */
+kve_status_t kve_snapkv_score_strided(const void* q_win, const kve_strides_t* q_strides,
+                                      const void* k, const kve_strides_t* k_strides,
+                                      kve_dtype_t dtype, int L, int B, int Hq, int Hkv, int N,
+                                      int W, int d, float scale, int pool_k, float* score,
+                                      void* workspace, size_t workspace_bytes, void* stream);
 
 /*
  * kve_snapkv_score with the window rows' statistics supplied by the caller:
@@ -432,6 +463,19 @@ kve_status_t kve_kv_compact(const void* k, const void* v, kve_dtype_t dtype,
                             const int32_t* idx, const int32_t* count,
                             int L, int B, int Hkv, int N, int d, int k_cap,
                             void* k_out, void* v_out, void* stream);
+
+/*
+ * kve_kv_compact reading k and v through strided views [L, B, Hkv, N, d]
+ * (kve_strides_t; NULL means dense), e.g. a token-major cache; the outputs
+ * are dense as for kve_kv_compact and bit-identical to it on dense copies.
+ * Errors: as for kve_kv_compact, and KVE_ERR_INVALID_ARG for strides the view
+ * rules exclude.
+ */
+kve_status_t kve_kv_compact_strided(const void* k, const kve_strides_t* k_strides,
+                                    const void* v, const kve_strides_t* v_strides,
+                                    kve_dtype_t dtype, const int32_t* idx, const int32_t* count,
+                                    int L, int B, int Hkv, int N, int d, int k_cap,
+                                    void* k_out, void* v_out, void* stream);
 
 /* ------------------------------------------------------------------------- */
 /* Decode through the keep-set (Algorithm 1, last step; §3 "Setup"; §6        */

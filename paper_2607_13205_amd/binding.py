@@ -35,11 +35,18 @@ EXPORTED = (
     "kve_role_allocate", "kve_role_allocate_fair", "kve_role_map", "kve_role_probe",
     "kve_topk_workspace_size", "kve_topk_select",
     "kve_role_hist_size", "kve_snapkv_score_hist", "kve_topk_select_hist",
-    "kve_kv_compact",
+    "kve_kv_compact", "kve_snapkv_score_strided", "kve_kv_compact_strided",
     "kve_decode_workspace_size", "kve_decode_attention",
     "kve_quest_workspace_size", "kve_quest_score",
     "kve_read_probe",
 )
+
+
+class Strides(ctypes.Structure):
+    """kve_strides_t: element strides of a [layer, batch, head, token] view of
+    rows of d contiguous elements."""
+    _fields_ = [("layer", ctypes.c_int64), ("batch", ctypes.c_int64), ("head", ctypes.c_int64),
+                ("token", ctypes.c_int64)]
 
 
 class KveError(RuntimeError):
@@ -87,6 +94,10 @@ def _load():
                                  [c_void, c_void, c_void, c_size, c_void]),
         "kve_kv_compact": (c_int, [c_void, c_void, c_int, c_void, c_void] + [c_int] * 6 +
                            [c_void, c_void, c_void]),
+        "kve_snapkv_score_strided": (c_int, [c_void, c_void, c_void, c_void, c_int] + [c_int] * 7 +
+                                     [c_float, c_int, c_void, c_void, c_size, c_void]),
+        "kve_kv_compact_strided": (c_int, [c_void, c_void, c_void, c_void, c_int, c_void, c_void] +
+                                   [c_int] * 6 + [c_void, c_void, c_void]),
         "kve_decode_workspace_size": (c_size, [c_int] * 6),
         "kve_quest_workspace_size": (c_size, [c_int] * 5),
         "kve_quest_score": (c_int, [c_void, c_void, c_int] + [c_int] * 8 + [c_void, c_void, c_size, c_void]),
@@ -155,6 +166,17 @@ def _dev(t, name):
     return ctypes.c_void_p(t.data_ptr())
 
 
+def _view(t, name):
+    """(pointer, Strides) of a 5-D device tensor whose last dimension is
+    contiguous, for the strided entry points."""
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a device tensor")
+    if t.dim() != 5 or (t.shape[4] > 1 and t.stride(4) != 1):
+        raise ValueError(f"{name} must be 5-D with a contiguous last dimension")
+    st = Strides(*(int(t.stride(i)) for i in range(4)))
+    return ctypes.c_void_p(t.data_ptr()), st
+
+
 def _stream(stream=None):
     torch = _torch()
     s = torch.cuda.current_stream() if stream is None else stream
@@ -195,12 +217,36 @@ def snapkv_score(q_win, k, pool_k: int, scale: float = 0.0, score=None, workspac
     Lk, Bk, Hkv, N, dk = k.shape
     if (L, B, d) != (Lk, Bk, dk) or q_win.dtype != k.dtype:
         raise ValueError("q_win and k disagree in L, B, d or dtype")
+    if not (q_win.is_contiguous() and k.is_contiguous()):
+        return snapkv_score_strided(q_win, k, pool_k, scale, score, workspace, stream)
     if score is None:
         score = torch.empty((L, B, Hkv, N), dtype=torch.float32, device=k.device)
     ws, wsb = _workspace(lambda: snapkv_workspace_size(L, B, Hq, Hkv, N, W, d), k.device, workspace)
     _check(LIB.kve_snapkv_score(_dev(q_win, "q_win"), _dev(k, "k"), _dtype_code(k),
                                 L, B, Hq, Hkv, N, W, d, float(scale), int(pool_k),
                                 _dev(score, "score"), _ptr(ws), wsb, _stream(stream)))
+    return score
+
+
+def snapkv_score_strided(q_win, k, pool_k: int, scale: float = 0.0, score=None, workspace=None,
+                         stream=None):
+    """snapkv_score on views: q_win [L, B, Hq, W, d] and k [L, B, Hkv, N, d]
+    may have any strides with a contiguous last dimension (e.g. q_full[..., -W:, :]
+    or a token-major cache permuted to [L, B, Hkv, N, d]); see
+    kve_snapkv_score_strided in include/kve.h."""
+    torch = _torch()
+    L, B, Hq, W, d = q_win.shape
+    Lk, Bk, Hkv, N, dk = k.shape
+    if (L, B, d) != (Lk, Bk, dk) or q_win.dtype != k.dtype:
+        raise ValueError("q_win and k disagree in L, B, d or dtype")
+    if score is None:
+        score = torch.empty((L, B, Hkv, N), dtype=torch.float32, device=k.device)
+    ws, wsb = _workspace(lambda: snapkv_workspace_size(L, B, Hq, Hkv, N, W, d), k.device, workspace)
+    qp, qs = _view(q_win, "q_win")
+    kp, ks = _view(k, "k")
+    _check(LIB.kve_snapkv_score_strided(qp, ctypes.byref(qs), kp, ctypes.byref(ks), _dtype_code(k),
+                                        L, B, Hq, Hkv, N, W, d, float(scale), int(pool_k),
+                                        _dev(score, "score"), _ptr(ws), wsb, _stream(stream)))
     return score
 
 
@@ -417,10 +463,37 @@ def kv_compact(k, v, idx, count, k_out=None, v_out=None, stream=None):
         k_out = torch.zeros((L, B, Hkv, k_cap, d), dtype=k.dtype, device=k.device)
     if v is not None and v_out is None:
         v_out = torch.zeros_like(k_out)
+    if not (k.is_contiguous() and (v is None or v.is_contiguous())):
+        return kv_compact_strided(k, v, idx, count, k_out, v_out, stream)
     _check(LIB.kve_kv_compact(_dev(k, "k"), None if v is None else _dev(v, "v"), _dtype_code(k),
                               _dev(idx, "idx"), _dev(count, "count"), L, B, Hkv, N, d, int(k_cap),
                               _dev(k_out, "k_out"), None if v is None else _dev(v_out, "v_out"),
                               _stream(stream)))
+    return k_out, v_out
+
+
+def kv_compact_strided(k, v, idx, count, k_out=None, v_out=None, stream=None):
+    """kv_compact reading k and v [L, B, Hkv, N, d] as views (any strides with
+    a contiguous last dimension); outputs dense.  See kve_kv_compact_strided."""
+    torch = _torch()
+    L, B, Hkv, N, d = k.shape
+    k_cap = idx.shape[-1]
+    if tuple(idx.shape[:3]) != (L, B, Hkv) or idx.dtype != torch.int32:
+        raise ValueError("idx must be int32 [L, B, Hkv, k_cap]")
+    if tuple(count.shape) != (L, B, Hkv) or count.dtype != torch.int32:
+        raise ValueError("count must be int32 [L, B, Hkv]")
+    if v is not None and (v.shape != k.shape or v.dtype != k.dtype):
+        raise ValueError("v must match k")
+    if k_out is None:
+        k_out = torch.zeros((L, B, Hkv, k_cap, d), dtype=k.dtype, device=k.device)
+    if v is not None and v_out is None:
+        v_out = torch.zeros_like(k_out)
+    kp, ks = _view(k, "k")
+    vp, vs = (None, None) if v is None else _view(v, "v")
+    _check(LIB.kve_kv_compact_strided(kp, ctypes.byref(ks), vp, None if v is None else ctypes.byref(vs),
+                                      _dtype_code(k), _dev(idx, "idx"), _dev(count, "count"), L, B, Hkv, N,
+                                      d, int(k_cap), _dev(k_out, "k_out"),
+                                      None if v is None else _dev(v_out, "v_out"), _stream(stream)))
     return k_out, v_out
 
 

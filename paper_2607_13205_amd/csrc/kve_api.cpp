@@ -135,18 +135,52 @@ int32_t allocate_sample(const long long* n, const double* alpha, int R, double b
     return (int32_t)sum;
 }
 
+// Largest token stride of a view, in bytes: the chunk loads keep the offsets
+// of 64 rows in 32 bits.
+constexpr long long kMaxTokenStrideBytes = 1LL << 25;
+
+// The view of a [L, B, H, T, d] input: dense when st is null, else checked
+// against the view rules of kve.h.
+kve_status_t make_view(const char* fn, const char* name, const void* p, const kve_strides_t* st, int B, int H,
+                       int T, int d, int es, kve::RowView* out) {
+    if (st == nullptr) {
+        *out = kve::dense_view(p, B, H, T, d, es);
+        return KVE_OK;
+    }
+    const long long s[4] = {st->layer, st->batch, st->head, st->token};
+    for (int i = 0; i < 4; ++i) {
+        if (s[i] < 0) return fail(KVE_ERR_INVALID_ARG, "%s: %s has a negative stride", fn, name);
+        if (s[i] > (1LL << 40)) return fail(KVE_ERR_INVALID_ARG, "%s: %s stride too large", fn, name);
+        if ((s[i] * es) % 16 != 0)
+            return fail(KVE_ERR_INVALID_ARG, "%s: %s stride %lld is not a multiple of 16 bytes", fn, name, s[i]);
+    }
+    if (s[3] * es > kMaxTokenStrideBytes)
+        return fail(KVE_ERR_INVALID_ARG, "%s: %s token stride of %lld bytes exceeds %lld", fn, name, s[3] * es,
+                    kMaxTokenStrideBytes);
+    if ((reinterpret_cast<uintptr_t>(p) & 15u) != 0)
+        return fail(KVE_ERR_INVALID_ARG, "%s: %s not 16-byte aligned", fn, name);
+    *out = kve::RowView{static_cast<const char*>(p), s[0] * es, s[1] * es, s[2] * es, s[3] * es};
+    return KVE_OK;
+}
+
 // use_scratch: the workspace is this GPU's static scratch array (workspace
 // and workspace_bytes are ignored); the plan must fit in it
 // roles/R/hist: the fused role epilogue (roles == nullptr: none)
+// q_st/k_st: strides of the inputs' views (null: dense)
 kve_status_t snapkv_common(const char* fn, const void* q_win, const void* k, const float* lse_win,
                            kve_dtype_t dtype, int L, int B, int Hq, int Hkv, int N, int W, int d, float scale,
                            int pool_k, float* score, void* workspace, size_t workspace_bytes, void* stream,
                            bool use_scratch = false, const int8_t* roles = nullptr, int R = 0,
-                           uint32_t* hist = nullptr) {
+                           uint32_t* hist = nullptr, const kve_strides_t* q_st = nullptr,
+                           const kve_strides_t* k_st = nullptr) {
     kve_status_t st = check_common(fn, L, B, Hq, Hkv, N, d, (int)dtype);
     if (st != KVE_OK) return st;
     if (q_win == nullptr || k == nullptr || score == nullptr)
         return fail(KVE_ERR_INVALID_ARG, "%s: null tensor pointer", fn);
+    const int es = dtype == KVE_DTYPE_BF16 ? 2 : 4;
+    kve::RowView qv, kv;
+    if ((st = make_view(fn, "q_win", q_win, q_st, B, Hq, W, d, es, &qv)) != KVE_OK) return st;
+    if ((st = make_view(fn, "k", k, k_st, B, Hkv, N, d, es, &kv)) != KVE_OK) return st;
     if (W < 1 || W > N) return fail(KVE_ERR_INVALID_ARG, "%s: need 1 <= W <= N (W=%d N=%d)", fn, W, N);
     if (pool_k < 1 || pool_k % 2 == 0 || pool_k > 255)
         return fail(KVE_ERR_INVALID_ARG, "%s: pool_k must be odd in [1, 255] (got %d)", fn, pool_k);
@@ -180,7 +214,7 @@ kve_status_t snapkv_common(const char* fn, const void* q_win, const void* k, con
         if (!aligned(workspace)) return fail(KVE_ERR_INVALID_ARG, "%s: workspace not 256-byte aligned", fn);
     }
     if (scale == 0.0f) scale = 1.0f / std::sqrt((float)d);
-    return from_hip(kve::launch_snapkv(q_win, k, lse_win, (int)dtype, L, B, Hq, Hkv, N, W, d, scale, pool_k,
+    return from_hip(kve::launch_snapkv(qv, kv, lse_win, (int)dtype, L, B, Hq, Hkv, N, W, d, scale, pool_k,
                                        score, roles, R, hist, workspace, static_cast<hipStream_t>(stream)),
                     fn);
 }
@@ -212,6 +246,32 @@ kve_status_t topk_common(const char* fn, const float* score, const int8_t* roles
                     fn);
 }
 
+// Checks of kve_kv_compact and its strided variant.
+kve_status_t compact_common(const char* fn, const void* k, const kve_strides_t* k_st, const void* v,
+                            const kve_strides_t* v_st, kve_dtype_t dtype, const int32_t* idx,
+                            const int32_t* count, int L, int B, int Hkv, int N, int d, int k_cap, void* k_out,
+                            void* v_out, void* stream) {
+    if (k == nullptr || idx == nullptr || count == nullptr || k_out == nullptr)
+        return fail(KVE_ERR_INVALID_ARG, "%s: null pointer", fn);
+    if ((v == nullptr) != (v_out == nullptr))
+        return fail(KVE_ERR_INVALID_ARG, "%s: v and v_out must both be given or both be NULL", fn);
+    if (L <= 0 || B <= 0 || Hkv <= 0 || N <= 0 || k_cap < 0)
+        return fail(KVE_ERR_INVALID_ARG, "%s: invalid sizes", fn);
+    if (dtype != KVE_DTYPE_BF16 && dtype != KVE_DTYPE_F32)
+        return fail(KVE_ERR_UNSUPPORTED, "%s: unknown dtype %d", fn, (int)dtype);
+    if (d != 64 && d != 128) return fail(KVE_ERR_UNSUPPORTED, "%s: head_dim %d not built", fn, d);
+    const long long segs = (long long)L * B * Hkv;
+    if (segs * ((k_cap + 63) / 64) > kMaxGrid) return fail(KVE_ERR_UNSUPPORTED, "%s: shape too large", fn);
+    const int es = dtype == KVE_DTYPE_BF16 ? 2 : 4;
+    kve::RowView kv, vv{};
+    kve_status_t st = make_view(fn, "k", k, k_st, B, Hkv, N, d, es, &kv);
+    if (st != KVE_OK) return st;
+    if (v != nullptr && (st = make_view(fn, "v", v, v_st, B, Hkv, N, d, es, &vv)) != KVE_OK) return st;
+    return from_hip(kve::launch_compact(kv, vv, es, idx, count, L, B, Hkv, N, d, k_cap, k_out, v_out,
+                                        static_cast<hipStream_t>(stream)),
+                    fn);
+}
+
 }  // namespace
 
 extern "C" {
@@ -239,6 +299,15 @@ kve_status_t kve_snapkv_score(const void* q_win, const void* k, kve_dtype_t dtyp
                               float* score, void* workspace, size_t workspace_bytes, void* stream) {
     return snapkv_common("kve_snapkv_score", q_win, k, nullptr, dtype, L, B, Hq, Hkv, N, W, d, scale, pool_k,
                          score, workspace, workspace_bytes, stream);
+}
+
+kve_status_t kve_snapkv_score_strided(const void* q_win, const kve_strides_t* q_strides, const void* k,
+                                      const kve_strides_t* k_strides, kve_dtype_t dtype, int L, int B, int Hq,
+                                      int Hkv, int N, int W, int d, float scale, int pool_k, float* score,
+                                      void* workspace, size_t workspace_bytes, void* stream) {
+    return snapkv_common("kve_snapkv_score_strided", q_win, k, nullptr, dtype, L, B, Hq, Hkv, N, W, d, scale,
+                         pool_k, score, workspace, workspace_bytes, stream, false, nullptr, 0, nullptr, q_strides,
+                         k_strides);
 }
 
 kve_status_t kve_snapkv_score_lse(const void* q_win, const void* k, const float* lse_win, kve_dtype_t dtype,
@@ -472,25 +541,20 @@ kve_status_t kve_snapkv_score_hist(const void* q_win, const void* k, kve_dtype_t
                          score, workspace, workspace_bytes, stream, false, roles, R, hist);
 }
 
+
 kve_status_t kve_kv_compact(const void* k, const void* v, kve_dtype_t dtype, const int32_t* idx,
                             const int32_t* count, int L, int B, int Hkv, int N, int d, int k_cap,
                             void* k_out, void* v_out, void* stream) {
-    const char* fn = "kve_kv_compact";
-    if (k == nullptr || idx == nullptr || count == nullptr || k_out == nullptr)
-        return fail(KVE_ERR_INVALID_ARG, "%s: null pointer", fn);
-    if ((v == nullptr) != (v_out == nullptr))
-        return fail(KVE_ERR_INVALID_ARG, "%s: v and v_out must both be given or both be NULL", fn);
-    if (L <= 0 || B <= 0 || Hkv <= 0 || N <= 0 || k_cap < 0)
-        return fail(KVE_ERR_INVALID_ARG, "%s: invalid sizes", fn);
-    if (dtype != KVE_DTYPE_BF16 && dtype != KVE_DTYPE_F32)
-        return fail(KVE_ERR_UNSUPPORTED, "%s: unknown dtype %d", fn, (int)dtype);
-    if (d != 64 && d != 128) return fail(KVE_ERR_UNSUPPORTED, "%s: head_dim %d not built", fn, d);
-    const long long segs = (long long)L * B * Hkv;
-    if (segs * ((k_cap + 63) / 64) > kMaxGrid) return fail(KVE_ERR_UNSUPPORTED, "%s: shape too large", fn);
-    const int es = dtype == KVE_DTYPE_BF16 ? 2 : 4;
-    return from_hip(kve::launch_compact(k, v, es, idx, count, L, B, Hkv, N, d, k_cap, k_out, v_out,
-                                        static_cast<hipStream_t>(stream)),
-                    fn);
+    return compact_common("kve_kv_compact", k, nullptr, v, nullptr, dtype, idx, count, L, B, Hkv, N, d, k_cap,
+                          k_out, v_out, stream);
+}
+
+kve_status_t kve_kv_compact_strided(const void* k, const kve_strides_t* k_strides, const void* v,
+                                    const kve_strides_t* v_strides, kve_dtype_t dtype, const int32_t* idx,
+                                    const int32_t* count, int L, int B, int Hkv, int N, int d, int k_cap,
+                                    void* k_out, void* v_out, void* stream) {
+    return compact_common("kve_kv_compact_strided", k, k_strides, v, v_strides, dtype, idx, count, L, B, Hkv, N,
+                          d, k_cap, k_out, v_out, stream);
 }
 
 kve_status_t kve_read_probe(const void* buf, size_t bytes, int nontemporal, float* sink, int blocks,

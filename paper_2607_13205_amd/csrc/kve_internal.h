@@ -92,11 +92,28 @@ inline QuestPlan quest_plan(int L, int B, int Hq, int Hkv, int N, int W, int d, 
     return p;
 }
 
+// A 4-D view [layer, batch, head, token] of rows of d contiguous elements:
+// byte strides of the four dimensions (each a multiple of 16, so that every
+// row starts 16-byte aligned).  Dense tensors [L, B, H, T, d] have strides
+// (B H T, H T, T, 1) rows of d elements.
+struct RowView {
+    const char* base;
+    long long s_layer, s_batch, s_head, s_token;
+};
+
+inline RowView dense_view(const void* p, int B, int H, int T, int d, int elem_bytes) {
+    const long long row = (long long)d * elem_bytes;
+    return RowView{static_cast<const char*>(p), (long long)B * H * T * row, (long long)H * T * row,
+                   (long long)T * row, row};
+}
+
 // lse_win: the window rows' natural-log log-sum-exp from the caller, or null
 // to compute it (pass 1 and the combine step).  roles: bucket labels [B, N] of
 // the fused role epilogue, or null; with them the call also writes the role
 // histograms hist [L*B*Hkv, R, kRoleHistBins] (zeroed and filled in the call).
-hipError_t launch_snapkv(const void* q, const void* k, const float* lse_win, int dtype, int L, int B, int Hq,
+// q: the window queries [L, B, Hq, W, d] as a view (head Hq, token W); k: the
+// keys [L, B, Hkv, N, d] as a view.
+hipError_t launch_snapkv(const RowView& q, const RowView& k, const float* lse_win, int dtype, int L, int B, int Hq,
                          int Hkv, int N, int W, int d, float scale, int pool_k, float* score, const int8_t* roles,
                          int R, uint32_t* hist, void* ws, hipStream_t st);
 
@@ -128,7 +145,8 @@ hipError_t launch_probe(const int32_t* ids, int B, int N, const float* weight, c
 hipError_t launch_read_probe(const void* buf, size_t bytes, int nontemporal, float* sink, int blocks,
                              hipStream_t st);
 
-hipError_t launch_compact(const void* k, const void* v, int elem_bytes, const int32_t* idx,
+// k, v: views [L, B, Hkv, N, d] (v.base null: keys only); outputs dense [L, B, Hkv, k_cap, d]
+hipError_t launch_compact(const RowView& k, const RowView& v, int elem_bytes, const int32_t* idx,
                           const int32_t* count, int L, int B, int Hkv, int N, int d, int k_cap,
                           void* k_out, void* v_out, hipStream_t st);
 

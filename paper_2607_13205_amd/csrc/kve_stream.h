@@ -96,28 +96,36 @@ struct ChunkReader {
 
 // Direct-to-LDS loads of whole chunks with the per-lane global offsets worked
 // out once per kernel.  Wave `wv` (wave-uniform) of NWAVES issues LPW loads
-// per chunk; load j lands at byte (j * NWAVES + wv) * 1024 of the slot.  A
-// chunk with fewer than KEYS valid rows reads row 0 in place of the missing
-// rows (never outside the segment), so the number of loads per chunk stays
-// fixed; callers mask those keys.  NT: non-temporal loads (see lds_dma16).
+// per chunk; load j lands at byte (j * NWAVES + wv) * 1024 of the slot.  Key
+// row r of a chunk starts r * row_stride bytes after the chunk's first row (a
+// multiple of 16, ROW for dense rows), so rows of a strided view (e.g. a
+// token-major cache) load the same way.  A chunk with fewer than KEYS valid
+// rows reads row 0 in place of the missing rows (never outside the segment),
+// so the number of loads per chunk stays fixed; callers mask those keys.
+// NT: non-temporal loads (see lds_dma16).
 template <typename T, int D, int KEYS, int NWAVES, bool NT = false>
 struct ChunkWriter {
     using C = KChunk<T, D, KEYS>;
     static constexpr int LPW = C::BYTES / (NWAVES * 1024);
     static_assert(C::BYTES % (NWAVES * 1024) == 0, "chunk must split into whole 1 KiB wave loads");
     unsigned goff[LPW];
-    int wv;
+    unsigned rstride;
+    int wv, lane;
 
-    __device__ __forceinline__ void init(int wv_uniform, int lane) {
+    __device__ __forceinline__ void init(int wv_uniform, int lane_, unsigned row_stride = C::ROW) {
         wv = wv_uniform;
+        lane = lane_;
+        rstride = row_stride;
 #pragma unroll
         for (int j = 0; j < LPW; ++j) {
+            const int r = row_of(j);
             const int o = (j * NWAVES + wv) * 1024 + lane * 16;
-            const int r = o / C::ROW;
             const int c = ((o - r * C::ROW) >> 4) ^ chunk_swz_bits<C::ROW>(r);  // inverse of chunk_swz
-            goff[j] = (unsigned)(r * C::ROW + c * 16);
+            goff[j] = (unsigned)r * row_stride + (unsigned)(c * 16);
         }
     }
+    // chunk row of this lane's load j
+    __device__ __forceinline__ int row_of(int j) const { return ((j * NWAVES + wv) * 1024 + lane * 16) / C::ROW; }
     // rows: first key row of the chunk (wave-uniform); valid: rows in bounds
     __device__ __forceinline__ void issue(char* slot, const char* rows, int valid) const {
         if (valid >= KEYS) {
@@ -126,9 +134,9 @@ struct ChunkWriter {
         } else {
 #pragma unroll
             for (int j = 0; j < LPW; ++j) {
-                const int r = (int)(goff[j] / C::ROW);
-                lds_dma16<NT>(rows, r < valid ? goff[j] : goff[j] - (unsigned)(r * C::ROW),
-                          slot + (j * NWAVES + wv) * 1024);
+                const int r = row_of(j);
+                lds_dma16<NT>(rows, r < valid ? goff[j] : goff[j] - (unsigned)r * rstride,
+                              slot + (j * NWAVES + wv) * 1024);
             }
         }
     }
@@ -200,8 +208,8 @@ struct ChunkRing {
     Wr wr;
     int nch;
 
-    __device__ __forceinline__ void open(int nchunks, int wave_uniform, int lane) {
-        wr.init(wave_uniform, lane);
+    __device__ __forceinline__ void open(int nchunks, int wave_uniform, int lane, unsigned row_stride = C::ROW) {
+        wr.init(wave_uniform, lane, row_stride);
         nch = nchunks;
     }
     template <typename Src>

@@ -115,10 +115,23 @@ __device__ __forceinline__ Span span_of(int nranges, int rgroups, int range_keys
 template <typename T, int D>
 using QRows = typename Mma<T>::frag[KChunk<T, D, kKeys>::NSTEP];
 
+// Start of segment seg's rows in a view whose head dimension has `heads`
+// heads per segment (1 for keys, G for the queries of a KV group): segments
+// are (layer, sample, KV head), KV head fastest.
+__device__ __forceinline__ const char* seg_rows(const RowView& v, int seg, int B, int Hkv, int heads) {
+    const int j = seg % Hkv;
+    const int lb = seg / Hkv;
+    return v.base + (long long)(lb / B) * v.s_layer + (long long)(lb % B) * v.s_batch +
+           (long long)j * heads * v.s_head;
+}
+
+// row: the segment's window row g W + i (query head g of the group, window
+// position i); qseg: the group's first query head (seg_rows with heads G)
 template <typename T, int D>
-__device__ __forceinline__ void load_q(QRows<T, D>& qf, const T* q, int seg, int rows, int row, int lane) {
+__device__ __forceinline__ void load_q(QRows<T, D>& qf, const char* qseg, const RowView& qv, int rows, int W,
+                                       int row, int lane) {
     using M = Mma<T>;
-    const T* base = q + ((size_t)seg * rows + row) * D;
+    const char* base = qseg + (long long)(row / W) * qv.s_head + (long long)(row % W) * qv.s_token;
 #pragma unroll
     for (int st = 0; st < KChunk<T, D, kKeys>::NSTEP; ++st) {
         qf[st] = row < rows ? M::load(base, st * M::KSTEP + (lane >> 5) * M::KPL) : M::zero();
@@ -126,22 +139,24 @@ __device__ __forceinline__ void load_q(QRows<T, D>& qf, const T* q, int seg, int
     }
 }
 
-// Chunks of a key range of one segment: chunk c starts at key t_begin + 64 c.
+// Chunks of a key range of one segment: chunk c starts at key t_begin + 64 c;
+// key rows are `stride` bytes apart.
 template <typename T, int D>
 struct KeyChunks {
     const char* kseg;
+    long long stride;
     int t_begin, t_end;
     __device__ __forceinline__ void operator()(int c, const char** rows, int* valid) const {
         const int t0 = t_begin + c * kKeys;
-        *rows = kseg + (size_t)t0 * KChunk<T, D, kKeys>::ROW;
+        *rows = kseg + (long long)t0 * stride;
         *valid = t_end - t0;
     }
 };
 
 template <typename T, int D, int RS>
 __global__ __launch_bounds__(kThreads, (TuneRS<T, RS>::kOcc1)) void snap_pass1(
-    const T* __restrict__ q, const T* __restrict__ k, int N, int W, int rows, int rgroups, int nranges,
-    int range_keys, float sl2, float* __restrict__ stats) {
+    RowView qv, RowView kv, int B, int Hkv, int N, int W, int rows, int rgroups, int nranges, int range_keys,
+    float sl2, float* __restrict__ stats) {
     constexpr int kRing = TuneRS<T, RS>::kRing1;
     constexpr int kRpg = RS * kSnapRowsPerGroup;
     using G = Geo<T, D, kRing>;
@@ -152,20 +167,20 @@ __global__ __launch_bounds__(kThreads, (TuneRS<T, RS>::kOcc1)) void snap_pass1(
     const int P_rows = N - W;
 
     // wave w holds rows 32 RS w .. 32 RS (w + 1) - 1 of the row group, in RS sets of 32
+    const char* qseg = seg_rows(qv, sp.seg, B, Hkv, rows / W);
     QRows<T, D> qf[RS];
     int lim[RS];
 #pragma unroll
     for (int rs = 0; rs < RS; ++rs) {
         const int qr = sp.rg * kRpg + (wave * RS + rs) * 32 + (lane & 31);  // this lane's query row
-        load_q<T, D>(qf[rs], q, sp.seg, rows, qr, lane);
+        load_q<T, D>(qf[rs], qseg, qv, rows, W, qr, lane);
         lim[rs] = qr < rows ? P_rows + qr % W : -1;  // last key the row sees
     }
     typename G::Rd rd;
     rd.init(lane, 0);
     typename G::Ring ring_io;
-    ring_io.open(sp.nch, wave, lane);
-    const KeyChunks<T, D> src{reinterpret_cast<const char*>(k) + (size_t)sp.seg * N * G::C::ROW, sp.t_begin,
-                              sp.t_end};
+    ring_io.open(sp.nch, wave, lane, (unsigned)kv.s_token);
+    const KeyChunks<T, D> src{seg_rows(kv, sp.seg, B, Hkv, 1), kv.s_token, sp.t_begin, sp.t_end};
     ring_io.prologue(ring, src);
 
     RowSum rsum[RS];
@@ -246,8 +261,8 @@ __global__ __launch_bounds__(2 * kSnapRowsPerGroup) void snap_import_lse(const f
 
 template <typename T, int D, int RS>
 __global__ __launch_bounds__(kThreads, (TuneRS<T, RS>::kOcc2)) void snap_pass2(
-    const T* __restrict__ q, const T* __restrict__ k, int N, int W, int rows, int rgroups, int nranges,
-    int range_keys, float sl2, const float* __restrict__ lse, int segs, float* __restrict__ raw) {
+    RowView qv, RowView kv, int B, int Hkv, int N, int W, int rows, int rgroups, int nranges, int range_keys,
+    float sl2, const float* __restrict__ lse, int segs, float* __restrict__ raw) {
     constexpr int kRing = TuneRS<T, RS>::kRing2;
     constexpr int kRpg = RS * kSnapRowsPerGroup;
     using G = Geo<T, D, kRing>;
@@ -271,10 +286,11 @@ __global__ __launch_bounds__(kThreads, (TuneRS<T, RS>::kOcc2)) void snap_pass2(
         swin[r] = (sp.rg * kRpg + r) % W;
     }
     // wave w holds rows 32 RS w .. 32 RS (w + 1) - 1 of the row group, in RS sets of 32
+    const char* qseg = seg_rows(qv, sp.seg, B, Hkv, rows / W);
     QRows<T, D> qf[RS];
 #pragma unroll
     for (int rs = 0; rs < RS; ++rs)
-        load_q<T, D>(qf[rs], q, sp.seg, rows, sp.rg * kRpg + (wave * RS + rs) * 32 + (lane & 31), lane);
+        load_q<T, D>(qf[rs], qseg, qv, rows, W, sp.rg * kRpg + (wave * RS + rs) * 32 + (lane & 31), lane);
     __syncthreads();  // sinit, swin written (nothing streams yet)
     // start values of this lane's 16 rows of each set, the same for every chunk
     f32x16 c_init[RS];
@@ -293,9 +309,8 @@ __global__ __launch_bounds__(kThreads, (TuneRS<T, RS>::kOcc2)) void snap_pass2(
     typename G::Rd rd;
     rd.init(lane, 0);
     typename G::Ring ring_io;
-    ring_io.open(sp.nch, wave, lane);
-    const KeyChunks<T, D> src{reinterpret_cast<const char*>(k) + (size_t)sp.seg * N * G::C::ROW, sp.t_begin,
-                              sp.t_end};
+    ring_io.open(sp.nch, wave, lane, (unsigned)kv.s_token);
+    const KeyChunks<T, D> src{seg_rows(kv, sp.seg, B, Hkv, 1), kv.s_token, sp.t_begin, sp.t_end};
     ring_io.prologue(ring, src);
     float* out = raw + ((size_t)sp.rg * segs + sp.seg) * N;
 
@@ -538,41 +553,40 @@ __global__ __launch_bounds__(kThreads) void snap_pool(const float* __restrict__ 
 }
 
 template <typename T, int D, int RS>
-void launch_passes(const T* qt, const T* kt, const float* lse_win, const SnapPlan& p, int N, int W, float sl2,
-                   float* stats, float* lse, float* raw, hipStream_t st) {
+void launch_passes(const RowView& qv, const RowView& kv, int B, int Hkv, const float* lse_win, const SnapPlan& p,
+                   int N, int W, float sl2, float* stats, float* lse, float* raw, hipStream_t st) {
     const dim3 grid((unsigned)((size_t)p.n_vsegs * p.nranges));
     if (lse_win != nullptr) {  // row statistics from the caller: one read of K
         hipLaunchKernelGGL(snap_import_lse, dim3((unsigned)p.n_vsegs), dim3(p.rpg), 0, st, lse_win, p.rows,
                            p.rgroups, lse);
     } else {
-        hipLaunchKernelGGL((snap_pass1<T, D, RS>), grid, dim3(kThreads), 0, st, qt, kt, N, W, p.rows, p.rgroups,
-                           p.nranges, p.range_keys, sl2, stats);
+        hipLaunchKernelGGL((snap_pass1<T, D, RS>), grid, dim3(kThreads), 0, st, qv, kv, B, Hkv, N, W, p.rows,
+                           p.rgroups, p.nranges, p.range_keys, sl2, stats);
         hipLaunchKernelGGL(snap_combine, dim3((unsigned)p.n_vsegs), dim3(p.rpg * kCombineSplit), 0, st, stats,
                            p.nranges, p.rows,
                            p.rgroups, lse);
     }
-    hipLaunchKernelGGL((snap_pass2<T, D, RS>), grid, dim3(kThreads), 0, st, qt, kt, N, W, p.rows, p.rgroups,
-                       p.nranges, p.range_keys, sl2, lse, p.segs, raw);
+    hipLaunchKernelGGL((snap_pass2<T, D, RS>), grid, dim3(kThreads), 0, st, qv, kv, B, Hkv, N, W, p.rows,
+                       p.rgroups, p.nranges, p.range_keys, sl2, lse, p.segs, raw);
 }
 
 template <typename T, int D>
-hipError_t run_snapkv(const void* q, const void* k, const float* lse_win, int L, int B, int Hq, int Hkv, int N,
-                      int W, float scale, int pool_k, float* score, const RoleHist& rh, void* ws, hipStream_t st) {
+hipError_t run_snapkv(const RowView& qv, const RowView& kv, const float* lse_win, int L, int B, int Hq, int Hkv,
+                      int N, int W, float scale, int pool_k, float* score, const RoleHist& rh, void* ws,
+                      hipStream_t st) {
     const SnapPlan p = snap_plan(L, B, Hq, Hkv, N, W, D, (int)sizeof(T));
     char* w = static_cast<char*>(ws);
     float* stats = reinterpret_cast<float*>(w + p.off_stats);
     float* lse = reinterpret_cast<float*>(w + p.off_lse);
     float* raw = reinterpret_cast<float*>(w + p.off_raw);
     const float sl2 = scale * kLog2e;
-    const T* qt = static_cast<const T*>(q);
-    const T* kt = static_cast<const T*>(k);
     if constexpr (sizeof(T) == 2) {
         if (p.sets == 2)
-            launch_passes<T, D, 2>(qt, kt, lse_win, p, N, W, sl2, stats, lse, raw, st);
+            launch_passes<T, D, 2>(qv, kv, B, Hkv, lse_win, p, N, W, sl2, stats, lse, raw, st);
         else
-            launch_passes<T, D, 1>(qt, kt, lse_win, p, N, W, sl2, stats, lse, raw, st);
+            launch_passes<T, D, 1>(qv, kv, B, Hkv, lse_win, p, N, W, sl2, stats, lse, raw, st);
     } else {
-        launch_passes<T, D, 1>(qt, kt, lse_win, p, N, W, sl2, stats, lse, raw, st);
+        launch_passes<T, D, 1>(qv, kv, B, Hkv, lse_win, p, N, W, sl2, stats, lse, raw, st);
     }
     const int tiles = (N + kPoolTile - 1) / kPoolTile;
     // label rows 4-byte aligned: the pool reads four labels at a time
@@ -608,7 +622,7 @@ hipError_t snapkv_scratch(void** out) {
     return hipSuccess;
 }
 
-hipError_t launch_snapkv(const void* q, const void* k, const float* lse_win, int dtype, int L, int B, int Hq,
+hipError_t launch_snapkv(const RowView& q, const RowView& k, const float* lse_win, int dtype, int L, int B, int Hq,
                          int Hkv, int N, int W, int d, float scale, int pool_k, float* score, const int8_t* roles,
                          int R, uint32_t* hist, void* ws, hipStream_t st) {
     // the largest pooled score is the sum over the G*W window rows of one

@@ -475,12 +475,13 @@ constexpr int kCompactRows = 64;
 
 // One workgroup per (segment, 64 kept rows); a row is PARTS pieces of 16 bytes
 // (8, 16 or 32), piece e of the block being part e % PARTS of row e / PARTS.
+// Source rows are read through views (any row strides), the compacted rows
+// are written dense.
 // Every thread takes 64 PARTS / 256 pieces, in rounds of at most four: it
 // issues the round's index loads, then its row loads, then its stores, so that
 // a block waits for memory about twice per round instead of once per piece.
 template <int PARTS>
-__global__ __launch_bounds__(kThreads) void compact_kernel(const char* __restrict__ k,
-                                                           const char* __restrict__ v,
+__global__ __launch_bounds__(kThreads) void compact_kernel(RowView kv, RowView vv_, int B, int Hkv,
                                                            const int32_t* __restrict__ idx,
                                                            const int32_t* __restrict__ count, int N,
                                                            int k_cap, int nblk, char* __restrict__ k_out,
@@ -495,6 +496,15 @@ __global__ __launch_bounds__(kThreads) void compact_kernel(const char* __restric
     const int m0 = blk * kCompactRows;
     if (m0 >= cnt) return;
     const int total = min(kCompactRows, cnt - m0) * PARTS;
+    // segments are (layer, sample, KV head), KV head fastest
+    const int lb = seg / Hkv;
+    const long long so_k = (long long)(lb / B) * kv.s_layer + (long long)(lb % B) * kv.s_batch +
+                           (long long)(seg % Hkv) * kv.s_head;
+    const long long so_v = (long long)(lb / B) * vv_.s_layer + (long long)(lb % B) * vv_.s_batch +
+                           (long long)(seg % Hkv) * vv_.s_head;
+    const char* k = kv.base + so_k;
+    const char* v = vv_.base != nullptr ? vv_.base + so_v : nullptr;
+    const bool same_rows = vv_.s_token == kv.s_token;  // K and V rows equally spaced: one offset for both
     for (int i0 = 0; i0 < kItems; i0 += kRound) {
         if (i0 * kThreads >= total) break;  // uniform
         int t[kRound];
@@ -503,22 +513,25 @@ __global__ __launch_bounds__(kThreads) void compact_kernel(const char* __restric
             const int e = min((i0 + i) * kThreads + (int)threadIdx.x, total - 1);
             t[i] = idx[(size_t)seg * k_cap + m0 + e / PARTS];
         }
-        u32x4 kv[kRound], vv[kRound];
+        u32x4 kr[kRound], vr[kRound];
 #pragma unroll
         for (int i = 0; i < kRound; ++i) {
             const int e = min((i0 + i) * kThreads + (int)threadIdx.x, total - 1);
             const int tt = min(max(t[i], 0), N - 1);  // out-of-range indices are skipped below
-            const size_t src = ((size_t)seg * N + tt) * kRowBytes + (size_t)(e % PARTS) * 16;
-            kv[i] = ld16(k + src);
-            if (v != nullptr) vv[i] = ld16(v + src);
+            // token strides are below 2^25 bytes (checked by the caller): 32 x 32-bit products
+            const unsigned piece = (unsigned)(e % PARTS) * 16u;
+            const unsigned long long ko = (unsigned long long)(unsigned)tt * (unsigned)kv.s_token + piece;
+            kr[i] = ld16(k + ko);
+            if (v != nullptr)
+                vr[i] = ld16(v + (same_rows ? ko : (unsigned long long)(unsigned)tt * (unsigned)vv_.s_token + piece));
         }
 #pragma unroll
         for (int i = 0; i < kRound; ++i) {
             const int e = (i0 + i) * kThreads + (int)threadIdx.x;
             if (e < total && t[i] >= 0 && t[i] < N) {
                 const size_t dst = ((size_t)seg * k_cap + m0 + e / PARTS) * kRowBytes + (size_t)(e % PARTS) * 16;
-                st16(k_out + dst, kv[i]);
-                if (v != nullptr) st16(v_out + dst, vv[i]);
+                st16(k_out + dst, kr[i]);
+                if (v != nullptr) st16(v_out + dst, vr[i]);
             }
         }
     }
@@ -571,29 +584,27 @@ hipError_t launch_topk(const float* score, const int8_t* roles, const int32_t* q
     return hipGetLastError();
 }
 
-hipError_t launch_compact(const void* k, const void* v, int elem_bytes, const int32_t* idx,
+hipError_t launch_compact(const RowView& k, const RowView& v, int elem_bytes, const int32_t* idx,
                           const int32_t* count, int L, int B, int Hkv, int N, int d, int k_cap,
                           void* k_out, void* v_out, hipStream_t st) {
     const size_t segs = (size_t)L * B * Hkv;
     const int nblk = (k_cap + kCompactRows - 1) / kCompactRows;
     if (nblk == 0 || segs == 0) return hipSuccess;
     const dim3 grid((unsigned)(segs * nblk));
-    const char* kc = static_cast<const char*>(k);
-    const char* vc = static_cast<const char*>(v);
     char* ko = static_cast<char*>(k_out);
     char* vo = static_cast<char*>(v_out);
     switch (d * elem_bytes / 16) {  // 16-byte pieces per row
         case 8:
-            hipLaunchKernelGGL(compact_kernel<8>, grid, dim3(kThreads), 0, st, kc, vc, idx, count, N, k_cap, nblk,
-                               ko, vo);
+            hipLaunchKernelGGL(compact_kernel<8>, grid, dim3(kThreads), 0, st, k, v, B, Hkv, idx, count, N, k_cap,
+                               nblk, ko, vo);
             break;
         case 16:
-            hipLaunchKernelGGL(compact_kernel<16>, grid, dim3(kThreads), 0, st, kc, vc, idx, count, N, k_cap, nblk,
-                               ko, vo);
+            hipLaunchKernelGGL(compact_kernel<16>, grid, dim3(kThreads), 0, st, k, v, B, Hkv, idx, count, N, k_cap,
+                               nblk, ko, vo);
             break;
         case 32:
-            hipLaunchKernelGGL(compact_kernel<32>, grid, dim3(kThreads), 0, st, kc, vc, idx, count, N, k_cap, nblk,
-                               ko, vo);
+            hipLaunchKernelGGL(compact_kernel<32>, grid, dim3(kThreads), 0, st, k, v, B, Hkv, idx, count, N, k_cap,
+                               nblk, ko, vo);
             break;
         default:
             return hipErrorInvalidValue;

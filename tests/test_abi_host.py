@@ -29,7 +29,7 @@ def _declared():
 
 def test_every_declared_symbol_is_exported(kve):
     names = _declared()
-    assert len(names) == 25
+    assert len(names) == 27
     assert sorted(kve.EXPORTED) == names
     lib = ctypes.CDLL(kve.binding._LIB_PATH)
     for n in names:
@@ -211,3 +211,36 @@ def test_workspace_sizes_are_aligned_and_monotone(kve):
     assert w % 256 == 0 and w >= 1024 * 32 * (128 + 2) * 4 // 8
     assert kve.decode_workspace_size(1, 1, 32, 8, 0, 128) == 0
     assert kve.quest_workspace_size(2, 1, 32, 8, 128) == 2 * 32 * 128 * 4
+
+
+def test_strided_entry_points_reject_bad_views_before_any_launch(kve):
+    """View checks run on the host before anything touches the device (the
+    pointers below are never dereferenced)."""
+    lib = kve.binding.LIB
+    S = kve.Strides
+    fake = ctypes.c_void_p(0x10000)
+    score = ctypes.c_void_p(0x20000)
+    ws = ctypes.c_void_p(0x40000)
+    dense_k = S(2 * 8 * 1024 * 128, 8 * 1024 * 128, 1024 * 128, 128)
+
+    def score_call(qs, ks, q=fake):
+        return lib.kve_snapkv_score_strided(q, None if qs is None else ctypes.byref(qs), fake,
+                                            None if ks is None else ctypes.byref(ks), 0, 1, 2, 8, 8, 1024, 16,
+                                            128, 0.0, 7, score, ws, 1 << 30, None)
+
+    bad = [S(-128, 0, 0, 128),                      # negative stride
+           S(0, 0, 0, 4),                           # 8 bytes: not a multiple of 16
+           S(0, 0, 0, (1 << 24) + 8)]               # token stride above 2^25 bytes
+    for st in bad:
+        assert score_call(None, st) == kve.binding.KVE_ERR_INVALID_ARG, st
+        assert "stride" in kve.last_error()
+        assert score_call(st, dense_k) == kve.binding.KVE_ERR_INVALID_ARG
+    # a misaligned base pointer of a strided view
+    assert score_call(S(0, 0, 16 * 128, 128), None, q=ctypes.c_void_p(0x10008)) == kve.binding.KVE_ERR_INVALID_ARG
+    assert "aligned" in kve.last_error()
+    idx = ctypes.c_void_p(0x50000)
+    cnt = ctypes.c_void_p(0x60000)
+    out = ctypes.c_void_p(0x70000)
+    st = lib.kve_kv_compact_strided(fake, ctypes.byref(dense_k), fake, ctypes.byref(S(0, 0, -1, 128)), 0, idx,
+                                    cnt, 1, 2, 8, 1024, 128, 64, out, out, None)
+    assert st == kve.binding.KVE_ERR_INVALID_ARG and "negative" in kve.last_error()

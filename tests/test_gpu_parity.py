@@ -108,6 +108,70 @@ def test_snapkv_explicit_scale(K):
     check_scores(f64(score), ref, "scale")
 
 
+# Strided views: the window queries as the last W rows of all prefill queries,
+# the keys from a token-major cache [L, B, N, Hkv, d] (optionally with padded
+# rows), through kve_snapkv_score_strided: the same arithmetic in the same order
+# as on dense copies, so the scores must be bit-identical; the dense scores are
+# checked against the oracle as well.
+STRIDED_CASES = [
+    custom("strided_bf16", 2, 2, 8, 2, 1000, 24, 128, 7, "bf16"),
+    custom("strided_rows256", 1, 2, 8, 2, 3000, 64, 128, 7, "bf16"),   # 256-row groups
+    custom("strided_f32", 1, 2, 4, 2, 333, 16, 64, 5, "f32"),
+]
+
+
+def _strided_views(q_win, k, pad):
+    """(q view, k view): q_win as the tail of a [L, B, Hq, N, d] tensor, k as a
+    permuted token-major tensor whose rows are d + pad elements apart."""
+    L, B, Hq, W, d = q_win.shape
+    N, Hkv = k.shape[3], k.shape[2]
+    q_full = torch.full((L, B, Hq, N, d), float("nan"), dtype=q_win.dtype, device=q_win.device)
+    q_full[:, :, :, N - W:, :] = q_win
+    k_tm = torch.full((L, B, N, Hkv, d + pad), float("nan"), dtype=k.dtype, device=k.device)
+    k_tm[..., :d] = k.permute(0, 1, 3, 2, 4)
+    return q_full[:, :, :, N - W:, :], k_tm[..., :d].permute(0, 1, 3, 2, 4)
+
+
+@pytest.mark.parametrize("wl", STRIDED_CASES, ids=lambda w: w.name)
+@pytest.mark.parametrize("pad", [0, 8])
+def test_snapkv_strided_views_match_dense(K, wl, pad):
+    note(f"snapkv strided views {wl} pad={pad}")
+    inp = WL.make_inputs(wl, device="cuda", with_v=False)
+    qv, kv = _strided_views(inp["q"], inp["k"], pad)
+    assert not qv.is_contiguous() and not kv.is_contiguous()
+    dense = run_snapkv(K, inp["q"], inp["k"], wl.pool_k)
+    strided = K.snapkv_score_strided(qv, kv, wl.pool_k)
+    torch.cuda.synchronize()
+    assert torch.equal(strided, dense)
+    check_scores(f64(dense), O.snapkv_score(f64(inp["q"]), f64(inp["k"]), wl.Hkv, wl.pool_k), wl.name)
+
+
+@pytest.mark.parametrize("dtype,d", [("bf16", 128), ("f32", 64)])
+def test_kv_compact_strided_views_match_dense(K, dtype, d):
+    rng = np.random.default_rng(5)
+    L, B, Hkv, N, k_cap = 2, 2, 3, 300, 48
+    tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
+    kk = torch.randn((L, B, Hkv, N, d)).to(tdt).cuda()
+    vv = torch.randn((L, B, Hkv, N, d)).to(tdt).cuda()
+    idx = np.full((L, B, Hkv, k_cap), -1, dtype=np.int32)
+    cnt = rng.integers(0, k_cap + 1, (L, B, Hkv)).astype(np.int32)
+    for s in np.ndindex(L, B, Hkv):
+        idx[s][:cnt[s]] = np.sort(rng.choice(N, cnt[s], replace=False))
+    idx_d, cnt_d = torch.from_numpy(idx).cuda(), torch.from_numpy(cnt).cuda()
+    ko, vo = K.kv_compact(kk, vv, idx_d, cnt_d)
+    # K token-major with padded rows, V token-major with dense rows: different row strides
+    k_tm = torch.zeros((L, B, N, Hkv, d + 16), dtype=tdt, device="cuda")
+    k_tm[..., :d] = kk.permute(0, 1, 3, 2, 4)
+    v_tm = vv.permute(0, 1, 3, 2, 4).contiguous()
+    ks, vs = K.kv_compact_strided(k_tm[..., :d].permute(0, 1, 3, 2, 4), v_tm.permute(0, 1, 3, 2, 4), idx_d, cnt_d)
+    torch.cuda.synchronize()
+    assert torch.equal(ks, ko) and torch.equal(vs, vo)
+    # keys only, through the dispatching wrapper
+    k_only, v_none = K.kv_compact(k_tm[..., :d].permute(0, 1, 3, 2, 4), None, idx_d, cnt_d)
+    torch.cuda.synchronize()
+    assert v_none is None and torch.equal(k_only, ko)
+
+
 H2O_CASES = [
     custom("h2o_small", 1, 1, 4, 2, 300, 0, 128, 1, "bf16", scorer="h2o"),
     custom("h2o_f32", 1, 1, 2, 1, 200, 0, 64, 1, "f32", scorer="h2o"),
