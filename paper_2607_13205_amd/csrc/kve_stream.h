@@ -376,6 +376,25 @@ struct RowSum {
     __device__ __forceinline__ float lse2() const { return (m != -INFINITY && l > 0.0f) ? m + log2f(l) : -INFINITY; }
 };
 
+// Issue order of a block with NTRANS exponentials and about twice as many other
+// vector instructions: one exponential, then two other vector instructions.
+// v_exp_f32 occupies the transcendental unit for 16 cycles and a wave issues in
+// order, so back-to-back exponentials stall the wave while independent vector
+// work waits behind them.
+#ifndef KVE_TRANS_SCHED
+#define KVE_TRANS_SCHED 1
+#endif
+template <int NTRANS>
+__device__ __forceinline__ void interleave_trans() {
+#if KVE_TRANS_SCHED
+#pragma unroll
+    for (int i = 0; i < NTRANS; ++i) {
+        __builtin_amdgcn_sched_group_barrier(0x400, 1, 0);  // one transcendental
+        __builtin_amdgcn_sched_group_barrier(0x002, 2, 0);  // two other vector instructions
+    }
+#endif
+}
+
 // RowSum::add for RS sets at once: the exponentials and sums of every set in
 // one block (one wave's vector work per chunk), then one test of all sums.
 template <int RS>
@@ -387,6 +406,7 @@ __device__ __forceinline__ void row_sums_add(RowSum (&r)[RS], const f32x16 (&x)[
         ln[rs] = r[rs].l + r[rs].part(x[rs], sl2);
         ok = ok && ln[rs] <= 0x1p64f;  // false for inf and NaN
     }
+    interleave_trans<32 * RS>();
     if (__builtin_expect(ok, 1)) {
 #pragma unroll
         for (int rs = 0; rs < RS; ++rs) r[rs].l = ln[rs];

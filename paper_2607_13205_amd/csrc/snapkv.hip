@@ -370,6 +370,7 @@ __global__ __launch_bounds__(kThreads, (TuneRS<T, RS>::kOcc2)) void snap_pass2(
                 }
                 v[kb] = half_wave_sum(c);
             }
+            interleave_trans<32 * RS>();
             scol[s & 1][lane][wave] = lane < 32 ? v[0] : v[1];
         }
     }
