@@ -221,6 +221,19 @@ kve_status_t kve_h2o_score(const void* q, const void* k, kve_dtype_t dtype,
                            float* score, void* workspace, size_t workspace_bytes,
                            void* stream);
 
+/*
+ * kve_h2o_score on strided views of its inputs (kve_strides_t; NULL means
+ * dense): q as [L, B, Hq, N, d] and k as [L, B, Hkv, N, d], e.g. token-major
+ * prefill tensors [L, B, N, H, d].  Same arithmetic in the same order: the
+ * scores are bit-identical to kve_h2o_score on dense copies.  Errors: as for
+ * kve_h2o_score, and KVE_ERR_INVALID_ARG for strides the view rules exclude.
+ */
+kve_status_t kve_h2o_score_strided(const void* q, const kve_strides_t* q_strides,
+                                   const void* k, const kve_strides_t* k_strides,
+                                   kve_dtype_t dtype, int L, int B, int Hq, int Hkv, int N,
+                                   int d, float scale, float* score, void* workspace,
+                                   size_t workspace_bytes, void* stream);
+
 /* ------------------------------------------------------------------------- */
 /* One-shot Quest analogue (paper §4.1 "Query-aware baseline"): page key bounds  */
 /* against the mean window query, a second scorer for the same selection.     */

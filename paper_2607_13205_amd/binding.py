@@ -31,7 +31,7 @@ EXPORTED = (
     "kve_version", "kve_last_error", "kve_source_hash",
     "kve_snapkv_workspace_size", "kve_snapkv_score", "kve_snapkv_score_lse",
     "kve_snapkv_score_noalloc", "kve_snapkv_scratch_bytes",
-    "kve_h2o_workspace_size", "kve_h2o_score",
+    "kve_h2o_workspace_size", "kve_h2o_score", "kve_h2o_score_strided",
     "kve_role_allocate", "kve_role_allocate_fair", "kve_role_map", "kve_role_probe",
     "kve_topk_workspace_size", "kve_topk_select",
     "kve_role_hist_size", "kve_snapkv_score_hist", "kve_topk_select_hist",
@@ -78,6 +78,8 @@ def _load():
         "kve_h2o_workspace_size": (c_size, [c_int] * 6),
         "kve_h2o_score": (c_int, [c_void, c_void, c_int] + [c_int] * 6 +
                           [c_float, c_void, c_void, c_size, c_void]),
+        "kve_h2o_score_strided": (c_int, [c_void, c_void, c_void, c_void, c_int] + [c_int] * 6 +
+                                  [c_float, c_void, c_void, c_size, c_void]),
         "kve_role_allocate": (c_int, [c_void, c_int, c_int, c_int, c_void, c_double, c_int,
                                       c_void, c_void, c_void]),
         "kve_role_allocate_fair": (c_int, [c_void, c_int, c_int, c_int, c_double, c_int,
@@ -298,11 +300,31 @@ def h2o_score(q, k, scale: float = 0.0, score=None, workspace=None, stream=None)
     Lk, Bk, Hkv, Nk, dk = k.shape
     if (L, B, N, d) != (Lk, Bk, Nk, dk) or q.dtype != k.dtype:
         raise ValueError("q and k disagree in L, B, N, d or dtype")
+    if not (q.is_contiguous() and k.is_contiguous()):
+        return h2o_score_strided(q, k, scale, score, workspace, stream)
     if score is None:
         score = torch.empty((L, B, Hkv, N), dtype=torch.float32, device=k.device)
     ws, wsb = _workspace(lambda: h2o_workspace_size(L, B, Hq, Hkv, N, d), k.device, workspace)
     _check(LIB.kve_h2o_score(_dev(q, "q"), _dev(k, "k"), _dtype_code(k), L, B, Hq, Hkv, N, d,
                              float(scale), _dev(score, "score"), _ptr(ws), wsb, _stream(stream)))
+    return score
+
+
+def h2o_score_strided(q, k, scale: float = 0.0, score=None, workspace=None, stream=None):
+    """h2o_score on views: q [L, B, Hq, N, d] and k [L, B, Hkv, N, d] with any
+    strides and a contiguous last dimension; see kve_h2o_score_strided."""
+    torch = _torch()
+    L, B, Hq, N, d = q.shape
+    Lk, Bk, Hkv, Nk, dk = k.shape
+    if (L, B, N, d) != (Lk, Bk, Nk, dk) or q.dtype != k.dtype:
+        raise ValueError("q and k disagree in L, B, N, d or dtype")
+    if score is None:
+        score = torch.empty((L, B, Hkv, N), dtype=torch.float32, device=k.device)
+    ws, wsb = _workspace(lambda: h2o_workspace_size(L, B, Hq, Hkv, N, d), k.device, workspace)
+    qp, qs = _view(q, "q")
+    kp, ks = _view(k, "k")
+    _check(LIB.kve_h2o_score_strided(qp, ctypes.byref(qs), kp, ctypes.byref(ks), _dtype_code(k), L, B, Hq, Hkv,
+                                     N, d, float(scale), _dev(score, "score"), _ptr(ws), wsb, _stream(stream)))
     return score
 
 

@@ -49,9 +49,14 @@ struct Geo {
     using Frags = typename Mma<T>::frag[C::NSTEP];
 };
 
+// Start of the rows of head h of sample `lb` (layer * B + sample) in a view.
+__device__ __forceinline__ const char* head_rows(const RowView& v, int lb, int B, int h) {
+    return v.base + (long long)(lb / B) * v.s_layer + (long long)(lb % B) * v.s_batch + (long long)h * v.s_head;
+}
+
 // Fragments of one row (key or query) of length D, zero when !valid.
 template <typename T, int D>
-__device__ __forceinline__ void load_row_frags(typename Geo<T, D>::Frags& f, const T* row, bool valid, int lane) {
+__device__ __forceinline__ void load_row_frags(typename Geo<T, D>::Frags& f, const char* row, bool valid, int lane) {
     using M = Mma<T>;
 #pragma unroll
     for (int st = 0; st < Geo<T, D>::C::NSTEP; ++st) {
@@ -60,14 +65,16 @@ __device__ __forceinline__ void load_row_frags(typename Geo<T, D>::Frags& f, con
     }
 }
 
-// Chunks of consecutive rows of one [N, D] matrix, from `first`.
+// Chunks of consecutive rows of one [N, D] matrix (rows `stride` bytes
+// apart), from `first`.
 template <typename T, int D>
 struct RowChunks {
     const char* base;
+    long long stride;
     int first, end;
     __device__ __forceinline__ void operator()(int c, const char** rows, int* valid) const {
         const int r0 = first + c * kKeys;
-        *rows = base + (size_t)r0 * Geo<T, D>::C::ROW;
+        *rows = base + (long long)r0 * stride;
         *valid = end - r0;
     }
 };
@@ -122,9 +129,9 @@ __device__ __forceinline__ void chunk_mma_x2(f32x16 (&acc)[2][2], const typename
 // the G heads of a KV group at 256/G consecutive positions, position-major;
 // wave w holds rows 64 w .. 64 w + 63 as two sets of 32.
 template <typename T, int D>
-__global__ __launch_bounds__(kThreads, 2) void h2o_pass1_x2(const T* __restrict__ q, const T* __restrict__ k,
-                                                            int Hq, int Hkv, int N, int NP, int npos, int nblk,
-                                                            float sl2, float* __restrict__ linit) {
+__global__ __launch_bounds__(kThreads, 2) void h2o_pass1_x2(RowView qv, RowView kv, int B, int Hq, int Hkv, int N,
+                                                            int NP, int npos, int nblk, float sl2,
+                                                            float* __restrict__ linit) {
     using G = Geo<T, D>;
     __shared__ __align__(16) char ring[kRing * G::C::BYTES];
     const int lane = threadIdx.x & 63;
@@ -147,7 +154,8 @@ __global__ __launch_bounds__(kThreads, 2) void h2o_pass1_x2(const T* __restrict_
         pos[rs] = p0 + r / Gh;
         valid[rs] = r < npos * Gh && pos[rs] < N;
         head[rs] = (size_t)lb * Hq + (size_t)j * Gh + g;
-        load_row_frags<T, D>(qf[rs], q + (head[rs] * N + (valid[rs] ? pos[rs] : 0)) * D, valid[rs], lane);
+        load_row_frags<T, D>(qf[rs], head_rows(qv, lb, B, j * Gh + g) + (long long)(valid[rs] ? pos[rs] : 0) * qv.s_token,
+                             valid[rs], lane);
         lim[rs] = valid[rs] ? pos[rs] : -1;  // last key the row sees
     }
     const int t_end = min(N, p0 + npos);  // keys up to the block's last position
@@ -155,8 +163,8 @@ __global__ __launch_bounds__(kThreads, 2) void h2o_pass1_x2(const T* __restrict_
     typename G::Rd rd;
     rd.init(lane, 0);
     typename G::Ring ring_io;
-    ring_io.open(nch, wave, lane);
-    const RowChunks<T, D> src{reinterpret_cast<const char*>(k) + ((size_t)lb * Hkv + j) * N * G::C::ROW, 0, t_end};
+    ring_io.open(nch, wave, lane, (unsigned)kv.s_token);
+    const RowChunks<T, D> src{head_rows(kv, lb, B, j), kv.s_token, 0, t_end};
     ring_io.prologue(ring, src);
 
     RowSum rsum[2];
@@ -192,9 +200,9 @@ __global__ __launch_bounds__(kThreads, 2) void h2o_pass1_x2(const T* __restrict_
 }
 
 template <typename T, int D>
-__global__ __launch_bounds__(kThreads, 2) void h2o_pass1(const T* __restrict__ q, const T* __restrict__ k,
-                                                         int Hq, int Hkv, int N, int NP, int npos, int nblk,
-                                                         float sl2, float* __restrict__ linit) {
+__global__ __launch_bounds__(kThreads, 2) void h2o_pass1(RowView qv, RowView kv, int B, int Hq, int Hkv, int N,
+                                                         int NP, int npos, int nblk, float sl2,
+                                                         float* __restrict__ linit) {
     using G = Geo<T, D>;
     __shared__ __align__(16) char ring[kRing * G::C::BYTES];
     const int lane = threadIdx.x & 63;
@@ -214,14 +222,15 @@ __global__ __launch_bounds__(kThreads, 2) void h2o_pass1(const T* __restrict__ q
     const size_t head = (size_t)lb * Hq + (size_t)j * Gh + g;
 
     typename G::Frags qf;
-    load_row_frags<T, D>(qf, q + (head * N + (valid ? pos : 0)) * D, valid, lane);
+    load_row_frags<T, D>(qf, head_rows(qv, lb, B, j * Gh + g) + (long long)(valid ? pos : 0) * qv.s_token, valid,
+                         lane);
     const int t_end = min(N, p0 + npos);  // keys up to the block's last position
     const int nch = (t_end + kKeys - 1) / kKeys;
     typename G::Rd rd;
     rd.init(lane, 0);
     typename G::Ring ring_io;
-    ring_io.open(nch, wave, lane);
-    const RowChunks<T, D> src{reinterpret_cast<const char*>(k) + ((size_t)lb * Hkv + j) * N * G::C::ROW, 0, t_end};
+    ring_io.open(nch, wave, lane, (unsigned)kv.s_token);
+    const RowChunks<T, D> src{head_rows(kv, lb, B, j), kv.s_token, 0, t_end};
     ring_io.prologue(ring, src);
 
     const int lim = valid ? pos : -1;  // last key the row sees
@@ -252,7 +261,7 @@ __global__ __launch_bounds__(kThreads, 2) void h2o_pass1(const T* __restrict__ q
 }
 
 template <typename T, int D>
-__global__ __launch_bounds__(kThreads, 2) void h2o_pass2(const T* __restrict__ q, const T* __restrict__ k,
+__global__ __launch_bounds__(kThreads, 2) void h2o_pass2(RowView qv, RowView kv, int B,
                                                          const float* __restrict__ linit, int heads, int Hq,
                                                          int Hkv, int N, int NP, float sl2,
                                                          float* __restrict__ colsum) {
@@ -269,20 +278,22 @@ __global__ __launch_bounds__(kThreads, 2) void h2o_pass2(const T* __restrict__ q
     const int key = kb0 + wave * 32 + (lane & 31);
 
     typename G::Frags kf;
-    load_row_frags<T, D>(kf, k + (lbj * N + (key < N ? key : 0)) * D, key < N, lane);
+    const char* qhead = head_rows(qv, (int)(head / Hq), B, (int)(head % Hq));
+    load_row_frags<T, D>(kf, head_rows(kv, (int)(lbj / Hkv), B, (int)(lbj % Hkv)) + (long long)(key < N ? key : 0) * kv.s_token,
+                         key < N, lane);
     // rows kb0 .. N - 1 of this head
     const int nch = (N - kb0 + kKeys - 1) / kKeys;
     typename G::Rd rd;
     rd.init(lane, 0);
     typename G::Wr wr;
-    wr.init(wave, lane);
+    wr.init(wave, lane, (unsigned)qv.s_token);
     // chunk c: rows from kb0 + 64 c, with their 64 start values (256 bytes:
     // four 16-byte pieces per wave, lanes 0..3).  r0 is a multiple of 64 below
     // N, so the 64 values lie inside the head's row of pitch NP and start
     // 256-byte aligned; rows past N are masked.
     auto issue = [&](int c, int slot) {
         const int r0 = kb0 + c * kKeys;
-        const char* rows = reinterpret_cast<const char*>(q) + (head * N + r0) * G::C::ROW;
+        const char* rows = qhead + (long long)r0 * qv.s_token;
         wr.issue(ring + slot * G::C::BYTES, rows, N - r0);
         if (lane < 4)
             lds_dma16(reinterpret_cast<const char*>(linit + head * NP + r0), (unsigned)(wave * 64 + lane * 16),
@@ -327,7 +338,7 @@ __global__ __launch_bounds__(kThreads, 2) void h2o_pass2(const T* __restrict__ q
 // wave w holding keys 64 w .. 64 w + 63 as two sets of 32; every chunk of
 // query rows read from LDS feeds both sets.
 template <typename T, int D>
-__global__ __launch_bounds__(kThreads, 2) void h2o_pass2_x2(const T* __restrict__ q, const T* __restrict__ k,
+__global__ __launch_bounds__(kThreads, 2) void h2o_pass2_x2(RowView qv, RowView kv, int B,
                                                             const float* __restrict__ linit, int heads, int Hq,
                                                             int Hkv, int N, int NP, float sl2,
                                                             float* __restrict__ colsum) {
@@ -347,19 +358,23 @@ __global__ __launch_bounds__(kThreads, 2) void h2o_pass2_x2(const T* __restrict_
 #pragma unroll
     for (int ks = 0; ks < 2; ++ks) {
         key[ks] = kb0 + wave * 64 + ks * 32 + (lane & 31);
-        load_row_frags<T, D>(kf[ks], k + (lbj * N + (key[ks] < N ? key[ks] : 0)) * D, key[ks] < N, lane);
+        load_row_frags<T, D>(kf[ks],
+                             head_rows(kv, (int)(lbj / Hkv), B, (int)(lbj % Hkv)) +
+                                 (long long)(key[ks] < N ? key[ks] : 0) * kv.s_token,
+                             key[ks] < N, lane);
     }
+    const char* qhead = head_rows(qv, (int)(head / Hq), B, (int)(head % Hq));
     // rows kb0 .. N - 1 of this head
     const int nch = (N - kb0 + kKeys - 1) / kKeys;
     typename G::Rd rd;
     rd.init(lane, 0);
     typename G::Wr wr;
-    wr.init(wave, lane);
+    wr.init(wave, lane, (unsigned)qv.s_token);
     // chunk c: rows from kb0 + 64 c, with their 64 start values (256 bytes:
     // four 16-byte pieces per wave, lanes 0..3); as in h2o_pass2
     auto issue = [&](int c, int slot) {
         const int r0 = kb0 + c * kKeys;
-        const char* rows = reinterpret_cast<const char*>(q) + (head * N + r0) * G::C::ROW;
+        const char* rows = qhead + (long long)r0 * qv.s_token;
         wr.issue(ring + slot * G::C::BYTES, rows, N - r0);
         if (lane < 4)
             lds_dma16(reinterpret_cast<const char*>(linit + head * NP + r0), (unsigned)(wave * 64 + lane * 16),
@@ -420,13 +435,11 @@ __global__ __launch_bounds__(kThreads) void h2o_heads(const float* __restrict__ 
 }
 
 template <typename T, int D>
-hipError_t run_h2o(const void* q, const void* k, int L, int B, int Hq, int Hkv, int N, float scale,
+hipError_t run_h2o(const RowView& qv, const RowView& kv, int L, int B, int Hq, int Hkv, int N, float scale,
                    float* score, void* ws, hipStream_t st) {
     float* linit = static_cast<float*>(ws);
     float* colsum = linit + h2o_colsum_offset(L, B, Hq, N);
     const float sl2 = scale * kLog2e;
-    const T* qt = static_cast<const T*>(q);
-    const T* kt = static_cast<const T*>(k);
     const int Gh = Hq / Hkv;
     const int NP = h2o_pitch(N);
     const int heads = L * B * Hq;
@@ -439,14 +452,14 @@ hipError_t run_h2o(const void* q, const void* k, int L, int B, int Hq, int Hkv, 
     const int nkb = (N + kblock - 1) / kblock;
     if constexpr (kX2) {
         hipLaunchKernelGGL((h2o_pass1_x2<T, D>), dim3((unsigned)((size_t)L * B * Hkv * nblk)), dim3(kThreads), 0,
-                           st, qt, kt, Hq, Hkv, N, NP, npos, nblk, sl2, linit);
-        hipLaunchKernelGGL((h2o_pass2_x2<T, D>), dim3((unsigned)((size_t)heads * nkb)), dim3(kThreads), 0, st, qt,
-                           kt, linit, heads, Hq, Hkv, N, NP, sl2, colsum);
+                           st, qv, kv, B, Hq, Hkv, N, NP, npos, nblk, sl2, linit);
+        hipLaunchKernelGGL((h2o_pass2_x2<T, D>), dim3((unsigned)((size_t)heads * nkb)), dim3(kThreads), 0, st, qv,
+                           kv, B, linit, heads, Hq, Hkv, N, NP, sl2, colsum);
     } else {
         hipLaunchKernelGGL((h2o_pass1<T, D>), dim3((unsigned)((size_t)L * B * Hkv * nblk)), dim3(kThreads), 0, st,
-                           qt, kt, Hq, Hkv, N, NP, npos, nblk, sl2, linit);
-        hipLaunchKernelGGL((h2o_pass2<T, D>), dim3((unsigned)((size_t)heads * nkb)), dim3(kThreads), 0, st, qt,
-                           kt, linit, heads, Hq, Hkv, N, NP, sl2, colsum);
+                           qv, kv, B, Hq, Hkv, N, NP, npos, nblk, sl2, linit);
+        hipLaunchKernelGGL((h2o_pass2<T, D>), dim3((unsigned)((size_t)heads * nkb)), dim3(kThreads), 0, st, qv,
+                           kv, B, linit, heads, Hq, Hkv, N, NP, sl2, colsum);
     }
     const size_t total = (size_t)L * B * Hkv * N;
     hipLaunchKernelGGL(h2o_heads, dim3((unsigned)std::min<size_t>((total + kThreads - 1) / kThreads, 4096)),
@@ -456,7 +469,7 @@ hipError_t run_h2o(const void* q, const void* k, int L, int B, int Hq, int Hkv, 
 
 }  // namespace
 
-hipError_t launch_h2o(const void* q, const void* k, int dtype, int L, int B, int Hq, int Hkv, int N,
+hipError_t launch_h2o(const RowView& q, const RowView& k, int dtype, int L, int B, int Hq, int Hkv, int N,
                       int d, float scale, float* score, void* ws, hipStream_t st) {
     if (dtype == 0) {
         if (d == 128) return run_h2o<__bf16, 128>(q, k, L, B, Hq, Hkv, N, scale, score, ws, st);

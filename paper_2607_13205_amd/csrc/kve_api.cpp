@@ -272,6 +272,37 @@ kve_status_t compact_common(const char* fn, const void* k, const kve_strides_t* 
                     fn);
 }
 
+// Checks of kve_h2o_score and its strided variant.
+kve_status_t h2o_common(const char* fn, const void* q, const kve_strides_t* q_st, const void* k,
+                        const kve_strides_t* k_st, kve_dtype_t dtype, int L, int B, int Hq, int Hkv, int N, int d,
+                        float scale, float* score, void* workspace, size_t workspace_bytes, void* stream) {
+    kve_status_t st = check_common(fn, L, B, Hq, Hkv, N, d, (int)dtype);
+    if (st != KVE_OK) return st;
+    if (q == nullptr || k == nullptr || score == nullptr)
+        return fail(KVE_ERR_INVALID_ARG, "%s: null tensor pointer", fn);
+    const int es = dtype == KVE_DTYPE_BF16 ? 2 : 4;
+    kve::RowView qv, kv;
+    if ((st = make_view(fn, "q", q, q_st, B, Hq, N, d, es, &qv)) != KVE_OK) return st;
+    if ((st = make_view(fn, "k", k, k_st, B, Hkv, N, d, es, &kv)) != KVE_OK) return st;
+    if (!(std::isfinite(scale) && scale >= 0.0f))
+        return fail(KVE_ERR_INVALID_ARG, "%s: scale must be finite and >= 0", fn);
+    const int G = Hq / Hkv;
+    if (G > kve::kH2oRowsPerGroup)
+        return fail(KVE_ERR_UNSUPPORTED, "%s: Hq/Hkv=%d exceeds %d", fn, G, kve::kH2oRowsPerGroup);
+    const long long nblk = (N + kve::kH2oRowsPerGroup / G - 1) / (kve::kH2oRowsPerGroup / G);
+    const long long nkb = (N + 127) / 128;  // pass-2 key blocks
+    if ((long long)L * B * Hkv * nblk > kMaxGrid || (long long)L * B * Hq * nkb > kMaxGrid)
+        return fail(KVE_ERR_UNSUPPORTED, "%s: shape too large", fn);
+    const size_t need = kve::h2o_workspace(L, B, Hq, N);
+    if (workspace_bytes < need || workspace == nullptr)
+        return fail(KVE_ERR_WORKSPACE, "%s: workspace of %zu bytes < %zu needed", fn, workspace_bytes, need);
+    if (!aligned(workspace)) return fail(KVE_ERR_INVALID_ARG, "%s: workspace not 256-byte aligned", fn);
+    if (scale == 0.0f) scale = 1.0f / std::sqrt((float)d);
+    return from_hip(kve::launch_h2o(qv, kv, (int)dtype, L, B, Hq, Hkv, N, d, scale, score, workspace,
+                                    static_cast<hipStream_t>(stream)),
+                    fn);
+}
+
 }  // namespace
 
 extern "C" {
@@ -334,31 +365,20 @@ size_t kve_h2o_workspace_size(int L, int B, int Hq, int Hkv, int N, int d) {
     return kve::h2o_workspace(L, B, Hq, N);
 }
 
+
 kve_status_t kve_h2o_score(const void* q, const void* k, kve_dtype_t dtype, int L, int B, int Hq,
                            int Hkv, int N, int d, float scale, float* score, void* workspace,
                            size_t workspace_bytes, void* stream) {
-    const char* fn = "kve_h2o_score";
-    kve_status_t st = check_common(fn, L, B, Hq, Hkv, N, d, (int)dtype);
-    if (st != KVE_OK) return st;
-    if (q == nullptr || k == nullptr || score == nullptr)
-        return fail(KVE_ERR_INVALID_ARG, "%s: null tensor pointer", fn);
-    if (!(std::isfinite(scale) && scale >= 0.0f))
-        return fail(KVE_ERR_INVALID_ARG, "%s: scale must be finite and >= 0", fn);
-    const int G = Hq / Hkv;
-    if (G > kve::kH2oRowsPerGroup)
-        return fail(KVE_ERR_UNSUPPORTED, "%s: Hq/Hkv=%d exceeds %d", fn, G, kve::kH2oRowsPerGroup);
-    const long long nblk = (N + kve::kH2oRowsPerGroup / G - 1) / (kve::kH2oRowsPerGroup / G);
-    const long long nkb = (N + 127) / 128;  // pass-2 key blocks
-    if ((long long)L * B * Hkv * nblk > kMaxGrid || (long long)L * B * Hq * nkb > kMaxGrid)
-        return fail(KVE_ERR_UNSUPPORTED, "%s: shape too large", fn);
-    const size_t need = kve::h2o_workspace(L, B, Hq, N);
-    if (workspace_bytes < need || workspace == nullptr)
-        return fail(KVE_ERR_WORKSPACE, "%s: workspace of %zu bytes < %zu needed", fn, workspace_bytes, need);
-    if (!aligned(workspace)) return fail(KVE_ERR_INVALID_ARG, "%s: workspace not 256-byte aligned", fn);
-    if (scale == 0.0f) scale = 1.0f / std::sqrt((float)d);
-    return from_hip(kve::launch_h2o(q, k, (int)dtype, L, B, Hq, Hkv, N, d, scale, score, workspace,
-                                    static_cast<hipStream_t>(stream)),
-                    fn);
+    return h2o_common("kve_h2o_score", q, nullptr, k, nullptr, dtype, L, B, Hq, Hkv, N, d, scale, score, workspace,
+                      workspace_bytes, stream);
+}
+
+kve_status_t kve_h2o_score_strided(const void* q, const kve_strides_t* q_strides, const void* k,
+                                   const kve_strides_t* k_strides, kve_dtype_t dtype, int L, int B, int Hq,
+                                   int Hkv, int N, int d, float scale, float* score, void* workspace,
+                                   size_t workspace_bytes, void* stream) {
+    return h2o_common("kve_h2o_score_strided", q, q_strides, k, k_strides, dtype, L, B, Hq, Hkv, N, d, scale,
+                      score, workspace, workspace_bytes, stream);
 }
 
 kve_status_t kve_role_allocate(const int8_t* roles, int B, int N, int R, const double* alpha,

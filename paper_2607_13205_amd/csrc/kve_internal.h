@@ -121,7 +121,8 @@ hipError_t launch_snapkv(const RowView& q, const RowView& k, const float* lse_wi
 // bytes), taken once per device with that device current.
 hipError_t snapkv_scratch(void** out);
 
-hipError_t launch_h2o(const void* q, const void* k, int dtype, int L, int B, int Hq, int Hkv,
+// q: all prefill queries [L, B, Hq, N, d] as a view; k: [L, B, Hkv, N, d] as a view
+hipError_t launch_h2o(const RowView& q, const RowView& k, int dtype, int L, int B, int Hq, int Hkv,
                       int N, int d, float scale, float* score, void* ws, hipStream_t st);
 
 // hist: the role histograms of the scores (as the fused SnapKV epilogue writes

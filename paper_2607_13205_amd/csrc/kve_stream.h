@@ -381,18 +381,13 @@ struct RowSum {
 // v_exp_f32 occupies the transcendental unit for 16 cycles and a wave issues in
 // order, so back-to-back exponentials stall the wave while independent vector
 // work waits behind them.
-#ifndef KVE_TRANS_SCHED
-#define KVE_TRANS_SCHED 1
-#endif
 template <int NTRANS>
 __device__ __forceinline__ void interleave_trans() {
-#if KVE_TRANS_SCHED
 #pragma unroll
     for (int i = 0; i < NTRANS; ++i) {
         __builtin_amdgcn_sched_group_barrier(0x400, 1, 0);  // one transcendental
         __builtin_amdgcn_sched_group_barrier(0x002, 2, 0);  // two other vector instructions
     }
-#endif
 }
 
 // RowSum::add for RS sets at once: the exponentials and sums of every set in

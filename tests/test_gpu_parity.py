@@ -197,6 +197,30 @@ def test_h2o_score_matches_oracle(K, wl):
     np.testing.assert_allclose(tot, wl.G * wl.N, rtol=1e-4)
 
 
+def _token_major(x, pad):
+    """x [L, B, H, T, d] as a view of a token-major tensor [L, B, T, H, d + pad]
+    (NaN in the padding, which must never be read)."""
+    L, B, H, T, d = x.shape
+    tm = torch.full((L, B, T, H, d + pad), float("nan"), dtype=x.dtype, device=x.device)
+    tm[..., :d] = x.permute(0, 1, 3, 2, 4)
+    return tm[..., :d].permute(0, 1, 3, 2, 4)
+
+
+@pytest.mark.parametrize("wl", [H2O_CASES[0], H2O_CASES[1], H2O_CASES[5]], ids=lambda w: w.name)
+@pytest.mark.parametrize("pad", [0, 8])
+def test_h2o_strided_views_match_dense(K, wl, pad):
+    """Token-major queries and keys through kve_h2o_score_strided: the same
+    arithmetic in the same order as the dense call, so bit-identical scores."""
+    note(f"h2o strided views {wl} pad={pad}")
+    inp = WL.make_inputs(wl, device="cuda", with_v=False)
+    qv, kv = _token_major(inp["q"], pad), _token_major(inp["k"], pad)
+    assert not qv.is_contiguous()  # (k with one KV head and no padding is dense either way)
+    dense = K.h2o_score(inp["q"], inp["k"])
+    strided = K.h2o_score_strided(qv, kv)
+    torch.cuda.synchronize()
+    assert torch.equal(strided, dense)
+
+
 def test_h2o_full_size_one_kv_head(K):
     """The 16k-token H2O workload at its real shape; the oracle recomputes the
     scores of one KV head (4 query heads x 16384 rows) in float64."""
