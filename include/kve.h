@@ -275,6 +275,20 @@ kve_status_t kve_quest_score(const void* q_win, const void* k, kve_dtype_t dtype
                              float* score, void* workspace, size_t workspace_bytes,
                              void* stream);
 
+/*
+ * kve_quest_score on strided views of its inputs (kve_strides_t; NULL means
+ * dense): q_win as [L, B, Hq, W, d] (e.g. the last W rows of the prefill
+ * queries) and k as [L, B, Hkv, N, d] (e.g. a token-major cache).  The same
+ * arithmetic in the same order: bit-identical to kve_quest_score on dense
+ * copies.  Errors: as for kve_quest_score, and KVE_ERR_INVALID_ARG for strides
+ * the view rules exclude.
+ */
+kve_status_t kve_quest_score_strided(const void* q_win, const kve_strides_t* q_strides,
+                                     const void* k, const kve_strides_t* k_strides,
+                                     kve_dtype_t dtype, int L, int B, int Hq, int Hkv, int N,
+                                     int W, int d, int page, float* score, void* workspace,
+                                     size_t workspace_bytes, void* stream);
+
 /* ------------------------------------------------------------------------- */
 /* Role-conditional allocation (paper §4.1 role policy; Algorithm 1,          */
 /* per-bucket top-k and redistribution steps).  HOST function.                */

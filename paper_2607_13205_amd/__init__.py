@@ -14,7 +14,7 @@ The hot path runs in libkve.so (HIP); this package is its thin Python binding:
   snapkv_score_hist / topk_select_hist  the same two calls with the role
                  histograms counted in the score's pool epilogue (fused)
   kv_compact     dense K/V cache of the kept rows
-  snapkv_score_strided, kv_compact_strided, h2o_score_strided
+  snapkv_score_strided, kv_compact_strided, h2o_score_strided, quest_score_strided
                  the same on strided views (e.g. a token-major cache)
   decode_attention  one decode query per head over the compacted cache
   pipeline.evict the whole step over resident tensors
@@ -26,10 +26,10 @@ from .binding import (EXPORTED, KveError, decode_attention, decode_workspace_siz
                       quest_workspace_size, role_allocate,
                       role_allocate_fair, role_map, role_probe, snapkv_score, snapkv_score_lse, snapkv_workspace_size,
                       topk_select, topk_workspace_size, Strides, snapkv_score_strided, kv_compact_strided,
-                      h2o_score_strided)
+                      h2o_score_strided, quest_score_strided)
 from . import pipeline  # noqa: F401
 
-__all__ = ["snapkv_score", "snapkv_score_strided", "kv_compact_strided", "Strides", "h2o_score", "h2o_score_strided", "role_allocate", "role_allocate_fair", "role_map",
+__all__ = ["snapkv_score", "snapkv_score_strided", "kv_compact_strided", "Strides", "h2o_score", "h2o_score_strided", "quest_score_strided", "role_allocate", "role_allocate_fair", "role_map",
            "topk_select", "kv_compact", "snapkv_workspace_size", "h2o_workspace_size", "KveError",
            "last_error", "pipeline", "decode_attention", "decode_workspace_size", "quest_score",
            "quest_workspace_size", "role_probe", "snapkv_score_lse", "topk_workspace_size", "source_hash",

@@ -37,7 +37,7 @@ EXPORTED = (
     "kve_role_hist_size", "kve_snapkv_score_hist", "kve_topk_select_hist",
     "kve_kv_compact", "kve_snapkv_score_strided", "kve_kv_compact_strided",
     "kve_decode_workspace_size", "kve_decode_attention",
-    "kve_quest_workspace_size", "kve_quest_score",
+    "kve_quest_workspace_size", "kve_quest_score", "kve_quest_score_strided",
     "kve_read_probe",
 )
 
@@ -103,6 +103,8 @@ def _load():
         "kve_decode_workspace_size": (c_size, [c_int] * 6),
         "kve_quest_workspace_size": (c_size, [c_int] * 5),
         "kve_quest_score": (c_int, [c_void, c_void, c_int] + [c_int] * 8 + [c_void, c_void, c_size, c_void]),
+        "kve_quest_score_strided": (c_int, [c_void, c_void, c_void, c_void, c_int] + [c_int] * 8 +
+                                    [c_void, c_void, c_size, c_void]),
         "kve_read_probe": (c_int, [c_void, c_size, c_int, c_void, c_int, c_void]),
         "kve_decode_attention": (c_int, [c_void, c_void, c_void, c_void, c_int] + [c_int] * 6 +
                                  [c_float, c_void, c_void, c_size, c_void]),
@@ -339,11 +341,31 @@ def quest_score(q_win, k, page: int = 16, score=None, workspace=None, stream=Non
     Lk, Bk, Hkv, N, dk = k.shape
     if (L, B, d) != (Lk, Bk, dk) or q_win.dtype != k.dtype:
         raise ValueError("q_win and k disagree in L, B, d or dtype")
+    if not (q_win.is_contiguous() and k.is_contiguous()):
+        return quest_score_strided(q_win, k, page, score, workspace, stream)
     if score is None:
         score = torch.empty((L, B, Hkv, N), dtype=torch.float32, device=k.device)
     ws, wsb = _workspace(lambda: quest_workspace_size(L, B, Hq, Hkv, d), k.device, workspace)
     _check(LIB.kve_quest_score(_dev(q_win, "q_win"), _dev(k, "k"), _dtype_code(k), L, B, Hq, Hkv, N, W, d,
                                int(page), _dev(score, "score"), _ptr(ws), wsb, _stream(stream)))
+    return score
+
+
+def quest_score_strided(q_win, k, page: int = 16, score=None, workspace=None, stream=None):
+    """quest_score on views (any strides, contiguous last dimension); see
+    kve_quest_score_strided."""
+    torch = _torch()
+    L, B, Hq, W, d = q_win.shape
+    Lk, Bk, Hkv, N, dk = k.shape
+    if (L, B, d) != (Lk, Bk, dk) or q_win.dtype != k.dtype:
+        raise ValueError("q_win and k disagree in L, B, d or dtype")
+    if score is None:
+        score = torch.empty((L, B, Hkv, N), dtype=torch.float32, device=k.device)
+    ws, wsb = _workspace(lambda: quest_workspace_size(L, B, Hq, Hkv, d), k.device, workspace)
+    qp, qs = _view(q_win, "q_win")
+    kp, ks = _view(k, "k")
+    _check(LIB.kve_quest_score_strided(qp, ctypes.byref(qs), kp, ctypes.byref(ks), _dtype_code(k), L, B, Hq, Hkv,
+                                       N, W, d, int(page), _dev(score, "score"), _ptr(ws), wsb, _stream(stream)))
     return score
 
 

@@ -303,6 +303,34 @@ kve_status_t h2o_common(const char* fn, const void* q, const kve_strides_t* q_st
                     fn);
 }
 
+// Checks of kve_quest_score and its strided variant.
+kve_status_t quest_common(const char* fn, const void* q_win, const kve_strides_t* q_st, const void* k,
+                          const kve_strides_t* k_st, kve_dtype_t dtype, int L, int B, int Hq, int Hkv, int N, int W,
+                          int d, int page, float* score, void* workspace, size_t workspace_bytes, void* stream) {
+    kve_status_t st = check_common(fn, L, B, Hq, Hkv, N, d, (int)dtype);
+    if (st != KVE_OK) return st;
+    if (q_win == nullptr || k == nullptr || score == nullptr)
+        return fail(KVE_ERR_INVALID_ARG, "%s: null tensor pointer", fn);
+    const int es = dtype == KVE_DTYPE_BF16 ? 2 : 4;
+    kve::RowView qv, kv;
+    if ((st = make_view(fn, "q_win", q_win, q_st, B, Hq, W, d, es, &qv)) != KVE_OK) return st;
+    if ((st = make_view(fn, "k", k, k_st, B, Hkv, N, d, es, &kv)) != KVE_OK) return st;
+    if (W < 1 || W > N) return fail(KVE_ERR_INVALID_ARG, "%s: need 1 <= W <= N (W=%d N=%d)", fn, W, N);
+    if (page < 1 || page > kve::kQuestMaxPage)
+        return fail(KVE_ERR_INVALID_ARG, "%s: page must be in [1, %d] (got %d)", fn, kve::kQuestMaxPage, page);
+    if (Hq / Hkv > kve::kQuestMaxGroup)
+        return fail(KVE_ERR_UNSUPPORTED, "%s: Hq/Hkv=%d exceeds %d", fn, Hq / Hkv, kve::kQuestMaxGroup);
+    const kve::QuestPlan p = kve::quest_plan(L, B, Hq, Hkv, N, W, d, dtype == KVE_DTYPE_BF16 ? 2 : 4, page);
+    if ((long long)p.segs * p.nranges > kMaxGrid) return fail(KVE_ERR_UNSUPPORTED, "%s: shape too large", fn);
+    if (workspace_bytes < p.total || workspace == nullptr)
+        return fail(KVE_ERR_WORKSPACE, "%s: workspace of %zu bytes < %zu needed", fn, workspace_bytes,
+                    p.total);
+    if (!aligned(workspace)) return fail(KVE_ERR_INVALID_ARG, "%s: workspace not 256-byte aligned", fn);
+    return from_hip(kve::launch_quest(qv, kv, (int)dtype, L, B, Hq, Hkv, N, W, d, page, score, workspace,
+                                      static_cast<hipStream_t>(stream)),
+                    fn);
+}
+
 }  // namespace
 
 extern "C" {
@@ -459,25 +487,16 @@ size_t kve_quest_workspace_size(int L, int B, int Hq, int Hkv, int d) {
 kve_status_t kve_quest_score(const void* q_win, const void* k, kve_dtype_t dtype, int L, int B, int Hq,
                              int Hkv, int N, int W, int d, int page, float* score, void* workspace,
                              size_t workspace_bytes, void* stream) {
-    const char* fn = "kve_quest_score";
-    kve_status_t st = check_common(fn, L, B, Hq, Hkv, N, d, (int)dtype);
-    if (st != KVE_OK) return st;
-    if (q_win == nullptr || k == nullptr || score == nullptr)
-        return fail(KVE_ERR_INVALID_ARG, "%s: null tensor pointer", fn);
-    if (W < 1 || W > N) return fail(KVE_ERR_INVALID_ARG, "%s: need 1 <= W <= N (W=%d N=%d)", fn, W, N);
-    if (page < 1 || page > kve::kQuestMaxPage)
-        return fail(KVE_ERR_INVALID_ARG, "%s: page must be in [1, %d] (got %d)", fn, kve::kQuestMaxPage, page);
-    if (Hq / Hkv > kve::kQuestMaxGroup)
-        return fail(KVE_ERR_UNSUPPORTED, "%s: Hq/Hkv=%d exceeds %d", fn, Hq / Hkv, kve::kQuestMaxGroup);
-    const kve::QuestPlan p = kve::quest_plan(L, B, Hq, Hkv, N, W, d, dtype == KVE_DTYPE_BF16 ? 2 : 4, page);
-    if ((long long)p.segs * p.nranges > kMaxGrid) return fail(KVE_ERR_UNSUPPORTED, "%s: shape too large", fn);
-    if (workspace_bytes < p.total || workspace == nullptr)
-        return fail(KVE_ERR_WORKSPACE, "%s: workspace of %zu bytes < %zu needed", fn, workspace_bytes,
-                    p.total);
-    if (!aligned(workspace)) return fail(KVE_ERR_INVALID_ARG, "%s: workspace not 256-byte aligned", fn);
-    return from_hip(kve::launch_quest(q_win, k, (int)dtype, L, B, Hq, Hkv, N, W, d, page, score, workspace,
-                                      static_cast<hipStream_t>(stream)),
-                    fn);
+    return quest_common("kve_quest_score", q_win, nullptr, k, nullptr, dtype, L, B, Hq, Hkv, N, W, d, page, score,
+                        workspace, workspace_bytes, stream);
+}
+
+kve_status_t kve_quest_score_strided(const void* q_win, const kve_strides_t* q_strides, const void* k,
+                                     const kve_strides_t* k_strides, kve_dtype_t dtype, int L, int B, int Hq,
+                                     int Hkv, int N, int W, int d, int page, float* score, void* workspace,
+                                     size_t workspace_bytes, void* stream) {
+    return quest_common("kve_quest_score_strided", q_win, q_strides, k, k_strides, dtype, L, B, Hq, Hkv, N, W, d,
+                        page, score, workspace, workspace_bytes, stream);
 }
 
 size_t kve_decode_workspace_size(int L, int B, int Hq, int Hkv, int k_cap, int d) {

@@ -135,7 +135,8 @@ hipError_t launch_decode(const void* q, const void* kc, const void* vc, const in
                          int B, int Hq, int Hkv, int k_cap, int d, float scale, float* out, void* ws,
                          hipStream_t st);
 
-hipError_t launch_quest(const void* q, const void* k, int dtype, int L, int B, int Hq, int Hkv, int N, int W,
+// q: window queries [L, B, Hq, W, d] as a view; k: keys [L, B, Hkv, N, d] as a view
+hipError_t launch_quest(const RowView& q, const RowView& k, int dtype, int L, int B, int Hq, int Hkv, int N, int W,
                         int d, int page, float* score, void* ws, hipStream_t st);
 
 hipError_t launch_probe(const int32_t* ids, int B, int N, const float* weight, const float* bias, int V, int R,

@@ -22,17 +22,24 @@ constexpr int kThreads = 256;
 constexpr int kWaves = kThreads / kWave;
 constexpr int kRowBatch = 16;  // key rows loaded before any is used
 
+// Start of the rows of head `h` of segment seg's (layer, sample) in a view:
+// segments are (layer, sample, KV head), KV head fastest.
+__device__ __forceinline__ const char* seg_head_rows(const RowView& v, int seg, int B, int Hkv, int h) {
+    const int lb = seg / Hkv;
+    return v.base + (long long)(lb / B) * v.s_layer + (long long)(lb % B) * v.s_batch + (long long)h * v.s_head;
+}
+
 // qbar[seg, h, c] = mean over the W window rows of head h (float32)
 template <typename T>
-__global__ __launch_bounds__(kThreads) void quest_qmean(const T* __restrict__ q, int W, int G, int D,
+__global__ __launch_bounds__(kThreads) void quest_qmean(RowView qv, int B, int Hkv, int W, int G, int D,
                                                         float* __restrict__ qbar) {
     const int seg = blockIdx.x;
     const float inv = 1.0f / (float)W;
     for (int e = threadIdx.x; e < G * D; e += kThreads) {
         const int h = e / D, c = e - (e / D) * D;
-        const T* rows = q + ((size_t)seg * G + h) * W * D + c;
+        const char* rows = seg_head_rows(qv, seg, B, Hkv, (seg % Hkv) * G + h) + (long long)c * sizeof(T);
         float acc = 0.0f;
-        for (int i = 0; i < W; ++i) acc += (float)rows[(size_t)i * D];
+        for (int i = 0; i < W; ++i) acc += (float)*reinterpret_cast<const T*>(rows + (long long)i * qv.s_token);
         qbar[(size_t)seg * G * D + e] = acc * inv;
     }
 }
@@ -40,7 +47,7 @@ __global__ __launch_bounds__(kThreads) void quest_qmean(const T* __restrict__ q,
 // One workgroup per (segment, range of pages).  NH: heads per KV head padded
 // to 4 or 8 (the padded heads have a zero mean query and add nothing).
 template <typename T, int D, int NH>
-__global__ __launch_bounds__(kThreads) void quest_pages(const T* __restrict__ k, const float* __restrict__ qbar,
+__global__ __launch_bounds__(kThreads) void quest_pages(RowView kv, int B, int Hkv, const float* __restrict__ qbar,
                                                         int N, int W, int G, int page, int n_pages, int nranges,
                                                         int range_pages, float* __restrict__ score) {
     using VP = VPiece<T>;
@@ -67,7 +74,7 @@ __global__ __launch_bounds__(kThreads) void quest_pages(const T* __restrict__ k,
 #pragma unroll
         for (int c = 0; c < CW; ++c) qv[h][c] = h < G ? qbar[((size_t)seg * G + h) * D + cg * CW + c] : 0.0f;
 
-    const T* ks = k + (size_t)seg * N * D + cg * CW;
+    const char* ks = seg_head_rows(kv, seg, B, Hkv, seg % Hkv) + (long long)cg * CW * sizeof(T);
     const int p0 = rg * range_pages, p1 = min(n_pages, p0 + range_pages);
     for (int base = p0 + wv * PPW; base < p1; base += kWaves * PPW) {
         const int pg = min(base + grp, p1 - 1);  // groups past the range redo the last page, unwritten
@@ -79,7 +86,7 @@ __global__ __launch_bounds__(kThreads) void quest_pages(const T* __restrict__ k,
             kmax[c] = -INFINITY;
         }
         // rows past a ragged last page repeat its last row: extremes unchanged
-        const T* pbase = ks + (size_t)t0 * D;
+        const char* pbase = ks + (long long)t0 * kv.s_token;
         const int last = t1 - t0 - 1;
         for (int r0 = 0; r0 < page; r0 += kRowBatch) {
             // every load of the batch in flight before the first is used;
@@ -87,7 +94,8 @@ __global__ __launch_bounds__(kThreads) void quest_pages(const T* __restrict__ k,
             u32x4 raw[kRowBatch];
 #pragma unroll
             for (int i = 0; i < kRowBatch; ++i)
-                raw[i] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(pbase + (size_t)min(r0 + i, last) * D));
+                raw[i] = __builtin_nontemporal_load(
+                    reinterpret_cast<const u32x4*>(pbase + (long long)min(r0 + i, last) * kv.s_token));
 #pragma unroll
             for (int i = 0; i < kRowBatch; i += 2) {
                 float fa[CW], fb[CW];
@@ -113,19 +121,18 @@ __global__ __launch_bounds__(kThreads) void quest_pages(const T* __restrict__ k,
 }
 
 template <typename T, int D, int NH>
-hipError_t run_quest(const void* q, const void* k, int L, int B, int Hq, int Hkv, int N, int W, int page,
+hipError_t run_quest(const RowView& q, const RowView& k, int L, int B, int Hq, int Hkv, int N, int W, int page,
                      float* score, void* ws, hipStream_t st) {
     const QuestPlan p = quest_plan(L, B, Hq, Hkv, N, W, D, (int)sizeof(T), page);
     float* qbar = static_cast<float*>(ws);
-    hipLaunchKernelGGL((quest_qmean<T>), dim3((unsigned)p.segs), dim3(kThreads), 0, st, static_cast<const T*>(q), W,
-                       p.G, D, qbar);
+    hipLaunchKernelGGL((quest_qmean<T>), dim3((unsigned)p.segs), dim3(kThreads), 0, st, q, B, Hkv, W, p.G, D, qbar);
     hipLaunchKernelGGL((quest_pages<T, D, NH>), dim3((unsigned)((size_t)p.segs * p.nranges)), dim3(kThreads), 0, st,
-                       static_cast<const T*>(k), qbar, N, W, p.G, page, p.n_pages, p.nranges, p.range_pages, score);
+                       k, B, Hkv, qbar, N, W, p.G, page, p.n_pages, p.nranges, p.range_pages, score);
     return hipGetLastError();
 }
 
 template <typename T, int D>
-hipError_t run_quest_g(const void* q, const void* k, int L, int B, int Hq, int Hkv, int N, int W, int page,
+hipError_t run_quest_g(const RowView& q, const RowView& k, int L, int B, int Hq, int Hkv, int N, int W, int page,
                        float* score, void* ws, hipStream_t st) {
     if (Hq / Hkv <= 4) return run_quest<T, D, 4>(q, k, L, B, Hq, Hkv, N, W, page, score, ws, st);
     return run_quest<T, D, 8>(q, k, L, B, Hq, Hkv, N, W, page, score, ws, st);
@@ -133,7 +140,7 @@ hipError_t run_quest_g(const void* q, const void* k, int L, int B, int Hq, int H
 
 }  // namespace
 
-hipError_t launch_quest(const void* q, const void* k, int dtype, int L, int B, int Hq, int Hkv, int N, int W,
+hipError_t launch_quest(const RowView& q, const RowView& k, int dtype, int L, int B, int Hq, int Hkv, int N, int W,
                         int d, int page, float* score, void* ws, hipStream_t st) {
     if (dtype == 0) {
         if (d == 128) return run_quest_g<__bf16, 128>(q, k, L, B, Hq, Hkv, N, W, page, score, ws, st);

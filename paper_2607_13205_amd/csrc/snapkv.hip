@@ -58,7 +58,8 @@ constexpr int kMaxPoolHalf = 127;
 // than a second chunk ahead: measured 1-2% faster than two chunks at three);
 // the extra workgroup also overlaps more of one wave's exponentials with
 // another's products.
-// fp32 fragments need twice the registers: two workgroups, three chunks ahead.
+// fp32 fragments need twice the registers: two workgroups, three chunks ahead
+// (one workgroup at d = 128, whose 32 KB chunks fill LDS with the ring).
 template <typename T>
 struct Tune {
     static constexpr int kRing1 = 4, kOcc1 = 2, kRing2 = 4, kOcc2 = 2;
@@ -154,7 +155,7 @@ struct KeyChunks {
 };
 
 template <typename T, int D, int RS>
-__global__ __launch_bounds__(kThreads, (TuneRS<T, RS>::kOcc1)) void snap_pass1(
+__global__ __launch_bounds__(kThreads, (sizeof(T) == 4 && D == 128 ? 1 : TuneRS<T, RS>::kOcc1)) void snap_pass1(
     RowView qv, RowView kv, int B, int Hkv, int N, int W, int rows, int rgroups, int nranges, int range_keys,
     float sl2, float* __restrict__ stats) {
     constexpr int kRing = TuneRS<T, RS>::kRing1;
@@ -260,7 +261,7 @@ __global__ __launch_bounds__(2 * kSnapRowsPerGroup) void snap_import_lse(const f
 }
 
 template <typename T, int D, int RS>
-__global__ __launch_bounds__(kThreads, (TuneRS<T, RS>::kOcc2)) void snap_pass2(
+__global__ __launch_bounds__(kThreads, (sizeof(T) == 4 && D == 128 ? 1 : TuneRS<T, RS>::kOcc2)) void snap_pass2(
     RowView qv, RowView kv, int B, int Hkv, int N, int W, int rows, int rgroups, int nranges, int range_keys,
     float sl2, const float* __restrict__ lse, int segs, float* __restrict__ raw) {
     constexpr int kRing = TuneRS<T, RS>::kRing2;
@@ -393,7 +394,6 @@ __global__ __launch_bounds__(kThreads, (TuneRS<T, RS>::kOcc2)) void snap_pass2(
 // and so the residency, it has without counting.  A tile whose bins do not fit
 // the window marks its record; the top-k then counts that segment itself.
 constexpr int kPoolHistWindow = kRoleHistWindow;
-constexpr uint32_t kNoBin = 0xffffffffu;
 
 __device__ __forceinline__ uint32_t role_bin(float m) { return score_key(m) >> (32 - kRoleHistBits); }
 

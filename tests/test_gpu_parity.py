@@ -957,6 +957,22 @@ QUEST_CASES = [
 ]
 
 
+@pytest.mark.parametrize("case", [QUEST_CASES[0], QUEST_CASES[3], QUEST_CASES[7]], ids=lambda c: c[0])
+@pytest.mark.parametrize("pad", [0, 8])
+def test_quest_strided_views_match_dense(K, case, pad):
+    """The window queries as the tail of all prefill queries and the keys
+    token-major through kve_quest_score_strided: bit-identical to the dense call."""
+    name, L, B, Hq, Hkv, N, W, d, dt, page = case
+    note(f"quest strided views {name} pad={pad}")
+    wl = custom(name, L, B, Hq, Hkv, N, W, d, 1, dt, scorer="quest")
+    inp = WL.make_inputs(wl, device="cuda", with_v=False)
+    qv, kv = _strided_views(inp["q"], inp["k"], pad)
+    dense = K.quest_score(inp["q"], inp["k"], page)
+    strided = K.quest_score_strided(qv, kv, page)
+    torch.cuda.synchronize()
+    assert torch.equal(strided, dense)
+
+
 @pytest.mark.parametrize("case", QUEST_CASES, ids=lambda c: c[0])
 def test_quest_score_matches_oracle(K, case):
     name, L, B, Hq, Hkv, N, W, d, dt, page = case
