@@ -539,6 +539,35 @@ def test_pipeline_small_workloads(K, name, budget):
     report(f"near-tie pairs vs oracle, {name} B={budget} (every segment)", ties)
 
 
+@pytest.mark.parametrize("scorer", ["snapkv", "quest", "h2o"])
+def test_pipeline_on_strided_views_matches_dense(K, scorer):
+    """The whole step on a token-major cache (keys [L, B, N, Hkv, d] with padded
+    rows, values [L, B, N, Hkv, d]) and, for SnapKV and Quest, the window
+    queries as the tail of all prefill queries: the same scores, kept indices,
+    counts and compacted rows as on dense tensors."""
+    from paper_2607_13205_amd import pipeline
+    h2o = scorer == "h2o"
+    wl = custom(f"views_{scorer}", 2, 2, 8, 2, 1200, 0 if h2o else 24, 128, 1 if h2o else 7, "bf16", scorer=scorer)
+    note(f"pipeline on strided views {wl}")
+    inp = WL.make_inputs(wl, device="cuda")
+    if h2o:
+        qv, kv = _token_major(inp["q"], 0), _token_major(inp["k"], 8)
+    else:
+        qv, kv = _strided_views(inp["q"], inp["k"], 8)
+    vv = _token_major(inp["v"], 0)
+    policy = pipeline.as_policy(WL.default_alpha(0.0))
+    _, _, k_cap = policy.allocate(inp["roles"], 0.1, wl.W)
+    out = []
+    for q, k, v in ((inp["q"], inp["k"], inp["v"]), (qv, kv, vv)):
+        bufs = pipeline.alloc_buffers(inp["k"], wl.Hq, wl.W, policy.R, k_cap, scorer=scorer)
+        pipeline.evict(q, k, v, inp["roles"], inp["roles_t"], policy, 0.1, wl.W, wl.pool_k, bufs, scorer=scorer)
+        torch.cuda.synchronize()
+        out.append(bufs)
+    d, s = out
+    assert torch.equal(d.score, s.score) and torch.equal(d.count, s.count) and torch.equal(d.idx, s.idx)
+    assert torch.equal(d.k_out, s.k_out) and torch.equal(d.v_out, s.v_out)
+
+
 def test_pipeline_alpha_key_nonzero_and_neutral(K):
     wl = WL.get_workload("layer8k").with_(Hq=8, Hkv=2)
     inp = WL.make_inputs(wl, device="cuda")
