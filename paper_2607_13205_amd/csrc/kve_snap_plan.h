@@ -22,7 +22,7 @@ constexpr int kSnapRowsPerGroup = 128;
 constexpr int kSnapMaxRows = 1024;
 constexpr int kSnapChunkKeys = 64;
 constexpr int kSnapTargetGroups = 4096;  // workgroups per pass the range size aims at
-constexpr int kSnapMaxRangeChunks = 32;  // at most 2048 keys per range
+constexpr int kSnapMaxRangeChunks = 128;  // at most 8192 keys per range
 
 // Fused role epilogue: per (segment, bucket), the number of candidate
 // positions by the top kRoleHistBits bits of their order-preserving score key
@@ -63,8 +63,9 @@ inline SnapPlan snap_plan(int L, int B, int Hq, int Hkv, int N, int W, int d, in
     p.rgroups = (p.rows + p.rpg - 1) / p.rpg;
     p.n_vsegs = p.segs * p.rgroups;
     p.planes = p.rgroups;
-    // whole chunks per range: about kSnapTargetGroups workgroups per pass (two
-    // per compute unit at a time), at most 32 chunks each, and at least as many
+    // whole chunks per range: about kSnapTargetGroups workgroups per pass, at
+    // most 128 chunks each (longer ranges start fewer workgroups, whose query
+    // fragments and first chunks are latency before any product), and at least as many
     // keys as the group has query rows (a workgroup loads its rows' queries
     // once, so its keys should outweigh them); short problems thus get short
     // ranges rather than a few workgroups walking many chunks in turn
