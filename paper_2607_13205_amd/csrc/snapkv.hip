@@ -48,8 +48,11 @@ namespace {
 constexpr int kWaves = 4;
 constexpr int kThreads = kWaves * 64;
 constexpr int kKeys = kSnapChunkKeys;  // keys per chunk
-constexpr int kPoolTile = kRoleHistTile;  // keys per pool workgroup (and per role-histogram tile)
-constexpr int kPoolKeysPerThread = kPoolTile / kThreads;  // consecutive keys per thread
+// keys per pool workgroup: 2048 when it only pools (twice the workgroups of
+// 4096-key tiles hide more of the plane reads: measured 97 -> 58 us on a 32k
+// stack), the role-histogram tile when it also counts (its records then stay
+// as few as the top-k reads)
+constexpr int kPoolTile = 2048;
 constexpr int kMaxPoolHalf = 127;
 
 // LDS ring depth and workgroups per compute unit of each pass.  bf16: both
@@ -379,9 +382,9 @@ __global__ __launch_bounds__(kThreads, (sizeof(T) == 4 && D == 128 ? 1 : TuneRS<
     reduce(sp.nch - 1);
 }
 
-// Pool: one workgroup per (segment, tile of kPoolTile keys).  The tile and its
-// halo of h keys on each side are summed over the planes into LDS (16 keys per
-// thread, loads first), then each key takes the max over its window, which
+// Pool: one workgroup per (segment, tile of TILE keys).  The tile and its
+// halo of h keys on each side are summed over the planes into LDS (TILE / 256
+// keys per thread, loads first), then each key takes the max over its window, which
 // stops at the end of the candidate prefix; window keys keep their raw score.
 // With a role histogram (rh.roles set) the workgroup also counts its candidate
 // keys per bucket and top key digit in LDS and adds the non-zero counts to the
@@ -397,22 +400,24 @@ constexpr int kPoolHistWindow = kRoleHistWindow;
 
 __device__ __forceinline__ uint32_t role_bin(float m) { return score_key(m) >> (32 - kRoleHistBits); }
 
+template <int TILE>
 __global__ __launch_bounds__(kThreads) void snap_pool(const float* __restrict__ raw, int planes, int segs,
                                                       int N, int W, int pool_k, int tiles,
                                                       float* __restrict__ score, RoleHist rh, int lab4) {
-    __shared__ __align__(16) float ss[kPoolTile + 2 * kMaxPoolHalf + 8];
+    __shared__ __align__(16) float ss[TILE + 2 * kMaxPoolHalf + 8];
     extern __shared__ __align__(16) uint32_t lh[];  // [R][kPoolHistWindow / 2] pairs of 16-bit counts when counting
+    constexpr int kPoolKeysPerThread = TILE / kThreads;  // consecutive keys per thread
     const int tile = blockIdx.x % tiles;
     const int seg = blockIdx.x / tiles;
     const int h = pool_k / 2;
     const int P = N - W;
-    const int t0 = tile * kPoolTile;
-    const int n = min(kPoolTile, N - t0) + 2 * h;  // staged keys t0 - h .. t0 + n - h - 1
+    const int t0 = tile * TILE;
+    const int n = min(TILE, N - t0) + 2 * h;  // staged keys t0 - h .. t0 + n - h - 1
     const bool counting = rh.roles != nullptr;
     const int8_t* ro = counting ? rh.roles + (size_t)((seg / rh.Hkv) % rh.B) * N : nullptr;
     if (counting)
         for (int e = threadIdx.x; e < rh.R * kPoolHistWindow / 2; e += kThreads) lh[e] = 0u;
-    constexpr int kPer = (kPoolTile + 2 * kMaxPoolHalf + kThreads - 1) / kThreads;
+    constexpr int kPer = (TILE + 2 * kMaxPoolHalf + kThreads - 1) / kThreads;
     const int e0 = kPoolKeysPerThread * (int)threadIdx.x;
     // labels of this thread's keys, loaded with the sums (their latency hidden
     // behind the pooling): four per word, four-byte loads when rows allow
@@ -447,17 +452,17 @@ __global__ __launch_bounds__(kThreads) void snap_pool(const float* __restrict__ 
         if (e < n) ss[e] = (u >= 0 && u < N) ? v[i] : -INFINITY;
     }
     __syncthreads();
-    // this thread's keys t0 + e0 .. t0 + e0 + 15: pooled values in mv, and the
+    // this thread's kPoolKeysPerThread keys from t0 + e0: pooled values in mv, and the
     // bucket of each candidate (R: not counted) in rv
     float mv[kPoolKeysPerThread];
     uint32_t rv[kPoolKeysPerThread];
-    // kernel 7 (the paper's), all 16 windows of this thread inside the prefix:
-    // the 22 staged values in registers, the window maxima built from pairwise
+    // kernel 7 (the paper's), all windows of this thread inside the prefix:
+    // the kPoolKeysPerThread + 6 staged values in registers, the window maxima built from pairwise
     // and four-wide maxima, written as 16-byte stores (rows of a multiple of 4
     // keys keep those aligned)
     const bool fast = h == 3 && (N & 3) == 0 && t0 + e0 + kPoolKeysPerThread - 1 + h < P;
     if (fast) {
-        float x[kPoolKeysPerThread + 8];  // staged keys t0 + e0 - 3 .. t0 + e0 + 18 (+ 2 unused)
+        float x[kPoolKeysPerThread + 8];  // staged keys from t0 + e0 - 3 (the last 2 unused)
 #pragma unroll
         for (int a = 0; a < (kPoolKeysPerThread + 8) / 4; ++a) {
             const float4 f = *reinterpret_cast<const float4*>(&ss[e0 + 4 * a]);
@@ -489,7 +494,7 @@ __global__ __launch_bounds__(kThreads) void snap_pool(const float* __restrict__ 
                 for (int b = 0; b < 4; ++b) rv[4 * a + b] = min((lab[a] >> (8 * b)) & 0xffu, (uint32_t)rh.R);
         }
     } else {
-        const int valid = min(kPoolTile, N - t0) - e0;  // keys of this thread inside the row
+        const int valid = min(TILE, N - t0) - e0;  // keys of this thread inside the row
 #pragma unroll
         for (int j = 0; j < kPoolKeysPerThread; ++j) {
             const int t = t0 + e0 + j;
@@ -589,12 +594,18 @@ hipError_t run_snapkv(const RowView& qv, const RowView& kv, const float* lse_win
     } else {
         launch_passes<T, D, 1>(qv, kv, B, Hkv, lse_win, p, N, W, sl2, stats, lse, raw, st);
     }
-    const int tiles = (N + kPoolTile - 1) / kPoolTile;
-    // label rows 4-byte aligned: the pool reads four labels at a time
-    const int lab4 = rh.roles != nullptr && N % 4 == 0 && (reinterpret_cast<uintptr_t>(rh.roles) & 3u) == 0;
-    const unsigned lds = rh.roles != nullptr ? (unsigned)(rh.R * kPoolHistWindow / 2 * sizeof(uint32_t)) : 0u;
-    hipLaunchKernelGGL(snap_pool, dim3((unsigned)(p.segs * tiles)), dim3(kThreads), lds, st, raw, p.planes, p.segs,
-                       N, W, pool_k, tiles, score, rh, lab4);
+    if (rh.roles != nullptr) {
+        // label rows 4-byte aligned: the pool reads four labels at a time
+        const int lab4 = N % 4 == 0 && (reinterpret_cast<uintptr_t>(rh.roles) & 3u) == 0;
+        const int tiles = role_hist_tiles(N);
+        const unsigned lds = (unsigned)(rh.R * kPoolHistWindow / 2 * sizeof(uint32_t));
+        hipLaunchKernelGGL(snap_pool<kRoleHistTile>, dim3((unsigned)(p.segs * tiles)), dim3(kThreads), lds, st, raw,
+                           p.planes, p.segs, N, W, pool_k, tiles, score, rh, lab4);
+    } else {
+        const int tiles = (N + kPoolTile - 1) / kPoolTile;
+        hipLaunchKernelGGL(snap_pool<kPoolTile>, dim3((unsigned)(p.segs * tiles)), dim3(kThreads), 0u, st, raw,
+                           p.planes, p.segs, N, W, pool_k, tiles, score, rh, 0);
+    }
     return hipGetLastError();
 }
 
