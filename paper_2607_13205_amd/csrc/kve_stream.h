@@ -108,7 +108,12 @@ struct ChunkWriter {
     using C = KChunk<T, D, KEYS>;
     static constexpr int LPW = C::BYTES / (NWAVES * 1024);
     static_assert(C::BYTES % (NWAVES * 1024) == 0, "chunk must split into whole 1 KiB wave loads");
-    unsigned goff[LPW];
+    // chunk rows between a lane's consecutive loads; when they span whole
+    // swizzle periods (16 rows) all loads of a lane share its column, so one
+    // offset serves them all and the wave-uniform base steps by RJ rows
+    static constexpr int RJ = NWAVES * 1024 / C::ROW;
+    static constexpr bool kOneOff = RJ % 16 == 0;
+    unsigned goff[kOneOff ? 1 : LPW];
     unsigned rstride;
     int wv, lane;
 
@@ -117,7 +122,7 @@ struct ChunkWriter {
         lane = lane_;
         rstride = row_stride;
 #pragma unroll
-        for (int j = 0; j < LPW; ++j) {
+        for (int j = 0; j < (kOneOff ? 1 : LPW); ++j) {
             const int r = row_of(j);
             const int o = (j * NWAVES + wv) * 1024 + lane * 16;
             const int c = ((o - r * C::ROW) >> 4) ^ chunk_swz_bits<C::ROW>(r);  // inverse of chunk_swz
@@ -126,17 +131,26 @@ struct ChunkWriter {
     }
     // chunk row of this lane's load j
     __device__ __forceinline__ int row_of(int j) const { return ((j * NWAVES + wv) * 1024 + lane * 16) / C::ROW; }
+    // byte offset of this lane's load j from the chunk's first row
+    __device__ __forceinline__ unsigned off_of(int j) const {
+        return kOneOff ? goff[0] + (unsigned)(j * RJ) * rstride : goff[j];
+    }
     // rows: first key row of the chunk (wave-uniform); valid: rows in bounds
     __device__ __forceinline__ void issue(char* slot, const char* rows, int valid) const {
         if (valid >= KEYS) {
 #pragma unroll
-            for (int j = 0; j < LPW; ++j) lds_dma16<NT>(rows, goff[j], slot + (j * NWAVES + wv) * 1024);
+            for (int j = 0; j < LPW; ++j) {
+                if constexpr (kOneOff)
+                    lds_dma16<NT>(rows + (size_t)(j * RJ) * rstride, goff[0], slot + (j * NWAVES + wv) * 1024);
+                else
+                    lds_dma16<NT>(rows, goff[j], slot + (j * NWAVES + wv) * 1024);
+            }
         } else {
 #pragma unroll
             for (int j = 0; j < LPW; ++j) {
                 const int r = row_of(j);
-                lds_dma16<NT>(rows, r < valid ? goff[j] : goff[j] - (unsigned)r * rstride,
-                              slot + (j * NWAVES + wv) * 1024);
+                const unsigned o = off_of(j);
+                lds_dma16<NT>(rows, r < valid ? o : o - (unsigned)r * rstride, slot + (j * NWAVES + wv) * 1024);
             }
         }
     }
@@ -407,6 +421,66 @@ __device__ __forceinline__ void row_sums_add(RowSum (&r)[RS], const f32x16 (&x)[
         for (int rs = 0; rs < RS; ++rs) r[rs].l = ln[rs];
         return;
     }
+#pragma unroll
+    for (int rs = 0; rs < RS; ++rs) {
+        if (ln[rs] <= 0x1p64f)
+            r[rs].l = ln[rs];
+        else
+            r[rs].reset(x[rs], sl2);
+    }
+}
+
+// Row sums of RS sets with the exponentials taken in place of the logits (x
+// is destroyed), which keeps a second copy of the chunk's values out of the
+// registers.  A set with no reference yet (a range's first chunk) takes the
+// chunk's largest logit as its reference first, as a reset would; a set whose
+// logits are all masked keeps no reference and adds 0.  Returns false when a
+// sum left [0, 2^64]: ln[] then holds every set's new sum, and the caller
+// takes the chunk's logits again and finishes with row_sums_fix.
+template <int RS>
+__device__ __forceinline__ bool row_sums_try(RowSum (&r)[RS], f32x16 (&x)[RS][2], float sl2, float (&ln)[RS]) {
+    bool fresh = false;
+#pragma unroll
+    for (int rs = 0; rs < RS; ++rs) fresh = fresh || r[rs].m == -INFINITY;
+    if (__builtin_amdgcn_ballot_w64(fresh) != 0) {  // wave-uniform, rare
+#pragma unroll
+        for (int rs = 0; rs < RS; ++rs) {
+            float mx = -INFINITY;
+#pragma unroll
+            for (int b = 0; b < 2; ++b)
+#pragma unroll
+                for (int i = 0; i < 16; ++i) mx = fmaxf(mx, x[rs][b][i]);
+            if (r[rs].m == -INFINITY) r[rs].m = mx * sl2;
+        }
+    }
+    bool ok = true;
+#pragma unroll
+    for (int rs = 0; rs < RS; ++rs) {
+        const float nm = r[rs].m == -INFINITY ? 0.0f : -r[rs].m;  // masked logits give 0 either way
+        float p[4];
+#pragma unroll
+        for (int b = 0; b < 2; ++b)
+#pragma unroll
+            for (int i = 0; i < 16; ++i) x[rs][b][i] = fast_exp2(fmaf(x[rs][b][i], sl2, nm));
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+            p[e] = (x[rs][0][e] + x[rs][0][e + 4]) + (x[rs][0][e + 8] + x[rs][0][e + 12]) +
+                   ((x[rs][1][e] + x[rs][1][e + 4]) + (x[rs][1][e + 8] + x[rs][1][e + 12]));
+        ln[rs] = r[rs].l + ((p[0] + p[1]) + (p[2] + p[3]));
+        ok = ok && ln[rs] <= 0x1p64f;  // false for inf and NaN
+    }
+    interleave_trans<32 * RS>();
+    if (__builtin_expect(ok, 1)) {
+#pragma unroll
+        for (int rs = 0; rs < RS; ++rs) r[rs].l = ln[rs];
+    }
+    return ok;
+}
+// The rest of row_sums_try after a false return, with x the chunk's logits:
+// sets whose sum stayed in range keep it, the others raise their reference.
+template <int RS>
+__device__ __forceinline__ void row_sums_fix(RowSum (&r)[RS], const f32x16 (&x)[RS][2], float sl2,
+                                             const float (&ln)[RS]) {
 #pragma unroll
     for (int rs = 0; rs < RS; ++rs) {
         if (ln[rs] <= 0x1p64f)
