@@ -108,6 +108,38 @@ def test_snapkv_explicit_scale(K):
     check_scores(f64(score), ref, "scale")
 
 
+# Logit spikes: every 97th key row scaled by 40, so that (with N(0, 1) inputs)
+# many rows meet a key whose logit lies more than 64, and some more than 128,
+# log2 units above the running reference of their range: the row sums leave
+# [0, 2^64] (or overflow) after the first chunk, and the kernels raise their
+# reference from the chunk's logits taken again.  One-set and two-set row
+# groups and float32.
+SPIKE_CASES = [
+    custom("spike_rows128", 1, 2, 8, 2, 3000, 16, 128, 7, "bf16"),
+    custom("spike_rows256", 1, 2, 8, 2, 5000, 64, 128, 7, "bf16"),
+    custom("spike_f32", 1, 1, 4, 2, 2000, 16, 128, 5, "f32"),
+]
+
+
+@pytest.mark.parametrize("wl", SPIKE_CASES, ids=lambda w: w.name)
+def test_snapkv_score_logit_spikes_match_oracle(K, wl):
+    note(f"snapkv parity with logit spikes {wl}")
+    inp = WL.make_inputs(wl, device="cuda", with_v=False)
+    k = inp["k"].clone()
+    k[:, :, :, 40::97, :] *= 40
+    q = inp["q"]
+    ref = O.snapkv_score(f64(q), f64(k), wl.Hkv, wl.pool_k)
+    # the case does what it is for: some window row meets a logit more than 128
+    # log2 units above its largest over the keys before the first spike
+    # (float64, from the same rounded inputs)
+    qq = f64(q).reshape(wl.L, wl.B, wl.Hkv, wl.G * wl.W, wl.d)
+    logit2 = np.matmul(qq, np.swapaxes(f64(k), -1, -2)) * (wl.d ** -0.5) * math.log2(math.e)
+    span = float((logit2.max(axis=-1) - logit2[..., :40].max(axis=-1)).max())
+    assert span > 128, span
+    score = run_snapkv(K, q, k, wl.pool_k)
+    check_scores(f64(score), ref, wl.name)
+
+
 # Strided views: the window queries as the last W rows of all prefill queries,
 # the keys from a token-major cache [L, B, N, Hkv, d] (optionally with padded
 # rows), through kve_snapkv_score_strided: the same arithmetic in the same order
