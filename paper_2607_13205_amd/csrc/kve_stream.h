@@ -434,9 +434,12 @@ __device__ __forceinline__ void row_sums_add(RowSum (&r)[RS], const f32x16 (&x)[
 // is destroyed), which keeps a second copy of the chunk's values out of the
 // registers.  A set with no reference yet (a range's first chunk) takes the
 // chunk's largest logit as its reference first, as a reset would; a set whose
-// logits are all masked keeps no reference and adds 0.  Returns false when a
-// sum left [0, 2^64]: ln[] then holds every set's new sum, and the caller
-// takes the chunk's logits again and finishes with row_sums_fix.
+// logits are all masked keeps no reference and adds 0.  Returns false, for
+// the whole wave, when a sum of any lane left [0, 2^64]: ln[] then holds every
+// set's new sum, lanes whose sums all stayed in range have already kept them,
+// and the caller takes the chunk's logits again on every lane (a matrix-core
+// product reads the fragments of every lane, so a lane left out would feed it
+// stale registers) and finishes with row_sums_fix.
 template <int RS>
 __device__ __forceinline__ bool row_sums_try(RowSum (&r)[RS], f32x16 (&x)[RS][2], float sl2, float (&ln)[RS]) {
     bool fresh = false;
@@ -474,10 +477,11 @@ __device__ __forceinline__ bool row_sums_try(RowSum (&r)[RS], f32x16 (&x)[RS][2]
 #pragma unroll
         for (int rs = 0; rs < RS; ++rs) r[rs].l = ln[rs];
     }
-    return ok;
+    return __builtin_amdgcn_ballot_w64(!ok) == 0;
 }
-// The rest of row_sums_try after a false return, with x the chunk's logits:
-// sets whose sum stayed in range keep it, the others raise their reference.
+// The rest of row_sums_try after a false return, with x the chunk's logits
+// (on every lane): sets whose sum stayed in range keep it (again, on lanes
+// that kept it already), the others raise their reference.
 template <int RS>
 __device__ __forceinline__ void row_sums_fix(RowSum (&r)[RS], const f32x16 (&x)[RS][2], float sl2,
                                              const float (&ln)[RS]) {
