@@ -307,13 +307,14 @@ __device__ __forceinline__ void chunk_mma(f32x16 (&acc)[2], const ChunkReader<T,
 // chunk_mma for RS sets of 32 register rows at once: acc[s][b] is register set
 // s against chunk block b, in the layout chunk_mma gives for one set.  Each
 // fragment read from LDS feeds RS products and the 2 RS accumulators are
-// independent chains.  c_init, when given, holds the start value of each set
-// (register rows, !LDS_A); otherwise the products start at zero.
+// independent chains.  The products start from acc itself with acc_init (the
+// caller filled it), else from c_init, when given (the start value of each
+// set: register rows, !LDS_A), else from zero.
 template <typename T, int D, int KEYS, bool LDS_A, int RS>
 __device__ __forceinline__ void chunk_mma_sets(f32x16 (&acc)[RS][2], const ChunkReader<T, D, KEYS>& rd,
                                                const char* slot,
                                                const typename Mma<T>::frag (&reg)[RS][KChunk<T, D, KEYS>::NSTEP],
-                                               const f32x16* c_init) {
+                                               const f32x16* c_init, bool acc_init = false) {
     using M = Mma<T>;
     constexpr int NS = KChunk<T, D, KEYS>::NSTEP;
 #pragma unroll
@@ -323,7 +324,7 @@ __device__ __forceinline__ void chunk_mma_sets(f32x16 (&acc)[RS][2], const Chunk
         for (int rs = 0; rs < RS; ++rs)
 #pragma unroll
             for (int b = 0; b < 2; ++b) {
-                const f32x16 c = st > 0 ? acc[rs][b] : (c_init != nullptr ? c_init[rs] : f32x16{});
+                const f32x16 c = (st > 0 || acc_init) ? acc[rs][b] : (c_init != nullptr ? c_init[rs] : f32x16{});
                 acc[rs][b] = LDS_A ? M::mma(f[b], reg[rs][st], c) : M::mma(reg[rs][st], f[b], c);
             }
     }

@@ -72,15 +72,16 @@ struct Tune<__bf16> {
     static constexpr int kRing1 = 2, kOcc1 = 4, kRing2 = 2, kOcc2 = 4;
 };
 // two 32-row sets per wave (bf16, windows of more than 128 rows): twice the
-// query fragments and accumulators, two chunks ahead; pass 1 takes its
-// exponentials in place of the logits and fits three workgroups per CU (168
-// registers; 4-5% faster than two on the 32-layer, N = 131072, W = 64
-// workload), pass 2 keeps its start values in registers and two
+// query fragments and accumulators, two chunks ahead, three workgroups per CU
+// (168 registers): pass 1 takes its exponentials in place of the logits, pass
+// 2 reads its start values from LDS into the accumulators at every chunk
+// (4-5% faster per pass than two workgroups on the 32-layer, N = 131072,
+// W = 64 workload)
 template <typename T, int RS>
 struct TuneRS : Tune<T> {};
 template <typename T>
 struct TuneRS<T, 2> {
-    static constexpr int kRing1 = 3, kOcc1 = 3, kRing2 = 3, kOcc2 = 2;
+    static constexpr int kRing1 = 3, kOcc1 = 3, kRing2 = 3, kOcc2 = 3;
 };
 
 // Each pass reads every key row once: non-temporal chunk loads (measured 3-4%
@@ -312,19 +313,26 @@ __global__ __launch_bounds__(kThreads, (sizeof(T) == 4 && D == 128 ? 1 : TuneRS<
     for (int rs = 0; rs < RS; ++rs)
         load_q<T, D>(qf[rs], qseg, qv, rows, W, sp.rg * kRpg + (wave * RS + rs) * 32 + (lane & 31), lane);
     __syncthreads();  // sinit, swin written (nothing streams yet)
-    // start values of this lane's 16 rows of each set, the same for every chunk
+    // start values of this lane's 16 rows of each set, the same for every
+    // chunk: held in registers with one set per wave; with two sets read from
+    // LDS into the accumulators at every chunk instead (32 registers fewer,
+    // which lets three workgroups share a CU; all 32 lanes of a half-wave read
+    // the same 16 bytes, so the reads are broadcasts)
+    constexpr bool kInitLds = RS == 2;
     f32x16 c_init[RS];
+    if constexpr (!kInitLds) {
 #pragma unroll
-    for (int rs = 0; rs < RS; ++rs) {
+        for (int rs = 0; rs < RS; ++rs) {
 #pragma unroll
-        for (int a = 0; a < 4; ++a) {
-            const float4 v = *reinterpret_cast<const float4*>(&sinit[(wave * RS + rs) * 32 + c_row(4 * a, lane)]);
-            c_init[rs][4 * a] = v.x;
-            c_init[rs][4 * a + 1] = v.y;
-            c_init[rs][4 * a + 2] = v.z;
-            c_init[rs][4 * a + 3] = v.w;
+            for (int a = 0; a < 4; ++a) {
+                const float4 v = *reinterpret_cast<const float4*>(&sinit[(wave * RS + rs) * 32 + c_row(4 * a, lane)]);
+                c_init[rs][4 * a] = v.x;
+                c_init[rs][4 * a + 1] = v.y;
+                c_init[rs][4 * a + 2] = v.z;
+                c_init[rs][4 * a + 3] = v.w;
+            }
+            pin(c_init[rs]);
         }
-        pin(c_init[rs]);
     }
     typename G::Rd rd;
     rd.init(lane, 0);
@@ -349,12 +357,28 @@ __global__ __launch_bounds__(kThreads, (sizeof(T) == 4 && D == 128 ? 1 : TuneRS<
         for (int u = 0; u < kRing; ++u) {
             const int s = s0 + u;
             if (s >= sp.nch) break;
+            f32x16 acc[RS][2];
+            if constexpr (kInitLds) {  // before the wait: the reads' latency hides behind it
+#pragma unroll
+                for (int rs = 0; rs < RS; ++rs)
+#pragma unroll
+                    for (int b = 0; b < 2; ++b)
+#pragma unroll
+                        for (int a = 0; a < 4; ++a) {
+                            const float4 v =
+                                *reinterpret_cast<const float4*>(&sinit[(wave * RS + rs) * 32 + c_row(4 * a, lane)]);
+                            acc[rs][b][4 * a] = v.x;
+                            acc[rs][b][4 * a + 1] = v.y;
+                            acc[rs][b][4 * a + 2] = v.z;
+                            acc[rs][b][4 * a + 3] = v.w;
+                        }
+            }
             // the barrier inside also orders the scol writes of chunk s - 1
             // before their sum, and that sum before chunk s + 1 reuses the buffer
             ring_io.advance(ring, s, u, src);
             if (s >= 1) reduce(s - 1);
-            f32x16 acc[RS][2];
-            chunk_mma_sets<T, D, kKeys, false, RS>(acc, rd, ring + u * G::C::BYTES, qf, c_init);
+            chunk_mma_sets<T, D, kKeys, false, RS>(acc, rd, ring + u * G::C::BYTES, qf, kInitLds ? nullptr : c_init,
+                                                   kInitLds);
             if (sp.t_begin + (s + 1) * kKeys > P_rows) {  // keys past the range end or inside the causal window
                 // key t is visible to window query i (position P_rows + i) iff t - P_rows <= i
 #pragma unroll
