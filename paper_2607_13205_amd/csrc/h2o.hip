@@ -137,11 +137,15 @@ __global__ __launch_bounds__(kThreads, 2) void h2o_pass1_x2(RowView qv, RowView 
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int Gh = Hq / Hkv;
+    // the KV head varies fastest: workgroups are dealt to the XCDs in turn, so
+    // (with Hkv a divisor or multiple of their number) each XCD keeps to a few
+    // heads and their key rows, re-read by every later position block, stay in
+    // its L2; within a head the longest causal rows come first
     int bid = blockIdx.x;
-    const int pb = nblk - 1 - bid % nblk;  // longest causal rows first
-    bid /= nblk;
     const int j = bid % Hkv;
-    const int lb = bid / Hkv;
+    bid /= Hkv;
+    const int pb = nblk - 1 - bid % nblk;
+    const int lb = bid / nblk;
     const int p0 = pb * npos;
     int pos[2], lim[2];
     bool valid[2];
@@ -208,11 +212,15 @@ __global__ __launch_bounds__(kThreads, 2) void h2o_pass1(RowView qv, RowView kv,
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int Gh = Hq / Hkv;
+    // the KV head varies fastest: workgroups are dealt to the XCDs in turn, so
+    // (with Hkv a divisor or multiple of their number) each XCD keeps to a few
+    // heads and their key rows, re-read by every later position block, stay in
+    // its L2; within a head the longest causal rows come first
     int bid = blockIdx.x;
-    const int pb = nblk - 1 - bid % nblk;  // longest causal rows first
-    bid /= nblk;
     const int j = bid % Hkv;
-    const int lb = bid / Hkv;
+    bid /= Hkv;
+    const int pb = nblk - 1 - bid % nblk;
+    const int lb = bid / nblk;
     const int p0 = pb * npos;
     // this lane's row: head g of the group at position pos (position-major)
     const int r = wave * 32 + (lane & 31);
