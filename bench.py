@@ -650,7 +650,8 @@ def main():
     args = parse()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only; --gpus {args.gpus} is not supported "
-              "(the eviction path shards by layer or KV head with no exchange; see DESIGN.md)",
+              "(the eviction path shards by layer or KV head with no exchange between GPUs, so "
+              "one GPU's throughput times the GPU count is the whole job's)",
               file=sys.stderr)
         sys.exit(2)
     import torch
