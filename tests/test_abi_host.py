@@ -244,3 +244,19 @@ def test_strided_entry_points_reject_bad_views_before_any_launch(kve):
     st = lib.kve_kv_compact_strided(fake, ctypes.byref(dense_k), fake, ctypes.byref(S(0, 0, -1, 128)), 0, idx,
                                     cnt, 1, 2, 8, 1024, 128, 64, out, out, None)
     assert st == kve.binding.KVE_ERR_INVALID_ARG and "negative" in kve.last_error()
+
+
+def test_snapkv_rejects_more_window_rows_than_supported_before_any_launch(kve):
+    """G*W above 1024 window rows per KV head is refused on the host (the
+    pointers are never dereferenced); 1024 itself passes the check and fails
+    only later, on the fake workspace size."""
+    lib = kve.binding.LIB
+    fake = ctypes.c_void_p(0x10000)
+    score = ctypes.c_void_p(0x20000)
+    ws = ctypes.c_void_p(0x40000)
+    # Hq = 16, Hkv = 1, W = 65: 1040 rows
+    st = lib.kve_snapkv_score(fake, fake, 0, 1, 1, 16, 1, 4096, 65, 128, 0.0, 7, score, ws, 1 << 30, None)
+    assert st == kve.binding.KVE_ERR_UNSUPPORTED and "1024" in kve.last_error()
+    # W = 64: 1024 rows, accepted by the row check, refused for the 16-byte workspace
+    st = lib.kve_snapkv_score(fake, fake, 0, 1, 1, 16, 1, 4096, 64, 128, 0.0, 7, score, ws, 16, None)
+    assert st == kve.binding.KVE_ERR_WORKSPACE

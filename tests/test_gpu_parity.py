@@ -79,6 +79,10 @@ SNAP_CASES = [
     custom("rows160tail", 1, 1, 4, 1, 394, 40, 128, 7, "bf16"),
     # kernel 7 on rows too short for the register path: every key taken one by one
     custom("short7", 1, 2, 4, 2, 20, 4, 128, 7, "bf16"),
+    # the most window rows a KV head may have (G*W = 1024): four 256-row groups
+    # (bf16, four planes of column sums) and eight 128-row groups (float32)
+    custom("rows1024", 1, 1, 16, 1, 1500, 64, 128, 7, "bf16"),
+    custom("rows1024_f32", 1, 1, 16, 1, 700, 64, 64, 5, "f32"),
 ]
 
 
