@@ -217,6 +217,9 @@ H2O_CASES = [
     custom("h2o_g8", 1, 1, 16, 2, 700, 0, 128, 1, "bf16", scorer="h2o"),
     custom("h2o_g3", 1, 2, 6, 2, 333, 0, 64, 1, "bf16", scorer="h2o"),
     custom("h2o_g1_f32", 1, 1, 2, 2, 260, 0, 128, 1, "f32", scorer="h2o"),
+    # three KV heads (neither a divisor nor a multiple of the eight XCDs pass 1
+    # spreads its heads over) in two layers and two samples
+    custom("h2o_kv3", 2, 2, 6, 3, 400, 0, 128, 1, "bf16", scorer="h2o"),
 ]
 
 
