@@ -292,8 +292,8 @@ def graph_leg(pipeline, inp, alpha, budget, W, pool, bufs, scorer, steps, lse_wi
     torch.cuda.synchronize()
     same = bool(torch.equal(bufs.idx, idx0) and torch.equal(bufs.count, cnt0))
     return {"ms_per_step": round(ms, 4), "matches_eager": same,
-            "launch": "one HIP graph replay per step (quota copy, score, top-k, compaction); "
-                      "allocation on the host"}
+            "launch": "two HIP graph replays per step (the score; the quota copy, top-k and "
+                      "compaction), the host allocation between them while the device scores"}
 
 
 def select_figures(wl, inp, bufs, ms_topk, ms_compact):

@@ -179,6 +179,22 @@ def _select(k, v, roles_dev, bufs, W, R, l0, l1, stream=None, events=None, fused
         events[2].record(stream)
 
 
+def _upload_quotas(policy, roles_host, budget, W, bufs):
+    """Work out the quotas on the host and queue their upload (pinned host
+    buffer to device) on the current stream; returns (quota, kept)."""
+    import torch
+    quota, kept, k_cap = policy.allocate(roles_host, budget, W)
+    if k_cap > bufs.k_cap:
+        raise ValueError(f"buffers hold {bufs.k_cap} rows, the allocation keeps {k_cap}")
+    if bufs.copy_done is None:
+        bufs.copy_done = torch.cuda.Event()
+    bufs.copy_done.synchronize()          # the previous upload has left quota_host
+    bufs.quota_host.numpy()[...] = quota
+    bufs.quota_dev.copy_(bufs.quota_host, non_blocking=True)
+    bufs.copy_done.record()
+    return quota, kept
+
+
 def evict(q, k, v, roles_host: np.ndarray, roles_dev, policy, budget: float, W: int,
           pool_k: int, bufs: EvictBuffers, scorer: str = "snapkv", scale: float = 0.0,
           score_events=None, page: int = 16, chunks: int = 1, side_stream=None, lse_win=None,
@@ -196,23 +212,19 @@ def evict(q, k, v, roles_host: np.ndarray, roles_dev, policy, budget: float, W: 
     the window rows' log-sum-exp [L, B, Hq, W] as the prefill attention
     returned it, lets the score read K once.
 
-    The quotas depend on the labels only, so they are worked out first.  With
-    ``chunks`` > 1 and a ``side_stream``, the layers are scored in that many
-    chunks on the current stream while the top-k and compaction of each scored
-    chunk run on the side stream, overlapping the scoring of the next; the
-    current stream waits for the side stream before returning."""
+    The score does not depend on the quotas: it is queued first, and the host
+    works the quotas out from the labels and queues their upload while the
+    device scores (the top-k, queued after the upload, uses them), so the host
+    allocation adds nothing to the step's device time.  A ValueError for
+    buffers too small for the allocation is therefore raised after the score
+    was queued.  With ``chunks`` > 1 and a ``side_stream``, the quotas come
+    first; the layers are then scored in that many chunks on the current stream
+    while the top-k and compaction of each scored chunk run on the side stream,
+    overlapping the scoring of the next; the current stream waits for the side
+    stream before returning."""
     import torch
     policy = as_policy(policy)
     R = policy.R
-    quota, kept, k_cap = policy.allocate(roles_host, budget, W)
-    if k_cap > bufs.k_cap:
-        raise ValueError(f"buffers hold {bufs.k_cap} rows, the allocation keeps {k_cap}")
-    if bufs.copy_done is None:
-        bufs.copy_done = torch.cuda.Event()
-    bufs.copy_done.synchronize()          # the previous upload has left quota_host
-    bufs.quota_host.numpy()[...] = quota
-    bufs.quota_dev.copy_(bufs.quota_host, non_blocking=True)
-    bufs.copy_done.record()
     L = k.shape[0]
     main = torch.cuda.current_stream()
     fused = _fused(bufs, scorer, lse_win)
@@ -223,8 +235,10 @@ def evict(q, k, v, roles_host: np.ndarray, roles_dev, policy, budget: float, W: 
                R=R)
         if score_events is not None:
             score_events[1].record(main)
+        quota, kept = _upload_quotas(policy, roles_host, budget, W, bufs)
         _select(k, v, roles_dev, bufs, W, R, 0, L, stream=main, events=select_events, fused=fused)
         return quota, kept
+    quota, kept = _upload_quotas(policy, roles_host, budget, W, bufs)
     side_stream.wait_stream(main)         # the quota upload and earlier work
     per = (L + chunks - 1) // chunks
     if score_events is not None:
@@ -248,14 +262,15 @@ class StepGraph:
     compaction) captured as a HIP graph and replayed, for callers that run the
     step inside captured work (serving loops, launch-bound small shapes).
 
-    Two graphs are captured, each copying the quotas from its own pinned host
-    buffer, and replays alternate between them: a replay writes the quotas the
-    host allocation has just produced into its buffer once the replay before
-    last (the previous user of that buffer) has finished, so the host work of
-    one step overlaps the device work of the previous one.  The inputs, labels
-    and buffers are the tensors given here (refill them in place between
-    replays).  The library launches no memset and allocates nothing, so each
-    graph holds only kernel nodes and the one copy."""
+    The score is one graph; the selection (quota upload, top-k, compaction)
+    is captured twice, each copy uploading the quotas from its own pinned host
+    buffer, and replays alternate between the two.  A replay queues the score
+    graph, works the quotas out on the host while the device scores, writes
+    them into its buffer once the replay before last (the previous user of
+    that buffer) has finished, and queues its selection graph.  The inputs,
+    labels and buffers are the tensors given here (refill them in place
+    between replays).  The library launches no memset and allocates nothing,
+    so the graphs hold only kernel nodes and the one copy."""
 
     def __init__(self, q, k, v, roles_dev, policy, W: int, pool_k: int, bufs: EvictBuffers,
                  scorer: str = "snapkv", scale: float = 0.0, page: int = 16, lse_win=None):
@@ -269,22 +284,28 @@ class StepGraph:
 
         fused = _fused(bufs, scorer, lse_win)
 
-        def step(src):
-            bufs.quota_dev.copy_(src, non_blocking=True)
+        def score():
             _score(q, k, bufs, scorer, pool_k, scale, page, 0, L, lse_win=lse_win, roles_dev=roles_dev, R=R)
+
+        def select(src):
+            bufs.quota_dev.copy_(src, non_blocking=True)
             _select(k, v, roles_dev, bufs, W, R, 0, L, fused=fused)
 
         side = torch.cuda.Stream()
         side.wait_stream(torch.cuda.current_stream())
         with torch.cuda.stream(side):
-            step(self.quota_host[0])    # one eager run on the capture stream first
+            score()                     # one eager run on the capture stream first
+            select(self.quota_host[0])
         torch.cuda.current_stream().wait_stream(side)
         torch.cuda.synchronize()
+        self.score_graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(self.score_graph, stream=side):
+            score()
         self.graphs = []
         for src in self.quota_host:
             g = torch.cuda.CUDAGraph()
             with torch.cuda.graph(g, stream=side):
-                step(src)
+                select(src)
             self.graphs.append(g)
         self.done = [torch.cuda.Event(), torch.cuda.Event()]
         for e in self.done:
@@ -292,8 +313,11 @@ class StepGraph:
         self.turn = 0
 
     def replay(self, roles_host: np.ndarray, budget: float):
-        """Allocate on the host for these bucket labels and budget, then replay
-        the captured step on the current stream; returns (quota, kept)."""
+        """Replay the captured step on the current stream for these bucket
+        labels and budget, allocating on the host while the device scores;
+        returns (quota, kept).  A ValueError for buffers too small for the
+        allocation is raised after the score was queued."""
+        self.score_graph.replay()
         quota, kept, k_cap = self.policy.allocate(roles_host, budget, self.W)
         if k_cap > self.bufs.k_cap:
             raise ValueError(f"buffers hold {self.bufs.k_cap} rows, the allocation keeps {k_cap}")
