@@ -320,8 +320,11 @@ def flushed_steps(run, steps, with_select=True):
     buffer before each (outside its events) so that neither the L2s nor the
     256 MB last-level cache hold anything of the previous step.  run(score_ev,
     select_ev) runs one step recording the given events.  Returns the median,
-    minimum and maximum step time and the mean score, top-k and compaction
-    times (ms)."""
+    minimum and maximum step time and the mean score time of those steps, and
+    (with_select) the mean top-k and compaction times of as many further steps
+    run the same way with events around those two calls as well: an event
+    between two kernels leaves the device idle for a few microseconds, so the
+    timed steps carry only the events around the score (ms)."""
     import statistics
     import torch
     scratch = torch.empty(512 << 20, dtype=torch.uint8, device="cuda")
@@ -333,9 +336,14 @@ def flushed_steps(run, steps, with_select=True):
     for i in range(steps):
         scratch.fill_(i & 0xff)
         step_ev[i][0].record()
-        run(score_ev[i], sel_ev[i] if with_select else None)
+        run(score_ev[i], None)
         step_ev[i][1].record()
         torch.cuda.synchronize()
+    if with_select:
+        for i in range(steps):
+            scratch.fill_(i & 0xff)
+            run(mk(2), sel_ev[i])
+            torch.cuda.synchronize()
     del scratch
     times = [a.elapsed_time(b) for a, b in step_ev]
     out = {"median_ms": statistics.median(times), "min_ms": min(times), "max_ms": max(times),
