@@ -321,7 +321,7 @@ def flushed_steps(run, steps, with_select=True):
     256 MB last-level cache hold anything of the previous step.  run(score_ev,
     select_ev) runs one step recording the given events.  Returns the median,
     minimum and maximum step time and the mean score time of those steps, and
-    (with_select) the mean top-k and compaction times of as many further steps
+    (with_select) the median top-k and compaction times of as many further steps
     run the same way with events around those two calls as well: an event
     between two kernels leaves the device idle for a few microseconds, so the
     timed steps carry only the events around the score (ms)."""
@@ -348,9 +348,9 @@ def flushed_steps(run, steps, with_select=True):
     times = [a.elapsed_time(b) for a, b in step_ev]
     out = {"median_ms": statistics.median(times), "min_ms": min(times), "max_ms": max(times),
            "score_ms": sum(a.elapsed_time(b) for a, b in score_ev) / steps}
-    if with_select:
-        out["topk_ms"] = sum(a.elapsed_time(b) for a, b, _ in sel_ev) / steps
-        out["compact_ms"] = sum(b.elapsed_time(c) for _, b, c in sel_ev) / steps
+    if with_select:  # medians: a host pause before a launch would otherwise land in a mean
+        out["topk_ms"] = statistics.median(a.elapsed_time(b) for a, b, _ in sel_ev)
+        out["compact_ms"] = statistics.median(b.elapsed_time(c) for _, b, c in sel_ev)
     return out
 
 
