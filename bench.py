@@ -69,7 +69,7 @@ def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=10)
-    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default="stack32k")
     ap.add_argument("--budget", type=float, default=None)
     ap.add_argument("--alpha-key", type=float, default=0.0)
