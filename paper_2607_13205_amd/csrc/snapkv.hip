@@ -6,10 +6,11 @@
 // (windowed-mass and pooling steps).
 //
 // A segment is one (layer, sample, KV head); its rows are the G*W window
-// queries of the group (head-major), taken in row groups of 128 (a virtual
-// segment, vseg, is one segment and one row group).  A workgroup of four waves
-// owns a vseg and a contiguous range of its keys; each wave owns a 32-row
-// block whose query fragments stay in registers.  Keys stream through an LDS
+// queries of the group (head-major), taken in row groups of 128, or of 256 for
+// bf16 windows of more than 128 rows (a virtual segment, vseg, is one segment
+// and one row group).  A workgroup of four waves owns a vseg and a contiguous
+// range of its keys; each wave owns one 32-row block, or two, whose query
+// fragments stay in registers.  Keys stream through an LDS
 // ring in chunks of 64 with direct-to-LDS loads issued one to three chunks
 // ahead, so every wave keeps HBM requests in flight while it multiplies on the
 // matrix cores (bf16 32x32x16, fp32 32x32x2).  No workgroup waits on another
