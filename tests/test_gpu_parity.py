@@ -236,6 +236,27 @@ def test_h2o_score_matches_oracle(K, wl):
     np.testing.assert_allclose(tot, wl.G * wl.N, rtol=1e-4)
 
 
+@pytest.mark.parametrize("wl", [custom("h2o_spike", 1, 1, 8, 2, 700, 0, 128, 1, "bf16", scorer="h2o"),
+                                custom("h2o_spike_f32", 1, 1, 4, 2, 500, 0, 64, 1, "f32", scorer="h2o")],
+                         ids=lambda w: w.name)
+def test_h2o_score_logit_spikes_match_oracle(K, wl):
+    """Every 97th key row scaled by 40: causal rows meet logits far above the
+    running reference of their first chunks, so the row sums of pass 1 leave
+    [0, 2^64] (or overflow) and raise their reference part way."""
+    note(f"h2o parity with logit spikes {wl}")
+    inp = WL.make_inputs(wl, device="cuda", with_v=False)
+    k = inp["k"].clone()
+    k[:, :, :, 40::97, :] *= 40
+    q = inp["q"]
+    qq = f64(q).reshape(wl.L, wl.B, wl.Hkv, wl.G * wl.N, wl.d)
+    logit2 = np.matmul(qq, np.swapaxes(f64(k), -1, -2)) * (wl.d ** -0.5) * math.log2(math.e)
+    assert float((logit2.max(axis=-1) - logit2[..., :40].max(axis=-1)).max()) > 128
+    score = K.h2o_score(q, k)
+    torch.cuda.synchronize()
+    ref = O.h2o_score(f64(q), f64(k), wl.Hkv)
+    check_scores(f64(score), ref, wl.name)
+
+
 def _token_major(x, pad):
     """x [L, B, H, T, d] as a view of a token-major tensor [L, B, T, H, d + pad]
     (NaN in the padding, which must never be read)."""
