@@ -105,7 +105,7 @@ def alloc_buffers(k, n_q_heads: int, W: int, R: int, k_cap: int, scorer: str = "
     pool epilogue counts the top-k's first digit per role bucket
     (snapkv_score_hist / topk_select_hist) and the histograms live here.  Off
     by default: on the 32-layer N = 32768 step the counting adds more to the
-    pool (about 60 us) than it takes off the top-k (about 25 us)."""
+    pool (about 100 us) than it takes off the top-k (about 25 us)."""
     import torch
     L, B, Hkv, N, d = k.shape
     dev = k.device
