@@ -35,7 +35,7 @@ inline size_t h2o_workspace(int L, int B, int Hq, int N) {
 // output o[d] and its (reference, denominator) pair, merged by a last step.
 // ---------------------------------------------------------------------------
 constexpr int kDecodeQuantum = 128;
-constexpr int kDecodeTargetGroups = 2048;
+constexpr int kDecodeTargetGroups = 1024;  // one split per segment once there are 1024 segments
 constexpr int kDecodeMaxGroup = 8;  // query heads per KV head
 
 struct DecodePlan {
