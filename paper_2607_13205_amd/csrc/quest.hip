@@ -29,18 +29,44 @@ __device__ __forceinline__ const char* seg_head_rows(const RowView& v, int seg, 
     return v.base + (long long)(lb / B) * v.s_layer + (long long)(lb % B) * v.s_batch + (long long)h * v.s_head;
 }
 
-// qbar[seg, h, c] = mean over the W window rows of head h (float32)
+// qbar[seg, h, c] = mean over the W window rows of head h (float32).  A thread
+// takes one 16-byte piece of a row (CW channels) of one head and adds the W
+// rows in order, eight rows' loads in flight at a time.
 template <typename T>
 __global__ __launch_bounds__(kThreads) void quest_qmean(RowView qv, int B, int Hkv, int W, int G, int D,
                                                         float* __restrict__ qbar) {
+    using VP = VPiece<T>;
+    constexpr int CW = VP::CW;
+    constexpr int kBatch = 8;
     const int seg = blockIdx.x;
     const float inv = 1.0f / (float)W;
-    for (int e = threadIdx.x; e < G * D; e += kThreads) {
-        const int h = e / D, c = e - (e / D) * D;
-        const char* rows = seg_head_rows(qv, seg, B, Hkv, (seg % Hkv) * G + h) + (long long)c * sizeof(T);
-        float acc = 0.0f;
-        for (int i = 0; i < W; ++i) acc += (float)*reinterpret_cast<const T*>(rows + (long long)i * qv.s_token);
-        qbar[(size_t)seg * G * D + e] = acc * inv;
+    const int pieces = D / CW;  // per row
+    for (int e = threadIdx.x; e < G * pieces; e += kThreads) {
+        const int h = e / pieces, pc = e - (e / pieces) * pieces;
+        const char* rows = seg_head_rows(qv, seg, B, Hkv, (seg % Hkv) * G + h) + (long long)pc * 16;
+        float acc[CW] = {};
+        int i = 0;
+        for (; i + kBatch <= W; i += kBatch) {
+            u32x4 raw[kBatch];
+#pragma unroll
+            for (int j = 0; j < kBatch; ++j) raw[j] = ld16(rows + (long long)(i + j) * qv.s_token);
+#pragma unroll
+            for (int j = 0; j < kBatch; ++j) {
+                float f[CW];
+                VP::to_f(raw[j], f);
+#pragma unroll
+                for (int c = 0; c < CW; ++c) acc[c] += f[c];
+            }
+        }
+        for (; i < W; ++i) {
+            float f[CW];
+            VP::to_f(ld16(rows + (long long)i * qv.s_token), f);
+#pragma unroll
+            for (int c = 0; c < CW; ++c) acc[c] += f[c];
+        }
+        float* dst = qbar + (size_t)seg * G * D + (size_t)h * D + (size_t)pc * CW;
+#pragma unroll
+        for (int c = 0; c < CW; ++c) dst[c] = acc[c] * inv;
     }
 }
 
