@@ -459,8 +459,8 @@ __global__ __launch_bounds__(NT) void topk_kernel(const float* __restrict__ scor
 #pragma unroll
             for (int r = 0; r < R; ++r) {
                 const uint64_t m = __ballot(c == 2 + r);
-                if (c == 2 + r) k = eq_seen[r] + __popcll(m & lt) < need[r];
-                eq_seen[r] += __popcll(m);
+                if (c == 2 + r) k = eq_seen[r] + (int)__popcll(m & lt) < need[r];
+                eq_seen[r] += (int)__popcll(m);
             }
         }
         const uint64_t km = __ballot(k);
