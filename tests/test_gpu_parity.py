@@ -83,6 +83,8 @@ SNAP_CASES = [
     # (bf16, four planes of column sums) and eight 128-row groups (float32)
     custom("rows1024", 1, 1, 16, 1, 1500, 64, 128, 7, "bf16"),
     custom("rows1024_f32", 1, 1, 16, 1, 700, 64, 64, 5, "f32"),
+    # three KV heads in two layers and two samples (segments not a power of two)
+    custom("kv3", 2, 2, 12, 3, 1000, 16, 128, 7, "bf16"),
 ]
 
 
@@ -1042,6 +1044,7 @@ QUEST_CASES = [
     ("wfull", 1, 1, 4, 1, 64, 64, 128, "bf16", 16),
     ("f32", 1, 2, 8, 2, 333, 16, 128, "f32", 16),
     ("f32d64", 1, 1, 8, 1, 500, 9, 64, "f32", 8),
+    ("kv3", 2, 2, 12, 3, 700, 13, 128, "bf16", 16),
     ("long", 2, 1, 8, 2, 20000, 32, 128, "bf16", 16),
 ]
 
