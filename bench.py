@@ -60,6 +60,9 @@ TRAFFIC_SUMMARY_LONG = os.path.join(ROOT, "profiles", "long128k_score_profile.md
 # sources of the kernels one score call launches
 SCORE_SOURCES = ("paper_2607_13205_amd/csrc/snapkv.hip", "paper_2607_13205_amd/csrc/kve_stream.h",
                  "paper_2607_13205_amd/csrc/kve_device.h", "paper_2607_13205_amd/csrc/kve_snap_plan.h")
+# untimed calls before each leg's timed ones: after a leg's set-up (new buffers,
+# host work) the latency-bound kernels and the clock take some 10 steps to settle
+LEG_WARMUP = 10
 COPY_BYTES = 1 << 30
 HBM_PEAK_GBS = 8000.0
 BF16_MFMA_PEAK_TFLOPS = 2500.0
@@ -219,7 +222,7 @@ def h2o_leg(K, WL, steps):
     score = torch.empty((wl.L, wl.B, wl.Hkv, wl.N), dtype=torch.float32, device="cuda")
     ws = torch.empty(K.h2o_workspace_size(wl.L, wl.B, wl.Hq, wl.Hkv, wl.N, wl.d),
                      dtype=torch.uint8, device="cuda")
-    for _ in range(2):
+    for _ in range(LEG_WARMUP):
         K.h2o_score(inp["q"], inp["k"], score=score, workspace=ws)
     torch.cuda.synchronize()
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -270,7 +273,7 @@ def fused_leg(pipeline, wl, inp, alpha, budget, W, pool, k_cap, steps):
     bufs = pipeline.alloc_buffers(inp["k"], wl.Hq, W, 4, k_cap, fused=True)
     run = lambda e, s_: pipeline.evict(inp["q"], inp["k"], inp["v"], inp["roles"], inp["roles_t"], alpha,  # noqa: E731
                                        budget, W, pool, bufs, score_events=e, select_events=s_)
-    for _ in range(2):
+    for _ in range(LEG_WARMUP):
         run(None, None)
     t = flushed_steps(run, steps)
     del bufs
@@ -282,7 +285,8 @@ def fused_leg(pipeline, wl, inp, alpha, budget, W, pool, k_cap, steps):
 
 def graph_leg(pipeline, inp, alpha, budget, W, pool, bufs, scorer, steps, lse_win=None):
     """Step time with the device part captured once as a HIP graph and replayed
-    (the host allocation still runs every step), and whether the replays give
+    (the host allocation runs between the score graph and the selection graph,
+    while the device scores), and whether the replays give
     the eager step's kept indices and counts."""
     import torch
     idx0, cnt0 = bufs.idx.clone(), bufs.count.clone()
@@ -383,7 +387,7 @@ def long_leg(K, WL, pipeline, alpha, steps):
             pipeline.evict(inp["q"], inp["k"], inp["v"], inp["roles"], inp["roles_t"], alpha, budget, wl.W,
                            wl.pool_k, bufs, score_events=e, select_events=s_)
 
-        for _ in range(2):
+        for _ in range(LEG_WARMUP):
             run()
         t = flushed_steps(run, steps)
         sb = snapkv_algorithmic_bytes(wl)
@@ -505,11 +509,11 @@ def _optional_leg(name, fn):
 
 def _median_calls(fn, steps):
     """Median time (ms) of `steps` single calls of fn, each bracketed by HIP
-    events and followed by a synchronisation (after two untimed calls): one
+    events and followed by a synchronisation (after LEG_WARMUP untimed calls): one
     host-side stall moves a mean of back-to-back calls, not this median."""
     import statistics
     import torch
-    for _ in range(2):
+    for _ in range(LEG_WARMUP):
         fn()
     torch.cuda.synchronize()
     times = []
@@ -525,7 +529,7 @@ def _median_calls(fn, steps):
 
 def _time_calls(fn, steps):
     import torch
-    for _ in range(2):
+    for _ in range(LEG_WARMUP):
         fn()
     torch.cuda.synchronize()
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
